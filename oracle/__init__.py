@@ -1,0 +1,297 @@
+"""Python access to the IsoQuant stage-1 oracle (``isoq_oracle.c``).
+
+TEST INFRASTRUCTURE ONLY: the test suite, the smoke check and the benchmark's
+CPU-baseline leg may use this package; the product path never does.  The
+oracle shares no code with the HIP library.  This wrapper only marshals
+arguments (numpy arrays in, numpy arrays out) and widens inputs to float64,
+which is exact for fp16 and fp32 values.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "isoq_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+FULL, FAST, PLANAR2D = 0, 1, 2
+VARIANTS = {"full": FULL, "fast": FAST, "2d": PLANAR2D}
+
+
+def build() -> str:
+    """Compile the oracle with gcc (IEEE double, no FMA contraction)."""
+    tmp = _LIB + ".tmp"
+    cmd = ["gcc", "-O2", "-std=gnu11", "-ffp-contract=off", "-fno-fast-math",
+           "-fPIC", "-shared", _SRC, "-o", tmp, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+            build()
+        L = ctypes.CDLL(_LIB)
+        dp = ctypes.POINTER(ctypes.c_double)
+        u8p = ctypes.POINTER(ctypes.c_uint8)
+        i64 = ctypes.c_int64
+        L.orc_qmul.argtypes = [dp, dp, dp]
+        L.orc_qconj.argtypes = [dp, dp]
+        L.orc_qnormalize.argtypes = [dp, dp]
+        L.orc_full_forward.argtypes = [dp, dp, dp, dp]
+        L.orc_full_inverse.argtypes = [dp, dp, dp, dp]
+        L.orc_fast_forward.argtypes = [dp, dp, dp]
+        L.orc_fast_inverse.argtypes = [dp, dp, dp]
+        L.orc_planar_forward.argtypes = [ctypes.c_double, dp, dp]
+        L.orc_planar_inverse.argtypes = [ctypes.c_double, dp, dp]
+        L.orc_thresholds.argtypes = [ctypes.c_int, dp, dp]
+        L.orc_lloyd_max_gaussian.argtypes = [ctypes.c_int, ctypes.c_double, ctypes.c_int, dp]
+        L.orc_lloyd_max_gaussian.restype = ctypes.c_int
+        L.orc_num_blocks.argtypes = [ctypes.c_int, ctypes.c_int]
+        L.orc_raw_params_per_set.argtypes = [ctypes.c_int, ctypes.c_int]
+        L.orc_table1_params.argtypes = [ctypes.c_int, ctypes.c_int]
+        L.orc_encode.argtypes = [ctypes.c_int, ctypes.c_int, dp, dp, dp]
+        L.orc_decode.argtypes = [ctypes.c_int, ctypes.c_int, dp, dp, dp]
+        L.orc_stage1.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, i64,
+                                 dp, dp, dp, i64, i64, u8p, dp, dp]
+        L.orc_stage1.restype = ctypes.c_int
+        L.orc_stage1_rows.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, i64,
+                                      dp, dp, ctypes.POINTER(ctypes.c_int64), i64, dp, u8p, dp, dp]
+        L.orc_stage1_rows.restype = ctypes.c_int
+        L.orc_dequantize.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, i64,
+                                     dp, dp, u8p, dp, i64, i64, dp]
+        L.orc_dequantize.restype = ctypes.c_int
+        L.orc_record_bytes.argtypes = [ctypes.c_int, ctypes.c_int]
+        L.orc_record_bytes.restype = i64
+        L.orc_pack.argtypes = [u8p, i64, ctypes.c_int, ctypes.c_int, u8p]
+        L.orc_unpack.argtypes = [u8p, i64, ctypes.c_int, ctypes.c_int, u8p]
+        L.orc_mul_count.restype = ctypes.c_uint64
+        _lib = L
+    return _lib
+
+
+def _d(a):
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+def _p(a, t=ctypes.c_double):
+    return a.ctypes.data_as(ctypes.POINTER(t))
+
+
+def _variant(v) -> int:
+    return VARIANTS[v] if isinstance(v, str) else int(v)
+
+
+# --- quaternion algebra (Sec. 4) ---------------------------------------------
+def qmul(p, q):
+    p, q, out = _d(p), _d(q), np.zeros(4)
+    lib().orc_qmul(_p(p), _p(q), _p(out))
+    return out
+
+
+def qconj(q):
+    q, out = _d(q), np.zeros(4)
+    lib().orc_qconj(_p(q), _p(out))
+    return out
+
+
+def qnormalize(u):
+    u, out = _d(u), np.zeros(4)
+    lib().orc_qnormalize(_p(u), _p(out))
+    return out
+
+
+def full_forward(qL, qR, v):
+    qL, qR, v, out = _d(qL), _d(qR), _d(v), np.zeros(4)
+    lib().orc_full_forward(_p(qL), _p(qR), _p(v), _p(out))
+    return out
+
+
+def full_inverse(qL, qR, v):
+    qL, qR, v, out = _d(qL), _d(qR), _d(v), np.zeros(4)
+    lib().orc_full_inverse(_p(qL), _p(qR), _p(v), _p(out))
+    return out
+
+
+def fast_forward(qL, v):
+    qL, v, out = _d(qL), _d(v), np.zeros(4)
+    lib().orc_fast_forward(_p(qL), _p(v), _p(out))
+    return out
+
+
+def fast_inverse(qL, v):
+    qL, v, out = _d(qL), _d(v), np.zeros(4)
+    lib().orc_fast_inverse(_p(qL), _p(v), _p(out))
+    return out
+
+
+def planar_forward(theta, u):
+    u, out = _d(u), np.zeros(2)
+    lib().orc_planar_forward(float(theta), _p(u), _p(out))
+    return out
+
+
+def planar_inverse(theta, u):
+    u, out = _d(u), np.zeros(2)
+    lib().orc_planar_inverse(float(theta), _p(u), _p(out))
+    return out
+
+
+# --- codebook ------------------------------------------------------------------
+def lloyd_max_gaussian(bits: int, sigma: float, iters: int = 200) -> np.ndarray:
+    out = np.zeros(1 << bits)
+    rc = lib().orc_lloyd_max_gaussian(int(bits), float(sigma), int(iters), _p(out))
+    if rc != 0:
+        raise ValueError("bad codebook arguments")
+    return out
+
+
+def codebook(bits: int, d: int, iters: int = 200) -> np.ndarray:
+    """Lloyd-Max levels for N(0, 1/d) (the reading used for every workload)."""
+    return lloyd_max_gaussian(bits, 1.0 / np.sqrt(d), iters)
+
+
+def thresholds(bits: int, levels) -> np.ndarray:
+    levels = _d(levels)
+    out = np.zeros((1 << bits) - 1)
+    lib().orc_thresholds(int(bits), _p(levels), _p(out))
+    return out
+
+
+# --- geometry / counts -----------------------------------------------------------
+def num_blocks(variant, d: int) -> int:
+    return lib().orc_num_blocks(_variant(variant), int(d))
+
+
+def raw_params_per_set(variant, d: int) -> int:
+    return lib().orc_raw_params_per_set(_variant(variant), int(d))
+
+
+def table1_params(variant, d: int) -> int:
+    return lib().orc_table1_params(_variant(variant), int(d))
+
+
+def padded_width(variant, d: int) -> int:
+    v = _variant(variant)
+    return num_blocks(v, d) * (2 if v == PLANAR2D else 4)
+
+
+def mul_count_reset():
+    lib().orc_mul_count_reset()
+
+
+def mul_count() -> int:
+    return int(lib().orc_mul_count())
+
+
+def encode(variant, d, rot, xbar):
+    v = _variant(variant)
+    rot, xbar = _d(rot), _d(xbar)
+    out = np.zeros(padded_width(v, d))
+    lib().orc_encode(v, int(d), _p(rot), _p(xbar), _p(out))
+    return out
+
+
+def decode(variant, d, rot, yhat):
+    v = _variant(variant)
+    rot, yhat = _d(rot), _d(yhat)
+    out = np.zeros(int(d))
+    lib().orc_decode(v, int(d), _p(rot), _p(yhat), _p(out))
+    return out
+
+
+# --- Algorithm 1 -------------------------------------------------------------------
+def stage1(variant, d: int, bits: int, rot, levels, x, n_sets: int = 1, rows_per_set: int = 1,
+           rows=None, want_idx=True, want_xhat=True):
+    """Run Algorithm 1 on rows of ``x`` ([n, d], any float dtype).
+
+    ``rows`` optionally selects a subset (array of row numbers); the set of a
+    row is computed from its global row number.  Returns (idx, rho, xhat) for
+    the selected rows; idx has ``padded_width`` columns.
+    """
+    v = _variant(variant)
+    rot = _d(rot)
+    levels = _d(levels)
+    x = np.asarray(x)
+    pw = padded_width(v, d)
+    L = lib()
+    if rows is None:
+        xd = _d(x.reshape(-1, d))
+        n = xd.shape[0]
+        idx = np.zeros((n, pw), np.uint8) if want_idx else None
+        rho = np.zeros(n)
+        xh = np.zeros((n, d)) if want_xhat else None
+        rc = L.orc_stage1(v, d, bits, n_sets, rows_per_set, _p(rot), _p(levels), _p(xd), 0, n,
+                          _p(idx, ctypes.c_uint8) if idx is not None else None, _p(rho),
+                          _p(xh) if xh is not None else None)
+        if rc != 0:
+            raise ValueError("orc_stage1 rejected its arguments")
+        return idx, rho, xh
+    rows = np.ascontiguousarray(rows, dtype=np.int64)
+    xs = _d(x.reshape(-1, d)[rows])
+    m = len(rows)
+    idx = np.zeros((m, pw), np.uint8)
+    rho = np.zeros(m)
+    xh = np.zeros((m, d))
+    rc = L.orc_stage1_rows(v, d, bits, n_sets, rows_per_set, _p(rot), _p(levels),
+                           _p(rows, ctypes.c_int64), m, _p(xs), _p(idx, ctypes.c_uint8), _p(rho),
+                           _p(xh))
+    if rc != 0:
+        raise ValueError("orc_stage1_rows rejected its arguments")
+    return idx, rho, xh
+
+
+def stage1_range(variant, d, bits, rot, levels, xd, row_begin, row_end, n_sets=1, rows_per_set=1,
+                 idx=None, rho=None, xh=None):
+    """Low-level entry used by the CPU baseline: rows [row_begin, row_end) of a
+    float64 [n, d] array, writing into preallocated outputs (ctypes releases
+    the GIL, so several Python threads can split the rows)."""
+    v = _variant(variant)
+    return lib().orc_stage1(v, d, bits, n_sets, rows_per_set, _p(rot), _p(levels), _p(xd),
+                            int(row_begin), int(row_end),
+                            _p(idx, ctypes.c_uint8) if idx is not None else None,
+                            _p(rho), _p(xh) if xh is not None else None)
+
+
+def dequantize(variant, d: int, bits: int, rot, levels, idx, rho, n_sets: int = 1,
+               rows_per_set: int = 1):
+    v = _variant(variant)
+    rot, levels, rho = _d(rot), _d(levels), _d(rho)
+    idx = np.ascontiguousarray(idx, dtype=np.uint8)
+    n = rho.shape[0]
+    xh = np.zeros((n, d))
+    rc = lib().orc_dequantize(v, d, bits, n_sets, rows_per_set, _p(rot), _p(levels),
+                              _p(idx, ctypes.c_uint8), _p(rho), 0, n, _p(xh))
+    if rc != 0:
+        raise ValueError("orc_dequantize rejected its arguments")
+    return xh
+
+
+# --- packing -------------------------------------------------------------------------
+def record_bytes(m: int, bits: int) -> int:
+    return int(lib().orc_record_bytes(int(m), int(bits)))
+
+
+def pack(idx, bits: int) -> np.ndarray:
+    idx = np.ascontiguousarray(idx, dtype=np.uint8)
+    n, m = idx.shape
+    out = np.zeros((n, record_bytes(m, bits)), np.uint8)
+    lib().orc_pack(_p(idx, ctypes.c_uint8), n, m, bits, _p(out, ctypes.c_uint8))
+    return out
+
+
+def unpack(packed, m: int, bits: int) -> np.ndarray:
+    packed = np.ascontiguousarray(packed, dtype=np.uint8)
+    n = packed.shape[0]
+    out = np.zeros((n, m), np.uint8)
+    lib().orc_unpack(_p(packed, ctypes.c_uint8), n, m, bits, _p(out, ctypes.c_uint8))
+    return out
