@@ -1,0 +1,256 @@
+#!/usr/bin/env python3
+"""Throughput of the IsoQuant stage-1 path on one MI355X.
+
+One step = one fused quantize->dequantize pass (isoq_roundtrip) over the whole
+batch: 1,048,576 unit-norm Gaussian fp16 vectors, d = 128, 3 bits,
+IsoQuant-Full (the headline configuration).  Inputs are resident in HBM
+before timing starts; the timed loop rotates over several input/output buffer
+sets so that the 256 MB Infinity Cache cannot serve them.  Timing uses HIP
+events on the stream the kernels are launched on.  The JSON line also carries
+the roofline of the kernel (algorithmic bytes per launch / average launch
+time against 8 TB/s), the HBM traffic counted by rocprofv3 when a profile of
+the same kernel source is committed under profiles/, side measurements
+(quantize, dequantize, other variants and bit widths, a plain device copy of
+the same size) and the CPU oracle timed on a bounded sample on the host.
+
+    python bench.py [--steps K] [--warmup W] [--variant full|fast|2d] [--bits 3]
+                    [--d 128] [--dtype f16|f32] [--n N] [--mode roundtrip|quantize|dequantize]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import threading
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBPS = 8000.0          # MI355X HBM3E, vendor figure
+METRIC = "fused quant-dequant vectors/s + effective HBM GB/s (% peak), d=128 3-bit fp16"
+KERNEL_SRC = os.path.join(ROOT, "paper_2603_28430_amd", "csrc", "isoq_kernels.hip")
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def kernel_source_hash() -> str:
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def algorithmic_bytes(mode: str, n: int, d: int, bits: int, esz: int) -> int:
+    """Bytes one launch must move: rows in/out, packed records (d*bits/8) and
+    fp32 norms; rotation parameters and codebook (a few KB) are left out."""
+    rec = (d * bits + 7) // 8
+    if mode == "roundtrip":
+        return n * 2 * d * esz
+    if mode == "quantize":
+        return n * (d * esz + rec + 4)
+    return n * (rec + 4 + d * esz)
+
+
+def measured_traffic(tag: str):
+    """HBM bytes per launch from a committed rocprofv3 PMC summary of the same
+    kernel source (or None)."""
+    path = os.path.join(PROFILES, f"{tag}_pmc.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m = re.search(r"kernel_source_sha256:\s*([0-9a-f]+)", text)
+    t = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not m or not t or m.group(1) != kernel_source_hash():
+        return None
+    return float(t.group(1))
+
+
+def time_launches(fn, steps: int, warmup: int, torch):
+    """Average milliseconds per launch over `steps` launches (events on the
+    current stream, which is the stream every launch uses)."""
+    for i in range(warmup):
+        fn(i)
+    torch.cuda.synchronize()
+    s = torch.cuda.Event(enable_timing=True)
+    e = torch.cuda.Event(enable_timing=True)
+    s.record()
+    for i in range(steps):
+        fn(i)
+    e.record()
+    e.synchronize()
+    torch.cuda.synchronize()
+    return s.elapsed_time(e) / steps
+
+
+def cpu_baseline(variant, d, bits, x_np, rot, levels, seconds: float):
+    """The oracle (plain C, double precision) on the first rows of the same
+    workload, rows split across host threads.  Returns the JSON object."""
+    import numpy as np
+
+    import oracle
+
+    try:
+        avail = len(os.sched_getaffinity(0))
+    except AttributeError:
+        avail = os.cpu_count() or 1
+    threads = max(1, min(16, avail))
+    probe = 2000
+    xd = np.ascontiguousarray(x_np[:probe], dtype=np.float64)
+    rho = np.zeros(probe)
+    xh = np.zeros((probe, d))
+    t0 = time.perf_counter()
+    oracle.stage1_range(variant, d, bits, rot, levels, xd, 0, probe, rho=rho, xh=xh)
+    per_row = (time.perf_counter() - t0) / probe
+    rows = int(min(len(x_np), max(threads * 1000, seconds * threads / per_row)))
+    xd = np.ascontiguousarray(x_np[:rows], dtype=np.float64)
+    rho = np.zeros(rows)
+    xh = np.zeros((rows, d))
+    bounds = np.linspace(0, rows, threads + 1).astype(np.int64)
+    work = [threading.Thread(target=oracle.stage1_range,
+                             args=(variant, d, bits, rot, levels, xd, int(bounds[i]),
+                                   int(bounds[i + 1])), kwargs={"rho": rho, "xh": xh})
+            for i in range(threads)]
+    t0 = time.perf_counter()
+    for w in work:
+        w.start()
+    for w in work:
+        w.join()
+    dt = time.perf_counter() - t0
+    return {"value": rows / dt, "unit": "vectors/s", "cores": threads, "kind": "oracle",
+            "sample": f"first {rows} of the {len(x_np)} input rows, fp64 C oracle "
+                      f"(Algorithm 1, indices not stored), {threads} threads, {dt:.1f} s"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--variant", default="full", choices=["full", "fast", "2d"])
+    ap.add_argument("--bits", type=int, default=3)
+    ap.add_argument("--d", type=int, default=128)
+    ap.add_argument("--dtype", default="f16", choices=["f16", "f32"])
+    ap.add_argument("--n", type=int, default=1 << 20)
+    ap.add_argument("--mode", default="roundtrip", choices=["roundtrip", "quantize", "dequantize"])
+    ap.add_argument("--buffer-sets", type=int, default=4)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extras", action="store_true")
+    ap.add_argument("--copy-only", action="store_true",
+                    help="only time a plain device copy of the input size (counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (rows are "
+              "independent, so a multi-GPU run is N copies of this one).", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    import paper_2603_28430_amd as iq
+    import workloads
+
+    torch.cuda.set_device(0)
+    tdt, ndt, esz = {"f16": (torch.float16, np.float16, 2), "f32": (torch.float32, np.float32, 4)}[args.dtype]
+    n, d, bits, S = args.n, args.d, args.bits, max(1, args.buffer_sets)
+    print(f"# inputs: {n} x {d} {args.dtype}", file=sys.stderr, flush=True)
+    x_np = workloads.unit_gaussian_rows(n, d, seed=0, dtype=ndt)
+    x0 = torch.from_numpy(x_np).cuda()
+    xs = [x0] + [x0.clone() for _ in range(S - 1)]
+    outs = [torch.empty_like(x0) for _ in range(S)]
+
+    if args.copy_only:
+        ms = time_launches(lambda i: outs[i % S].copy_(xs[i % S]), args.steps, args.warmup, torch)
+        b = 2 * x0.numel() * esz
+        print(json.dumps({"copy_bytes_per_launch": b, "ms_per_launch": ms, "GBps": b / ms / 1e6}))
+        return 0
+
+    def setup(variant, bits_):
+        rot = workloads.rotation_draws(variant, d, 1, seed=1)
+        return iq.isoq_params_init(variant, d, bits_, 1, rot=rot), rot
+
+    def measure(variant, bits_, mode, steps, warmup):
+        p, _ = setup(variant, bits_)
+        if mode == "roundtrip":
+            fn = lambda i: iq.isoq_roundtrip(p, xs[i % S], x_hat=outs[i % S])
+        else:
+            recs = [torch.empty((n, p.record_bytes), dtype=torch.uint8, device="cuda") for _ in range(S)]
+            norms = [torch.empty((n,), dtype=torch.float32, device="cuda") for _ in range(S)]
+            for i in range(S):
+                iq.isoq_quantize(p, xs[i], idx_packed=recs[i], norms=norms[i])
+            if mode == "quantize":
+                fn = lambda i: iq.isoq_quantize(p, xs[i % S], idx_packed=recs[i % S], norms=norms[i % S])
+            else:
+                fn = lambda i: iq.isoq_dequantize(p, recs[i % S], norms[i % S], x_hat=outs[i % S])
+        ms = time_launches(fn, steps, warmup, torch)
+        b = algorithmic_bytes(mode, n, d, bits_, esz)
+        return ms, b
+
+    # ---- the timed headline: K steps of the fused path ----
+    print(f"# timing {args.mode} {args.variant} b={bits}", file=sys.stderr, flush=True)
+    ms, abytes = measure(args.variant, bits, args.mode, args.steps, args.warmup)
+    gbps = abytes / ms / 1e6
+    tag = f"{args.mode}_{args.variant}_d{d}_b{bits}_{args.dtype}_n{n}"
+    result = {
+        "metric": METRIC,
+        "value": n / (ms / 1e3),
+        "unit": "vectors/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic: i.i.d. N(0,1) rows scaled to unit norm (seed 0), raw rotation draws "
+                "from Philox4x32-10 (seed 1), Lloyd-Max codebook for N(0,1/d), 200 iterations",
+        "config": {"workload": f"IsoQuant-{args.variant} stage-1 {args.mode}, {n} vectors x d={d}, "
+                               f"{bits}-bit, {args.dtype} rows (fp32 arithmetic)",
+                   "variant": args.variant, "d": d, "bits": bits, "io_dtype": args.dtype, "n": n,
+                   "mode": args.mode, "buffer_sets": S},
+        "effective_GBps": gbps,
+        "pct_of_peak_hbm": 100.0 * gbps / PEAK_HBM_GBPS,
+        "roofline": {"bound": "hbm", "achieved": gbps, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                     "frac": gbps / PEAK_HBM_GBPS, "traffic": measured_traffic(tag),
+                     "algorithmic_bytes_per_launch": abytes,
+                     "kernel": f"stage1_kernel<{args.variant},{d},{bits},{args.dtype},{args.mode}>",
+                     "kernel_source_sha256": kernel_source_hash()},
+    }
+
+    if not args.no_extras:
+        extra = {}
+        print("# side measurements", file=sys.stderr, flush=True)
+        cms = time_launches(lambda i: outs[i % S].copy_(xs[i % S]), 50, 5, torch)
+        extra["device_copy_same_size"] = {"GBps": 2 * x0.numel() * esz / cms / 1e6, "ms": cms}
+        paths = {}
+        for mode in ("quantize", "dequantize"):
+            m_ms, m_b = measure(args.variant, bits, mode, 100, 10)
+            paths[mode] = {"ms": m_ms, "vectors_per_s": n / (m_ms / 1e3), "GBps": m_b / m_ms / 1e6,
+                           "frac": m_b / m_ms / 1e6 / PEAK_HBM_GBPS}
+        extra["paths"] = paths
+        sweep = {}
+        for variant in ("full", "fast", "2d"):
+            for b_ in (2, 3, 4):
+                m_ms, m_b = measure(variant, b_, "roundtrip", 100, 10)
+                sweep[f"{variant}_b{b_}"] = {"ms": m_ms, "vectors_per_s": n / (m_ms / 1e3),
+                                             "GBps": m_b / m_ms / 1e6,
+                                             "frac": m_b / m_ms / 1e6 / PEAK_HBM_GBPS}
+        extra["roundtrip_sweep"] = sweep
+        result["extra"] = extra
+
+    if not args.no_cpu_baseline:
+        import oracle
+
+        print("# cpu baseline (oracle)", file=sys.stderr, flush=True)
+        _, rot = setup(args.variant, bits)
+        levels = oracle.codebook(bits, d)
+        result["cpu_baseline"] = cpu_baseline(args.variant, d, bits, x_np, rot, levels,
+                                              args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,175 @@
+/*
+ * isoquant.h -- C ABI of the IsoQuant stage-1 quantize/dequantize library for
+ * AMD Instinct MI355X (gfx950).
+ *
+ * IsoQuant (arXiv 2603.28430) compresses a d-dimensional vector x in four
+ * steps (Algorithm 1): split off the norm rho = ||x|| (Sec. 3); rotate the
+ * direction block by block, with 4-D quaternion blocks v -> q_L v conj(q_R)
+ * (IsoQuant-Full, Sec. 5.2), v -> q_L v (IsoQuant-Fast, Sec. 5.3) or 2-D
+ * planar rotations (Sec. 5.4); quantize every rotated coordinate with one
+ * shared b-bit Lloyd-Max codebook; then dequantize, rotate back and multiply
+ * by rho.
+ *
+ * Conventions shared by every call:
+ *   - Status codes are returned, never exceptions.  Arguments are validated
+ *     before any device work; a call that returns an error launched nothing.
+ *   - Rows are contiguous, row-major [n][d].  Coordinate 4i of a row is the
+ *     real part of quaternion block i; the 2-D case pairs (2j, 2j+1).
+ *   - Device buffers are owned by the caller and must live on the device that
+ *     was current at isoq_params_init.  Row buffers (fp16/fp32) must be
+ *     16-byte aligned, index records and norm arrays 4-byte aligned.
+ *   - `stream` is a hipStream_t (NULL = the null stream).  Calls are
+ *     asynchronous on it and never synchronise the device.  n = 0 is a valid
+ *     no-op.  Output buffers must not overlap inputs, except that the
+ *     reconstruction may be written in place over the input of
+ *     isoq_roundtrip (x_hat == x exactly).
+ *   - A parameter handle is immutable after init; concurrent calls that share
+ *     it are safe.  Only init and destroy allocate or free device memory.
+ *   - Supported shapes in this version: d in {128, 256, 512}, bits in
+ *     {2, 3, 4}, fp16 or fp32 rows (arithmetic is fp32 in every case).
+ *   - Rows must be finite.  The squared norm is accumulated in fp32, so an
+ *     fp32 row must have 1e-18 <= ||x|| <= 1e18 or be exactly zero (every fp16
+ *     row qualifies); a zero row gives rho = 0, x_hat = 0 and every index
+ *     2^(bits-1) - 1.
+ */
+#ifndef ISOQUANT_H
+#define ISOQUANT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum isoq_status {
+    ISOQ_OK = 0,
+    ISOQ_E_INVALID = 1,     /* bad enum value, n < 0, rows_per_set < 1, bad codebook  */
+    ISOQ_E_UNSUPPORTED = 2, /* valid request outside the shapes listed above           */
+    ISOQ_E_NULL = 3,        /* required pointer is NULL                                */
+    ISOQ_E_ALIGN = 4,       /* pointer misaligned                                      */
+    ISOQ_E_HIP = 5,         /* HIP runtime error (launch failure, no device, ...)      */
+    ISOQ_E_NOMEM = 6,       /* device or host allocation failed                        */
+    ISOQ_E_DEVICE = 7       /* called with a device other than the handle's            */
+} isoq_status;
+
+/* variants (Sec. 5.2, 5.3, 5.4) */
+enum { ISOQ_FULL = 0, ISOQ_FAST = 1, ISOQ_PLANAR2D = 2 };
+/* row element types */
+enum { ISOQ_F32 = 0, ISOQ_F16 = 1 };
+
+typedef struct isoq_params isoq_params;
+
+/*
+ * isoq_params_init -- build the rotation parameters and the codebook of one
+ * quantizer and copy them to the current device.
+ *
+ *   variant   ISOQ_FULL, ISOQ_FAST or ISOQ_PLANAR2D.
+ *   d, bits   vector width and bits per coordinate.
+ *   n_sets    number of independent rotation sets (e.g. one per attention
+ *             head); row r of a later call uses set (r / rows_per_set) mod
+ *             n_sets.  The codebook is shared by all sets.
+ *   rot_host  NULL, or host array of raw draws (Sec. 5.5: unconstrained
+ *             vectors normalised on the fly), n_sets * isoq_raw_params_per_set
+ *             doubles: Full, per set and block i, u_L[4] then u_R[4]; Fast,
+ *             u_L[4] per block; 2-D, one angle theta (radians) per coordinate
+ *             pair.  Quaternions are normalised here (u / ||u||); a zero u is
+ *             ISOQ_E_INVALID.
+ *             NULL: draw them from `seed` (Haar sampling, Sec. 5.5): u ~ N(0,I4)
+ *             and theta ~ U[0, 2 pi) from Philox4x32-10 with key = seed and
+ *             counter (block, set, stream, 0), stream 0 for u_L, 1 for u_R, 2 for
+ *             theta; Box-Muller maps the four 32-bit words (w0..w3) to
+ *             (z0, z1) = sqrt(-2 ln U1) (cos 2 pi U2, sin 2 pi U2) with
+ *             U1 = (w0 + 1/2) / 2^32, U2 = w1 / 2^32, likewise (z2, z3) from
+ *             (w2, w3); theta = 2 pi w0 / 2^32.
+ *   codebook_host  NULL, or host array of 2^bits levels, strictly increasing
+ *             and symmetric about 0 (|c_k + c_{K-1-k}| <= 1e-6 max|c|; they are
+ *             then symmetrised exactly).  NULL: Lloyd-Max levels for N(0, 1/d)
+ *             after 200 Lloyd iterations from levels evenly spaced on
+ *             [-3/sqrt(d), 3/sqrt(d)].  Decision thresholds are the midpoints
+ *             of adjacent levels; a value equal to a threshold goes to the
+ *             lower level.
+ *   out       receives the handle (set to NULL on error).
+ * Host arrays are only read during the call; the caller keeps ownership.
+ */
+isoq_status isoq_params_init(isoq_params **out, int variant, int d, int bits, int n_sets,
+                             const double *rot_host, const double *codebook_host, uint64_t seed);
+
+/* Free the handle and its device memory (NULL is accepted).  Must not race
+ * with calls still running on the GPU that use the handle: synchronise their
+ * streams first. */
+isoq_status isoq_params_destroy(isoq_params *p);
+
+/*
+ * isoq_params_export -- copy out the values the device uses (fp32).  Any
+ * output may be NULL.
+ *   rot_out        n_sets * isoq_export_params_per_set floats: Full, per
+ *                  block q_L[4] then q_R[4] (unit); Fast q_L[4]; 2-D
+ *                  (cos theta, sin theta) per pair.  These are the parameter
+ *                  counts of Table 1 (8 g4, 4 g4, 2 g2 per set).
+ *   levels_out     2^bits levels, ascending.
+ *   thresholds_out 2^bits - 1 decision thresholds, ascending.
+ */
+isoq_status isoq_params_export(const isoq_params *p, float *rot_out, float *levels_out,
+                               float *thresholds_out);
+
+/* Read back the shape of a handle (any output may be NULL). */
+isoq_status isoq_params_info(const isoq_params *p, int *variant, int *d, int *bits, int *n_sets);
+
+/*
+ * isoq_quantize -- encoder half of Algorithm 1: norm split, blockwise rotation,
+ * scalar quantization.
+ *   x          device, [n][d] rows of `dtype`.
+ *   idx_packed device, [n][isoq_packed_bytes(d, bits)] bytes: per row one record
+ *              in which rotated coordinate j occupies bits [j*bits, (j+1)*bits),
+ *              bit m being bit (m mod 8) of byte m/8 (least significant first).
+ *   norms      device, [n] fp32 rho = ||x||_2.
+ * Index of a coordinate y: number of thresholds t_k with y > t_k applied to the
+ * direction x / max(rho, 1e-12).
+ */
+isoq_status isoq_quantize(const isoq_params *p, int dtype, const void *x, int64_t n,
+                          int64_t rows_per_set, uint8_t *idx_packed, float *norms, void *stream);
+
+/*
+ * isoq_dequantize -- decoder half of Algorithm 1: level lookup, inverse block
+ * rotation, multiplication by rho.  Inputs as produced by isoq_quantize; output
+ * x_hat device [n][d] rows of `dtype` (fp16 is rounded to nearest even).
+ */
+isoq_status isoq_dequantize(const isoq_params *p, int dtype, const uint8_t *idx_packed,
+                            const float *norms, int64_t n, int64_t rows_per_set, void *x_hat,
+                            void *stream);
+
+/*
+ * isoq_roundtrip -- the fused stage-1 path x -> x_hat of Algorithm 1 with no
+ * index traffic to memory.  Bitwise equal to isoq_quantize followed by
+ * isoq_dequantize on the same handle, rows_per_set and dtype.
+ */
+isoq_status isoq_roundtrip(const isoq_params *p, int dtype, const void *x, int64_t n,
+                           int64_t rows_per_set, void *x_hat, void *stream);
+
+/* Sizes: bytes of one packed index record, ceil(d * bits / 8); raw draws per
+ * set for rot_host (Full 8 g4, Fast 4 g4, 2-D g2); exported parameters per set
+ * (Full 8 g4, Fast 4 g4, 2-D 2 g2), with g4 = ceil(d/4), g2 = ceil(d/2).
+ * Return 0 for invalid arguments. */
+size_t isoq_packed_bytes(int d, int bits);
+size_t isoq_raw_params_per_set(int variant, int d);
+size_t isoq_export_params_per_set(int variant, int d);
+
+/*
+ * Host-only helpers (no device needed), the same computations init performs:
+ *   isoq_codebook_lloyd   2^bits Lloyd-Max levels for N(0, 1/d) after `iters`
+ *                         iterations (see isoq_params_init), as doubles.
+ *   isoq_rotation_draws   the seeded raw draws init uses when rot_host is NULL,
+ *                         n_sets * isoq_raw_params_per_set doubles.
+ */
+isoq_status isoq_codebook_lloyd(int bits, int d, int iters, double *levels_out);
+isoq_status isoq_rotation_draws(int variant, int d, int n_sets, uint64_t seed, double *out);
+
+/* Static text for a status code. */
+const char *isoq_status_string(isoq_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ISOQUANT_H */

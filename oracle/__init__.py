@@ -62,10 +62,11 @@ def lib():
         L.orc_encode.argtypes = [ctypes.c_int, ctypes.c_int, dp, dp, dp]
         L.orc_decode.argtypes = [ctypes.c_int, ctypes.c_int, dp, dp, dp]
         L.orc_stage1.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, i64,
-                                 dp, dp, dp, i64, i64, u8p, dp, dp]
+                                 dp, dp, dp, i64, i64, u8p, dp, dp, dp]
         L.orc_stage1.restype = ctypes.c_int
         L.orc_stage1_rows.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, i64,
-                                      dp, dp, ctypes.POINTER(ctypes.c_int64), i64, dp, u8p, dp, dp]
+                                      dp, dp, ctypes.POINTER(ctypes.c_int64), i64, dp, u8p, dp, dp,
+                                      dp]
         L.orc_stage1_rows.restype = ctypes.c_int
         L.orc_dequantize.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, i64,
                                      dp, dp, u8p, dp, i64, i64, dp]
@@ -211,12 +212,14 @@ def decode(variant, d, rot, yhat):
 
 # --- Algorithm 1 -------------------------------------------------------------------
 def stage1(variant, d: int, bits: int, rot, levels, x, n_sets: int = 1, rows_per_set: int = 1,
-           rows=None, want_idx=True, want_xhat=True):
+           rows=None, want_idx=True, want_xhat=True, want_ytil=False, selected=False):
     """Run Algorithm 1 on rows of ``x`` ([n, d], any float dtype).
 
     ``rows`` optionally selects a subset (array of row numbers); the set of a
-    row is computed from its global row number.  Returns (idx, rho, xhat) for
-    the selected rows; idx has ``padded_width`` columns.
+    row is computed from its global row number.  With ``selected``, ``x`` holds
+    just those rows, in that order.  Returns (idx, rho, xhat) for the selected
+    rows, plus ytil (rotated normalised coordinates before Q) when
+    ``want_ytil``; idx and ytil have ``padded_width`` columns.
     """
     v = _variant(variant)
     rot = _d(rot)
@@ -225,29 +228,28 @@ def stage1(variant, d: int, bits: int, rot, levels, x, n_sets: int = 1, rows_per
     pw = padded_width(v, d)
     L = lib()
     if rows is None:
-        xd = _d(x.reshape(-1, d))
-        n = xd.shape[0]
-        idx = np.zeros((n, pw), np.uint8) if want_idx else None
-        rho = np.zeros(n)
-        xh = np.zeros((n, d)) if want_xhat else None
-        rc = L.orc_stage1(v, d, bits, n_sets, rows_per_set, _p(rot), _p(levels), _p(xd), 0, n,
-                          _p(idx, ctypes.c_uint8) if idx is not None else None, _p(rho),
-                          _p(xh) if xh is not None else None)
-        if rc != 0:
-            raise ValueError("orc_stage1 rejected its arguments")
-        return idx, rho, xh
-    rows = np.ascontiguousarray(rows, dtype=np.int64)
-    xs = _d(x.reshape(-1, d)[rows])
-    m = len(rows)
-    idx = np.zeros((m, pw), np.uint8)
+        xs = _d(x.reshape(-1, d))
+    else:
+        rows = np.ascontiguousarray(rows, dtype=np.int64)
+        xs = _d(x.reshape(-1, d)) if selected else _d(x.reshape(-1, d)[rows])
+        if xs.shape[0] != len(rows):
+            raise ValueError("selected rows and row numbers differ in count")
+    m = xs.shape[0]
+    idx = np.zeros((m, pw), np.uint8) if want_idx else None
     rho = np.zeros(m)
-    xh = np.zeros((m, d))
-    rc = L.orc_stage1_rows(v, d, bits, n_sets, rows_per_set, _p(rot), _p(levels),
-                           _p(rows, ctypes.c_int64), m, _p(xs), _p(idx, ctypes.c_uint8), _p(rho),
-                           _p(xh))
+    xh = np.zeros((m, d)) if want_xhat else None
+    yt = np.zeros((m, pw)) if want_ytil else None
+    opt = lambda a, t=ctypes.c_double: _p(a, t) if a is not None else None
+    if rows is None:
+        rc = L.orc_stage1(v, d, bits, n_sets, rows_per_set, _p(rot), _p(levels), _p(xs), 0, m,
+                          opt(idx, ctypes.c_uint8), _p(rho), opt(xh), opt(yt))
+    else:
+        rc = L.orc_stage1_rows(v, d, bits, n_sets, rows_per_set, _p(rot), _p(levels),
+                               _p(rows, ctypes.c_int64), m, _p(xs), opt(idx, ctypes.c_uint8),
+                               _p(rho), opt(xh), opt(yt))
     if rc != 0:
-        raise ValueError("orc_stage1_rows rejected its arguments")
-    return idx, rho, xh
+        raise ValueError("the oracle rejected its arguments")
+    return (idx, rho, xh, yt) if want_ytil else (idx, rho, xh)
 
 
 def stage1_range(variant, d, bits, rot, levels, xd, row_begin, row_end, n_sets=1, rows_per_set=1,
@@ -259,7 +261,7 @@ def stage1_range(variant, d, bits, rot, levels, xd, row_begin, row_end, n_sets=1
     return lib().orc_stage1(v, d, bits, n_sets, rows_per_set, _p(rot), _p(levels), _p(xd),
                             int(row_begin), int(row_end),
                             _p(idx, ctypes.c_uint8) if idx is not None else None,
-                            _p(rho), _p(xh) if xh is not None else None)
+                            _p(rho), _p(xh) if xh is not None else None, None)
 
 
 def dequantize(variant, d: int, bits: int, rot, levels, idx, rho, n_sets: int = 1,

@@ -349,10 +349,11 @@ static int stage1_args_ok(int variant, int d, int bits, int n_sets, int64_t rows
 }
 
 /* Algorithm 1 on one row.  xr: d inputs; rs: raw draws of the row's set;
- * outputs idx_row[pg], *rho_out, xhat_row[d] (each may be NULL). */
+ * outputs idx_row[pg], *rho_out, xhat_row[d] and the rotated normalised
+ * coordinates ytil_row[pg] (each may be NULL). */
 static void stage1_row(int variant, int d, int bits, const double *rs, const double *levels,
                        const double *thr, const double *xr, uint8_t *idx_row, double *rho_out,
-                       double *xhat_row)
+                       double *xhat_row, double *ytil_row)
 {
     int blk = block_width(variant), g = orc_num_blocks(variant, d), pg = blk * g;
     double xbar[4096], ytil[4100], yhat[4100], rec[4096];
@@ -366,6 +367,8 @@ static void stage1_row(int variant, int d, int bits, const double *rs, const dou
         xbar[j] = xr[j] / den;
     /* steps: partition into zero-padded blocks and rotate each block */
     orc_encode(variant, d, rs, xbar, ytil);
+    if (ytil_row)
+        memcpy(ytil_row, ytil, sizeof(double) * (size_t)pg);
     /* step: coordinate-wise scalar quantization in the rotated basis */
     for (int j = 0; j < pg; j++) {
         int q = quantize_index(bits, thr, ytil[j]);
@@ -391,12 +394,13 @@ static void stage1_row(int variant, int d, int bits, const double *rs, const dou
  *   idx    : [n][pg] codebook index per rotated coordinate, pg = blk*g (padded)
  *   rho    : [n] norms
  *   xhat   : [n][d] reconstruction
+ *   ytil   : [n][pg] rotated coordinates of the normalised row (before Q)
  * The set of row r is (r / rows_per_set) mod n_sets.
  * ------------------------------------------------------------------------- */
 int orc_stage1(int variant, int d, int bits, int n_sets, int64_t rows_per_set,
                const double *rot, const double *levels, const double *x,
                int64_t row_begin, int64_t row_end,
-               uint8_t *idx, double *rho, double *xhat)
+               uint8_t *idx, double *rho, double *xhat, double *ytil)
 {
     if (!stage1_args_ok(variant, d, bits, n_sets, rows_per_set))
         return -1;
@@ -407,7 +411,7 @@ int orc_stage1(int variant, int d, int bits, int n_sets, int64_t rows_per_set,
     for (int64_t r = row_begin; r < row_end; r++)
         stage1_row(variant, d, bits, rot + set_of_row(r, n_sets, rows_per_set) * rp, levels, thr,
                    x + r * d, idx ? idx + r * pg : NULL, rho ? rho + r : NULL,
-                   xhat ? xhat + r * d : NULL);
+                   xhat ? xhat + r * d : NULL, ytil ? ytil + r * pg : NULL);
     return 0;
 }
 
@@ -415,7 +419,7 @@ int orc_stage1(int variant, int d, int bits, int n_sets, int64_t rows_per_set,
  * row number is rows[t]; outputs are written at position t. */
 int orc_stage1_rows(int variant, int d, int bits, int n_sets, int64_t rows_per_set,
                     const double *rot, const double *levels, const int64_t *rows, int64_t m,
-                    const double *xs, uint8_t *idx, double *rho, double *xhat)
+                    const double *xs, uint8_t *idx, double *rho, double *xhat, double *ytil)
 {
     if (!stage1_args_ok(variant, d, bits, n_sets, rows_per_set))
         return -1;
@@ -426,7 +430,7 @@ int orc_stage1_rows(int variant, int d, int bits, int n_sets, int64_t rows_per_s
     for (int64_t t = 0; t < m; t++)
         stage1_row(variant, d, bits, rot + set_of_row(rows[t], n_sets, rows_per_set) * rp, levels,
                    thr, xs + t * d, idx ? idx + t * pg : NULL, rho ? rho + t : NULL,
-                   xhat ? xhat + t * d : NULL);
+                   xhat ? xhat + t * d : NULL, ytil ? ytil + t * pg : NULL);
     return 0;
 }
 

@@ -1,0 +1,401 @@
+// C ABI of the IsoQuant stage-1 library (declared in include/isoquant.h):
+// argument validation, the parameter handle, and kernel launches.
+#include <hip/hip_runtime_api.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <mutex>
+#include <new>
+#include <unordered_map>
+#include <vector>
+
+#include "isoq_internal.h"
+#include "isoquant.h"
+
+struct isoq_params {
+    int variant, d, bits, n_sets;
+    int device;
+    float *dparams;                 // device, [n_sets][d/8][params_per_lane]
+    std::vector<float> exported;    // unit parameters as used (Table 1 layout)
+    float levels[16], thresholds[15];
+};
+
+namespace {
+
+using namespace isoq;
+
+bool valid_variant(int v) { return v == ISOQ_FULL || v == ISOQ_FAST || v == ISOQ_PLANAR2D; }
+bool supported_d(int d) { return d == 128 || d == 256 || d == 512; }
+bool supported_bits(int b) { return b >= 2 && b <= 4; }
+bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+// Persistent grid size per kernel: resident blocks per CU times CU count.
+struct DeviceInfo {
+    int cus = 0;
+};
+std::mutex g_mu;
+std::unordered_map<int, DeviceInfo> g_dev;
+std::unordered_map<const void *, int> g_occ;
+
+isoq_status launch_geometry(const void *fn, int device, int &blocks_per_cu, int &cus)
+{
+    std::lock_guard<std::mutex> lk(g_mu);
+    auto it = g_dev.find(device);
+    if (it == g_dev.end()) {
+        int c = 0;
+        if (hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess || c <= 0)
+            return ISOQ_E_HIP;
+        it = g_dev.emplace(device, DeviceInfo{c}).first;
+    }
+    cus = it->second.cus;
+    auto jt = g_occ.find(fn);
+    if (jt == g_occ.end()) {
+        int b = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, fn, kBlockThreads, 0) != hipSuccess || b <= 0)
+            return ISOQ_E_HIP;
+        jt = g_occ.emplace(fn, b).first;
+    }
+    blocks_per_cu = jt->second;
+    return ISOQ_OK;
+}
+
+isoq_status check_common(const isoq_params *p, int dtype, int64_t n, int64_t rows_per_set)
+{
+    if (!p)
+        return ISOQ_E_NULL;
+    if (dtype != ISOQ_F32 && dtype != ISOQ_F16)
+        return ISOQ_E_INVALID;
+    if (n < 0 || rows_per_set < 1)
+        return ISOQ_E_INVALID;
+    return ISOQ_OK;
+}
+
+isoq_status check_device(const isoq_params *p)
+{
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess)
+        return ISOQ_E_HIP;
+    return dev == p->device ? ISOQ_OK : ISOQ_E_DEVICE;
+}
+
+isoq_status run(const isoq_params *p, int dtype, int mode, KArgs &a, void *stream)
+{
+    const bool f16 = dtype == ISOQ_F16;
+    const int rows_per_wave = 64 / (p->d / kCoordsPerLane);
+    const bool multi = p->n_sets > 1;
+    const bool generic = multi && (a.rows_per_set % rows_per_wave) != 0;
+    const void *fn = kernel_for(p->variant, p->d, p->bits, f16, generic, mode);
+    if (!fn)
+        return ISOQ_E_UNSUPPORTED;
+    int bpc = 0, cus = 0;
+    isoq_status st = launch_geometry(fn, p->device, bpc, cus);
+    if (st != ISOQ_OK)
+        return st;
+    const int64_t groups = (a.n + rows_per_wave - 1) / rows_per_wave;
+    const int waves_per_block = kBlockThreads / 64;
+    const int64_t resident = (int64_t)bpc * cus * waves_per_block;
+    int64_t waves;
+    if (generic) {
+        // contiguous runs of row groups, one per resident wave
+        a.per_wave = (groups + resident - 1) / resident;
+        waves = (groups + a.per_wave - 1) / a.per_wave;
+        a.groups_per_seg = groups;
+        a.chunks_per_seg = waves;
+    } else {
+        // segments of rows_per_set rows share a set; waves never cross one
+        const int64_t gps = multi ? std::min<int64_t>(groups, a.rows_per_set / rows_per_wave) : groups;
+        const int64_t nseg = (groups + gps - 1) / gps;
+        const int64_t want = std::max<int64_t>(1, (resident + nseg - 1) / nseg);
+        a.per_wave = (gps + want - 1) / want;
+        a.chunks_per_seg = (gps + a.per_wave - 1) / a.per_wave;
+        a.groups_per_seg = gps;
+        waves = nseg * a.chunks_per_seg;
+    }
+    const int64_t blocks = (waves + waves_per_block - 1) / waves_per_block;
+    if (blocks > 0x7FFFFFFF)
+        return ISOQ_E_UNSUPPORTED;
+    const int H = 1 << (p->bits - 1);
+    for (int k = 0; k < H; k++)
+        a.lev_pos[k] = p->levels[H + k];
+    for (int k = 0; k + 1 < H; k++)
+        a.thr_pos[k] = p->thresholds[H + k];
+    for (int k = 0; k < 2 * H; k++)
+        a.lev_all[k] = p->levels[k];
+    a.params = p->dparams;
+    a.n_sets = p->n_sets;
+    void *args[] = {&a};
+    hipError_t e = hipLaunchKernel(fn, dim3((unsigned)blocks), dim3(kBlockThreads), args, 0,
+                                   static_cast<hipStream_t>(stream));
+    if (e != hipSuccess || hipGetLastError() != hipSuccess)
+        return ISOQ_E_HIP;
+    return ISOQ_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *isoq_status_string(isoq_status s)
+{
+    switch (s) {
+    case ISOQ_OK: return "ok";
+    case ISOQ_E_INVALID: return "invalid argument";
+    case ISOQ_E_UNSUPPORTED: return "unsupported shape (d in {128,256,512}, bits in {2,3,4})";
+    case ISOQ_E_NULL: return "null pointer";
+    case ISOQ_E_ALIGN: return "misaligned pointer";
+    case ISOQ_E_HIP: return "HIP runtime error";
+    case ISOQ_E_NOMEM: return "out of memory";
+    case ISOQ_E_DEVICE: return "current device differs from the handle's device";
+    }
+    return "unknown status";
+}
+
+size_t isoq_packed_bytes(int d, int bits)
+{
+    if (d < 1 || bits < 1 || bits > 8)
+        return 0;
+    return ((size_t)d * bits + 7) / 8;
+}
+
+size_t isoq_raw_params_per_set(int variant, int d)
+{
+    if (!valid_variant(variant) || d < 1)
+        return 0;
+    return raw_per_set(variant, d);
+}
+
+size_t isoq_export_params_per_set(int variant, int d)
+{
+    if (!valid_variant(variant) || d < 1)
+        return 0;
+    return export_per_set(variant, d);
+}
+
+isoq_status isoq_codebook_lloyd(int bits, int d, int iters, double *levels_out)
+{
+    if (!levels_out)
+        return ISOQ_E_NULL;
+    if (d < 1 || iters < 0 || bits < 1 || bits > 8)
+        return ISOQ_E_INVALID;
+    if (!supported_bits(bits))
+        return ISOQ_E_UNSUPPORTED;
+    return lloyd_levels(bits, 1.0 / std::sqrt((double)d), iters, levels_out) ? ISOQ_OK : ISOQ_E_INVALID;
+}
+
+isoq_status isoq_rotation_draws(int variant, int d, int n_sets, uint64_t seed, double *out)
+{
+    if (!out)
+        return ISOQ_E_NULL;
+    if (!valid_variant(variant) || d < 1 || n_sets < 1)
+        return ISOQ_E_INVALID;
+    seeded_draws(variant, d, n_sets, seed, out);
+    return ISOQ_OK;
+}
+
+isoq_status isoq_params_init(isoq_params **out, int variant, int d, int bits, int n_sets,
+                             const double *rot_host, const double *codebook_host, uint64_t seed)
+{
+    if (!out)
+        return ISOQ_E_NULL;
+    *out = nullptr;
+    if (!valid_variant(variant) || d < 1 || bits < 1 || bits > 8 || n_sets < 1)
+        return ISOQ_E_INVALID;
+    if (!supported_d(d) || !supported_bits(bits))
+        return ISOQ_E_UNSUPPORTED;
+
+    const int K = 1 << bits;
+    double lev[16];
+    if (codebook_host) {
+        double mx = 0;
+        for (int k = 0; k < K; k++) {
+            if (!std::isfinite(codebook_host[k]))
+                return ISOQ_E_INVALID;
+            mx = std::max(mx, std::fabs(codebook_host[k]));
+        }
+        for (int k = 0; k + 1 < K; k++)
+            if (!(codebook_host[k] < codebook_host[k + 1]))
+                return ISOQ_E_INVALID;
+        for (int k = 0; k < K / 2; k++) {
+            if (std::fabs(codebook_host[k] + codebook_host[K - 1 - k]) > 1e-6 * mx)
+                return ISOQ_E_INVALID;
+            const double m = 0.5 * (codebook_host[K - 1 - k] - codebook_host[k]);
+            lev[k] = -m;
+            lev[K - 1 - k] = m;
+        }
+    } else if (!lloyd_levels(bits, 1.0 / std::sqrt((double)d), 200, lev)) {
+        return ISOQ_E_INVALID;
+    }
+
+    std::vector<double> drawn;
+    const double *raw = rot_host;
+    if (!raw) {
+        try {
+            drawn.resize((size_t)n_sets * raw_per_set(variant, d));
+        } catch (const std::bad_alloc &) {
+            return ISOQ_E_NOMEM;
+        }
+        seeded_draws(variant, d, n_sets, seed, drawn.data());
+        raw = drawn.data();
+    }
+    isoq_params *p = new (std::nothrow) isoq_params();
+    if (!p)
+        return ISOQ_E_NOMEM;
+    p->variant = variant;
+    p->d = d;
+    p->bits = bits;
+    p->n_sets = n_sets;
+    p->dparams = nullptr;
+    std::vector<float> layout;
+    try {
+        if (!build_rotation(variant, d, n_sets, raw, p->exported, layout)) {
+            delete p;
+            return ISOQ_E_INVALID;
+        }
+    } catch (const std::bad_alloc &) {
+        delete p;
+        return ISOQ_E_NOMEM;
+    }
+    for (int k = 0; k < K; k++)
+        p->levels[k] = (float)lev[k];
+    for (int k = 0; k + 1 < K; k++)
+        p->thresholds[k] = (float)(0.5 * (lev[k] + lev[k + 1]));
+    p->thresholds[K / 2 - 1] = 0.0f;
+
+    if (hipGetDevice(&p->device) != hipSuccess) {
+        delete p;
+        return ISOQ_E_HIP;
+    }
+    const size_t bytes = layout.size() * sizeof(float);
+    if (hipMalloc(reinterpret_cast<void **>(&p->dparams), bytes) != hipSuccess) {
+        delete p;
+        return ISOQ_E_NOMEM;
+    }
+    if (hipMemcpy(p->dparams, layout.data(), bytes, hipMemcpyHostToDevice) != hipSuccess) {
+        (void)hipFree(p->dparams);
+        delete p;
+        return ISOQ_E_HIP;
+    }
+    *out = p;
+    return ISOQ_OK;
+}
+
+isoq_status isoq_params_destroy(isoq_params *p)
+{
+    if (!p)
+        return ISOQ_OK;
+    isoq_status st = ISOQ_OK;
+    if (p->dparams) {
+        int prev = -1;
+        (void)hipGetDevice(&prev);
+        if (prev != p->device)
+            (void)hipSetDevice(p->device);
+        if (hipFree(p->dparams) != hipSuccess)
+            st = ISOQ_E_HIP;
+        if (prev >= 0 && prev != p->device)
+            (void)hipSetDevice(prev);
+    }
+    delete p;
+    return st;
+}
+
+isoq_status isoq_params_export(const isoq_params *p, float *rot_out, float *levels_out,
+                               float *thresholds_out)
+{
+    if (!p)
+        return ISOQ_E_NULL;
+    const int K = 1 << p->bits;
+    if (rot_out)
+        std::memcpy(rot_out, p->exported.data(), p->exported.size() * sizeof(float));
+    if (levels_out)
+        std::memcpy(levels_out, p->levels, K * sizeof(float));
+    if (thresholds_out)
+        std::memcpy(thresholds_out, p->thresholds, (K - 1) * sizeof(float));
+    return ISOQ_OK;
+}
+
+isoq_status isoq_params_info(const isoq_params *p, int *variant, int *d, int *bits, int *n_sets)
+{
+    if (!p)
+        return ISOQ_E_NULL;
+    if (variant)
+        *variant = p->variant;
+    if (d)
+        *d = p->d;
+    if (bits)
+        *bits = p->bits;
+    if (n_sets)
+        *n_sets = p->n_sets;
+    return ISOQ_OK;
+}
+
+isoq_status isoq_roundtrip(const isoq_params *p, int dtype, const void *x, int64_t n,
+                           int64_t rows_per_set, void *x_hat, void *stream)
+{
+    isoq_status st = check_common(p, dtype, n, rows_per_set);
+    if (st != ISOQ_OK)
+        return st;
+    if (n == 0)
+        return ISOQ_OK;
+    if (!x || !x_hat)
+        return ISOQ_E_NULL;
+    if (!aligned(x, 16) || !aligned(x_hat, 16))
+        return ISOQ_E_ALIGN;
+    if ((st = check_device(p)) != ISOQ_OK)
+        return st;
+    KArgs a{};
+    a.x = x;
+    a.y = x_hat;
+    a.n = n;
+    a.rows_per_set = rows_per_set;
+    return run(p, dtype, MODE_ROUNDTRIP, a, stream);
+}
+
+isoq_status isoq_quantize(const isoq_params *p, int dtype, const void *x, int64_t n,
+                          int64_t rows_per_set, uint8_t *idx_packed, float *norms, void *stream)
+{
+    isoq_status st = check_common(p, dtype, n, rows_per_set);
+    if (st != ISOQ_OK)
+        return st;
+    if (n == 0)
+        return ISOQ_OK;
+    if (!x || !idx_packed || !norms)
+        return ISOQ_E_NULL;
+    if (!aligned(x, 16) || !aligned(idx_packed, 4) || !aligned(norms, 4))
+        return ISOQ_E_ALIGN;
+    if ((st = check_device(p)) != ISOQ_OK)
+        return st;
+    KArgs a{};
+    a.x = x;
+    a.rec_out = idx_packed;
+    a.norms_out = norms;
+    a.n = n;
+    a.rows_per_set = rows_per_set;
+    return run(p, dtype, MODE_QUANTIZE, a, stream);
+}
+
+isoq_status isoq_dequantize(const isoq_params *p, int dtype, const uint8_t *idx_packed,
+                            const float *norms, int64_t n, int64_t rows_per_set, void *x_hat,
+                            void *stream)
+{
+    isoq_status st = check_common(p, dtype, n, rows_per_set);
+    if (st != ISOQ_OK)
+        return st;
+    if (n == 0)
+        return ISOQ_OK;
+    if (!idx_packed || !norms || !x_hat)
+        return ISOQ_E_NULL;
+    if (!aligned(x_hat, 16) || !aligned(idx_packed, 4) || !aligned(norms, 4))
+        return ISOQ_E_ALIGN;
+    if ((st = check_device(p)) != ISOQ_OK)
+        return st;
+    KArgs a{};
+    a.y = x_hat;
+    a.rec_in = idx_packed;
+    a.norms_in = norms;
+    a.n = n;
+    a.rows_per_set = rows_per_set;
+    return run(p, dtype, MODE_DEQUANTIZE, a, stream);
+}
+
+}  // extern "C"

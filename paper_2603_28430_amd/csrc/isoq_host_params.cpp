@@ -1,0 +1,223 @@
+// Host-side construction of the quantizer state: Lloyd-Max codebook, seeded
+// rotation draws, normalisation (Sec. 5.5) and the per-lane device layout.
+// All of it runs once, at isoq_params_init, in double precision.
+#include <cmath>
+#include <cstring>
+
+#include "isoq_internal.h"
+
+namespace isoq {
+
+// ---------------------------------------------------------------- codebook
+// Lloyd's fixed-point iteration for a Gaussian source N(0, sigma^2), in units
+// of sigma: the decision points are the midpoints of neighbouring levels, and
+// each level moves to the conditional mean of its cell,
+//   E[Z | a < Z <= b] = (phi(a) - phi(b)) / (Phi(b) - Phi(a)).
+// Start: levels evenly spaced on [-3, 3].  The source is symmetric, so the
+// result is made exactly odd before scaling.
+namespace {
+double gauss_pdf(double z) { return std::exp(-0.5 * z * z) * 0.39894228040143267794; }
+
+// P(Z > z) with Z ~ N(0,1); +inf and -inf handled
+double gauss_sf(double z)
+{
+    if (std::isinf(z))
+        return z > 0 ? 0.0 : 1.0;
+    return 0.5 * std::erfc(z * 0.70710678118654752440);
+}
+}  // namespace
+
+bool lloyd_levels(int bits, double sigma, int iters, double *levels)
+{
+    if (bits < 1 || bits > 4 || !(sigma > 0) || iters < 0)
+        return false;
+    const int K = 1 << bits;
+    double c[16], edge[17];
+    for (int k = 0; k < K; k++)
+        c[k] = K > 1 ? 6.0 * k / (K - 1) - 3.0 : 0.0;
+    for (int it = 0; it < iters; it++) {
+        edge[0] = -INFINITY;
+        edge[K] = INFINITY;
+        for (int k = 1; k < K; k++)
+            edge[k] = 0.5 * (c[k - 1] + c[k]);
+        for (int k = 0; k < K; k++) {
+            const double lo = edge[k], hi = edge[k + 1];
+            const double num = (std::isinf(lo) ? 0.0 : gauss_pdf(lo)) - (std::isinf(hi) ? 0.0 : gauss_pdf(hi));
+            // mass of the cell from the side whose tail is smaller
+            const double mass = lo >= 0 ? gauss_sf(lo) - gauss_sf(hi) : gauss_sf(-hi) - gauss_sf(-lo);
+            c[k] = num / mass;
+        }
+    }
+    for (int k = 0; k < K / 2; k++) {
+        const double m = 0.5 * (c[K - 1 - k] - c[k]);
+        c[k] = -m;
+        c[K - 1 - k] = m;
+    }
+    for (int k = 0; k < K; k++)
+        levels[k] = sigma * c[k];
+    return true;
+}
+
+// ------------------------------------------------------------ rotation draws
+size_t raw_per_set(int variant, int d)
+{
+    if (variant == VAR_PLANAR2D)
+        return (size_t)(d + 1) / 2;
+    const size_t g = (size_t)(d + 3) / 4;
+    return variant == VAR_FULL ? 8 * g : 4 * g;
+}
+
+size_t export_per_set(int variant, int d)
+{
+    if (variant == VAR_PLANAR2D)
+        return 2 * ((size_t)(d + 1) / 2);
+    const size_t g = (size_t)(d + 3) / 4;
+    return variant == VAR_FULL ? 8 * g : 4 * g;
+}
+
+namespace {
+// Philox4x32-10 (Salmon et al., SC 2011): ten rounds of two 32x32->64-bit
+// multiplications, with the Weyl key schedule between rounds.
+void philox4x32_10(uint32_t ctr[4], uint32_t k0, uint32_t k1)
+{
+    for (int round = 0; round < 10; round++) {
+        if (round > 0) {
+            k0 += 0x9E3779B9u;
+            k1 += 0xBB67AE85u;
+        }
+        const uint64_t p0 = (uint64_t)0xD2511F53u * ctr[0];
+        const uint64_t p1 = (uint64_t)0xCD9E8D57u * ctr[2];
+        const uint32_t n0 = (uint32_t)(p1 >> 32) ^ ctr[1] ^ k0;
+        const uint32_t n1 = (uint32_t)p1;
+        const uint32_t n2 = (uint32_t)(p0 >> 32) ^ ctr[3] ^ k1;
+        const uint32_t n3 = (uint32_t)p0;
+        ctr[0] = n0;
+        ctr[1] = n1;
+        ctr[2] = n2;
+        ctr[3] = n3;
+    }
+}
+
+void normal_pair(uint32_t a, uint32_t b, double *z)
+{
+    const double two_pi = 6.283185307179586476925;
+    const double u1 = ((double)a + 0.5) * 0x1p-32;
+    const double u2 = (double)b * 0x1p-32;
+    const double r = std::sqrt(-2.0 * std::log(u1));
+    z[0] = r * std::cos(two_pi * u2);
+    z[1] = r * std::sin(two_pi * u2);
+}
+}  // namespace
+
+void seeded_draws(int variant, int d, int n_sets, uint64_t seed, double *out)
+{
+    const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
+    size_t o = 0;
+    if (variant == VAR_PLANAR2D) {
+        const int g2 = (d + 1) / 2;
+        for (int s = 0; s < n_sets; s++)
+            for (int j = 0; j < g2; j++) {
+                uint32_t c[4] = {(uint32_t)j, (uint32_t)s, 2u, 0u};
+                philox4x32_10(c, k0, k1);
+                out[o++] = 6.283185307179586476925 * ((double)c[0] * 0x1p-32);
+            }
+        return;
+    }
+    const int g = (d + 3) / 4;
+    const int sides = variant == VAR_FULL ? 2 : 1;
+    for (int s = 0; s < n_sets; s++)
+        for (int i = 0; i < g; i++)
+            for (int side = 0; side < sides; side++) {
+                uint32_t c[4] = {(uint32_t)i, (uint32_t)s, (uint32_t)side, 0u};
+                philox4x32_10(c, k0, k1);
+                normal_pair(c[0], c[1], out + o);
+                normal_pair(c[2], c[3], out + o + 2);
+                o += 4;
+            }
+}
+
+// --------------------------------------------------- normalisation and layout
+namespace {
+// Hamilton product, written out from ij = k, jk = i, ki = j (i^2 = j^2 = k^2 = -1).
+void hamilton(const double p[4], const double q[4], double r[4])
+{
+    r[0] = p[0] * q[0] - p[1] * q[1] - p[2] * q[2] - p[3] * q[3];
+    r[1] = p[0] * q[1] + p[1] * q[0] + p[2] * q[3] - p[3] * q[2];
+    r[2] = p[0] * q[2] - p[1] * q[3] + p[2] * q[0] + p[3] * q[1];
+    r[3] = p[0] * q[3] + p[1] * q[2] - p[2] * q[1] + p[3] * q[0];
+}
+
+bool unit4(const double *u, double q[4])
+{
+    const double n = std::sqrt(u[0] * u[0] + u[1] * u[1] + u[2] * u[2] + u[3] * u[3]);
+    if (!(n > 0) || !std::isfinite(n))
+        return false;
+    for (int c = 0; c < 4; c++)
+        q[c] = u[c] / n;
+    return true;
+}
+}  // namespace
+
+bool build_rotation(int variant, int d, int n_sets, const double *raw, std::vector<float> &exported,
+                    std::vector<float> &device_layout)
+{
+    const int lpv = d / kCoordsPerLane;
+    const int pl = params_per_lane(variant);
+    const size_t rp = raw_per_set(variant, d);
+    exported.assign((size_t)n_sets * export_per_set(variant, d), 0.f);
+    device_layout.assign((size_t)n_sets * lpv * pl, 0.f);
+    for (int s = 0; s < n_sets; s++) {
+        const double *rs = raw + s * rp;
+        float *ex = exported.data() + s * export_per_set(variant, d);
+        float *dv = device_layout.data() + (size_t)s * lpv * pl;
+        if (variant == VAR_PLANAR2D) {
+            // lane l owns pairs 4l .. 4l+3: (cos, sin) each
+            for (int j = 0; j < d / 2; j++) {
+                if (!std::isfinite(rs[j]))
+                    return false;
+                const double c = std::cos(rs[j]), sn = std::sin(rs[j]);
+                ex[2 * j] = (float)c;
+                ex[2 * j + 1] = (float)sn;
+                dv[2 * j] = (float)c;
+                dv[2 * j + 1] = (float)sn;
+            }
+            continue;
+        }
+        for (int i = 0; i < d / 4; i++) {
+            double qL[4], qR[4] = {1, 0, 0, 0};
+            if (!unit4(rs + (variant == VAR_FULL ? 8 : 4) * i, qL))
+                return false;
+            if (variant == VAR_FULL && !unit4(rs + 8 * i + 4, qR))
+                return false;
+            if (variant == VAR_FAST) {
+                for (int c = 0; c < 4; c++) {
+                    ex[4 * i + c] = (float)qL[c];
+                    dv[4 * i + c] = (float)qL[c];  // lane l: blocks 2l, 2l+1 -> floats 8l..8l+7
+                }
+                continue;
+            }
+            for (int c = 0; c < 4; c++) {
+                ex[8 * i + c] = (float)qL[c];
+                ex[8 * i + 4 + c] = (float)qR[c];
+            }
+            // M = matrix of v -> q_L v conj(q_R): column c is the image of e_c
+            const double qRc[4] = {qR[0], -qR[1], -qR[2], -qR[3]};
+            double M[4][4];
+            for (int c = 0; c < 4; c++) {
+                double e[4] = {0, 0, 0, 0}, t[4], col[4];
+                e[c] = 1.0;
+                hamilton(qL, e, t);
+                hamilton(t, qRc, col);
+                for (int r = 0; r < 4; r++)
+                    M[r][c] = col[r];
+            }
+            // lane l: blocks 2l, 2l+1 -> 16 floats each, row-major
+            for (int r = 0; r < 4; r++)
+                for (int c = 0; c < 4; c++)
+                    dv[16 * i + 4 * r + c] = (float)M[r][c];
+        }
+    }
+    return true;
+}
+
+}  // namespace isoq

@@ -1,0 +1,63 @@
+// Internal declarations shared by the library's host code (isoq_api.cpp,
+// isoq_host_params.cpp) and its kernels (isoq_kernels.hip).
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <vector>
+
+namespace isoq {
+
+enum Mode { MODE_ROUNDTRIP = 0, MODE_QUANTIZE = 1, MODE_DEQUANTIZE = 2 };
+enum Variant { VAR_FULL = 0, VAR_FAST = 1, VAR_PLANAR2D = 2 };
+
+// Every lane owns 8 consecutive coordinates of a row (two quaternion blocks or
+// four planar pairs), so a row spans d/8 lanes and a wave holds 512/d rows.
+constexpr int kCoordsPerLane = 8;
+constexpr int kBlockThreads = 256;
+
+// Device rotation parameters per lane, in floats: Full keeps the two 4x4
+// matrices M = L(q_L) R(conj q_R) row-major, Fast the two unit quaternions,
+// 2-D (cos, sin) of the four pairs.
+inline int params_per_lane(int variant) { return variant == VAR_FULL ? 32 : 8; }
+
+// Kernel arguments, passed by value (they land in scalar registers).
+struct KArgs {
+    const void *x;           // roundtrip / quantize: input rows
+    void *y;                 // roundtrip / dequantize: output rows
+    uint8_t *rec_out;        // quantize: packed index records
+    const uint8_t *rec_in;   // dequantize: packed index records
+    float *norms_out;        // quantize: rho per row
+    const float *norms_in;   // dequantize: rho per row
+    const float *params;     // [n_sets][d/8][params_per_lane]
+    int64_t n;               // rows
+    int64_t rows_per_set;    // rows per parameter set (>= 1)
+    int64_t per_wave;        // row groups handled by one wave
+    int64_t groups_per_seg;  // row groups per segment of rows_per_set rows
+    int64_t chunks_per_seg;  // waves per segment
+    int32_t n_sets;
+    int32_t pad0;
+    float lev_pos[8];        // c_{K/2} .. c_{K-1}   (positive half of the codebook)
+    float thr_pos[8];        // t_{K/2} .. t_{K-2}   (positive thresholds; t_{K/2-1} = 0)
+    float lev_all[16];       // c_0 .. c_{K-1}
+};
+
+// Kernel entry for (variant, d, bits, fp16 rows?, generic set indexing?, mode),
+// or nullptr.  Generic set indexing is needed when rows_per_set is not a
+// multiple of the rows per wave (512 / d) and there is more than one set.
+const void *kernel_for(int variant, int d, int bits, bool f16, bool generic_sets, int mode);
+
+// ---- host-side parameter construction (isoq_host_params.cpp) -------------
+// Lloyd-Max levels for N(0, sigma^2) (ascending, symmetrised).
+bool lloyd_levels(int bits, double sigma, int iters, double *levels);
+// Seeded raw draws (Philox4x32-10 + Box-Muller), layout of the public header.
+void seeded_draws(int variant, int d, int n_sets, uint64_t seed, double *out);
+size_t raw_per_set(int variant, int d);
+size_t export_per_set(int variant, int d);
+// From raw draws to (a) the exported unit parameters and (b) the device
+// layout.  Returns false when a quaternion draw is zero or not finite.
+bool build_rotation(int variant, int d, int n_sets, const double *raw, std::vector<float> &exported,
+                    std::vector<float> &device_layout);
+
+}  // namespace isoq

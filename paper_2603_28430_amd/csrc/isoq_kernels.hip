@@ -1,0 +1,535 @@
+// IsoQuant stage-1 kernels for gfx950 (MI355X).
+//
+// One template covers the three entry points of Algorithm 1:
+//   MODE_ROUNDTRIP   x -> x_hat fused (norm, rotation, quantizer, inverse)
+//   MODE_QUANTIZE    x -> packed indices + rho
+//   MODE_DEQUANTIZE  packed indices + rho -> x_hat
+//
+// Mapping.  A lane owns 8 consecutive coordinates of one row: 16 bytes of
+// fp16 (one global_load_dwordx4) or 32 bytes of fp32 (two).  Those 8
+// coordinates are two quaternion blocks (Full/Fast, Sec. 5.2-5.3) or four
+// planar pairs (Sec. 5.4), so the rotation never leaves the lane.  A row spans
+// d/8 lanes (16, 32 or 64) and a wave holds 512/d rows; the squared norm is
+// reduced with DPP row operations inside each 16-lane row and with lane
+// swizzles across rows.  Every lane keeps the parameters of its own blocks in
+// VGPRs for the whole kernel; the codebook sits in kernel-argument SGPRs.
+//
+// The grid is persistent: each wave walks a contiguous range of row groups,
+// prefetching the next group while it computes the current one.  The path is
+// bound by HBM bandwidth, so the arithmetic is plain fp32 VALU work and uses
+// no MFMA.
+//
+// Quantizer (shared b-bit codebook, symmetric): the rotated value y of the
+// unnormalised row is compared with rho' t_k (rho' = max(rho, 1e-12)), which
+// equals comparing y / rho' with t_k; the magnitude index m counts the
+// positive thresholds below |y|, the sign decision is y > 0 (the middle
+// threshold t_{K/2-1} = 0), and the selected level is pre-multiplied by rho so
+// that the inverse rotation directly yields rho * rec (Algorithm 1, last step).
+#include <hip/hip_runtime.h>
+
+#include "isoq_internal.h"
+
+namespace isoq {
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+
+constexpr float kEps = 1e-12f;
+
+// DPP controls (data-parallel primitives on 16-lane rows)
+constexpr int DPP_QUAD_1032 = 0xB1;   // quad_perm [1,0,3,2]
+constexpr int DPP_QUAD_2301 = 0x4E;   // quad_perm [2,3,0,1]
+constexpr int DPP_QUAD_1233 = 0xF9;   // quad_perm [1,2,3,3]
+constexpr int DPP_ROW_MIRROR = 0x140;
+constexpr int DPP_ROW_HALF_MIRROR = 0x141;
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v)
+{
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u(uint32_t v)
+{
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
+}
+
+// Sum over the LPV lanes of a row; every lane of the row gets the same bits.
+template <int LPV>
+__device__ __forceinline__ float row_sum(float v)
+{
+    v += dpp_f<DPP_QUAD_1032>(v);
+    v += dpp_f<DPP_QUAD_2301>(v);
+    v += dpp_f<DPP_ROW_HALF_MIRROR>(v);
+    v += dpp_f<DPP_ROW_MIRROR>(v);
+    if constexpr (LPV >= 32)
+        v += __shfl_xor(v, 16);
+    if constexpr (LPV >= 64)
+        v += __shfl_xor(v, 32);
+    return v;
+}
+
+template <bool F16>
+struct Raw {
+    u32x4 w[F16 ? 1 : 2];
+};
+
+template <bool F16>
+__device__ __forceinline__ void load_row_chunk(const char *p, Raw<F16> &r)
+{
+    const u32x4 *q = reinterpret_cast<const u32x4 *>(p);
+    r.w[0] = __builtin_nontemporal_load(q);
+    if constexpr (!F16)
+        r.w[1] = __builtin_nontemporal_load(q + 1);
+}
+
+template <bool F16>
+__device__ __forceinline__ void unpack(const Raw<F16> &r, float x[8])
+{
+    // Vector elements are copied to scalars before __builtin_bit_cast: applied
+    // to an ext_vector element lvalue directly, it reads element 0 every time.
+    if constexpr (F16) {
+#pragma unroll
+        for (int k = 0; k < 4; k++) {
+            const uint32_t e = r.w[0][k];
+            const f16x2 h = __builtin_bit_cast(f16x2, e);
+            x[2 * k] = (float)h.x;
+            x[2 * k + 1] = (float)h.y;
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k < 4; k++) {
+            const uint32_t e0 = r.w[0][k], e1 = r.w[1][k];
+            x[k] = __uint_as_float(e0);
+            x[4 + k] = __uint_as_float(e1);
+        }
+    }
+}
+
+template <bool F16>
+__device__ __forceinline__ float sum_squares(const Raw<F16> &r, const float x[8])
+{
+    float s = 0.f;
+    if constexpr (F16) {
+#pragma unroll
+        for (int k = 0; k < 4; k++) {
+            const uint32_t e = r.w[0][k];
+            const f16x2 h = __builtin_bit_cast(f16x2, e);
+            s = __builtin_amdgcn_fdot2(h, h, s, false);
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k < 8; k++)
+            s = fmaf(x[k], x[k], s);
+    }
+    return s;
+}
+
+template <bool F16>
+__device__ __forceinline__ void store_row_chunk(char *p, const float o[8])
+{
+    u32x4 *q = reinterpret_cast<u32x4 *>(p);
+    if constexpr (F16) {
+        u32x4 w;
+#pragma unroll
+        for (int k = 0; k < 4; k++) {
+            f16x2 h;
+            h.x = (_Float16)o[2 * k];  // round to nearest even
+            h.y = (_Float16)o[2 * k + 1];
+            w[k] = __builtin_bit_cast(uint32_t, h);
+        }
+        __builtin_nontemporal_store(w, q);
+    } else {
+        u32x4 a, b;
+#pragma unroll
+        for (int k = 0; k < 4; k++) {
+            a[k] = __float_as_uint(o[k]);
+            b[k] = __float_as_uint(o[4 + k]);
+        }
+        __builtin_nontemporal_store(a, q);
+        __builtin_nontemporal_store(b, q + 1);
+    }
+}
+
+// ---- block rotations -------------------------------------------------------
+// Full: y = M v with M = L(q_L) R(conj q_R) (the sandwich of Sec. 5.2 as one
+// 4x4 orthogonal matrix, precomputed at init); inverse v = M^T y (Prop. 1).
+// Fast: y = q_L v through the left-multiplication matrix of q_L = (a,b,c,d);
+// inverse conj(q_L) y = L(q_L)^T y.  2-D: y = R(theta) u, inverse R(-theta).
+template <int VAR>
+__device__ __forceinline__ void rotate_forward(const float *P, const float x[8], float y[8])
+{
+    if constexpr (VAR == VAR_FULL) {
+#pragma unroll
+        for (int b = 0; b < 2; b++) {
+            const float *M = P + 16 * b;
+            const float *v = x + 4 * b;
+#pragma unroll
+            for (int r = 0; r < 4; r++) {
+                float acc = M[4 * r] * v[0];
+                acc = fmaf(M[4 * r + 1], v[1], acc);
+                acc = fmaf(M[4 * r + 2], v[2], acc);
+                acc = fmaf(M[4 * r + 3], v[3], acc);
+                y[4 * b + r] = acc;
+            }
+        }
+    } else if constexpr (VAR == VAR_FAST) {
+#pragma unroll
+        for (int b = 0; b < 2; b++) {
+            const float a = P[4 * b], bb = P[4 * b + 1], c = P[4 * b + 2], d = P[4 * b + 3];
+            const float *v = x + 4 * b;
+            y[4 * b + 0] = fmaf(-d, v[3], fmaf(-c, v[2], fmaf(-bb, v[1], a * v[0])));
+            y[4 * b + 1] = fmaf(c, v[3], fmaf(-d, v[2], fmaf(a, v[1], bb * v[0])));
+            y[4 * b + 2] = fmaf(-bb, v[3], fmaf(a, v[2], fmaf(d, v[1], c * v[0])));
+            y[4 * b + 3] = fmaf(a, v[3], fmaf(bb, v[2], fmaf(-c, v[1], d * v[0])));
+        }
+    } else {
+#pragma unroll
+        for (int p = 0; p < 4; p++) {
+            const float c = P[2 * p], s = P[2 * p + 1];
+            y[2 * p] = fmaf(-s, x[2 * p + 1], c * x[2 * p]);
+            y[2 * p + 1] = fmaf(c, x[2 * p + 1], s * x[2 * p]);
+        }
+    }
+}
+
+template <int VAR>
+__device__ __forceinline__ void rotate_inverse(const float *P, const float y[8], float o[8])
+{
+    if constexpr (VAR == VAR_FULL) {
+#pragma unroll
+        for (int b = 0; b < 2; b++) {
+            const float *M = P + 16 * b;
+            const float *v = y + 4 * b;
+#pragma unroll
+            for (int c = 0; c < 4; c++) {
+                float acc = M[c] * v[0];
+                acc = fmaf(M[4 + c], v[1], acc);
+                acc = fmaf(M[8 + c], v[2], acc);
+                acc = fmaf(M[12 + c], v[3], acc);
+                o[4 * b + c] = acc;
+            }
+        }
+    } else if constexpr (VAR == VAR_FAST) {
+#pragma unroll
+        for (int b = 0; b < 2; b++) {
+            const float a = P[4 * b], bb = P[4 * b + 1], c = P[4 * b + 2], d = P[4 * b + 3];
+            const float *v = y + 4 * b;
+            o[4 * b + 0] = fmaf(d, v[3], fmaf(c, v[2], fmaf(bb, v[1], a * v[0])));
+            o[4 * b + 1] = fmaf(-c, v[3], fmaf(d, v[2], fmaf(a, v[1], -bb * v[0])));
+            o[4 * b + 2] = fmaf(bb, v[3], fmaf(a, v[2], fmaf(-d, v[1], -c * v[0])));
+            o[4 * b + 3] = fmaf(a, v[3], fmaf(-bb, v[2], fmaf(c, v[1], -d * v[0])));
+        }
+    } else {
+#pragma unroll
+        for (int p = 0; p < 4; p++) {
+            const float c = P[2 * p], s = P[2 * p + 1];
+            o[2 * p] = fmaf(s, y[2 * p + 1], c * y[2 * p]);
+            o[2 * p + 1] = fmaf(c, y[2 * p + 1], -s * y[2 * p]);
+        }
+    }
+}
+
+template <int PL>
+__device__ __forceinline__ void load_params(const float *base, float P[PL])
+{
+    const u32x4 *q = reinterpret_cast<const u32x4 *>(base);
+#pragma unroll
+    for (int k = 0; k < PL / 4; k++) {
+        const u32x4 w = q[k];
+        const uint32_t e0 = w[0], e1 = w[1], e2 = w[2], e3 = w[3];
+        P[4 * k] = __uint_as_float(e0);
+        P[4 * k + 1] = __uint_as_float(e1);
+        P[4 * k + 2] = __uint_as_float(e2);
+        P[4 * k + 3] = __uint_as_float(e3);
+    }
+}
+
+// ---- packed index records --------------------------------------------------
+// Lane `sub` of a row owns coordinates 8 sub .. 8 sub + 7, i.e. bits
+// [8 sub * BITS, 8 (sub + 1) * BITS) of the row's record: a 16-bit half-word
+// (2 bits), a 32-bit word (4 bits), or 24 bits at byte 3 sub (3 bits), which
+// the four lanes of a DPP quad merge into three aligned words.
+template <int BITS>
+__device__ __forceinline__ void store_bits(uint8_t *rec, int sub, uint32_t p)
+{
+    if constexpr (BITS == 2) {
+        reinterpret_cast<uint16_t *>(rec)[sub] = (uint16_t)p;
+    } else if constexpr (BITS == 4) {
+        reinterpret_cast<uint32_t *>(rec)[sub] = p;
+    } else {
+        const uint32_t nb = dpp_u<DPP_QUAD_1233>(p);  // bits of the next lane in the quad
+        const int k = sub & 3;
+        const uint32_t lo = p | (nb << 24);
+        const uint32_t hi = nb >> 8;
+        const uint32_t w = (uint32_t)((((uint64_t)hi << 32) | lo) >> (8 * k));
+        if (k < 3)
+            reinterpret_cast<uint32_t *>(rec + 12 * (sub >> 2))[k] = w;
+    }
+}
+
+template <int BITS>
+__device__ __forceinline__ uint32_t load_bits(const uint8_t *rec, int sub)
+{
+    if constexpr (BITS == 2) {
+        return reinterpret_cast<const uint16_t *>(rec)[sub];
+    } else if constexpr (BITS == 4) {
+        return reinterpret_cast<const uint32_t *>(rec)[sub];
+    } else {
+        const uint32_t *q = reinterpret_cast<const uint32_t *>(rec + 12 * (sub >> 2));
+        const uint32_t w0 = q[0], w1 = q[1], w2 = q[2];
+        const int k = sub & 3;  // 24 k = 32 lo_word + shift
+        const uint32_t lo = k < 2 ? w0 : (k == 2 ? w1 : w2);
+        const uint32_t hi = k < 2 ? w1 : (k == 2 ? w2 : 0u);
+        const int sh = (24 * k) & 31;
+        return (uint32_t)((((uint64_t)hi << 32) | lo) >> sh) & 0xFFFFFFu;
+    }
+}
+
+// ---- the kernel ---------------------------------------------------------------
+// Work split.  Rows are cut into segments of rows_per_set rows (one segment
+// when there is a single parameter set); every wave takes a contiguous run of
+// row groups inside one segment, so its parameter set is wave-uniform and its
+// parameters are loaded once.  When rows_per_set is not a multiple of the
+// rows per wave (GENERIC_SETS), a group can straddle sets: then each lane
+// finds its set for every group and reloads its parameters.
+template <int VAR, int D, int BITS, bool F16, int MODE, bool GENERIC_SETS>
+struct Stage1 {
+    static constexpr int LPV = D / kCoordsPerLane;      // lanes per row
+    static constexpr int VPW = 64 / LPV;                // rows per wave
+    static constexpr int H = 1 << (BITS - 1);           // positive levels
+    static constexpr int PL = VAR == VAR_FULL ? 32 : 8; // parameter floats per lane
+    static constexpr int64_t ROWB = (int64_t)D * (F16 ? 2 : 4);  // bytes per row
+    static constexpr int64_t RECB = (int64_t)D * BITS / 8;       // bytes per index record
+    static constexpr int LANEB = F16 ? 16 : 32;         // row bytes per lane
+
+    struct In {
+        Raw<F16> raw;
+        uint32_t bits;
+        float rho;
+    };
+
+    __device__ static __forceinline__ void fetch(const KArgs &a, int64_t g, int sub, int slot, In &in)
+    {
+        int64_t row = g * VPW + slot;
+        row = row < a.n ? row : a.n - 1;  // lanes past the end take the last row (see compute)
+        if constexpr (MODE == MODE_DEQUANTIZE) {
+            in.bits = load_bits<BITS>(a.rec_in + row * RECB, sub);
+            in.rho = a.norms_in[row];
+        } else {
+            load_row_chunk<F16>(static_cast<const char *>(a.x) + row * ROWB + sub * LANEB, in.raw);
+        }
+    }
+
+    __device__ static __forceinline__ void compute(const KArgs &a, const float *P, const float *lev,
+                                                   const float *thr, const float *lds_levels,
+                                                   const In &in, int64_t g, int sub, int slot)
+    {
+        // Lanes past the last row were fed the last row (see fetch); they
+        // recompute it and store the same bits to the same place.  The loop has
+        // no divergent branch, so the compiler keeps loads and waits in order.
+        int64_t row = g * VPW + slot;
+        row = row < a.n ? row : a.n - 1;
+        float yq[8];
+        if constexpr (MODE == MODE_DEQUANTIZE) {
+#pragma unroll
+            for (int j = 0; j < 8; j++) {
+                const uint32_t idx = (in.bits >> (BITS * j)) & (2 * H - 1);
+                yq[j] = lds_levels[idx] * in.rho;
+            }
+        } else {
+            float x[8];
+            unpack<F16>(in.raw, x);
+            const float rho = __builtin_amdgcn_sqrtf(row_sum<LPV>(sum_squares<F16>(in.raw, x)));
+            const float rho_e = fmaxf(rho, kEps);
+            float y[8], m[8];
+            rotate_forward<VAR>(P, x, y);
+#pragma unroll
+            for (int j = 0; j < 8; j++)
+                m[j] = fabsf(y[j]);
+            float ths[H > 1 ? H - 1 : 1];
+#pragma unroll
+            for (int k = 0; k < H - 1; k++)
+                ths[k] = thr[k] * rho_e;
+            if constexpr (MODE == MODE_ROUNDTRIP) {
+                float lvs[H];
+#pragma unroll
+                for (int k = 0; k < H; k++)
+                    lvs[k] = lev[k] * rho;
+                float L[8];
+#pragma unroll
+                for (int j = 0; j < 8; j++)
+                    L[j] = lvs[0];
+                // thresholds outer, coordinates inner: independent compares
+                // fill the distance between each compare and its select
+#pragma unroll
+                for (int k = 0; k < H - 1; k++)
+#pragma unroll
+                    for (int j = 0; j < 8; j++)
+                        L[j] = m[j] > ths[k] ? lvs[k + 1] : L[j];
+#pragma unroll
+                for (int j = 0; j < 8; j++)
+                    yq[j] = y[j] > 0.f ? L[j] : -L[j];
+            } else {
+                uint32_t q[8];
+#pragma unroll
+                for (int j = 0; j < 8; j++)
+                    q[j] = 0;
+#pragma unroll
+                for (int k = 0; k < H - 1; k++)
+#pragma unroll
+                    for (int j = 0; j < 8; j++)
+                        q[j] = m[j] > ths[k] ? (uint32_t)(k + 1) : q[j];
+                uint32_t p = 0;
+#pragma unroll
+                for (int j = 0; j < 8; j++)
+                    p |= (q[j] ^ (y[j] > 0.f ? (uint32_t)H : (uint32_t)(H - 1))) << (BITS * j);
+                store_bits<BITS>(a.rec_out + row * RECB, sub, p);
+                if (sub == 0)
+                    a.norms_out[row] = rho;
+            }
+        }
+        if constexpr (MODE != MODE_QUANTIZE) {
+            float o[8];
+            rotate_inverse<VAR>(P, yq, o);
+            store_row_chunk<F16>(static_cast<char *>(a.y) + row * ROWB + sub * LANEB, o);
+        }
+    }
+
+    // parameter set of `row` (GENERIC_SETS only)
+    __device__ static __forceinline__ int set_of(const KArgs &a, int64_t row)
+    {
+        return (int)((row / a.rows_per_set) % a.n_sets);
+    }
+
+    __device__ static void run(const KArgs &a, const float *lds_levels)
+    {
+        const int lane = threadIdx.x & 63;
+        const int sub = lane % LPV;
+        const int slot = lane / LPV;
+        const int64_t wave =
+            (int64_t)blockIdx.x * (kBlockThreads / 64) + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+        const int64_t groups = (a.n + VPW - 1) / VPW;
+
+        // this wave's range [g, g_end) and (fast path) its set
+        int64_t g, g_end;
+        int set = 0;
+        if constexpr (GENERIC_SETS) {
+            g = wave * a.per_wave;
+            g_end = min(groups, g + a.per_wave);
+        } else {
+            const int64_t seg = wave / a.chunks_per_seg;
+            const int64_t c = wave - seg * a.chunks_per_seg;
+            g = seg * a.groups_per_seg + c * a.per_wave;
+            g_end = min(min(groups, (seg + 1) * a.groups_per_seg), g + a.per_wave);
+            set = (int)(seg % a.n_sets);
+        }
+        if (g >= g_end)
+            return;
+
+        float lev[H], thr[H > 1 ? H - 1 : 1];
+#pragma unroll
+        for (int k = 0; k < H; k++)
+            lev[k] = a.lev_pos[k];
+#pragma unroll
+        for (int k = 0; k < H - 1; k++)
+            thr[k] = a.thr_pos[k];
+
+        float P[PL];
+        if constexpr (!GENERIC_SETS)
+            load_params<PL>(a.params + ((int64_t)set * LPV + sub) * PL, P);
+
+        // two register buffers, prefetching one group ahead; the prefetch
+        // address is clamped so that it is always issued (plain in-order waits)
+        In A, B;
+        const int64_t last = g_end - 1;
+        // (the scheduling barriers keep each prefetch at the top of its half,
+        // ahead of the arithmetic that waits for the previous buffer)
+        fetch(a, g, sub, slot, A);
+        for (;;) {
+            fetch(a, min(g + 1, last), sub, slot, B);
+            if constexpr (GENERIC_SETS)
+                load_params<PL>(a.params + ((int64_t)set_of(a, min(g * VPW + slot, a.n - 1)) * LPV + sub) * PL, P);
+            __builtin_amdgcn_sched_barrier(0);
+            compute(a, P, lev, thr, lds_levels, A, g, sub, slot);
+            if (++g >= g_end)
+                break;
+            fetch(a, min(g + 1, last), sub, slot, A);
+            if constexpr (GENERIC_SETS)
+                load_params<PL>(a.params + ((int64_t)set_of(a, min(g * VPW + slot, a.n - 1)) * LPV + sub) * PL, P);
+            __builtin_amdgcn_sched_barrier(0);
+            compute(a, P, lev, thr, lds_levels, B, g, sub, slot);
+            if (++g >= g_end)
+                break;
+        }
+    }
+};
+
+template <int VAR, int D, int BITS, bool F16, int MODE, bool GENERIC_SETS>
+__global__ __launch_bounds__(kBlockThreads) void stage1_kernel(const KArgs a)
+{
+    __shared__ float lds_levels[16];
+    if constexpr (MODE == MODE_DEQUANTIZE) {
+        if (threadIdx.x < (1u << BITS))
+            lds_levels[threadIdx.x] = a.lev_all[threadIdx.x];
+        __syncthreads();
+    }
+    Stage1<VAR, D, BITS, F16, MODE, GENERIC_SETS>::run(a, lds_levels);
+}
+
+template <int VAR, int D, int BITS, bool F16, bool GEN>
+const void *pick_mode(int mode)
+{
+    switch (mode) {
+    case MODE_ROUNDTRIP: return reinterpret_cast<const void *>(&stage1_kernel<VAR, D, BITS, F16, MODE_ROUNDTRIP, GEN>);
+    case MODE_QUANTIZE: return reinterpret_cast<const void *>(&stage1_kernel<VAR, D, BITS, F16, MODE_QUANTIZE, GEN>);
+    case MODE_DEQUANTIZE: return reinterpret_cast<const void *>(&stage1_kernel<VAR, D, BITS, F16, MODE_DEQUANTIZE, GEN>);
+    }
+    return nullptr;
+}
+
+template <int VAR, int D, int BITS>
+const void *pick_dtype(bool f16, bool gen, int mode)
+{
+    if (f16)
+        return gen ? pick_mode<VAR, D, BITS, true, true>(mode) : pick_mode<VAR, D, BITS, true, false>(mode);
+    return gen ? pick_mode<VAR, D, BITS, false, true>(mode) : pick_mode<VAR, D, BITS, false, false>(mode);
+}
+
+template <int VAR, int D>
+const void *pick_bits(int bits, bool f16, bool gen, int mode)
+{
+    switch (bits) {
+    case 2: return pick_dtype<VAR, D, 2>(f16, gen, mode);
+    case 3: return pick_dtype<VAR, D, 3>(f16, gen, mode);
+    case 4: return pick_dtype<VAR, D, 4>(f16, gen, mode);
+    }
+    return nullptr;
+}
+
+template <int VAR>
+const void *pick_d(int d, int bits, bool f16, bool gen, int mode)
+{
+    switch (d) {
+    case 128: return pick_bits<VAR, 128>(bits, f16, gen, mode);
+    case 256: return pick_bits<VAR, 256>(bits, f16, gen, mode);
+    case 512: return pick_bits<VAR, 512>(bits, f16, gen, mode);
+    }
+    return nullptr;
+}
+
+}  // namespace
+
+const void *kernel_for(int variant, int d, int bits, bool f16, bool generic_sets, int mode)
+{
+    switch (variant) {
+    case VAR_FULL: return pick_d<VAR_FULL>(d, bits, f16, generic_sets, mode);
+    case VAR_FAST: return pick_d<VAR_FAST>(d, bits, f16, generic_sets, mode);
+    case VAR_PLANAR2D: return pick_d<VAR_PLANAR2D>(d, bits, f16, generic_sets, mode);
+    }
+    return nullptr;
+}
+
+}  // namespace isoq

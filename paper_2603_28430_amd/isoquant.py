@@ -1,0 +1,237 @@
+"""Python binding of libisoquant.so (declared in include/isoquant.h).
+
+Argument marshalling only: every step of the quantize/dequantize path runs in
+the library's HIP kernels.  PyTorch provides device memory and streams; tensors
+are passed as raw device pointers together with the current HIP stream.  The
+functions carry the C names; device outputs are allocated here when the caller
+does not pass them.  A missing library is an ImportError, never a fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libisoquant.so")
+
+ISOQ_FULL, ISOQ_FAST, ISOQ_PLANAR2D = 0, 1, 2
+ISOQ_F32, ISOQ_F16 = 0, 1
+VARIANTS = {"full": ISOQ_FULL, "fast": ISOQ_FAST, "2d": ISOQ_PLANAR2D}
+
+STATUS = {0: "ISOQ_OK", 1: "ISOQ_E_INVALID", 2: "ISOQ_E_UNSUPPORTED", 3: "ISOQ_E_NULL",
+          4: "ISOQ_E_ALIGN", 5: "ISOQ_E_HIP", 6: "ISOQ_E_NOMEM", 7: "ISOQ_E_DEVICE"}
+
+
+class IsoqError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {STATUS.get(status, status)} ({isoq_status_string(status)})")
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2603_28430_amd.build`")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, dp, fp, i64 = ctypes.c_void_p, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_float), ctypes.c_int64
+    c_int = ctypes.c_int
+    L.isoq_params_init.argtypes = [ctypes.POINTER(vp), c_int, c_int, c_int, c_int, dp, dp, ctypes.c_uint64]
+    L.isoq_params_destroy.argtypes = [vp]
+    L.isoq_params_export.argtypes = [vp, fp, fp, fp]
+    L.isoq_params_info.argtypes = [vp] + [ctypes.POINTER(c_int)] * 4
+    L.isoq_quantize.argtypes = [vp, c_int, vp, i64, i64, vp, vp, vp]
+    L.isoq_dequantize.argtypes = [vp, c_int, vp, vp, i64, i64, vp, vp]
+    L.isoq_roundtrip.argtypes = [vp, c_int, vp, i64, i64, vp, vp]
+    L.isoq_packed_bytes.argtypes = [c_int, c_int]
+    L.isoq_packed_bytes.restype = ctypes.c_size_t
+    L.isoq_raw_params_per_set.argtypes = [c_int, c_int]
+    L.isoq_raw_params_per_set.restype = ctypes.c_size_t
+    L.isoq_export_params_per_set.argtypes = [c_int, c_int]
+    L.isoq_export_params_per_set.restype = ctypes.c_size_t
+    L.isoq_codebook_lloyd.argtypes = [c_int, c_int, c_int, dp]
+    L.isoq_rotation_draws.argtypes = [c_int, c_int, c_int, ctypes.c_uint64, dp]
+    L.isoq_status_string.argtypes = [c_int]
+    L.isoq_status_string.restype = ctypes.c_char_p
+    for f in ("isoq_params_init", "isoq_params_destroy", "isoq_params_export", "isoq_params_info",
+              "isoq_quantize", "isoq_dequantize", "isoq_roundtrip", "isoq_codebook_lloyd",
+              "isoq_rotation_draws"):
+        getattr(L, f).restype = c_int
+    return L
+
+
+lib = _load()
+
+
+def _check(st: int, where: str):
+    if st != 0:
+        raise IsoqError(st, where)
+
+
+def _variant(v) -> int:
+    return VARIANTS[v] if isinstance(v, str) else int(v)
+
+
+def isoq_status_string(status: int) -> str:
+    return lib.isoq_status_string(int(status)).decode()
+
+
+def isoq_packed_bytes(d: int, bits: int) -> int:
+    return int(lib.isoq_packed_bytes(int(d), int(bits)))
+
+
+def isoq_raw_params_per_set(variant, d: int) -> int:
+    return int(lib.isoq_raw_params_per_set(_variant(variant), int(d)))
+
+
+def isoq_export_params_per_set(variant, d: int) -> int:
+    return int(lib.isoq_export_params_per_set(_variant(variant), int(d)))
+
+
+def isoq_codebook_lloyd(bits: int, d: int, iters: int = 200) -> np.ndarray:
+    out = np.zeros(1 << bits)
+    _check(lib.isoq_codebook_lloyd(int(bits), int(d), int(iters),
+                                   out.ctypes.data_as(ctypes.POINTER(ctypes.c_double))),
+           "isoq_codebook_lloyd")
+    return out
+
+
+def isoq_rotation_draws(variant, d: int, n_sets: int = 1, seed: int = 1) -> np.ndarray:
+    v = _variant(variant)
+    out = np.zeros(n_sets * isoq_raw_params_per_set(v, d))
+    _check(lib.isoq_rotation_draws(v, int(d), int(n_sets), int(seed),
+                                   out.ctypes.data_as(ctypes.POINTER(ctypes.c_double))),
+           "isoq_rotation_draws")
+    return out
+
+
+class Params:
+    """Owner of an isoq_params handle (freed by close() or garbage collection)."""
+
+    def __init__(self, handle: int, variant: int, d: int, bits: int, n_sets: int):
+        self.handle = ctypes.c_void_p(handle)
+        self.variant, self.d, self.bits, self.n_sets = variant, d, bits, n_sets
+
+    def close(self):
+        if self.handle:
+            _check(lib.isoq_params_destroy(self.handle), "isoq_params_destroy")
+            self.handle = ctypes.c_void_p(None)
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    @property
+    def record_bytes(self) -> int:
+        return isoq_packed_bytes(self.d, self.bits)
+
+
+def isoq_params_init(variant, d: int, bits: int, n_sets: int = 1, rot=None, codebook=None,
+                     seed: int = 1) -> Params:
+    """Create a handle on the current device (see include/isoquant.h)."""
+    v = _variant(variant)
+    dp = ctypes.POINTER(ctypes.c_double)
+    rot_a = None if rot is None else np.ascontiguousarray(rot, dtype=np.float64)
+    cb_a = None if codebook is None else np.ascontiguousarray(codebook, dtype=np.float64)
+    if rot_a is not None and rot_a.size != n_sets * isoq_raw_params_per_set(v, d):
+        raise ValueError("rot has the wrong number of raw draws")
+    if cb_a is not None and cb_a.size != (1 << bits):
+        raise ValueError("codebook must have 2**bits levels")
+    h = ctypes.c_void_p()
+    _check(lib.isoq_params_init(ctypes.byref(h), v, int(d), int(bits), int(n_sets),
+                                None if rot_a is None else rot_a.ctypes.data_as(dp),
+                                None if cb_a is None else cb_a.ctypes.data_as(dp), int(seed)),
+           "isoq_params_init")
+    return Params(h.value, v, int(d), int(bits), int(n_sets))
+
+
+def isoq_params_destroy(p: Params) -> None:
+    p.close()
+
+
+def isoq_params_export(p: Params):
+    """(unit rotation parameters [n_sets * per_set], levels [2^b], thresholds [2^b - 1]), fp32."""
+    rot = np.zeros(p.n_sets * isoq_export_params_per_set(p.variant, p.d), np.float32)
+    lev = np.zeros(1 << p.bits, np.float32)
+    thr = np.zeros((1 << p.bits) - 1, np.float32)
+    fp = ctypes.POINTER(ctypes.c_float)
+    _check(lib.isoq_params_export(p.handle, rot.ctypes.data_as(fp), lev.ctypes.data_as(fp),
+                                  thr.ctypes.data_as(fp)), "isoq_params_export")
+    return rot, lev, thr
+
+
+def isoq_params_info(p: Params):
+    vals = [ctypes.c_int() for _ in range(4)]
+    _check(lib.isoq_params_info(p.handle, *[ctypes.byref(v) for v in vals]), "isoq_params_info")
+    return tuple(v.value for v in vals)
+
+
+# --- device calls ----------------------------------------------------------------
+def _torch():
+    import torch
+    return torch
+
+
+def _stream_ptr(stream):
+    torch = _torch()
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _dtype_code(t) -> int:
+    torch = _torch()
+    if t == torch.float16:
+        return ISOQ_F16
+    if t == torch.float32:
+        return ISOQ_F32
+    raise TypeError(f"rows must be float16 or float32, got {t}")
+
+
+def _rows(x, d):
+    if not x.is_cuda:
+        raise ValueError("tensor must be on the GPU")
+    if not x.is_contiguous():
+        raise ValueError("tensor must be contiguous")
+    if x.shape[-1] != d:
+        raise ValueError(f"last dimension must be d={d}")
+    return x.numel() // d
+
+
+def isoq_roundtrip(p: Params, x, rows_per_set: int = 1, x_hat=None, stream=None):
+    """x_hat = stage-1 quantize->dequantize of x (same shape and dtype)."""
+    n = _rows(x, p.d)
+    if x_hat is None:
+        x_hat = _torch().empty_like(x)
+    _check(lib.isoq_roundtrip(p.handle, _dtype_code(x.dtype), ctypes.c_void_p(x.data_ptr()), n,
+                              int(rows_per_set), ctypes.c_void_p(x_hat.data_ptr()), _stream_ptr(stream)),
+           "isoq_roundtrip")
+    return x_hat
+
+
+def isoq_quantize(p: Params, x, rows_per_set: int = 1, idx_packed=None, norms=None, stream=None):
+    """(packed index records [n, isoq_packed_bytes] uint8, norms [n] fp32)."""
+    torch = _torch()
+    n = _rows(x, p.d)
+    if idx_packed is None:
+        idx_packed = torch.empty((n, p.record_bytes), dtype=torch.uint8, device=x.device)
+    if norms is None:
+        norms = torch.empty((n,), dtype=torch.float32, device=x.device)
+    _check(lib.isoq_quantize(p.handle, _dtype_code(x.dtype), ctypes.c_void_p(x.data_ptr()), n,
+                             int(rows_per_set), ctypes.c_void_p(idx_packed.data_ptr()),
+                             ctypes.c_void_p(norms.data_ptr()), _stream_ptr(stream)), "isoq_quantize")
+    return idx_packed, norms
+
+
+def isoq_dequantize(p: Params, idx_packed, norms, dtype=None, rows_per_set: int = 1, x_hat=None,
+                    stream=None):
+    """Rows [n, d] of `dtype` (default float16) from packed records and norms."""
+    torch = _torch()
+    n = norms.numel()
+    if x_hat is None:
+        x_hat = torch.empty((n, p.d), dtype=dtype or torch.float16, device=norms.device)
+    _check(lib.isoq_dequantize(p.handle, _dtype_code(x_hat.dtype), ctypes.c_void_p(idx_packed.data_ptr()),
+                               ctypes.c_void_p(norms.data_ptr()), n, int(rows_per_set),
+                               ctypes.c_void_p(x_hat.data_ptr()), _stream_ptr(stream)), "isoq_dequantize")
+    return x_hat
