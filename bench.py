@@ -66,12 +66,19 @@ def measured_traffic(tag: str):
     return float(t.group(1))
 
 
-def time_launches(fn, steps: int, warmup: int, torch):
+def time_launches(fn, steps: int, warmup: int, torch, warm_seconds: float = 0.0):
     """Average milliseconds per launch over `steps` launches (events on the
-    current stream, which is the stream every launch uses)."""
+    current stream, which is the stream every launch uses).  Before timing:
+    `warmup` launches, then more until `warm_seconds` have passed (the first
+    launches after a pause run at lower clocks)."""
     for i in range(warmup):
         fn(i)
     torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < warm_seconds:
+        for i in range(20):
+            fn(i)
+        torch.cuda.synchronize()
     s = torch.cuda.Event(enable_timing=True)
     e = torch.cuda.Event(enable_timing=True)
     s.record()
@@ -107,18 +114,23 @@ def cpu_baseline(variant, d, bits, x_np, rot, levels, seconds: float):
     rho = np.zeros(rows)
     xh = np.zeros((rows, d))
     bounds = np.linspace(0, rows, threads + 1).astype(np.int64)
-    work = [threading.Thread(target=oracle.stage1_range,
-                             args=(variant, d, bits, rot, levels, xd, int(bounds[i]),
-                                   int(bounds[i + 1])), kwargs={"rho": rho, "xh": xh})
-            for i in range(threads)]
+    passes = 0
     t0 = time.perf_counter()
-    for w in work:
-        w.start()
-    for w in work:
-        w.join()
-    dt = time.perf_counter() - t0
-    return {"value": rows / dt, "unit": "vectors/s", "cores": threads, "kind": "oracle",
-            "sample": f"first {rows} of the {len(x_np)} input rows, fp64 C oracle "
+    while True:
+        work = [threading.Thread(target=oracle.stage1_range,
+                                 args=(variant, d, bits, rot, levels, xd, int(bounds[i]),
+                                       int(bounds[i + 1])), kwargs={"rho": rho, "xh": xh})
+                for i in range(threads)]
+        for w in work:
+            w.start()
+        for w in work:
+            w.join()
+        passes += 1
+        dt = time.perf_counter() - t0
+        if dt >= seconds or passes >= 100:
+            break
+    return {"value": rows * passes / dt, "unit": "vectors/s", "cores": threads, "kind": "oracle",
+            "sample": f"first {rows} of the {len(x_np)} input rows x {passes} passes, fp64 C oracle "
                       f"(Algorithm 1, indices not stored), {threads} threads, {dt:.1f} s"}
 
 
@@ -134,6 +146,7 @@ def main() -> int:
     ap.add_argument("--n", type=int, default=1 << 20)
     ap.add_argument("--mode", default="roundtrip", choices=["roundtrip", "quantize", "dequantize"])
     ap.add_argument("--buffer-sets", type=int, default=4)
+    ap.add_argument("--warm-seconds", type=float, default=1.0)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true")
@@ -161,7 +174,8 @@ def main() -> int:
     outs = [torch.empty_like(x0) for _ in range(S)]
 
     if args.copy_only:
-        ms = time_launches(lambda i: outs[i % S].copy_(xs[i % S]), args.steps, args.warmup, torch)
+        ms = time_launches(lambda i: outs[i % S].copy_(xs[i % S]), args.steps, args.warmup, torch,
+                           args.warm_seconds)
         b = 2 * x0.numel() * esz
         print(json.dumps({"copy_bytes_per_launch": b, "ms_per_launch": ms, "GBps": b / ms / 1e6}))
         return 0
@@ -170,7 +184,7 @@ def main() -> int:
         rot = workloads.rotation_draws(variant, d, 1, seed=1)
         return iq.isoq_params_init(variant, d, bits_, 1, rot=rot), rot
 
-    def measure(variant, bits_, mode, steps, warmup):
+    def measure(variant, bits_, mode, steps, warmup, warm_seconds=0.0):
         p, _ = setup(variant, bits_)
         if mode == "roundtrip":
             fn = lambda i: iq.isoq_roundtrip(p, xs[i % S], x_hat=outs[i % S])
@@ -183,13 +197,13 @@ def main() -> int:
                 fn = lambda i: iq.isoq_quantize(p, xs[i % S], idx_packed=recs[i % S], norms=norms[i % S])
             else:
                 fn = lambda i: iq.isoq_dequantize(p, recs[i % S], norms[i % S], x_hat=outs[i % S])
-        ms = time_launches(fn, steps, warmup, torch)
+        ms = time_launches(fn, steps, warmup, torch, warm_seconds)
         b = algorithmic_bytes(mode, n, d, bits_, esz)
         return ms, b
 
     # ---- the timed headline: K steps of the fused path ----
     print(f"# timing {args.mode} {args.variant} b={bits}", file=sys.stderr, flush=True)
-    ms, abytes = measure(args.variant, bits, args.mode, args.steps, args.warmup)
+    ms, abytes = measure(args.variant, bits, args.mode, args.steps, args.warmup, args.warm_seconds)
     gbps = abytes / ms / 1e6
     tag = f"{args.mode}_{args.variant}_d{d}_b{bits}_{args.dtype}_n{n}"
     result = {
@@ -222,18 +236,18 @@ def main() -> int:
     if not args.no_extras:
         extra = {}
         print("# side measurements", file=sys.stderr, flush=True)
-        cms = time_launches(lambda i: outs[i % S].copy_(xs[i % S]), 50, 5, torch)
+        cms = time_launches(lambda i: outs[i % S].copy_(xs[i % S]), 50, 5, torch, 0.2)
         extra["device_copy_same_size"] = {"GBps": 2 * x0.numel() * esz / cms / 1e6, "ms": cms}
         paths = {}
         for mode in ("quantize", "dequantize"):
-            m_ms, m_b = measure(args.variant, bits, mode, 100, 10)
+            m_ms, m_b = measure(args.variant, bits, mode, 100, 10, 0.2)
             paths[mode] = {"ms": m_ms, "vectors_per_s": n / (m_ms / 1e3), "GBps": m_b / m_ms / 1e6,
                            "frac": m_b / m_ms / 1e6 / PEAK_HBM_GBPS}
         extra["paths"] = paths
         sweep = {}
         for variant in ("full", "fast", "2d"):
             for b_ in (2, 3, 4):
-                m_ms, m_b = measure(variant, b_, "roundtrip", 100, 10)
+                m_ms, m_b = measure(variant, b_, "roundtrip", 100, 10, 0.2)
                 sweep[f"{variant}_b{b_}"] = {"ms": m_ms, "vectors_per_s": n / (m_ms / 1e3),
                                              "GBps": m_b / m_ms / 1e6,
                                              "frac": m_b / m_ms / 1e6 / PEAK_HBM_GBPS}

@@ -168,6 +168,11 @@ isoq_status isoq_rotation_draws(int variant, int d, int n_sets, uint64_t seed, d
 /* Static text for a status code. */
 const char *isoq_status_string(isoq_status s);
 
+/* The HIP call and error text behind the last ISOQ_E_HIP (or a hipMalloc
+ * ISOQ_E_NOMEM) returned on the calling thread; "" if none.  Valid until the
+ * next call on the same thread. */
+const char *isoq_last_hip_error(void);
+
 #ifdef __cplusplus
 }
 #endif

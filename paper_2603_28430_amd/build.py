@@ -1,6 +1,9 @@
 """Build libisoquant.so in-tree: HIP kernels for gfx950 plus host C++.
 
-    python -m paper_2603_28430_amd.build
+    python paper_2603_28430_amd/build.py
+
+(run as a script, or loaded by file path: importing the package itself loads
+the library this script produces).
 """
 from __future__ import annotations
 

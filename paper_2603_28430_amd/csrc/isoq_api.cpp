@@ -4,10 +4,9 @@
 
 #include <algorithm>
 #include <cmath>
+#include <cstdio>
 #include <cstring>
-#include <mutex>
 #include <new>
-#include <unordered_map>
 #include <vector>
 
 #include "isoq_internal.h"
@@ -25,40 +24,20 @@ namespace {
 
 using namespace isoq;
 
+// Text of the last HIP error seen by a call on this thread.
+thread_local char g_last_hip_error[160] = "";
+
+isoq_status hip_fail(hipError_t e, const char *where, isoq_status st = ISOQ_E_HIP)
+{
+    std::snprintf(g_last_hip_error, sizeof g_last_hip_error, "%s: %s (%d)", where,
+                  hipGetErrorString(e), (int)e);
+    return st;
+}
+
 bool valid_variant(int v) { return v == ISOQ_FULL || v == ISOQ_FAST || v == ISOQ_PLANAR2D; }
 bool supported_d(int d) { return d == 128 || d == 256 || d == 512; }
 bool supported_bits(int b) { return b >= 2 && b <= 4; }
 bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
-
-// Persistent grid size per kernel: resident blocks per CU times CU count.
-struct DeviceInfo {
-    int cus = 0;
-};
-std::mutex g_mu;
-std::unordered_map<int, DeviceInfo> g_dev;
-std::unordered_map<const void *, int> g_occ;
-
-isoq_status launch_geometry(const void *fn, int device, int &blocks_per_cu, int &cus)
-{
-    std::lock_guard<std::mutex> lk(g_mu);
-    auto it = g_dev.find(device);
-    if (it == g_dev.end()) {
-        int c = 0;
-        if (hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess || c <= 0)
-            return ISOQ_E_HIP;
-        it = g_dev.emplace(device, DeviceInfo{c}).first;
-    }
-    cus = it->second.cus;
-    auto jt = g_occ.find(fn);
-    if (jt == g_occ.end()) {
-        int b = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, fn, kBlockThreads, 0) != hipSuccess || b <= 0)
-            return ISOQ_E_HIP;
-        jt = g_occ.emplace(fn, b).first;
-    }
-    blocks_per_cu = jt->second;
-    return ISOQ_OK;
-}
 
 isoq_status check_common(const isoq_params *p, int dtype, int64_t n, int64_t rows_per_set)
 {
@@ -74,8 +53,9 @@ isoq_status check_common(const isoq_params *p, int dtype, int64_t n, int64_t row
 isoq_status check_device(const isoq_params *p)
 {
     int dev = -1;
-    if (hipGetDevice(&dev) != hipSuccess)
-        return ISOQ_E_HIP;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess)
+        return hip_fail(e, "hipGetDevice");
     return dev == p->device ? ISOQ_OK : ISOQ_E_DEVICE;
 }
 
@@ -83,36 +63,12 @@ isoq_status run(const isoq_params *p, int dtype, int mode, KArgs &a, void *strea
 {
     const bool f16 = dtype == ISOQ_F16;
     const int rows_per_wave = 64 / (p->d / kCoordsPerLane);
-    const bool multi = p->n_sets > 1;
-    const bool generic = multi && (a.rows_per_set % rows_per_wave) != 0;
+    const int64_t rows_per_block = (int64_t)rows_per_wave * (kBlockThreads / 64) * kTileGroups;
+    const bool generic = p->n_sets > 1 && (a.rows_per_set % rows_per_block) != 0;
     const void *fn = kernel_for(p->variant, p->d, p->bits, f16, generic, mode);
     if (!fn)
         return ISOQ_E_UNSUPPORTED;
-    int bpc = 0, cus = 0;
-    isoq_status st = launch_geometry(fn, p->device, bpc, cus);
-    if (st != ISOQ_OK)
-        return st;
-    const int64_t groups = (a.n + rows_per_wave - 1) / rows_per_wave;
-    const int waves_per_block = kBlockThreads / 64;
-    const int64_t resident = (int64_t)bpc * cus * waves_per_block;
-    int64_t waves;
-    if (generic) {
-        // contiguous runs of row groups, one per resident wave
-        a.per_wave = (groups + resident - 1) / resident;
-        waves = (groups + a.per_wave - 1) / a.per_wave;
-        a.groups_per_seg = groups;
-        a.chunks_per_seg = waves;
-    } else {
-        // segments of rows_per_set rows share a set; waves never cross one
-        const int64_t gps = multi ? std::min<int64_t>(groups, a.rows_per_set / rows_per_wave) : groups;
-        const int64_t nseg = (groups + gps - 1) / gps;
-        const int64_t want = std::max<int64_t>(1, (resident + nseg - 1) / nseg);
-        a.per_wave = (gps + want - 1) / want;
-        a.chunks_per_seg = (gps + a.per_wave - 1) / a.per_wave;
-        a.groups_per_seg = gps;
-        waves = nseg * a.chunks_per_seg;
-    }
-    const int64_t blocks = (waves + waves_per_block - 1) / waves_per_block;
+    const int64_t blocks = (a.n + rows_per_block - 1) / rows_per_block;
     if (blocks > 0x7FFFFFFF)
         return ISOQ_E_UNSUPPORTED;
     const int H = 1 << (p->bits - 1);
@@ -127,14 +83,19 @@ isoq_status run(const isoq_params *p, int dtype, int mode, KArgs &a, void *strea
     void *args[] = {&a};
     hipError_t e = hipLaunchKernel(fn, dim3((unsigned)blocks), dim3(kBlockThreads), args, 0,
                                    static_cast<hipStream_t>(stream));
-    if (e != hipSuccess || hipGetLastError() != hipSuccess)
-        return ISOQ_E_HIP;
+    if (e != hipSuccess)
+        return hip_fail(e, "hipLaunchKernel");
+    e = hipGetLastError();
+    if (e != hipSuccess)
+        return hip_fail(e, "after hipLaunchKernel");
     return ISOQ_OK;
 }
 
 }  // namespace
 
 extern "C" {
+
+const char *isoq_last_hip_error(void) { return g_last_hip_error; }
 
 const char *isoq_status_string(isoq_status s)
 {
@@ -262,19 +223,22 @@ isoq_status isoq_params_init(isoq_params **out, int variant, int d, int bits, in
         p->thresholds[k] = (float)(0.5 * (lev[k] + lev[k + 1]));
     p->thresholds[K / 2 - 1] = 0.0f;
 
-    if (hipGetDevice(&p->device) != hipSuccess) {
+    hipError_t e = hipGetDevice(&p->device);
+    if (e != hipSuccess) {
         delete p;
-        return ISOQ_E_HIP;
+        return hip_fail(e, "hipGetDevice");
     }
     const size_t bytes = layout.size() * sizeof(float);
-    if (hipMalloc(reinterpret_cast<void **>(&p->dparams), bytes) != hipSuccess) {
+    e = hipMalloc(reinterpret_cast<void **>(&p->dparams), bytes);
+    if (e != hipSuccess) {
         delete p;
-        return ISOQ_E_NOMEM;
+        return hip_fail(e, "hipMalloc", e == hipErrorOutOfMemory ? ISOQ_E_NOMEM : ISOQ_E_HIP);
     }
-    if (hipMemcpy(p->dparams, layout.data(), bytes, hipMemcpyHostToDevice) != hipSuccess) {
+    e = hipMemcpy(p->dparams, layout.data(), bytes, hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
         (void)hipFree(p->dparams);
         delete p;
-        return ISOQ_E_HIP;
+        return hip_fail(e, "hipMemcpy");
     }
     *out = p;
     return ISOQ_OK;

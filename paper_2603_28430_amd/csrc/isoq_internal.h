@@ -17,6 +17,10 @@ enum Variant { VAR_FULL = 0, VAR_FAST = 1, VAR_PLANAR2D = 2 };
 constexpr int kCoordsPerLane = 8;
 constexpr int kBlockThreads = 256;
 
+// Row groups per wave in one block (a block covers 4 * kTileGroups groups,
+// i.e. 64 rows of d = 128): four 16-byte loads in flight per lane.
+constexpr int kTileGroups = 4;
+
 // Device rotation parameters per lane, in floats: Full keeps the two 4x4
 // matrices M = L(q_L) R(conj q_R) row-major, Fast the two unit quaternions,
 // 2-D (cos, sin) of the four pairs.
@@ -33,9 +37,6 @@ struct KArgs {
     const float *params;     // [n_sets][d/8][params_per_lane]
     int64_t n;               // rows
     int64_t rows_per_set;    // rows per parameter set (>= 1)
-    int64_t per_wave;        // row groups handled by one wave
-    int64_t groups_per_seg;  // row groups per segment of rows_per_set rows
-    int64_t chunks_per_seg;  // waves per segment
     int32_t n_sets;
     int32_t pad0;
     float lev_pos[8];        // c_{K/2} .. c_{K-1}   (positive half of the codebook)
@@ -44,8 +45,8 @@ struct KArgs {
 };
 
 // Kernel entry for (variant, d, bits, fp16 rows?, generic set indexing?, mode),
-// or nullptr.  Generic set indexing is needed when rows_per_set is not a
-// multiple of the rows per wave (512 / d) and there is more than one set.
+// or nullptr.  Generic set indexing is needed when there is more than one
+// set and rows_per_set is not a multiple of the rows of a block.
 const void *kernel_for(int variant, int d, int bits, bool f16, bool generic_sets, int mode);
 
 // ---- host-side parameter construction (isoq_host_params.cpp) -------------

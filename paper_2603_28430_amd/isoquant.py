@@ -27,12 +27,21 @@ STATUS = {0: "ISOQ_OK", 1: "ISOQ_E_INVALID", 2: "ISOQ_E_UNSUPPORTED", 3: "ISOQ_E
 class IsoqError(RuntimeError):
     def __init__(self, status: int, where: str):
         self.status = status
-        super().__init__(f"{where}: {STATUS.get(status, status)} ({isoq_status_string(status)})")
+        detail = lib.isoq_last_hip_error().decode() if status in (5, 6) else ""
+        super().__init__(f"{where}: {STATUS.get(status, status)} ({isoq_status_string(status)})"
+                         + (f" [{detail}]" if detail else ""))
 
 
 def _load():
     if not os.path.exists(LIB_PATH):
-        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2603_28430_amd.build`")
+        raise ImportError(f"{LIB_PATH} is not built; run `python paper_2603_28430_amd/build.py`")
+    # PyTorch ships its own HIP runtime (same soname).  Loading torch first
+    # makes the library bind to that runtime instead of a second copy, which
+    # would not see the GPU that torch has already opened.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     L = ctypes.CDLL(LIB_PATH)
     vp, dp, fp, i64 = ctypes.c_void_p, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_float), ctypes.c_int64
     c_int = ctypes.c_int
@@ -53,6 +62,8 @@ def _load():
     L.isoq_rotation_draws.argtypes = [c_int, c_int, c_int, ctypes.c_uint64, dp]
     L.isoq_status_string.argtypes = [c_int]
     L.isoq_status_string.restype = ctypes.c_char_p
+    L.isoq_last_hip_error.argtypes = []
+    L.isoq_last_hip_error.restype = ctypes.c_char_p
     for f in ("isoq_params_init", "isoq_params_destroy", "isoq_params_export", "isoq_params_info",
               "isoq_quantize", "isoq_dequantize", "isoq_roundtrip", "isoq_codebook_lloyd",
               "isoq_rotation_draws"):
