@@ -15,7 +15,10 @@
 struct isoq_params {
     int variant, d, bits, n_sets;
     int device;
-    float *dparams;                 // device, [n_sets][d/8][params_per_lane]
+    float *dparams;                 // device, [n_sets][d/8][params_per_lane], then the LUT
+    size_t lut_offset;              // floats from dparams to the magnitude LUT (0: none)
+    int lut_cells;
+    float lut_inv_h;
     std::vector<float> exported;    // unit parameters as used (Table 1 layout)
     float levels[16], thresholds[15];
 };
@@ -80,6 +83,9 @@ isoq_status run(const isoq_params *p, int dtype, int mode, KArgs &a, void *strea
         a.lev_all[k] = p->levels[k];
     a.params = p->dparams;
     a.n_sets = p->n_sets;
+    a.lut = p->lut_offset ? p->dparams + p->lut_offset : nullptr;
+    a.lut_inv_h = p->lut_inv_h;
+    a.lut_cells = p->lut_cells;
     void *args[] = {&a};
     hipError_t e = hipLaunchKernel(fn, dim3((unsigned)blocks), dim3(kBlockThreads), args, 0,
                                    static_cast<hipStream_t>(stream));
@@ -222,6 +228,28 @@ isoq_status isoq_params_init(isoq_params **out, int variant, int d, int bits, in
     for (int k = 0; k + 1 < K; k++)
         p->thresholds[k] = (float)(0.5 * (lev[k] + lev[k + 1]));
     p->thresholds[K / 2 - 1] = 0.0f;
+    p->lut_offset = 0;
+    p->lut_cells = 0;
+    p->lut_inv_h = 0.f;
+    if (bits == 4) {
+        // thresholds and levels of the positive half, in fp32 as the kernels use them
+        const int H = K / 2;
+        double tau[8], levp[8], inv_h = 0;
+        for (int i = 0; i + 1 < H; i++)
+            tau[i] = (double)p->thresholds[H + i];
+        for (int i = 0; i < H; i++)
+            levp[i] = (double)p->levels[H + i];
+        std::vector<LutEntry> lut;
+        if (!build_magnitude_lut(H, tau, levp, &inv_h, lut)) {
+            delete p;
+            return ISOQ_E_UNSUPPORTED;
+        }
+        p->lut_offset = layout.size();
+        p->lut_cells = (int)lut.size();
+        p->lut_inv_h = (float)inv_h;
+        const float *f = reinterpret_cast<const float *>(lut.data());
+        layout.insert(layout.end(), f, f + 4 * lut.size());
+    }
 
     hipError_t e = hipGetDevice(&p->device);
     if (e != hipSuccess) {

@@ -1,6 +1,7 @@
 // Host-side construction of the quantizer state: Lloyd-Max codebook, seeded
 // rotation draws, normalisation (Sec. 5.5) and the per-lane device layout.
 // All of it runs once, at isoq_params_init, in double precision.
+#include <algorithm>
 #include <cmath>
 #include <cstring>
 
@@ -217,6 +218,53 @@ bool build_rotation(int variant, int d, int n_sets, const double *raw, std::vect
                     dv[16 * i + 4 * r + c] = (float)M[r][c];
         }
     }
+    return true;
+}
+
+// ------------------------------------------------------- magnitude lookup table
+bool build_magnitude_lut(int H, const double *tau, const double *lev, double *inv_h,
+                         std::vector<LutEntry> &lut)
+{
+    double gap = tau[0];
+    for (int i = 0; i + 1 < H - 1; i++)
+        gap = std::min(gap, tau[i + 1] - tau[i]);
+    if (!(gap > 0))
+        return false;
+    // cell width: below the smallest gap, and with every threshold at least
+    // 2% of a cell away from a cell edge (rounding of the cell index then
+    // never moves a value across a threshold)
+    double h = 0;
+    for (double f = 0.95; f > 0.5; f -= 0.005) {
+        const double hh = gap * f;
+        bool ok = true;
+        for (int i = 0; i < H - 1 && ok; i++) {
+            const double u = tau[i] / hh, frac = u - std::floor(u);
+            ok = frac > 0.02 && frac < 0.98;
+        }
+        if (ok) {
+            h = hh;
+            break;
+        }
+    }
+    if (!(h > 0))
+        return false;
+    const int cells = (int)std::floor(tau[H - 2] / h) + 2;
+    if (cells > kLutMaxCells)
+        return false;
+    lut.assign(cells, LutEntry{});
+    for (int c = 0; c < cells; c++) {
+        const double lo_edge = c * h, hi_edge = (c + 1) * h;
+        int m = 0;
+        while (m < H - 1 && tau[m] < lo_edge)
+            m++;
+        LutEntry e;
+        e.m = (uint32_t)m;
+        e.lo = (float)lev[m];
+        e.hi = (float)lev[std::min(m + 1, H - 1)];
+        e.t = (m < H - 1 && tau[m] < hi_edge) ? (float)(tau[m] / h) : INFINITY;
+        lut[c] = e;
+    }
+    *inv_h = 1.0 / h;
     return true;
 }
 

@@ -39,6 +39,9 @@ struct KArgs {
     int64_t rows_per_set;    // rows per parameter set (>= 1)
     int32_t n_sets;
     int32_t pad0;
+    const float *lut;        // magnitude lookup table (4-bit codebooks), [lut_cells][4]
+    float lut_inv_h;         // 1 / cell width, in units of the normalised coordinate
+    int32_t lut_cells;
     float lev_pos[8];        // c_{K/2} .. c_{K-1}   (positive half of the codebook)
     float thr_pos[8];        // t_{K/2} .. t_{K-2}   (positive thresholds; t_{K/2-1} = 0)
     float lev_all[16];       // c_0 .. c_{K-1}
@@ -49,7 +52,25 @@ struct KArgs {
 // set and rows_per_set is not a multiple of the rows of a block.
 const void *kernel_for(int variant, int d, int bits, bool f16, bool generic_sets, int mode);
 
+// Magnitude lookup table, used for 4-bit codebooks.  The magnitude axis of
+// the normalised coordinate is cut into cells of width h, h smaller than every
+// gap between consecutive positive thresholds (and than the first one), so a
+// cell holds at most one threshold.  Entry c = {threshold inside the cell in
+// cell units (+inf if none), level below it, level above it, magnitude index
+// below it}; values past the last cell use the last entry.
+constexpr int kLutMaxCells = 256;
+struct LutEntry {
+    float t, lo, hi;
+    uint32_t m;
+};
+static_assert(sizeof(LutEntry) == 16, "LUT entries are 16 bytes");
+
 // ---- host-side parameter construction (isoq_host_params.cpp) -------------
+// Build the table from the positive thresholds tau[0..H-2] and the positive
+// levels lev[0..H-1] (H = 2^(bits-1)).  Returns false if more than
+// kLutMaxCells cells would be needed.
+bool build_magnitude_lut(int H, const double *tau, const double *lev, double *inv_h,
+                         std::vector<LutEntry> &lut);
 // Lloyd-Max levels for N(0, sigma^2) (ascending, symmetrised).
 bool lloyd_levels(int bits, double sigma, int iters, double *levels);
 // Seeded raw draws (Philox4x32-10 + Box-Muller), layout of the public header.

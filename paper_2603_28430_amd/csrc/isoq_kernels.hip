@@ -132,13 +132,17 @@ __device__ __forceinline__ void store_row_chunk(char *p, const float o[8])
 {
     u32x4 *q = reinterpret_cast<u32x4 *>(p);
     if constexpr (F16) {
+        // fp32 -> fp16 with one explicit v_cvt_pk_f16_f32 (round to nearest
+        // even).  Left to itself the compiler folds the last FMA and the
+        // conversion into a mixed-precision FMA (rounding once, straight to
+        // fp16) in some kernels and not in others, which would let the fused
+        // and the two-pass paths round the same value differently.
         u32x4 w;
 #pragma unroll
         for (int k = 0; k < 4; k++) {
-            f16x2 h;
-            h.x = (_Float16)o[2 * k];  // round to nearest even
-            h.y = (_Float16)o[2 * k + 1];
-            w[k] = __builtin_bit_cast(uint32_t, h);
+            uint32_t h;
+            asm("v_cvt_pk_f16_f32 %0, %1, %2" : "=v"(h) : "v"(o[2 * k]), "v"(o[2 * k + 1]));
+            w[k] = h;
         }
         __builtin_nontemporal_store(w, q);
     } else {
@@ -310,6 +314,7 @@ struct Stage1 {
     static constexpr int64_t ROWB = (int64_t)D * (F16 ? 2 : 4);  // bytes per row
     static constexpr int64_t RECB = (int64_t)D * BITS / 8;       // bytes per index record
     static constexpr int LANEB = F16 ? 16 : 32;         // row bytes per lane
+    static constexpr bool kUseLut = BITS == 4;           // magnitude lookup table
 
     struct In {
         Raw<F16> raw;
@@ -317,27 +322,35 @@ struct Stage1 {
         float rho;
     };
 
-    __device__ static __forceinline__ void fetch(const KArgs &a, int64_t g, int sub, int slot, In &in)
+    // Row addressing.  In a full tile every row exists: row = row0 + r with
+    // row0 block-uniform and r < 64 rows, so addresses are a scalar base plus a
+    // 32-bit lane offset.  In the last (tail) tile, lanes past the end take
+    // the last row: they recompute it and store the same bits to the same
+    // place, which keeps the loop free of divergent branches.
+    template <bool TAIL>
+    __device__ static __forceinline__ int64_t row_of(const KArgs &a, int64_t row0, int r)
     {
-        int64_t row = g * VPW + slot;
-        row = row < a.n ? row : a.n - 1;  // lanes past the end take the last row (see compute)
+        if constexpr (TAIL)
+            return min(row0 + r, a.n - 1) - row0;
+        return r;
+    }
+
+    __device__ static __forceinline__ void fetch(const KArgs &a, int64_t row0, int64_t r, int sub, In &in)
+    {
         if constexpr (MODE == MODE_DEQUANTIZE) {
-            in.bits = load_bits<BITS>(a.rec_in + row * RECB, sub);
-            in.rho = a.norms_in[row];
+            in.bits = load_bits<BITS>(a.rec_in + row0 * RECB + (uint32_t)(r * RECB), sub);
+            in.rho = a.norms_in[row0 + r];
         } else {
-            load_row_chunk<F16>(static_cast<const char *>(a.x) + row * ROWB + sub * LANEB, in.raw);
+            load_row_chunk<F16>(static_cast<const char *>(a.x) + row0 * ROWB + (uint32_t)(r * ROWB + sub * LANEB),
+                                in.raw);
         }
     }
 
     __device__ static __forceinline__ void compute(const KArgs &a, const float *P, const float *lev,
                                                    const float *thr, const float *lds_levels,
-                                                   const In &in, int64_t g, int sub, int slot)
+                                                   const LutEntry *lut, const In &in, int64_t row0,
+                                                   int64_t r, int sub)
     {
-        // Lanes past the last row were fed the last row (see fetch); they
-        // recompute it and store the same bits to the same place.  The loop has
-        // no divergent branch, so the compiler keeps loads and waits in order.
-        int64_t row = g * VPW + slot;
-        row = row < a.n ? row : a.n - 1;
         float yq[8];
         if constexpr (MODE == MODE_DEQUANTIZE) {
 #pragma unroll
@@ -355,6 +368,31 @@ struct Stage1 {
 #pragma unroll
             for (int j = 0; j < 8; j++)
                 m[j] = fabsf(y[j]);
+            if constexpr (kUseLut) {
+                // 4 bits: cell of the normalised magnitude, one compare against
+                // the cell's threshold (quantize and round trip use the same t)
+                const float s = a.lut_inv_h * __builtin_amdgcn_rcpf(rho_e);
+                const float last = (float)(a.lut_cells - 1);
+                uint32_t p = 0;
+#pragma unroll
+                for (int j = 0; j < 8; j++) {
+                    const float t = m[j] * s;
+                    const LutEntry e = lut[(uint32_t)fminf(t, last)];
+                    const bool above = t > e.t;
+                    if constexpr (MODE == MODE_ROUNDTRIP) {
+                        const float L = above ? e.hi : e.lo;
+                        yq[j] = (y[j] > 0.f ? L : -L) * rho;
+                    } else {
+                        const uint32_t q = e.m + (above ? 1u : 0u);
+                        p |= (q ^ (y[j] > 0.f ? (uint32_t)H : (uint32_t)(H - 1))) << (BITS * j);
+                    }
+                }
+                if constexpr (MODE == MODE_QUANTIZE) {
+                    store_bits<BITS>(a.rec_out + row0 * RECB + (uint32_t)(r * RECB), sub, p);
+                    if (sub == 0)
+                        a.norms_out[row0 + r] = rho;
+                }
+            } else {
             float ths[H > 1 ? H - 1 : 1];
 #pragma unroll
             for (int k = 0; k < H - 1; k++)
@@ -379,28 +417,43 @@ struct Stage1 {
                 for (int j = 0; j < 8; j++)
                     yq[j] = y[j] > 0.f ? L[j] : -L[j];
             } else {
+                // m = number of positive thresholds below |y|; the index is
+                // H + m for y > 0 and H - 1 - m otherwise, i.e. m ^ H or
+                // m ^ (H - 1)
                 uint32_t q[8];
+                if constexpr (H == 4) {
+                    // three thresholds: binary search (compare with the middle
+                    // one, then with the one it selects)
 #pragma unroll
-                for (int j = 0; j < 8; j++)
-                    q[j] = 0;
-#pragma unroll
-                for (int k = 0; k < H - 1; k++)
+                    for (int j = 0; j < 8; j++) {
+                        const bool hi = m[j] > ths[1];
+                        const bool lo = m[j] > (hi ? ths[2] : ths[0]);
+                        q[j] = (hi ? 2u : 0u) + (lo ? 1u : 0u);
+                    }
+                } else {
 #pragma unroll
                     for (int j = 0; j < 8; j++)
-                        q[j] = m[j] > ths[k] ? (uint32_t)(k + 1) : q[j];
+                        q[j] = 0;
+#pragma unroll
+                    for (int k = 0; k < H - 1; k++)
+#pragma unroll
+                        for (int j = 0; j < 8; j++)
+                            q[j] = m[j] > ths[k] ? (uint32_t)(k + 1) : q[j];
+                }
                 uint32_t p = 0;
 #pragma unroll
                 for (int j = 0; j < 8; j++)
                     p |= (q[j] ^ (y[j] > 0.f ? (uint32_t)H : (uint32_t)(H - 1))) << (BITS * j);
-                store_bits<BITS>(a.rec_out + row * RECB, sub, p);
+                store_bits<BITS>(a.rec_out + row0 * RECB + (uint32_t)(r * RECB), sub, p);
                 if (sub == 0)
-                    a.norms_out[row] = rho;
+                    a.norms_out[row0 + r] = rho;
+            }
             }
         }
         if constexpr (MODE != MODE_QUANTIZE) {
             float o[8];
             rotate_inverse<VAR>(P, yq, o);
-            store_row_chunk<F16>(static_cast<char *>(a.y) + row * ROWB + sub * LANEB, o);
+            store_row_chunk<F16>(static_cast<char *>(a.y) + row0 * ROWB + (uint32_t)(r * ROWB + sub * LANEB), o);
         }
     }
 
@@ -410,7 +463,7 @@ struct Stage1 {
         return (int)((row / a.rows_per_set) % a.n_sets);
     }
 
-    __device__ static void run(const KArgs &a, float *lds_levels, float *lds_params)
+    __device__ static void run(const KArgs &a, float *lds_levels, float *lds_params, LutEntry *lds_lut)
     {
         const int lane = threadIdx.x & 63;
         const int sub = lane % LPV;
@@ -425,6 +478,12 @@ struct Stage1 {
             if (threadIdx.x < 2 * H)
                 lds_levels[threadIdx.x] = a.lev_all[threadIdx.x];
         }
+        if constexpr (kUseLut && MODE != MODE_DEQUANTIZE) {
+            const u32x4 *s4 = reinterpret_cast<const u32x4 *>(a.lut);
+            u32x4 *d4 = reinterpret_cast<u32x4 *>(lds_lut);
+            for (int i = threadIdx.x; i < a.lut_cells; i += kBlockThreads)
+                d4[i] = s4[i];
+        }
         float P[PL];
         if constexpr (!GENERIC_SETS) {
             const int64_t set = a.n_sets > 1 ? (base * VPW / a.rows_per_set) % a.n_sets : 0;
@@ -433,21 +492,12 @@ struct Stage1 {
             for (int i = threadIdx.x; i < LPV * PL / 4; i += kBlockThreads)
                 d4[i] = s4[i];
         }
-        if constexpr (MODE == MODE_DEQUANTIZE || !GENERIC_SETS)
+        if constexpr (MODE == MODE_DEQUANTIZE || !GENERIC_SETS || kUseLut)
             __syncthreads();
         if constexpr (!GENERIC_SETS)
             load_params<PL>(lds_params + sub * PL, P);
         if (base + w >= groups)
             return;
-
-        // 2. every load of the tile (groups past the end re-read the last
-        //    group and are neither computed nor stored), kept together in
-        //    flight by the scheduling barrier
-        In buf[kTileGroups];
-#pragma unroll
-        for (int u = 0; u < kTileGroups; u++)
-            fetch(a, min(base + 4 * u + w, groups - 1), sub, slot, buf[u]);
-        __builtin_amdgcn_sched_barrier(0);
 
         float lev[H], thr[H > 1 ? H - 1 : 1];
 #pragma unroll
@@ -457,15 +507,39 @@ struct Stage1 {
         for (int k = 0; k < H - 1; k++)
             thr[k] = a.thr_pos[k];
 
-        // 3. compute and store group by group
+        const int64_t row0 = base * VPW;  // first row of the block
+        if ((base + (kBlockThreads / 64) * kTileGroups) * VPW <= a.n)
+            tile<false>(a, P, lev, thr, lds_levels, lds_lut, row0, groups, base, w, sub, slot);
+        else
+            tile<true>(a, P, lev, thr, lds_levels, lds_lut, row0, groups, base, w, sub, slot);
+    }
+
+    // The wave's kTileGroups groups: every load first (a group past the end
+    // re-reads the last group and is neither computed nor stored), kept in
+    // flight together by the scheduling barrier; then compute and store group
+    // by group.
+    template <bool TAIL>
+    __device__ static __forceinline__ void tile(const KArgs &a, float *P, const float *lev,
+                                                const float *thr, const float *lds_levels,
+                                                const LutEntry *lut, int64_t row0, int64_t groups,
+                                                int64_t base, int w, int sub, int slot)
+    {
+        In buf[kTileGroups];
 #pragma unroll
         for (int u = 0; u < kTileGroups; u++) {
-            const int64_t g = base + 4 * u + w;
-            if (g >= groups)
+            const int gl = TAIL ? (int)(min(base + 4 * u + w, groups - 1) - base) : 4 * u + w;
+            fetch(a, row0, row_of<TAIL>(a, row0, gl * VPW + slot), sub, buf[u]);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int u = 0; u < kTileGroups; u++) {
+            const int gl = 4 * u + w;
+            if (TAIL && base + gl >= groups)
                 break;
+            const int64_t r = row_of<TAIL>(a, row0, gl * VPW + slot);
             if constexpr (GENERIC_SETS)
-                load_params<PL>(a.params + ((int64_t)set_of(a, min(g * VPW + slot, a.n - 1)) * LPV + sub) * PL, P);
-            compute(a, P, lev, thr, lds_levels, buf[u], g, sub, slot);
+                load_params<PL>(a.params + ((int64_t)set_of(a, row0 + r) * LPV + sub) * PL, P);
+            compute(a, P, lev, thr, lds_levels, lut, buf[u], row0, r, sub);
         }
     }
 };
@@ -476,7 +550,8 @@ __global__ __launch_bounds__(kBlockThreads) void stage1_kernel(const KArgs a)
     using S = Stage1<VAR, D, BITS, F16, MODE, GENERIC_SETS>;
     __shared__ float lds_levels[16];
     __shared__ __align__(16) float lds_params[GENERIC_SETS ? 4 : S::LPV * S::PL];
-    S::run(a, lds_levels, lds_params);
+    __shared__ __align__(16) LutEntry lds_lut[S::kUseLut && MODE != MODE_DEQUANTIZE ? kLutMaxCells : 1];
+    S::run(a, lds_levels, lds_params, lds_lut);
 }
 
 template <int VAR, int D, int BITS, bool F16, bool GEN>
