@@ -134,6 +134,41 @@ def cpu_baseline(variant, d, bits, x_np, rot, levels, seconds: float):
                       f"(Algorithm 1, indices not stored), {threads} threads, {dt:.1f} s"}
 
 
+def other_configs(measure, entry, torch, np, workloads):
+    """Side measurements of the other workloads (their parity is tested in
+    tests/test_gpu_full_sizes.py): d = 256 fp16 and d = 512 fp32 round trips
+    and quantize, Full and Fast, 2-4 bits; the K/V cache stream
+    [8, 32, 32768, 128] fp16, Fast 3-bit quantize, one quaternion set per head
+    (one step = K then V)."""
+    out = {}
+    for name, d_, n_, tdt, ndt in (("d256_f16_n1048576", 256, 1 << 20, torch.float16, np.float16),
+                                   ("d512_f32_n262144", 512, 1 << 18, torch.float32, np.float32)):
+        print(f"# config {name}", file=sys.stderr, flush=True)
+        x0 = torch.from_numpy(workloads.unit_gaussian_rows(n_, d_, seed=0, dtype=ndt)).cuda()
+        ins = [x0] + [x0.clone() for _ in range(2)]
+        outs_ = [torch.empty_like(x0) for _ in range(3)]
+        res = {}
+        for variant in ("full", "fast"):
+            for b_ in (2, 3, 4):
+                res[f"{variant}_b{b_}"] = entry(*measure(variant, b_, "roundtrip", 50, 5, 0.2, ins, outs_, d_))
+                res[f"{variant}_b{b_}_quantize"] = entry(*measure(variant, b_, "quantize", 50, 5, 0.2, ins,
+                                                                  outs_, d_))
+        out[name] = res
+        del x0, ins, outs_
+        torch.cuda.empty_cache()
+    print("# config kv cache", file=sys.stderr, flush=True)
+    B, H, T, d_ = 8, 32, 32768, 128
+    kv = [workloads.kv_stream_torch(B, H, T, d_, seed, "cuda").view(B * H * T, d_) for seed in (2, 3)]
+    ms, b, n_ = measure("fast", 3, "quantize", 40, 4, 0.2, kv, kv, d_, n_sets=H, rows_per_set=T)
+    step = 2 * ms  # K and V: two launches of the same size
+    out["kv_cache_fast_b3_quantize"] = {
+        "shape": [B, H, T, d_], "tensors": 2, "ms_per_step": step, "rows_per_s": 2 * n_ / (step / 1e3),
+        "GBps": 2 * b / step / 1e6, "frac": 2 * b / step / 1e6 / PEAK_HBM_GBPS}
+    del kv
+    torch.cuda.empty_cache()
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -150,6 +185,8 @@ def main() -> int:
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the side measurements of the d=256, d=512 and KV-cache workloads")
     ap.add_argument("--copy-only", action="store_true",
                     help="only time a plain device copy of the input size (counter calibration)")
     args = ap.parse_args()
@@ -180,30 +217,43 @@ def main() -> int:
         print(json.dumps({"copy_bytes_per_launch": b, "ms_per_launch": ms, "GBps": b / ms / 1e6}))
         return 0
 
-    def setup(variant, bits_):
-        rot = workloads.rotation_draws(variant, d, 1, seed=1)
-        return iq.isoq_params_init(variant, d, bits_, 1, rot=rot), rot
+    def setup(variant, bits_, d_=d, n_sets=1):
+        rot = workloads.rotation_draws(variant, d_, n_sets, seed=1)
+        return iq.isoq_params_init(variant, d_, bits_, n_sets, rot=rot), rot
 
-    def measure(variant, bits_, mode, steps, warmup, warm_seconds=0.0):
-        p, _ = setup(variant, bits_)
+    def measure(variant, bits_, mode, steps, warmup, warm_seconds=0.0, ins=None, outs_=None,
+                d_=d, n_sets=1, rows_per_set=1):
+        """ms per launch of `mode` over the buffer sets `ins` (rows) / `outs_`."""
+        ins = xs if ins is None else ins
+        outs_ = outs if outs_ is None else outs_
+        S_ = len(ins)
+        n_ = ins[0].numel() // d_
+        p, _ = setup(variant, bits_, d_, n_sets)
         if mode == "roundtrip":
-            fn = lambda i: iq.isoq_roundtrip(p, xs[i % S], x_hat=outs[i % S])
+            fn = lambda i: iq.isoq_roundtrip(p, ins[i % S_], rows_per_set, x_hat=outs_[i % S_])
         else:
-            recs = [torch.empty((n, p.record_bytes), dtype=torch.uint8, device="cuda") for _ in range(S)]
-            norms = [torch.empty((n,), dtype=torch.float32, device="cuda") for _ in range(S)]
-            for i in range(S):
-                iq.isoq_quantize(p, xs[i], idx_packed=recs[i], norms=norms[i])
+            recs = [torch.empty((n_, p.record_bytes), dtype=torch.uint8, device="cuda") for _ in range(S_)]
+            norms = [torch.empty((n_,), dtype=torch.float32, device="cuda") for _ in range(S_)]
+            for i in range(S_):
+                iq.isoq_quantize(p, ins[i], rows_per_set, idx_packed=recs[i], norms=norms[i])
             if mode == "quantize":
-                fn = lambda i: iq.isoq_quantize(p, xs[i % S], idx_packed=recs[i % S], norms=norms[i % S])
+                fn = lambda i: iq.isoq_quantize(p, ins[i % S_], rows_per_set, idx_packed=recs[i % S_],
+                                                norms=norms[i % S_])
             else:
-                fn = lambda i: iq.isoq_dequantize(p, recs[i % S], norms[i % S], x_hat=outs[i % S])
+                fn = lambda i: iq.isoq_dequantize(p, recs[i % S_], norms[i % S_], rows_per_set=rows_per_set,
+                                                  x_hat=outs_[i % S_])
         ms = time_launches(fn, steps, warmup, torch, warm_seconds)
-        b = algorithmic_bytes(mode, n, d, bits_, esz)
-        return ms, b
+        b = algorithmic_bytes(mode, n_, d_, bits_, ins[0].element_size())
+        p.close()
+        return ms, b, n_
+
+    def entry(ms, b, n_):
+        return {"ms": ms, "vectors_per_s": n_ / (ms / 1e3), "GBps": b / ms / 1e6,
+                "frac": b / ms / 1e6 / PEAK_HBM_GBPS}
 
     # ---- the timed headline: K steps of the fused path ----
     print(f"# timing {args.mode} {args.variant} b={bits}", file=sys.stderr, flush=True)
-    ms, abytes = measure(args.variant, bits, args.mode, args.steps, args.warmup, args.warm_seconds)
+    ms, abytes, _ = measure(args.variant, bits, args.mode, args.steps, args.warmup, args.warm_seconds)
     gbps = abytes / ms / 1e6
     tag = f"{args.mode}_{args.variant}_d{d}_b{bits}_{args.dtype}_n{n}"
     result = {
@@ -240,18 +290,18 @@ def main() -> int:
         extra["device_copy_same_size"] = {"GBps": 2 * x0.numel() * esz / cms / 1e6, "ms": cms}
         paths = {}
         for mode in ("quantize", "dequantize"):
-            m_ms, m_b = measure(args.variant, bits, mode, 100, 10, 0.2)
-            paths[mode] = {"ms": m_ms, "vectors_per_s": n / (m_ms / 1e3), "GBps": m_b / m_ms / 1e6,
-                           "frac": m_b / m_ms / 1e6 / PEAK_HBM_GBPS}
+            paths[mode] = entry(*measure(args.variant, bits, mode, 100, 10, 0.2))
         extra["paths"] = paths
         sweep = {}
         for variant in ("full", "fast", "2d"):
             for b_ in (2, 3, 4):
-                m_ms, m_b = measure(variant, b_, "roundtrip", 100, 10, 0.2)
-                sweep[f"{variant}_b{b_}"] = {"ms": m_ms, "vectors_per_s": n / (m_ms / 1e3),
-                                             "GBps": m_b / m_ms / 1e6,
-                                             "frac": m_b / m_ms / 1e6 / PEAK_HBM_GBPS}
+                sweep[f"{variant}_b{b_}"] = entry(*measure(variant, b_, "roundtrip", 100, 10, 0.2))
+                if d == 128 and args.dtype == "f16" and n == 1 << 20:
+                    sweep[f"{variant}_b{b_}_quantize"] = entry(*measure(variant, b_, "quantize", 100, 10, 0.2))
         extra["roundtrip_sweep"] = sweep
+        del xs[1:], outs[1:]
+        if not args.no_configs:
+            extra["configs"] = other_configs(measure, entry, torch, np, workloads)
         result["extra"] = extra
 
     if not args.no_cpu_baseline:

@@ -64,10 +64,19 @@ __device__ __forceinline__ float row_sum(float v)
     v += dpp_f<DPP_QUAD_2301>(v);
     v += dpp_f<DPP_ROW_HALF_MIRROR>(v);
     v += dpp_f<DPP_ROW_MIRROR>(v);
-    if constexpr (LPV >= 32)
-        v += __shfl_xor(v, 16);
-    if constexpr (LPV >= 64)
-        v += __shfl_xor(v, 32);
+    // across 16-lane rows: v_permlane16_swap exchanges odd rows of its first
+    // operand with even rows of its second, v_permlane32_swap the upper half
+    // of the first with the lower half of the second; with both operands v,
+    // the two results are (v of row r, v of row r ^ 1) (resp. r ^ 2) in the
+    // same order on both rows, so every lane adds the same two values
+    if constexpr (LPV >= 32) {
+        const auto s = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+        v = __uint_as_float(s[0]) + __uint_as_float(s[1]);
+    }
+    if constexpr (LPV >= 64) {
+        const auto s = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+        v = __uint_as_float(s[0]) + __uint_as_float(s[1]);
+    }
     return v;
 }
 
@@ -152,8 +161,11 @@ __device__ __forceinline__ void store_row_chunk(char *p, const float o[8])
             a[k] = __float_as_uint(o[k]);
             b[k] = __float_as_uint(o[4 + k]);
         }
-        __builtin_nontemporal_store(a, q);
-        __builtin_nontemporal_store(b, q + 1);
+        // plain (write-back) stores: each instruction covers half of every
+        // 32-byte span of the wave's rows; L2 merges the two halves before the
+        // line goes out (streaming stores wrote such lines out twice)
+        q[0] = a;
+        q[1] = b;
     }
 }
 
@@ -264,13 +276,12 @@ __device__ __forceinline__ void store_bits(uint8_t *rec, int sub, uint32_t p)
     } else if constexpr (BITS == 4) {
         reinterpret_cast<uint32_t *>(rec)[sub] = p;
     } else {
+        // lane k of a quad holds bits [24 k, 24 k + 24) of 96; lanes 0..2
+        // write word k = p_k >> 8 k | p_(k+1) << (24 - 8 k)
         const uint32_t nb = dpp_u<DPP_QUAD_1233>(p);  // bits of the next lane in the quad
         const int k = sub & 3;
-        const uint32_t lo = p | (nb << 24);
-        const uint32_t hi = nb >> 8;
-        const uint32_t w = (uint32_t)((((uint64_t)hi << 32) | lo) >> (8 * k));
         if (k < 3)
-            reinterpret_cast<uint32_t *>(rec + 12 * (sub >> 2))[k] = w;
+            reinterpret_cast<uint32_t *>(rec)[3 * (sub >> 2) + k] = (p >> (8 * k)) | (nb << (24 - 8 * k));
     }
 }
 
@@ -290,6 +301,50 @@ __device__ __forceinline__ uint32_t load_bits(const uint8_t *rec, int sub)
         const int sh = (24 * k) & 31;
         return (uint32_t)((((uint64_t)hi << 32) | lo) >> sh) & 0xFFFFFFu;
     }
+}
+
+// Append the lane's bit of each mask to p, first mask first (p = 2 p + bit):
+// v_addc_co_u32 with the mask as carry-in does the shift and the insert in one
+// instruction.  The masks are written by VALU compares; a VALU read of an SGPR
+// as carry-in needs wait states after such a write, which the compiler cannot
+// insert inside an asm statement, so the block starts with s_nop 4.
+__device__ __forceinline__ uint32_t push_bits8(uint32_t p, const uint64_t m[8])
+{
+    asm("s_nop 4\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %1\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %2\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %3\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %4\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %5\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %6\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %7\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %8"
+        : "+v"(p)
+        : "s"(m[0]), "s"(m[1]), "s"(m[2]), "s"(m[3]), "s"(m[4]), "s"(m[5]), "s"(m[6]), "s"(m[7])
+        : "vcc");
+    return p;
+}
+
+__device__ __forceinline__ uint32_t push_bits12(uint32_t p, const uint64_t m[12])
+{
+    asm("s_nop 4\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %1\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %2\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %3\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %4\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %5\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %6\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %7\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %8\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %9\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %10\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %11\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %12"
+        : "+v"(p)
+        : "s"(m[0]), "s"(m[1]), "s"(m[2]), "s"(m[3]), "s"(m[4]), "s"(m[5]), "s"(m[6]), "s"(m[7]),
+          "s"(m[8]), "s"(m[9]), "s"(m[10]), "s"(m[11])
+        : "vcc");
+    return p;
 }
 
 // ---- the kernel ---------------------------------------------------------------
@@ -322,34 +377,35 @@ struct Stage1 {
         float rho;
     };
 
-    // Row addressing.  In a full tile every row exists: row = row0 + r with
-    // row0 block-uniform and r < 64 rows, so addresses are a scalar base plus a
-    // 32-bit lane offset.  In the last (tail) tile, lanes past the end take
-    // the last row: they recompute it and store the same bits to the same
-    // place, which keeps the loop free of divergent branches.
+    // Row addressing.  The row of a lane is grow + lr: grow, the first row of
+    // the group, is wave-uniform, and lr < VPW is the lane's row slot, so
+    // addresses are a scalar base plus a loop-invariant lane offset.  In the
+    // last (tail) tile, lanes past the end take the last row: they recompute
+    // it and store the same bits to the same place, which keeps the loop free
+    // of divergent branches.
     template <bool TAIL>
-    __device__ static __forceinline__ int64_t row_of(const KArgs &a, int64_t row0, int r)
+    __device__ static __forceinline__ int lane_row(const KArgs &a, int64_t grow, int slot)
     {
         if constexpr (TAIL)
-            return min(row0 + r, a.n - 1) - row0;
-        return r;
+            return (int)(min(grow + slot, a.n - 1) - grow);
+        return slot;
     }
 
-    __device__ static __forceinline__ void fetch(const KArgs &a, int64_t row0, int64_t r, int sub, In &in)
+    __device__ static __forceinline__ void fetch(const KArgs &a, int64_t grow, int lr, int sub, In &in)
     {
         if constexpr (MODE == MODE_DEQUANTIZE) {
-            in.bits = load_bits<BITS>(a.rec_in + row0 * RECB + (uint32_t)(r * RECB), sub);
-            in.rho = a.norms_in[row0 + r];
+            in.bits = load_bits<BITS>(a.rec_in + grow * RECB + (uint32_t)(lr * RECB), sub);
+            in.rho = (a.norms_in + grow)[lr];
         } else {
-            load_row_chunk<F16>(static_cast<const char *>(a.x) + row0 * ROWB + (uint32_t)(r * ROWB + sub * LANEB),
+            load_row_chunk<F16>(static_cast<const char *>(a.x) + grow * ROWB + (uint32_t)(lr * ROWB + sub * LANEB),
                                 in.raw);
         }
     }
 
     __device__ static __forceinline__ void compute(const KArgs &a, const float *P, const float *lev,
                                                    const float *thr, const float *lds_levels,
-                                                   const LutEntry *lut, const In &in, int64_t row0,
-                                                   int64_t r, int sub)
+                                                   const LutEntry *lut, const In &in, int64_t grow,
+                                                   int lr, int sub)
     {
         float yq[8];
         if constexpr (MODE == MODE_DEQUANTIZE) {
@@ -388,9 +444,9 @@ struct Stage1 {
                     }
                 }
                 if constexpr (MODE == MODE_QUANTIZE) {
-                    store_bits<BITS>(a.rec_out + row0 * RECB + (uint32_t)(r * RECB), sub, p);
+                    store_bits<BITS>(a.rec_out + grow * RECB + (uint32_t)(lr * RECB), sub, p);
                     if (sub == 0)
-                        a.norms_out[row0 + r] = rho;
+                        (a.norms_out + grow)[lr] = rho;
                 }
             } else {
             float ths[H > 1 ? H - 1 : 1];
@@ -420,40 +476,47 @@ struct Stage1 {
                 // m = number of positive thresholds below |y|; the index is
                 // H + m for y > 0 and H - 1 - m otherwise, i.e. m ^ H or
                 // m ^ (H - 1)
-                uint32_t q[8];
-                if constexpr (H == 4) {
-                    // three thresholds: binary search (compare with the middle
-                    // one, then with the one it selects)
+                // For y > 0 the index is H + m, otherwise (H - 1) - m: its top
+                // bit is the sign decision and every lower bit is the matching
+                // bit of the magnitude index m, inverted when y <= 0.  The
+                // lane masks of those bits are pushed into the record word
+                // from its most significant end: coordinate 7's top bit first.
+                // m: 3 bits, binary search (compare with the middle positive
+                // threshold, then with the one it selects); 2 bits, one compare.
+                uint64_t mk[8 * BITS];  // BITS masks per coordinate
 #pragma unroll
-                    for (int j = 0; j < 8; j++) {
+                for (int j = 7; j >= 0; j--) {
+                    uint64_t *o = mk + (7 - j) * BITS;
+                    const uint64_t pos = __builtin_amdgcn_ballot_w64(y[j] > 0.f);
+                    o[0] = pos;
+                    if constexpr (H == 4) {
                         const bool hi = m[j] > ths[1];
                         const bool lo = m[j] > (hi ? ths[2] : ths[0]);
-                        q[j] = (hi ? 2u : 0u) + (lo ? 1u : 0u);
+                        o[1] = ~(__builtin_amdgcn_ballot_w64(hi) ^ pos);
+                        o[2] = ~(__builtin_amdgcn_ballot_w64(lo) ^ pos);
+                    } else {
+                        o[1] = ~(__builtin_amdgcn_ballot_w64(m[j] > ths[0]) ^ pos);
                     }
-                } else {
-#pragma unroll
-                    for (int j = 0; j < 8; j++)
-                        q[j] = 0;
-#pragma unroll
-                    for (int k = 0; k < H - 1; k++)
-#pragma unroll
-                        for (int j = 0; j < 8; j++)
-                            q[j] = m[j] > ths[k] ? (uint32_t)(k + 1) : q[j];
                 }
+                static_assert(BITS == 2 || BITS == 3, "2 or 3 bits on this branch");
                 uint32_t p = 0;
-#pragma unroll
-                for (int j = 0; j < 8; j++)
-                    p |= (q[j] ^ (y[j] > 0.f ? (uint32_t)H : (uint32_t)(H - 1))) << (BITS * j);
-                store_bits<BITS>(a.rec_out + row0 * RECB + (uint32_t)(r * RECB), sub, p);
+                if constexpr (H == 4) {
+                    p = push_bits12(p, mk);
+                    p = push_bits12(p, mk + 12);
+                } else {
+                    p = push_bits8(p, mk);
+                    p = push_bits8(p, mk + 8);
+                }
+                store_bits<BITS>(a.rec_out + grow * RECB + (uint32_t)(lr * RECB), sub, p);
                 if (sub == 0)
-                    a.norms_out[row0 + r] = rho;
+                    (a.norms_out + grow)[lr] = rho;
             }
             }
         }
         if constexpr (MODE != MODE_QUANTIZE) {
             float o[8];
             rotate_inverse<VAR>(P, yq, o);
-            store_row_chunk<F16>(static_cast<char *>(a.y) + row0 * ROWB + (uint32_t)(r * ROWB + sub * LANEB), o);
+            store_row_chunk<F16>(static_cast<char *>(a.y) + grow * ROWB + (uint32_t)(lr * ROWB + sub * LANEB), o);
         }
     }
 
@@ -528,7 +591,8 @@ struct Stage1 {
 #pragma unroll
         for (int u = 0; u < kTileGroups; u++) {
             const int gl = TAIL ? (int)(min(base + 4 * u + w, groups - 1) - base) : 4 * u + w;
-            fetch(a, row0, row_of<TAIL>(a, row0, gl * VPW + slot), sub, buf[u]);
+            const int64_t grow = row0 + (int64_t)gl * VPW;
+            fetch(a, grow, lane_row<TAIL>(a, grow, slot), sub, buf[u]);
         }
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
@@ -536,10 +600,11 @@ struct Stage1 {
             const int gl = 4 * u + w;
             if (TAIL && base + gl >= groups)
                 break;
-            const int64_t r = row_of<TAIL>(a, row0, gl * VPW + slot);
+            const int64_t grow = row0 + (int64_t)gl * VPW;
+            const int lr = lane_row<TAIL>(a, grow, slot);
             if constexpr (GENERIC_SETS)
-                load_params<PL>(a.params + ((int64_t)set_of(a, row0 + r) * LPV + sub) * PL, P);
-            compute(a, P, lev, thr, lds_levels, lut, buf[u], row0, r, sub);
+                load_params<PL>(a.params + ((int64_t)set_of(a, grow + lr) * LPV + sub) * PL, P);
+            compute(a, P, lev, thr, lds_levels, lut, buf[u], grow, lr, sub);
         }
     }
 };
