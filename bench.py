@@ -134,6 +134,48 @@ def cpu_baseline(variant, d, bits, x_np, rot, levels, seconds: float):
                       f"(Algorithm 1, indices not stored), {threads} threads, {dt:.1f} s"}
 
 
+def kv_append_side(torch, workloads):
+    """isoq_kv_append (quantize K and V into a paged cache, one launch): a
+    decode step (32 sequences x 1 token) and a prefill-sized append (8
+    sequences x 4,096 tokens), 32 heads, d = 128, Fast, 3 bits, fp16, block
+    size 16, one quaternion set per head; each sequence owns randomly placed
+    cache blocks and fills them in order.  Algorithmic bytes per row: the fp16
+    row, the 48-byte record and the 4-byte norm (plus 8 bytes of slot per
+    token)."""
+    import paper_2603_28430_amd as iq
+
+    H, d, bs, bits = 32, 128, 16, 3
+    res = {}
+    for name, n_seq, per_seq in (("decode_32x1", 32, 1), ("prefill_8x4096", 8, 4096)):
+        n_tok = n_seq * per_seq
+        n_blocks = max(4096, 2 * n_tok // bs)
+        print(f"# kv append {name}", file=sys.stderr, flush=True)
+        rot = workloads.rotation_draws("fast", d, H, seed=1)
+        pk = iq.isoq_params_init("fast", d, bits, H, rot=rot)
+        pv = iq.isoq_params_init("fast", d, bits, H, rot=workloads.rotation_draws("fast", d, H, seed=2))
+        # per-head AR(1) token streams, laid out token-major [n_tok, H, d]
+        k = workloads.kv_stream_torch(1, H, n_tok, d, 2, "cuda")[0].transpose(0, 1).contiguous()
+        v = workloads.kv_stream_torch(1, H, n_tok, d, 3, "cuda")[0].transpose(0, 1).contiguous()
+        # sequence b, position t (decode: the next position of a 1,000-token history)
+        blocks_per_seq = (per_seq + 1000 + bs - 1) // bs + 1
+        tables = torch.randperm(n_blocks, device="cuda")[: n_seq * blocks_per_seq].view(n_seq, -1)
+        pos = torch.arange(per_seq, device="cuda") + (1000 if per_seq == 1 else 0)
+        slots = (tables[:, pos // bs] * bs + pos % bs).reshape(-1).to(torch.int64)
+        R = pk.record_bytes
+        caches = [torch.empty((n_blocks, H, bs, R), dtype=torch.uint8, device="cuda") for _ in range(2)]
+        rhos = [torch.empty((n_blocks, H, bs), dtype=torch.float32, device="cuda") for _ in range(2)]
+        fn = lambda i: iq.isoq_kv_append(pk, k, slots, caches[0], rhos[0], pv, v, caches[1], rhos[1])
+        steps = 200 if n_tok < 1000 else 50
+        ms = time_launches(fn, steps, 10, torch, 0.2)
+        b = 2 * n_tok * (H * (d * 2 + R + 4) + 8)
+        res[name] = {"tokens": n_tok, "heads": H, "us_per_call": ms * 1e3, "GBps": b / ms / 1e6,
+                     "frac": b / ms / 1e6 / PEAK_HBM_GBPS}
+        pk.close()
+        pv.close()
+        del k, v, caches, rhos
+    return res
+
+
 def other_configs(measure, entry, torch, np, workloads):
     """Side measurements of the other workloads (their parity is tested in
     tests/test_gpu_full_sizes.py): d = 256 fp16 and d = 512 fp32 round trips
@@ -156,6 +198,7 @@ def other_configs(measure, entry, torch, np, workloads):
         out[name] = res
         del x0, ins, outs_
         torch.cuda.empty_cache()
+    out["kv_append"] = kv_append_side(torch, workloads)
     print("# config kv cache", file=sys.stderr, flush=True)
     B, H, T, d_ = 8, 32, 32768, 128
     kv = [workloads.kv_stream_torch(B, H, T, d_, seed, "cuda").view(B * H * T, d_) for seed in (2, 3)]

@@ -147,6 +147,40 @@ isoq_status isoq_dequantize(const isoq_params *p, int dtype, const uint8_t *idx_
 isoq_status isoq_roundtrip(const isoq_params *p, int dtype, const void *x, int64_t n,
                            int64_t rows_per_set, void *x_hat, void *stream);
 
+/*
+ * isoq_kv_append -- quantize-on-append into a paged K/V cache, for
+ * autoregressive decoding (the fused KV-cache compression the paper names as
+ * its next step, Sec. 10): the new key and value rows are encoded as by
+ * isoq_quantize (Algorithm 1's encoder) and their index records and norms are
+ * written straight into the cache slots of their tokens, in one launch.
+ *
+ *   pk, pv      handles of the K and V quantizers.  They must agree in variant,
+ *               d and bits; each has n_sets == 1 or n_sets == n_heads, and the
+ *               row of (token t, head h) uses set h (resp. set 0).  pv may be
+ *               pk.  pv, v_new, v_idx and v_rho all NULL: keys only.
+ *   dtype       ISOQ_F16 or ISOQ_F32, the element type of k_new and v_new.
+ *   k_new, v_new  device, [n_tokens][n_heads][d] rows (16-byte aligned).
+ *   slot_mapping  device, int64 [n_tokens] (8-byte aligned): cache slot of
+ *               token t; a slot < 0 or >= n_blocks * block_size skips the token
+ *               (padding), its rows are not written.
+ *   k_idx, v_idx  device, [n_blocks][n_heads][block_size][isoq_packed_bytes]
+ *               bytes (4-byte aligned): slot s is position s mod block_size of
+ *               cache block s / block_size; a head's records of one block are
+ *               contiguous.  Record format as in isoq_quantize.
+ *   k_rho, v_rho  device, fp32 [n_blocks][n_heads][block_size].
+ * Limits: n_tokens * n_heads < 2^31, n_blocks * block_size < 2^31, n_heads and
+ * block_size >= 1, and at most 65,535 launch blocks of tokens (n_tokens up to
+ * 4,194,240 at d = 128, 2,097,120 at d = 256, 1,048,560 at d = 512); beyond
+ * that ISOQ_E_UNSUPPORTED.  Distinct tokens must map to distinct slots (a repeated slot
+ * is written by both rows in an unspecified order).  Slots not named are left
+ * untouched.  n_tokens = 0 is a no-op.
+ */
+isoq_status isoq_kv_append(const isoq_params *pk, const isoq_params *pv, int dtype,
+                           const void *k_new, const void *v_new, const int64_t *slot_mapping,
+                           int64_t n_tokens, int n_heads, uint8_t *k_idx, float *k_rho,
+                           uint8_t *v_idx, float *v_rho, int64_t n_blocks, int block_size,
+                           void *stream);
+
 /* Sizes: bytes of one packed index record, ceil(d * bits / 8); raw draws per
  * set for rot_host (Full 8 g4, Fast 4 g4, 2-D g2); exported parameters per set
  * (Full 8 g4, Fast 4 g4, 2-D 2 g2), with g4 = ceil(d/4), g2 = ceil(d/2).

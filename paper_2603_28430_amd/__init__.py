@@ -5,14 +5,15 @@ include/isoquant.h); this package is its Python binding.
 """
 from .isoquant import (ISOQ_F16, ISOQ_F32, ISOQ_FAST, ISOQ_FULL, ISOQ_PLANAR2D, IsoqError,
                        LIB_PATH, Params, isoq_codebook_lloyd, isoq_dequantize,
-                       isoq_export_params_per_set, isoq_packed_bytes, isoq_params_destroy,
+                       isoq_export_params_per_set, isoq_kv_append, isoq_packed_bytes,
+                       isoq_params_destroy,
                        isoq_params_export, isoq_params_info, isoq_params_init, isoq_quantize,
                        isoq_raw_params_per_set, isoq_rotation_draws, isoq_roundtrip,
                        isoq_status_string)
 
 __all__ = [
     "ISOQ_F16", "ISOQ_F32", "ISOQ_FAST", "ISOQ_FULL", "ISOQ_PLANAR2D", "IsoqError", "LIB_PATH",
-    "Params", "isoq_codebook_lloyd", "isoq_dequantize", "isoq_export_params_per_set",
+    "Params", "isoq_codebook_lloyd", "isoq_dequantize", "isoq_export_params_per_set", "isoq_kv_append",
     "isoq_packed_bytes", "isoq_params_destroy", "isoq_params_export", "isoq_params_info",
     "isoq_params_init", "isoq_quantize", "isoq_raw_params_per_set", "isoq_rotation_draws",
     "isoq_roundtrip", "isoq_status_string",

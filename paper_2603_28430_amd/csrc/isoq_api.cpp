@@ -62,18 +62,15 @@ isoq_status check_device(const isoq_params *p)
     return dev == p->device ? ISOQ_OK : ISOQ_E_DEVICE;
 }
 
-isoq_status run(const isoq_params *p, int dtype, int mode, KArgs &a, void *stream)
+// Rows of one block of the stage-1 kernels (a wave holds 512/d rows).
+int64_t rows_per_block(const isoq_params *p)
 {
-    const bool f16 = dtype == ISOQ_F16;
-    const int rows_per_wave = 64 / (p->d / kCoordsPerLane);
-    const int64_t rows_per_block = (int64_t)rows_per_wave * (kBlockThreads / 64) * kTileGroups;
-    const bool generic = p->n_sets > 1 && (a.rows_per_set % rows_per_block) != 0;
-    const void *fn = kernel_for(p->variant, p->d, p->bits, f16, generic, mode);
-    if (!fn)
-        return ISOQ_E_UNSUPPORTED;
-    const int64_t blocks = (a.n + rows_per_block - 1) / rows_per_block;
-    if (blocks > 0x7FFFFFFF)
-        return ISOQ_E_UNSUPPORTED;
+    return (int64_t)(64 / (p->d / kCoordsPerLane)) * (kBlockThreads / 64) * kTileGroups;
+}
+
+// Per-handle kernel arguments: codebook halves, parameters, lookup table.
+void fill_args(const isoq_params *p, KArgs &a)
+{
     const int H = 1 << (p->bits - 1);
     for (int k = 0; k < H; k++)
         a.lev_pos[k] = p->levels[H + k];
@@ -86,15 +83,33 @@ isoq_status run(const isoq_params *p, int dtype, int mode, KArgs &a, void *strea
     a.lut = p->lut_offset ? p->dparams + p->lut_offset : nullptr;
     a.lut_inv_h = p->lut_inv_h;
     a.lut_cells = p->lut_cells;
-    void *args[] = {&a};
-    hipError_t e = hipLaunchKernel(fn, dim3((unsigned)blocks), dim3(kBlockThreads), args, 0,
-                                   static_cast<hipStream_t>(stream));
+}
+
+isoq_status launch(const void *fn, dim3 grid, void **args, void *stream)
+{
+    hipError_t e = hipLaunchKernel(fn, grid, dim3(kBlockThreads), args, 0, static_cast<hipStream_t>(stream));
     if (e != hipSuccess)
         return hip_fail(e, "hipLaunchKernel");
     e = hipGetLastError();
     if (e != hipSuccess)
         return hip_fail(e, "after hipLaunchKernel");
     return ISOQ_OK;
+}
+
+isoq_status run(const isoq_params *p, int dtype, int mode, KArgs &a, void *stream)
+{
+    const bool f16 = dtype == ISOQ_F16;
+    const int64_t rpb = rows_per_block(p);
+    const bool generic = p->n_sets > 1 && (a.rows_per_set % rpb) != 0;
+    const void *fn = kernel_for(p->variant, p->d, p->bits, f16, generic, mode);
+    if (!fn)
+        return ISOQ_E_UNSUPPORTED;
+    const int64_t blocks = (a.n + rpb - 1) / rpb;
+    if (blocks > 0x7FFFFFFF)
+        return ISOQ_E_UNSUPPORTED;
+    fill_args(p, a);
+    void *args[] = {&a};
+    return launch(fn, dim3((unsigned)blocks), args, stream);
 }
 
 }  // namespace
@@ -108,7 +123,7 @@ const char *isoq_status_string(isoq_status s)
     switch (s) {
     case ISOQ_OK: return "ok";
     case ISOQ_E_INVALID: return "invalid argument";
-    case ISOQ_E_UNSUPPORTED: return "unsupported shape (d in {128,256,512}, bits in {2,3,4})";
+    case ISOQ_E_UNSUPPORTED: return "unsupported shape (d in {128,256,512}, bits in {2,3,4}) or size limit";
     case ISOQ_E_NULL: return "null pointer";
     case ISOQ_E_ALIGN: return "misaligned pointer";
     case ISOQ_E_HIP: return "HIP runtime error";
@@ -388,6 +403,65 @@ isoq_status isoq_dequantize(const isoq_params *p, int dtype, const uint8_t *idx_
     a.n = n;
     a.rows_per_set = rows_per_set;
     return run(p, dtype, MODE_DEQUANTIZE, a, stream);
+}
+
+isoq_status isoq_kv_append(const isoq_params *pk, const isoq_params *pv, int dtype,
+                           const void *k_new, const void *v_new, const int64_t *slot_mapping,
+                           int64_t n_tokens, int n_heads, uint8_t *k_idx, float *k_rho,
+                           uint8_t *v_idx, float *v_rho, int64_t n_blocks, int block_size,
+                           void *stream)
+{
+    if (!pk)
+        return ISOQ_E_NULL;
+    if (dtype != ISOQ_F32 && dtype != ISOQ_F16)
+        return ISOQ_E_INVALID;
+    if (n_tokens < 0 || n_heads < 1 || block_size < 1 || n_blocks < 0)
+        return ISOQ_E_INVALID;
+    const bool has_v = pv || v_new || v_idx || v_rho;
+    if (has_v && !(pv && v_new && v_idx && v_rho))
+        return ISOQ_E_NULL;
+    if (has_v && (pv->variant != pk->variant || pv->d != pk->d || pv->bits != pk->bits ||
+                  pv->device != pk->device))
+        return ISOQ_E_INVALID;
+    if ((pk->n_sets != 1 && pk->n_sets != n_heads) || (has_v && pv->n_sets != 1 && pv->n_sets != n_heads))
+        return ISOQ_E_INVALID;
+    if (n_tokens > 0x7FFFFFFF / n_heads || n_blocks > 0x7FFFFFFF / block_size)
+        return ISOQ_E_UNSUPPORTED;
+    if (n_tokens == 0 || n_blocks == 0)
+        return ISOQ_OK;
+    if (!k_new || !slot_mapping || !k_idx || !k_rho)
+        return ISOQ_E_NULL;
+    if (!aligned(k_new, 16) || !aligned(slot_mapping, 8) || !aligned(k_idx, 4) || !aligned(k_rho, 4))
+        return ISOQ_E_ALIGN;
+    if (has_v && (!aligned(v_new, 16) || !aligned(v_idx, 4) || !aligned(v_rho, 4)))
+        return ISOQ_E_ALIGN;
+    isoq_status st = check_device(pk);
+    if (st != ISOQ_OK)
+        return st;
+    // one kernel for both tensors; block (x, y, z) = (head, token range, K|V)
+    const void *fn = kernel_for(pk->variant, pk->d, pk->bits, dtype == ISOQ_F16, false, MODE_APPEND);
+    if (!fn)
+        return ISOQ_E_UNSUPPORTED;
+    const int64_t blocks = (n_tokens + rows_per_block(pk) - 1) / rows_per_block(pk);
+    if (blocks > 65535)
+        return ISOQ_E_UNSUPPORTED;
+    KArgs ak{}, av{};
+    for (int t = 0; t < (has_v ? 2 : 1); t++) {
+        KArgs &a = t == 0 ? ak : av;
+        fill_args(t == 0 ? pk : pv, a);
+        a.x = t == 0 ? k_new : v_new;
+        a.rec_out = t == 0 ? k_idx : v_idx;
+        a.norms_out = t == 0 ? k_rho : v_rho;
+        a.n = n_tokens;
+        a.rows_per_set = 1;
+        a.slots = slot_mapping;
+        a.n_slots = n_blocks * block_size;
+        a.n_heads = (uint32_t)n_heads;
+        a.block_size = (uint32_t)block_size;
+        a.div_block = make_fastdiv((uint32_t)block_size);
+    }
+    void *args[] = {&ak, &av};
+    return launch(fn, dim3((unsigned)n_heads, (unsigned)blocks, has_v ? 2 : 1), args, stream);
 }
 
 }  // extern "C"

@@ -9,7 +9,7 @@
 
 namespace isoq {
 
-enum Mode { MODE_ROUNDTRIP = 0, MODE_QUANTIZE = 1, MODE_DEQUANTIZE = 2 };
+enum Mode { MODE_ROUNDTRIP = 0, MODE_QUANTIZE = 1, MODE_DEQUANTIZE = 2, MODE_APPEND = 3 };
 enum Variant { VAR_FULL = 0, VAR_FAST = 1, VAR_PLANAR2D = 2 };
 
 // Every lane owns 8 consecutive coordinates of a row (two quaternion blocks or
@@ -25,6 +25,25 @@ constexpr int kTileGroups = 4;
 // matrices M = L(q_L) R(conj q_R) row-major, Fast the two unit quaternions,
 // 2-D (cos, sin) of the four pairs.
 inline int params_per_lane(int variant) { return variant == VAR_FULL ? 32 : 8; }
+
+// Division of 32-bit unsigned integers by a run-time constant d >= 1 through
+// one multiply-high, two shifts and two adds (Granlund and Montgomery,
+// "Division by invariant integers using multiplication", PLDI 1994, Fig. 4.1):
+// t = mulhi(n, m), n / d = (t + ((n - t) >> s1)) >> s2, with
+// l = ceil(log2 d), m = floor(2^32 (2^l - d) / d) + 1, s1 = min(l, 1),
+// s2 = max(l - 1, 0).  Exact for every n < 2^32.
+struct FastDiv {
+    uint32_t m, s1, s2;
+};
+
+inline FastDiv make_fastdiv(uint32_t d)
+{
+    int l = 0;
+    while ((1ull << l) < d)
+        l++;
+    const uint64_t m = ((1ull << 32) * ((1ull << l) - d)) / d + 1;
+    return FastDiv{(uint32_t)m, (uint32_t)(l < 1 ? l : 1), (uint32_t)(l > 1 ? l - 1 : 0)};
+}
 
 // Kernel arguments, passed by value (they land in scalar registers).
 struct KArgs {
@@ -45,6 +64,11 @@ struct KArgs {
     float lev_pos[8];        // c_{K/2} .. c_{K-1}   (positive half of the codebook)
     float thr_pos[8];        // t_{K/2} .. t_{K-2}   (positive thresholds; t_{K/2-1} = 0)
     float lev_all[16];       // c_0 .. c_{K-1}
+    // append into a paged cache (n = tokens; the head is blockIdx.y)
+    const int64_t *slots;    // [n_tokens] cache slot of each token
+    int64_t n_slots;         // cache capacity in slots (n_blocks * block_size)
+    uint32_t n_heads, block_size;
+    FastDiv div_block;
 };
 
 // Kernel entry for (variant, d, bits, fp16 rows?, generic set indexing?, mode),

@@ -4,6 +4,9 @@
 //   MODE_ROUNDTRIP   x -> x_hat fused (norm, rotation, quantizer, inverse)
 //   MODE_QUANTIZE    x -> packed indices + rho
 //   MODE_DEQUANTIZE  packed indices + rho -> x_hat
+//   MODE_APPEND      quantize (token, head) rows into the slots of a paged
+//                    K/V cache: blockIdx.x is the head, blockIdx.y the token
+//                    range, blockIdx.z selects K or V
 //
 // Mapping.  A lane owns 8 consecutive coordinates of one row: 16 bytes of
 // fp16 (one global_load_dwordx4) or 32 bytes of fp32 (two).  Those 8
@@ -54,6 +57,12 @@ template <int CTRL>
 __device__ __forceinline__ uint32_t dpp_u(uint32_t v)
 {
     return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
+}
+
+__device__ __forceinline__ uint32_t fast_div(uint32_t n, const FastDiv &f)
+{
+    const uint32_t t = __umulhi(n, f.m);
+    return (t + ((n - t) >> f.s1)) >> f.s2;
 }
 
 // Sum over the LPV lanes of a row; every lane of the row gets the same bits.
@@ -269,18 +278,20 @@ __device__ __forceinline__ void load_params(const float *base, float P[PL])
 // (2 bits), a 32-bit word (4 bits), or 24 bits at byte 3 sub (3 bits), which
 // the four lanes of a DPP quad merge into three aligned words.
 template <int BITS>
-__device__ __forceinline__ void store_bits(uint8_t *rec, int sub, uint32_t p)
+__device__ __forceinline__ void store_bits(uint8_t *rec, int sub, uint32_t p, bool ok)
 {
     if constexpr (BITS == 2) {
-        reinterpret_cast<uint16_t *>(rec)[sub] = (uint16_t)p;
+        if (ok)
+            reinterpret_cast<uint16_t *>(rec)[sub] = (uint16_t)p;
     } else if constexpr (BITS == 4) {
-        reinterpret_cast<uint32_t *>(rec)[sub] = p;
+        if (ok)
+            reinterpret_cast<uint32_t *>(rec)[sub] = p;
     } else {
         // lane k of a quad holds bits [24 k, 24 k + 24) of 96; lanes 0..2
         // write word k = p_k >> 8 k | p_(k+1) << (24 - 8 k)
         const uint32_t nb = dpp_u<DPP_QUAD_1233>(p);  // bits of the next lane in the quad
         const int k = sub & 3;
-        if (k < 3)
+        if (ok && k < 3)
             reinterpret_cast<uint32_t *>(rec)[3 * (sub >> 2) + k] = (p >> (8 * k)) | (nb << (24 - 8 * k));
     }
 }
@@ -370,6 +381,7 @@ struct Stage1 {
     static constexpr int64_t RECB = (int64_t)D * BITS / 8;       // bytes per index record
     static constexpr int LANEB = F16 ? 16 : 32;         // row bytes per lane
     static constexpr bool kUseLut = BITS == 4;           // magnitude lookup table
+    static constexpr bool kEncode = MODE == MODE_QUANTIZE || MODE == MODE_APPEND;  // records out
 
     struct In {
         Raw<F16> raw;
@@ -396,6 +408,12 @@ struct Stage1 {
         if constexpr (MODE == MODE_DEQUANTIZE) {
             in.bits = load_bits<BITS>(a.rec_in + grow * RECB + (uint32_t)(lr * RECB), sub);
             in.rho = (a.norms_in + grow)[lr];
+        } else if constexpr (MODE == MODE_APPEND) {
+            // token grow + lr, head blockIdx.x of rows [n_tokens][n_heads][d]
+            const int64_t tstride = (int64_t)a.n_heads * ROWB;
+            load_row_chunk<F16>(static_cast<const char *>(a.x) + grow * tstride + (int64_t)blockIdx.x * ROWB +
+                                    (uint32_t)(lr * (uint32_t)tstride + sub * LANEB),
+                                in.raw);
         } else {
             load_row_chunk<F16>(static_cast<const char *>(a.x) + grow * ROWB + (uint32_t)(lr * ROWB + sub * LANEB),
                                 in.raw);
@@ -443,11 +461,8 @@ struct Stage1 {
                         p |= (q ^ (y[j] > 0.f ? (uint32_t)H : (uint32_t)(H - 1))) << (BITS * j);
                     }
                 }
-                if constexpr (MODE == MODE_QUANTIZE) {
-                    store_bits<BITS>(a.rec_out + grow * RECB + (uint32_t)(lr * RECB), sub, p);
-                    if (sub == 0)
-                        (a.norms_out + grow)[lr] = rho;
-                }
+                if constexpr (kEncode)
+                    emit(a, grow, lr, sub, p, rho);
             } else {
             float ths[H > 1 ? H - 1 : 1];
 #pragma unroll
@@ -507,16 +522,40 @@ struct Stage1 {
                     p = push_bits8(p, mk);
                     p = push_bits8(p, mk + 8);
                 }
-                store_bits<BITS>(a.rec_out + grow * RECB + (uint32_t)(lr * RECB), sub, p);
-                if (sub == 0)
-                    (a.norms_out + grow)[lr] = rho;
+                emit(a, grow, lr, sub, p, rho);
             }
             }
         }
-        if constexpr (MODE != MODE_QUANTIZE) {
+        if constexpr (!kEncode) {
             float o[8];
             rotate_inverse<VAR>(P, yq, o);
             store_row_chunk<F16>(static_cast<char *>(a.y) + grow * ROWB + (uint32_t)(lr * ROWB + sub * LANEB), o);
+        }
+    }
+
+    // Write one row's index record and norm: to row grow + lr (quantize), or
+    // to the cache slot of token grow + lr for head blockIdx.x (append): slot
+    // s is position s mod block_size of cache block s / block_size, and a
+    // cache block holds [n_heads][block_size] records.  A skipped slot writes
+    // nothing; the quad exchange inside store_bits runs on every lane either
+    // way.
+    __device__ static __forceinline__ void emit(const KArgs &a, int64_t grow, int lr, int sub,
+                                                uint32_t p, float rho)
+    {
+        if constexpr (MODE == MODE_QUANTIZE) {
+            store_bits<BITS>(a.rec_out + grow * RECB + (uint32_t)(lr * RECB), sub, p, true);
+            if (sub == 0)
+                (a.norms_out + grow)[lr] = rho;
+        } else {
+            const uint32_t h = blockIdx.x;
+            const int64_t s = (a.slots + grow)[lr];
+            const bool ok = s >= 0 && s < a.n_slots;
+            const uint32_t su = ok ? (uint32_t)s : 0u;
+            const uint32_t blk = fast_div(su, a.div_block);
+            const int64_t crow = ((int64_t)blk * a.n_heads + h) * a.block_size + (su - blk * a.block_size);
+            store_bits<BITS>(a.rec_out + crow * RECB, sub, p, ok);
+            if (ok && sub == 0)
+                a.norms_out[crow] = rho;
         }
     }
 
@@ -533,7 +572,10 @@ struct Stage1 {
         const int slot = lane / LPV;
         const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
         const int64_t groups = (a.n + VPW - 1) / VPW;
-        const int64_t base = (int64_t)blockIdx.x * (kBlockThreads / 64) * kTileGroups;
+        // append: blocks (head, token range) are dispatched head-fastest, so
+        // the blocks in flight read all heads of the same tokens, one span
+        const int64_t base = (int64_t)(MODE == MODE_APPEND ? blockIdx.y : blockIdx.x) * (kBlockThreads / 64) *
+                             kTileGroups;
 
         // 1. block-wide tables: the codebook (dequantize) and the rotation
         //    parameters of the block's set, staged through LDS
@@ -549,7 +591,10 @@ struct Stage1 {
         }
         float P[PL];
         if constexpr (!GENERIC_SETS) {
-            const int64_t set = a.n_sets > 1 ? (base * VPW / a.rows_per_set) % a.n_sets : 0;
+            // append: the block's head (every set is a head, or there is one)
+            const int64_t set = a.n_sets <= 1           ? 0
+                                : MODE == MODE_APPEND ? (int64_t)blockIdx.x
+                                                      : (base * VPW / a.rows_per_set) % a.n_sets;
             const u32x4 *s4 = reinterpret_cast<const u32x4 *>(a.params + set * (LPV * PL));
             u32x4 *d4 = reinterpret_cast<u32x4 *>(lds_params);
             for (int i = threadIdx.x; i < LPV * PL / 4; i += kBlockThreads)
@@ -619,10 +664,24 @@ __global__ __launch_bounds__(kBlockThreads) void stage1_kernel(const KArgs a)
     S::run(a, lds_levels, lds_params, lds_lut);
 }
 
+// K and V in one launch: blockIdx.z = 0 encodes the keys, 1 the values;
+// blockIdx.x is the head, whose parameter set the block stages once, and
+// blockIdx.y the range of tokens.
+template <int VAR, int D, int BITS, bool F16>
+__global__ __launch_bounds__(kBlockThreads) void append_kernel(const KArgs k, const KArgs v)
+{
+    using S = Stage1<VAR, D, BITS, F16, MODE_APPEND, false>;
+    __shared__ float lds_levels[16];
+    __shared__ __align__(16) float lds_params[S::LPV * S::PL];
+    __shared__ __align__(16) LutEntry lds_lut[S::kUseLut ? kLutMaxCells : 1];
+    S::run(blockIdx.z == 0 ? k : v, lds_levels, lds_params, lds_lut);
+}
+
 template <int VAR, int D, int BITS, bool F16, bool GEN>
 const void *pick_mode(int mode)
 {
     switch (mode) {
+    case MODE_APPEND: return GEN ? nullptr : reinterpret_cast<const void *>(&append_kernel<VAR, D, BITS, F16>);
     case MODE_ROUNDTRIP: return reinterpret_cast<const void *>(&stage1_kernel<VAR, D, BITS, F16, MODE_ROUNDTRIP, GEN>);
     case MODE_QUANTIZE: return reinterpret_cast<const void *>(&stage1_kernel<VAR, D, BITS, F16, MODE_QUANTIZE, GEN>);
     case MODE_DEQUANTIZE: return reinterpret_cast<const void *>(&stage1_kernel<VAR, D, BITS, F16, MODE_DEQUANTIZE, GEN>);

@@ -52,6 +52,7 @@ def _load():
     L.isoq_quantize.argtypes = [vp, c_int, vp, i64, i64, vp, vp, vp]
     L.isoq_dequantize.argtypes = [vp, c_int, vp, vp, i64, i64, vp, vp]
     L.isoq_roundtrip.argtypes = [vp, c_int, vp, i64, i64, vp, vp]
+    L.isoq_kv_append.argtypes = [vp, vp, c_int, vp, vp, vp, i64, c_int, vp, vp, vp, vp, i64, c_int, vp]
     L.isoq_packed_bytes.argtypes = [c_int, c_int]
     L.isoq_packed_bytes.restype = ctypes.c_size_t
     L.isoq_raw_params_per_set.argtypes = [c_int, c_int]
@@ -65,7 +66,7 @@ def _load():
     L.isoq_last_hip_error.argtypes = []
     L.isoq_last_hip_error.restype = ctypes.c_char_p
     for f in ("isoq_params_init", "isoq_params_destroy", "isoq_params_export", "isoq_params_info",
-              "isoq_quantize", "isoq_dequantize", "isoq_roundtrip", "isoq_codebook_lloyd",
+              "isoq_quantize", "isoq_dequantize", "isoq_roundtrip", "isoq_kv_append", "isoq_codebook_lloyd",
               "isoq_rotation_draws"):
         getattr(L, f).restype = c_int
     return L
@@ -246,3 +247,42 @@ def isoq_dequantize(p: Params, idx_packed, norms, dtype=None, rows_per_set: int 
                                ctypes.c_void_p(norms.data_ptr()), n, int(rows_per_set),
                                ctypes.c_void_p(x_hat.data_ptr()), _stream_ptr(stream)), "isoq_dequantize")
     return x_hat
+
+
+def _ptr(t):
+    return ctypes.c_void_p(None if t is None else t.data_ptr())
+
+
+def isoq_kv_append(pk: Params, k_new, slot_mapping, k_idx, k_rho, pv: Params = None, v_new=None,
+                   v_idx=None, v_rho=None, stream=None):
+    """Quantize new rows k_new (and v_new) [n_tokens, n_heads, d] into paged caches
+    k_idx (v_idx) [n_blocks, n_heads, block_size, record_bytes] uint8 and k_rho
+    (v_rho) [n_blocks, n_heads, block_size] fp32 at the slots slot_mapping
+    [n_tokens] int64 (see include/isoquant.h)."""
+    torch = _torch()
+    if k_new.dim() != 3 or k_idx.dim() != 4 or k_rho.dim() != 3:
+        raise ValueError("k_new [n_tokens, n_heads, d], k_idx [n_blocks, n_heads, block_size, R], "
+                         "k_rho [n_blocks, n_heads, block_size]")
+    n_tokens, n_heads, d = k_new.shape
+    n_blocks, nh, block_size, rb = k_idx.shape
+    if d != pk.d or nh != n_heads or rb != pk.record_bytes or tuple(k_rho.shape) != (n_blocks, nh, block_size):
+        raise ValueError("cache shapes do not match the rows and the handle")
+    if slot_mapping.dtype != torch.int64 or slot_mapping.numel() != n_tokens:
+        raise ValueError("slot_mapping must be int64 [n_tokens]")
+    if k_idx.dtype != torch.uint8 or k_rho.dtype != torch.float32:
+        raise TypeError("k_idx uint8, k_rho float32")
+    ts = [k_new, slot_mapping, k_idx, k_rho]
+    if v_new is not None:
+        if pv is None or v_idx is None or v_rho is None:
+            raise ValueError("v_new needs pv, v_idx and v_rho")
+        if (tuple(v_new.shape) != tuple(k_new.shape) or tuple(v_idx.shape) != tuple(k_idx.shape)
+                or tuple(v_rho.shape) != tuple(k_rho.shape) or v_new.dtype != k_new.dtype):
+            raise ValueError("V tensors must have the shapes and dtype of the K tensors")
+        ts += [v_new, v_idx, v_rho]
+    for t in ts:
+        if not t.is_cuda or not t.is_contiguous():
+            raise ValueError("tensors must be contiguous and on the GPU")
+    _check(lib.isoq_kv_append(pk.handle, None if pv is None else pv.handle, _dtype_code(k_new.dtype),
+                              _ptr(k_new), _ptr(v_new), _ptr(slot_mapping), int(n_tokens), int(n_heads),
+                              _ptr(k_idx), _ptr(k_rho), _ptr(v_idx), _ptr(v_rho), int(n_blocks),
+                              int(block_size), _stream_ptr(stream)), "isoq_kv_append")
