@@ -278,6 +278,22 @@ def dequantize(variant, d: int, bits: int, rot, levels, idx, rho, n_sets: int = 
     return xh
 
 
+# --- attention logits against quantized keys --------------------------------------
+def attention_scores(variant, d: int, bits: int, rot, levels, q, idx, rho, scale: float = 1.0,
+                     set_index: int = 0):
+    """Attention logits of queries against quantized keys, by definition:
+    s[g, t] = scale * <q_g, xhat_t>, where xhat_t = rho_t * T^{-1}(c[idx_t]) is
+    the oracle's dequantization (Algorithm 1, last steps) of key t with the
+    rotation set ``set_index``.  q: [G, d] (or [d]); idx: unpacked [n, padded]
+    indices; rho: [n].  Returns float64 [G, n] (or [n])."""
+    v = _variant(variant)
+    per = raw_params_per_set(v, d)
+    rot_s = _d(rot).reshape(-1)[set_index * per:(set_index + 1) * per]
+    xh = dequantize(v, d, bits, rot_s, levels, idx, rho)
+    qd = _d(q)
+    return scale * (qd @ xh.T)
+
+
 # --- packing -------------------------------------------------------------------------
 def record_bytes(m: int, bits: int) -> int:
     return int(lib().orc_record_bytes(int(m), int(bits)))
