@@ -176,6 +176,36 @@ def kv_append_side(torch, workloads):
     return res
 
 
+def kv_scores_side(torch, workloads):
+    """isoq_kv_scores: attention logits of one decoding query per head against
+    a paged cache of quantized keys, 8 sequences x 32,768 positions x 32 heads,
+    d = 128, Fast, 3 bits, block size 16, blocks placed at random.  The cache
+    content is random index bytes and norms (the cost does not depend on it).
+    Algorithmic bytes per key: its 48-byte record, 4-byte norm and 4-byte
+    logit."""
+    import paper_2603_28430_amd as iq
+
+    B, H, T, d, bs, bits = 8, 32, 32768, 128, 16, 3
+    print("# kv scores", file=sys.stderr, flush=True)
+    p = iq.isoq_params_init("fast", d, bits, H, rot=workloads.rotation_draws("fast", d, H, seed=1))
+    nb = B * T // bs
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(4)
+    rec = torch.randint(0, 256, (nb, H, bs, p.record_bytes), dtype=torch.uint8, device="cuda", generator=gen)
+    rho = torch.rand((nb, H, bs), device="cuda", generator=gen) + 0.5
+    table = torch.randperm(nb, device="cuda", generator=gen).to(torch.int32).view(B, T // bs)
+    lens = torch.full((B,), T, dtype=torch.int32, device="cuda")
+    q = torch.randn((B, H, d), device="cuda", generator=gen).to(torch.float16)
+    out = torch.empty((B, H, T), dtype=torch.float32, device="cuda")
+    fn = lambda i: iq.isoq_kv_scores(p, q, rec, rho, table, lens, 0.0884, max_len=T, scores=out)
+    ms = time_launches(fn, 50, 5, torch, 0.2)
+    keys = B * H * T
+    b = keys * (p.record_bytes + 4 + 4)
+    p.close()
+    return {"shape": [B, H, T, d], "us_per_call": ms * 1e3, "keys_per_s": keys / (ms / 1e3),
+            "GBps": b / ms / 1e6, "frac": b / ms / 1e6 / PEAK_HBM_GBPS}
+
+
 def other_configs(measure, entry, torch, np, workloads):
     """Side measurements of the other workloads (their parity is tested in
     tests/test_gpu_full_sizes.py): d = 256 fp16 and d = 512 fp32 round trips
@@ -199,6 +229,7 @@ def other_configs(measure, entry, torch, np, workloads):
         del x0, ins, outs_
         torch.cuda.empty_cache()
     out["kv_append"] = kv_append_side(torch, workloads)
+    out["kv_scores"] = kv_scores_side(torch, workloads)
     print("# config kv cache", file=sys.stderr, flush=True)
     B, H, T, d_ = 8, 32, 32768, 128
     kv = [workloads.kv_stream_torch(B, H, T, d_, seed, "cuda").view(B * H * T, d_) for seed in (2, 3)]

@@ -181,6 +181,41 @@ isoq_status isoq_kv_append(const isoq_params *pk, const isoq_params *pv, int dty
                            uint8_t *v_idx, float *v_rho, int64_t n_blocks, int block_size,
                            void *stream);
 
+/*
+ * isoq_kv_scores -- attention logits of decoding queries against the keys of
+ * a paged cache written by isoq_kv_append, without dequantizing the keys.  A
+ * key's reconstruction is rho T^{-1}(c[idx]) and T is orthogonal (Prop. 1), so
+ * <q, k_hat> = rho <T q, c[idx]>: each query is rotated once and the logits
+ * are sums of table lookups over the packed index records.
+ *
+ *   pk          the K quantizer (n_sets == 1 or n_sets == n_kv_heads; key head h
+ *               uses set h, resp. 0).
+ *   dtype       ISOQ_F16 or ISOQ_F32, the element type of q.
+ *   q           device, [n_seqs][n_q_heads][d] (16-byte aligned).  Query head hq
+ *               reads key head hq / (n_q_heads / n_kv_heads) (grouped-query
+ *               attention; n_q_heads must be a multiple of n_kv_heads).
+ *   k_idx, k_rho  the cache, laid out as in isoq_kv_append (k_idx 16-byte
+ *               aligned), n_blocks cache blocks of block_size positions.
+ *   block_table device, int32 [n_seqs][max_blocks_per_seq]: cache block of the
+ *               sequence's positions [j * block_size, (j+1) * block_size).
+ *   seq_lens    device, int32 [n_seqs]: positions of each sequence.
+ *   scores      device, fp32 [n_seqs][n_q_heads][max_len]:
+ *               scores[s][hq][t] = scale * <q[s][hq], k_hat(s, t)> for
+ *               t < min(seq_lens[s], max_len, max_blocks_per_seq * block_size).
+ *               Other positions, and positions whose block id lies outside
+ *               [0, n_blocks), are not written.
+ * Limits: n_seqs <= 65535, max_blocks_per_seq * block_size < 2^31, and the
+ * tables of one key head's query group must fit in LDS: group * (d/F * 2^(F
+ * bits) + d) * 4 bytes with F = 2 for 2 and 3 bits, F = 1 for 4 bits
+ * (ISOQ_E_UNSUPPORTED otherwise; e.g. at d = 128, 3 bits, 16.9 KB per query
+ * head).  Logits are accumulated in fp32.
+ */
+isoq_status isoq_kv_scores(const isoq_params *pk, int dtype, const void *q, int n_seqs,
+                           int n_q_heads, int n_kv_heads, const uint8_t *k_idx, const float *k_rho,
+                           int64_t n_blocks, int block_size, const int32_t *block_table,
+                           int max_blocks_per_seq, const int32_t *seq_lens, float scale,
+                           float *scores, int64_t max_len, void *stream);
+
 /* Sizes: bytes of one packed index record, ceil(d * bits / 8); raw draws per
  * set for rot_host (Full 8 g4, Fast 4 g4, 2-D g2); exported parameters per set
  * (Full 8 g4, Fast 4 g4, 2-D 2 g2), with g4 = ceil(d/4), g2 = ceil(d/2).

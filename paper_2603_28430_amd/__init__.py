@@ -5,7 +5,8 @@ include/isoquant.h); this package is its Python binding.
 """
 from .isoquant import (ISOQ_F16, ISOQ_F32, ISOQ_FAST, ISOQ_FULL, ISOQ_PLANAR2D, IsoqError,
                        LIB_PATH, Params, isoq_codebook_lloyd, isoq_dequantize,
-                       isoq_export_params_per_set, isoq_kv_append, isoq_packed_bytes,
+                       isoq_export_params_per_set, isoq_kv_append, isoq_kv_scores,
+                       isoq_packed_bytes,
                        isoq_params_destroy,
                        isoq_params_export, isoq_params_info, isoq_params_init, isoq_quantize,
                        isoq_raw_params_per_set, isoq_rotation_draws, isoq_roundtrip,
@@ -14,6 +15,7 @@ from .isoquant import (ISOQ_F16, ISOQ_F32, ISOQ_FAST, ISOQ_FULL, ISOQ_PLANAR2D, 
 __all__ = [
     "ISOQ_F16", "ISOQ_F32", "ISOQ_FAST", "ISOQ_FULL", "ISOQ_PLANAR2D", "IsoqError", "LIB_PATH",
     "Params", "isoq_codebook_lloyd", "isoq_dequantize", "isoq_export_params_per_set", "isoq_kv_append",
+    "isoq_kv_scores",
     "isoq_packed_bytes", "isoq_params_destroy", "isoq_params_export", "isoq_params_info",
     "isoq_params_init", "isoq_quantize", "isoq_raw_params_per_set", "isoq_rotation_draws",
     "isoq_roundtrip", "isoq_status_string",

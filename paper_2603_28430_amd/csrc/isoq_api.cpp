@@ -464,4 +464,81 @@ isoq_status isoq_kv_append(const isoq_params *pk, const isoq_params *pv, int dty
     return launch(fn, dim3((unsigned)n_heads, (unsigned)blocks, has_v ? 2 : 1), args, stream);
 }
 
+isoq_status isoq_kv_scores(const isoq_params *pk, int dtype, const void *q, int n_seqs,
+                           int n_q_heads, int n_kv_heads, const uint8_t *k_idx, const float *k_rho,
+                           int64_t n_blocks, int block_size, const int32_t *block_table,
+                           int max_blocks_per_seq, const int32_t *seq_lens, float scale,
+                           float *scores, int64_t max_len, void *stream)
+{
+    if (!pk)
+        return ISOQ_E_NULL;
+    if (dtype != ISOQ_F32 && dtype != ISOQ_F16)
+        return ISOQ_E_INVALID;
+    if (n_seqs < 0 || n_q_heads < 1 || n_kv_heads < 1 || n_q_heads % n_kv_heads != 0 ||
+        block_size < 1 || n_blocks < 0 || max_blocks_per_seq < 0 || max_len < 0 || !std::isfinite(scale))
+        return ISOQ_E_INVALID;
+    if (pk->n_sets != 1 && pk->n_sets != n_kv_heads)
+        return ISOQ_E_INVALID;
+    const int64_t max_pos = std::min<int64_t>(max_len, (int64_t)max_blocks_per_seq * block_size);
+    if (n_seqs > 65535 || (int64_t)max_blocks_per_seq * block_size > 0x7FFFFFFF ||
+        (max_pos + kScoreChunk - 1) / kScoreChunk > 65535)
+        return ISOQ_E_UNSUPPORTED;
+    if (n_seqs == 0 || max_pos == 0 || n_blocks == 0)
+        return ISOQ_OK;
+    if (!q || !k_idx || !k_rho || !block_table || !seq_lens || !scores)
+        return ISOQ_E_NULL;
+    if (!aligned(q, 16) || !aligned(k_idx, 16) || !aligned(k_rho, 4) || !aligned(block_table, 4) ||
+        !aligned(seq_lens, 4) || !aligned(scores, 4))
+        return ISOQ_E_ALIGN;
+    isoq_status st = check_device(pk);
+    if (st != ISOQ_OK)
+        return st;
+    const int group = n_q_heads / n_kv_heads;
+    const ScoreKernel sk = score_kernel_for(pk->variant, pk->d, pk->bits, dtype == ISOQ_F16, group);
+    if (!sk.fn)
+        return ISOQ_E_UNSUPPORTED;
+    const void *fn = sk.fn;
+    const size_t lds = sk.dyn_lds;
+    int lds_max = 0;
+    hipError_t e = hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, pk->device);
+    if (e != hipSuccess)
+        return hip_fail(e, "hipDeviceGetAttribute");
+    if (lds > (size_t)lds_max)
+        return ISOQ_E_UNSUPPORTED;
+    if (lds > 65536) {
+        e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess)
+            return hip_fail(e, "hipFuncSetAttribute");
+    }
+    SArgs a{};
+    a.q = q;
+    a.k_idx = k_idx;
+    a.k_rho = k_rho;
+    a.block_table = block_table;
+    a.seq_lens = seq_lens;
+    a.scores = scores;
+    a.params = pk->dparams;
+    a.max_len = max_len;
+    a.n_blocks = n_blocks;
+    a.n_q_heads = n_q_heads;
+    a.n_kv_heads = n_kv_heads;
+    a.group = group;
+    a.block_size = block_size;
+    a.max_blocks = max_blocks_per_seq;
+    a.n_sets = pk->n_sets;
+    a.scale = scale;
+    a.div_block = make_fastdiv((uint32_t)block_size);
+    for (int k = 0; k < (1 << pk->bits); k++)
+        a.lev_all[k] = pk->levels[k];
+    void *args[] = {&a};
+    const dim3 grid((unsigned)n_kv_heads, (unsigned)((max_pos + kScoreChunk - 1) / kScoreChunk), (unsigned)n_seqs);
+    e = hipLaunchKernel(fn, grid, dim3(256), args, lds, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess)
+        return hip_fail(e, "hipLaunchKernel");
+    e = hipGetLastError();
+    if (e != hipSuccess)
+        return hip_fail(e, "after hipLaunchKernel");
+    return ISOQ_OK;
+}
+
 }  // extern "C"

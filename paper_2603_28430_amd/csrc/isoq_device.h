@@ -1,0 +1,252 @@
+// Device helpers shared by the library's kernels (isoq_kernels.hip,
+// isoq_scores.hip): vector types, cross-lane reductions, row chunk loads and
+// stores, the block rotations of Sec. 5.2-5.4 on a lane's 8 coordinates, and
+// division by run-time constants.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "isoq_internal.h"
+
+namespace isoq {
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+
+constexpr float kEps = 1e-12f;
+
+// DPP controls (data-parallel primitives on 16-lane rows)
+constexpr int DPP_QUAD_1032 = 0xB1;   // quad_perm [1,0,3,2]
+constexpr int DPP_QUAD_2301 = 0x4E;   // quad_perm [2,3,0,1]
+constexpr int DPP_QUAD_1233 = 0xF9;   // quad_perm [1,2,3,3]
+constexpr int DPP_ROW_MIRROR = 0x140;
+constexpr int DPP_ROW_HALF_MIRROR = 0x141;
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v)
+{
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u(uint32_t v)
+{
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
+}
+
+__device__ __forceinline__ uint32_t fast_div(uint32_t n, const FastDiv &f)
+{
+    const uint32_t t = __umulhi(n, f.m);
+    return (t + ((n - t) >> f.s1)) >> f.s2;
+}
+
+// Sum over the LPV lanes of a row; every lane of the row gets the same bits.
+template <int LPV>
+__device__ __forceinline__ float row_sum(float v)
+{
+    v += dpp_f<DPP_QUAD_1032>(v);
+    v += dpp_f<DPP_QUAD_2301>(v);
+    v += dpp_f<DPP_ROW_HALF_MIRROR>(v);
+    v += dpp_f<DPP_ROW_MIRROR>(v);
+    // across 16-lane rows: v_permlane16_swap exchanges odd rows of its first
+    // operand with even rows of its second, v_permlane32_swap the upper half
+    // of the first with the lower half of the second; with both operands v,
+    // the two results are (v of row r, v of row r ^ 1) (resp. r ^ 2) in the
+    // same order on both rows, so every lane adds the same two values
+    if constexpr (LPV >= 32) {
+        const auto s = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+        v = __uint_as_float(s[0]) + __uint_as_float(s[1]);
+    }
+    if constexpr (LPV >= 64) {
+        const auto s = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+        v = __uint_as_float(s[0]) + __uint_as_float(s[1]);
+    }
+    return v;
+}
+
+template <bool F16>
+struct Raw {
+    u32x4 w[F16 ? 1 : 2];
+};
+
+template <bool F16>
+__device__ __forceinline__ void load_row_chunk(const char *p, Raw<F16> &r)
+{
+    const u32x4 *q = reinterpret_cast<const u32x4 *>(p);
+    r.w[0] = __builtin_nontemporal_load(q);
+    if constexpr (!F16)
+        r.w[1] = __builtin_nontemporal_load(q + 1);
+}
+
+template <bool F16>
+__device__ __forceinline__ void unpack(const Raw<F16> &r, float x[8])
+{
+    // Vector elements are copied to scalars before __builtin_bit_cast: applied
+    // to an ext_vector element lvalue directly, it reads element 0 every time.
+    if constexpr (F16) {
+#pragma unroll
+        for (int k = 0; k < 4; k++) {
+            const uint32_t e = r.w[0][k];
+            const f16x2 h = __builtin_bit_cast(f16x2, e);
+            x[2 * k] = (float)h.x;
+            x[2 * k + 1] = (float)h.y;
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k < 4; k++) {
+            const uint32_t e0 = r.w[0][k], e1 = r.w[1][k];
+            x[k] = __uint_as_float(e0);
+            x[4 + k] = __uint_as_float(e1);
+        }
+    }
+}
+
+template <bool F16>
+__device__ __forceinline__ float sum_squares(const Raw<F16> &r, const float x[8])
+{
+    float s = 0.f;
+    if constexpr (F16) {
+#pragma unroll
+        for (int k = 0; k < 4; k++) {
+            const uint32_t e = r.w[0][k];
+            const f16x2 h = __builtin_bit_cast(f16x2, e);
+            s = __builtin_amdgcn_fdot2(h, h, s, false);
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k < 8; k++)
+            s = fmaf(x[k], x[k], s);
+    }
+    return s;
+}
+
+template <bool F16>
+__device__ __forceinline__ void store_row_chunk(char *p, const float o[8])
+{
+    u32x4 *q = reinterpret_cast<u32x4 *>(p);
+    if constexpr (F16) {
+        // fp32 -> fp16 with one explicit v_cvt_pk_f16_f32 (round to nearest
+        // even).  Left to itself the compiler folds the last FMA and the
+        // conversion into a mixed-precision FMA (rounding once, straight to
+        // fp16) in some kernels and not in others, which would let the fused
+        // and the two-pass paths round the same value differently.
+        u32x4 w;
+#pragma unroll
+        for (int k = 0; k < 4; k++) {
+            uint32_t h;
+            asm("v_cvt_pk_f16_f32 %0, %1, %2" : "=v"(h) : "v"(o[2 * k]), "v"(o[2 * k + 1]));
+            w[k] = h;
+        }
+        __builtin_nontemporal_store(w, q);
+    } else {
+        u32x4 a, b;
+#pragma unroll
+        for (int k = 0; k < 4; k++) {
+            a[k] = __float_as_uint(o[k]);
+            b[k] = __float_as_uint(o[4 + k]);
+        }
+        // plain (write-back) stores: each instruction covers half of every
+        // 32-byte span of the wave's rows; L2 merges the two halves before the
+        // line goes out (streaming stores wrote such lines out twice)
+        q[0] = a;
+        q[1] = b;
+    }
+}
+
+// ---- block rotations -------------------------------------------------------
+// Full: y = M v with M = L(q_L) R(conj q_R) (the sandwich of Sec. 5.2 as one
+// 4x4 orthogonal matrix, precomputed at init); inverse v = M^T y (Prop. 1).
+// Fast: y = q_L v through the left-multiplication matrix of q_L = (a,b,c,d);
+// inverse conj(q_L) y = L(q_L)^T y.  2-D: y = R(theta) u, inverse R(-theta).
+template <int VAR>
+__device__ __forceinline__ void rotate_forward(const float *P, const float x[8], float y[8])
+{
+    if constexpr (VAR == VAR_FULL) {
+#pragma unroll
+        for (int b = 0; b < 2; b++) {
+            const float *M = P + 16 * b;
+            const float *v = x + 4 * b;
+#pragma unroll
+            for (int r = 0; r < 4; r++) {
+                float acc = M[4 * r] * v[0];
+                acc = fmaf(M[4 * r + 1], v[1], acc);
+                acc = fmaf(M[4 * r + 2], v[2], acc);
+                acc = fmaf(M[4 * r + 3], v[3], acc);
+                y[4 * b + r] = acc;
+            }
+        }
+    } else if constexpr (VAR == VAR_FAST) {
+#pragma unroll
+        for (int b = 0; b < 2; b++) {
+            const float a = P[4 * b], bb = P[4 * b + 1], c = P[4 * b + 2], d = P[4 * b + 3];
+            const float *v = x + 4 * b;
+            y[4 * b + 0] = fmaf(-d, v[3], fmaf(-c, v[2], fmaf(-bb, v[1], a * v[0])));
+            y[4 * b + 1] = fmaf(c, v[3], fmaf(-d, v[2], fmaf(a, v[1], bb * v[0])));
+            y[4 * b + 2] = fmaf(-bb, v[3], fmaf(a, v[2], fmaf(d, v[1], c * v[0])));
+            y[4 * b + 3] = fmaf(a, v[3], fmaf(bb, v[2], fmaf(-c, v[1], d * v[0])));
+        }
+    } else {
+#pragma unroll
+        for (int p = 0; p < 4; p++) {
+            const float c = P[2 * p], s = P[2 * p + 1];
+            y[2 * p] = fmaf(-s, x[2 * p + 1], c * x[2 * p]);
+            y[2 * p + 1] = fmaf(c, x[2 * p + 1], s * x[2 * p]);
+        }
+    }
+}
+
+template <int VAR>
+__device__ __forceinline__ void rotate_inverse(const float *P, const float y[8], float o[8])
+{
+    if constexpr (VAR == VAR_FULL) {
+#pragma unroll
+        for (int b = 0; b < 2; b++) {
+            const float *M = P + 16 * b;
+            const float *v = y + 4 * b;
+#pragma unroll
+            for (int c = 0; c < 4; c++) {
+                float acc = M[c] * v[0];
+                acc = fmaf(M[4 + c], v[1], acc);
+                acc = fmaf(M[8 + c], v[2], acc);
+                acc = fmaf(M[12 + c], v[3], acc);
+                o[4 * b + c] = acc;
+            }
+        }
+    } else if constexpr (VAR == VAR_FAST) {
+#pragma unroll
+        for (int b = 0; b < 2; b++) {
+            const float a = P[4 * b], bb = P[4 * b + 1], c = P[4 * b + 2], d = P[4 * b + 3];
+            const float *v = y + 4 * b;
+            o[4 * b + 0] = fmaf(d, v[3], fmaf(c, v[2], fmaf(bb, v[1], a * v[0])));
+            o[4 * b + 1] = fmaf(-c, v[3], fmaf(d, v[2], fmaf(a, v[1], -bb * v[0])));
+            o[4 * b + 2] = fmaf(bb, v[3], fmaf(a, v[2], fmaf(-d, v[1], -c * v[0])));
+            o[4 * b + 3] = fmaf(a, v[3], fmaf(-bb, v[2], fmaf(c, v[1], -d * v[0])));
+        }
+    } else {
+#pragma unroll
+        for (int p = 0; p < 4; p++) {
+            const float c = P[2 * p], s = P[2 * p + 1];
+            o[2 * p] = fmaf(s, y[2 * p + 1], c * y[2 * p]);
+            o[2 * p + 1] = fmaf(c, y[2 * p + 1], -s * y[2 * p]);
+        }
+    }
+}
+
+template <int PL>
+__device__ __forceinline__ void load_params(const float *base, float P[PL])
+{
+    const u32x4 *q = reinterpret_cast<const u32x4 *>(base);
+#pragma unroll
+    for (int k = 0; k < PL / 4; k++) {
+        const u32x4 w = q[k];
+        const uint32_t e0 = w[0], e1 = w[1], e2 = w[2], e3 = w[3];
+        P[4 * k] = __uint_as_float(e0);
+        P[4 * k + 1] = __uint_as_float(e1);
+        P[4 * k + 2] = __uint_as_float(e2);
+        P[4 * k + 3] = __uint_as_float(e3);
+    }
+}
+
+}  // namespace
+}  // namespace isoq

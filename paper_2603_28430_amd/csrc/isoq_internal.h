@@ -71,6 +71,35 @@ struct KArgs {
     FastDiv div_block;
 };
 
+// Attention logits against a paged cache of quantized keys (isoq_scores.hip).
+struct SArgs {
+    const void *q;               // [n_seqs][n_q_heads][d] queries
+    const uint8_t *k_idx;        // [n_blocks][n_kv_heads][block_size][record]
+    const float *k_rho;          // [n_blocks][n_kv_heads][block_size]
+    const int32_t *block_table;  // [n_seqs][max_blocks]
+    const int32_t *seq_lens;     // [n_seqs]
+    float *scores;               // [n_seqs][n_q_heads][max_len]
+    const float *params;         // rotation parameters, device layout of the stage-1 kernels
+    int64_t max_len, n_blocks;
+    int32_t n_q_heads, n_kv_heads, group, block_size, max_blocks, n_sets;
+    float scale;
+    int32_t pad0;
+    FastDiv div_block;
+    float lev_all[16];           // c_0 .. c_{K-1}
+};
+
+// Keys per workgroup of the score kernel.
+constexpr int kScoreChunk = 1024;
+
+// Score kernel for (variant, d, bits, fp16 queries?, query heads per key
+// head) and the dynamic LDS bytes it needs (0 when its LDS is static), or
+// {nullptr, 0}.
+struct ScoreKernel {
+    const void *fn;
+    size_t dyn_lds;
+};
+ScoreKernel score_kernel_for(int variant, int d, int bits, bool f16, int group);
+
 // Kernel entry for (variant, d, bits, fp16 rows?, generic set indexing?, mode),
 // or nullptr.  Generic set indexing is needed when there is more than one
 // set and rows_per_set is not a multiple of the rows of a block.

@@ -53,6 +53,8 @@ def _load():
     L.isoq_dequantize.argtypes = [vp, c_int, vp, vp, i64, i64, vp, vp]
     L.isoq_roundtrip.argtypes = [vp, c_int, vp, i64, i64, vp, vp]
     L.isoq_kv_append.argtypes = [vp, vp, c_int, vp, vp, vp, i64, c_int, vp, vp, vp, vp, i64, c_int, vp]
+    L.isoq_kv_scores.argtypes = [vp, c_int, vp, c_int, c_int, c_int, vp, vp, i64, c_int, vp, c_int, vp,
+                                 ctypes.c_float, vp, i64, vp]
     L.isoq_packed_bytes.argtypes = [c_int, c_int]
     L.isoq_packed_bytes.restype = ctypes.c_size_t
     L.isoq_raw_params_per_set.argtypes = [c_int, c_int]
@@ -66,7 +68,7 @@ def _load():
     L.isoq_last_hip_error.argtypes = []
     L.isoq_last_hip_error.restype = ctypes.c_char_p
     for f in ("isoq_params_init", "isoq_params_destroy", "isoq_params_export", "isoq_params_info",
-              "isoq_quantize", "isoq_dequantize", "isoq_roundtrip", "isoq_kv_append", "isoq_codebook_lloyd",
+              "isoq_quantize", "isoq_dequantize", "isoq_roundtrip", "isoq_kv_append", "isoq_kv_scores", "isoq_codebook_lloyd",
               "isoq_rotation_draws"):
         getattr(L, f).restype = c_int
     return L
@@ -286,3 +288,40 @@ def isoq_kv_append(pk: Params, k_new, slot_mapping, k_idx, k_rho, pv: Params = N
                               _ptr(k_new), _ptr(v_new), _ptr(slot_mapping), int(n_tokens), int(n_heads),
                               _ptr(k_idx), _ptr(k_rho), _ptr(v_idx), _ptr(v_rho), int(n_blocks),
                               int(block_size), _stream_ptr(stream)), "isoq_kv_append")
+
+
+def isoq_kv_scores(pk: Params, q, k_idx, k_rho, block_table, seq_lens, scale: float = 1.0,
+                   max_len=None, scores=None, stream=None):
+    """Attention logits scale * <q, k_hat> of queries q [n_seqs, n_q_heads, d]
+    against the paged key cache k_idx [n_blocks, n_kv_heads, block_size, R] /
+    k_rho [n_blocks, n_kv_heads, block_size], with block_table int32
+    [n_seqs, max_blocks] and seq_lens int32 [n_seqs].  Returns fp32 scores
+    [n_seqs, n_q_heads, max_len]; positions at or past a sequence's length are
+    not written (see include/isoquant.h)."""
+    torch = _torch()
+    if q.dim() != 3 or k_idx.dim() != 4 or k_rho.dim() != 3 or block_table.dim() != 2:
+        raise ValueError("q [n_seqs, n_q_heads, d], k_idx [n_blocks, n_kv_heads, block_size, R], "
+                         "k_rho [n_blocks, n_kv_heads, block_size], block_table [n_seqs, max_blocks]")
+    n_seqs, n_q_heads, d = q.shape
+    n_blocks, n_kv_heads, block_size, rb = k_idx.shape
+    if d != pk.d or rb != pk.record_bytes or tuple(k_rho.shape) != (n_blocks, n_kv_heads, block_size):
+        raise ValueError("cache shapes do not match the queries and the handle")
+    if block_table.shape[0] != n_seqs or seq_lens.numel() != n_seqs:
+        raise ValueError("block_table and seq_lens need one row per sequence")
+    if block_table.dtype != torch.int32 or seq_lens.dtype != torch.int32:
+        raise TypeError("block_table and seq_lens must be int32")
+    max_blocks = block_table.shape[1]
+    if max_len is None:
+        max_len = max_blocks * block_size
+    if scores is None:
+        scores = torch.empty((n_seqs, n_q_heads, max_len), dtype=torch.float32, device=q.device)
+    elif tuple(scores.shape) != (n_seqs, n_q_heads, max_len) or scores.dtype != torch.float32:
+        raise ValueError("scores must be fp32 [n_seqs, n_q_heads, max_len]")
+    for t in (q, k_idx, k_rho, block_table, seq_lens, scores):
+        if not t.is_cuda or not t.is_contiguous():
+            raise ValueError("tensors must be contiguous and on the GPU")
+    _check(lib.isoq_kv_scores(pk.handle, _dtype_code(q.dtype), _ptr(q), int(n_seqs), int(n_q_heads),
+                              int(n_kv_heads), _ptr(k_idx), _ptr(k_rho), int(n_blocks), int(block_size),
+                              _ptr(block_table), int(max_blocks), _ptr(seq_lens), float(scale),
+                              _ptr(scores), int(max_len), _stream_ptr(stream)), "isoq_kv_scores")
+    return scores

@@ -29,7 +29,7 @@ def test_header_declares_the_boundary():
     names = _declared()
     for required in ("isoq_params_init", "isoq_params_destroy", "isoq_params_export",
                      "isoq_quantize", "isoq_dequantize", "isoq_roundtrip", "isoq_kv_append",
-                     "isoq_packed_bytes",
+                     "isoq_kv_scores", "isoq_packed_bytes",
                      "isoq_status_string"):
         assert required in names
 
@@ -107,6 +107,9 @@ def test_argument_validation_before_any_device_call():
     # isoq_kv_append: NULL K handle
     assert binding.lib.isoq_kv_append(None, None, 1, None, None, None, 4, 2, None, None, None, None,
                                       8, 16, None) == 3
+    # isoq_kv_scores: NULL K handle
+    assert binding.lib.isoq_kv_scores(None, 1, None, 1, 1, 1, None, None, 1, 16, None, 1, None, 1.0,
+                                      None, 16, None) == 3
     assert binding.lib.isoq_params_destroy(None) == 0
     assert binding.lib.isoq_params_export(None, None, None, None) == 3
 
