@@ -261,6 +261,8 @@ def main() -> int:
     ap.add_argument("--no-extras", action="store_true")
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the side measurements of the d=256, d=512 and KV-cache workloads")
+    ap.add_argument("--side", choices=["kv-append", "kv-scores"],
+                    help="run only this side measurement and print its JSON")
     ap.add_argument("--copy-only", action="store_true",
                     help="only time a plain device copy of the input size (counter calibration)")
     args = ap.parse_args()
@@ -276,6 +278,10 @@ def main() -> int:
     import workloads
 
     torch.cuda.set_device(0)
+    if args.side:
+        fn = {"kv-append": kv_append_side, "kv-scores": kv_scores_side}[args.side]
+        print(json.dumps({"side": args.side, **fn(torch, workloads)}), flush=True)
+        return 0
     tdt, ndt, esz = {"f16": (torch.float16, np.float16, 2), "f32": (torch.float32, np.float32, 4)}[args.dtype]
     n, d, bits, S = args.n, args.d, args.bits, max(1, args.buffer_sets)
     print(f"# inputs: {n} x {d} {args.dtype}", file=sys.stderr, flush=True)
