@@ -294,6 +294,34 @@ def attention_scores(variant, d: int, bits: int, rot, levels, q, idx, rho, scale
     return scale * (qd @ xh.T)
 
 
+# --- stage 2: QJL residual sketch (Sec. 8) ------------------------------------------
+def qjl_encode(variant, d: int, bits: int, rot, levels, S, x, n_sets: int = 1, rows_per_set: int = 1):
+    """Stage-2 sketch of the stage-1 residual, by definition (Sec. 8 keeps
+    TurboQuant's residual correction: r = x - x_hat, projected by a quantized
+    Johnson-Lindenstrauss transform): with S [m, d] Gaussian,
+        z_i = [ (S r)_i > 0 ],  gamma = ||r||.
+    Returns (z [n, m] uint8 in {0, 1}, gamma [n], p = S r [n, m], idx, rho,
+    x_hat) in float64."""
+    idx, rho, xh = stage1(variant, d, bits, rot, levels, x, n_sets=n_sets, rows_per_set=rows_per_set)
+    r = _d(x).reshape(-1, d) - xh
+    p = r @ _d(S).T
+    z = (p > 0).astype(np.uint8)
+    return z, np.linalg.norm(r, axis=1), p, idx, rho, xh
+
+
+def qjl_inner_product(q, xhat, z, gamma, S):
+    """Two-stage inner-product estimate of <q, x> (TurboQuant's product
+    estimator, QJL on the residual): <q, x_hat> + sqrt(pi/2)/m * gamma *
+    <S q, 2 z - 1>.  q: [d] or [G, d]; xhat [n, d]; z [n, m]; gamma [n].
+    Returns [n] or [G, n]."""
+    S = _d(S)
+    m = S.shape[0]
+    qd = _d(q)
+    sq = qd @ S.T                                    # [.., m]
+    signs = 2.0 * np.asarray(z, np.float64) - 1.0    # [n, m]
+    return qd @ _d(xhat).T + np.sqrt(np.pi / 2.0) / m * (sq @ signs.T) * _d(gamma)
+
+
 # --- packing -------------------------------------------------------------------------
 def record_bytes(m: int, bits: int) -> int:
     return int(lib().orc_record_bytes(int(m), int(bits)))

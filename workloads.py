@@ -12,6 +12,7 @@ initialisation implements the same definition independently):
 
     key     = (seed mod 2^32, seed div 2^32)
     counter = (block, set, stream, 0), stream 0 = u_L, 1 = u_R, 2 = angle
+              (and (column group, row, 3, 0) for the stage-2 projection)
     u       = (z0, z1, z2, z3) with (z0, z1) = BM(w0, w1), (z2, z3) = BM(w2, w3)
     BM(a, b) = sqrt(-2 ln U1) * (cos 2 pi U2, sin 2 pi U2),
                U1 = (a + 0.5) / 2^32, U2 = b / 2^32
@@ -109,6 +110,15 @@ def rotation_draws(variant, d: int, n_sets: int = 1, seed: int = 1) -> np.ndarra
         return uL.reshape(-1)
     uR = philox_gaussian4(b, s, 1, seed)
     return np.concatenate([uL, uR], axis=-1).reshape(-1)  # [n_sets, g, 8]
+
+
+def qjl_matrix(m: int, d: int, seed: int = 7) -> np.ndarray:
+    """The stage-2 projection S, [m, d] i.i.d. N(0, 1): S[i, 4g:4g+4] is the
+    Philox/Box-Muller quadruple of counter (g, i, 3, 0) (stream 3; the HIP
+    library's seeded sketch implements the same definition independently)."""
+    g4 = (d + 3) // 4
+    g, i = np.meshgrid(np.arange(g4), np.arange(m))
+    return philox_gaussian4(g, i, 3, seed).reshape(m, 4 * g4)[:, :d].copy()
 
 
 def unit_gaussian_rows(n: int, d: int, seed: int = 0, dtype=np.float16, chunk: int = 1 << 16):
