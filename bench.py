@@ -206,6 +206,38 @@ def kv_scores_side(torch, workloads):
             "GBps": b / ms / 1e6, "frac": b / ms / 1e6 / PEAK_HBM_GBPS}
 
 
+def qjl_side(torch, workloads):
+    """isoq_quantize_qjl: stage-1 quantize plus the stage-2 residual sketch,
+    1,048,576 unit-norm fp16 rows, d = 128, 3 bits, m = 128 and 64 sign bits.
+    Algorithmic bytes per row: the fp16 row, the 48-byte record, the 4-byte
+    norm, m/8 sign bytes and the 4-byte gamma; the projection adds 2 m d flops
+    per row on MFMA."""
+    import numpy as np
+
+    import paper_2603_28430_amd as iq
+
+    n, d, bits = 1 << 20, 128, 3
+    print("# qjl quantize", file=sys.stderr, flush=True)
+    x0 = torch.from_numpy(workloads.unit_gaussian_rows(n, d, seed=0, dtype=np.float16)).cuda()
+    xs = [x0] + [x0.clone() for _ in range(3)]
+    out = {}
+    for variant in ("full", "fast"):
+        p = iq.isoq_params_init(variant, d, bits, 1, rot=workloads.rotation_draws(variant, d, 1, seed=1))
+        for m in (128, 64):
+            sk = iq.isoq_sketch_init(p, m)
+            bufs = [iq.isoq_quantize_qjl(p, sk, xs[i]) for i in range(4)]
+            fn = lambda i: iq.isoq_quantize_qjl(p, sk, xs[i % 4], idx_packed=bufs[i % 4][0], norms=bufs[i % 4][1],
+                                                signs=bufs[i % 4][2], gamma=bufs[i % 4][3])
+            ms = time_launches(fn, 100, 10, torch, 0.2)
+            b = n * (d * 2 + d * bits // 8 + 4 + m // 8 + 4)
+            out[f"{variant}_m{m}"] = {"us": ms * 1e3, "vectors_per_s": n / (ms / 1e3), "GBps": b / ms / 1e6,
+                                      "frac": b / ms / 1e6 / PEAK_HBM_GBPS,
+                                      "mfma_TFLOPs": 2.0 * m * d * n / ms / 1e9}
+            sk.close()
+        p.close()
+    return out
+
+
 def other_configs(measure, entry, torch, np, workloads):
     """Side measurements of the other workloads (their parity is tested in
     tests/test_gpu_full_sizes.py): d = 256 fp16 and d = 512 fp32 round trips
@@ -230,6 +262,7 @@ def other_configs(measure, entry, torch, np, workloads):
         torch.cuda.empty_cache()
     out["kv_append"] = kv_append_side(torch, workloads)
     out["kv_scores"] = kv_scores_side(torch, workloads)
+    out["qjl_quantize"] = qjl_side(torch, workloads)
     print("# config kv cache", file=sys.stderr, flush=True)
     B, H, T, d_ = 8, 32, 32768, 128
     kv = [workloads.kv_stream_torch(B, H, T, d_, seed, "cuda").view(B * H * T, d_) for seed in (2, 3)]
@@ -261,7 +294,7 @@ def main() -> int:
     ap.add_argument("--no-extras", action="store_true")
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the side measurements of the d=256, d=512 and KV-cache workloads")
-    ap.add_argument("--side", choices=["kv-append", "kv-scores"],
+    ap.add_argument("--side", choices=["kv-append", "kv-scores", "qjl"],
                     help="run only this side measurement and print its JSON")
     ap.add_argument("--copy-only", action="store_true",
                     help="only time a plain device copy of the input size (counter calibration)")
@@ -279,7 +312,7 @@ def main() -> int:
 
     torch.cuda.set_device(0)
     if args.side:
-        fn = {"kv-append": kv_append_side, "kv-scores": kv_scores_side}[args.side]
+        fn = {"kv-append": kv_append_side, "kv-scores": kv_scores_side, "qjl": qjl_side}[args.side]
         print(json.dumps({"side": args.side, **fn(torch, workloads)}), flush=True)
         return 0
     tdt, ndt, esz = {"f16": (torch.float16, np.float16, 2), "f32": (torch.float32, np.float32, 4)}[args.dtype]

@@ -216,6 +216,46 @@ isoq_status isoq_kv_scores(const isoq_params *pk, int dtype, const void *q, int 
                            int max_blocks_per_seq, const int32_t *seq_lens, float scale,
                            float *scores, int64_t max_len, void *stream);
 
+/*
+ * Stage-2 residual sketch (Sec. 8: the stage-1 residual r = x - x_hat is
+ * projected by a quantized Johnson-Lindenstrauss transform and corrects inner
+ * products without bias).  A sketch handle holds a Gaussian projection S
+ * [m][d]; a row is stored as its stage-1 record and rho plus the m sign bits
+ * z_i = [(S r)_i > 0] and gamma = ||r||, and <q, x> is estimated by
+ *     <q, x_hat> + sqrt(pi/2) / m * gamma * <S q, 2 z - 1>.
+ *
+ * isoq_sketch_init -- build the sketch of quantizer p on the current device.
+ *   m       sketch bits per row: 64 or 128 at d = 128, 64 at d = 256.
+ *   S_host  NULL, or host array [m][d] of doubles (row-major).  NULL: S is
+ *           drawn from `seed`: S[i][4g .. 4g+3] is the Box-Muller quadruple of
+ *           Philox4x32-10 with key = seed and counter (g, i, 3, 0) (the
+ *           mapping of isoq_params_init).
+ * The sketch is bound to p's rotation (it stores S T^{-1} for every set); use
+ * it only with the handle it was built from.  Only init and destroy allocate.
+ */
+typedef struct isoq_sketch isoq_sketch;
+isoq_status isoq_sketch_init(isoq_sketch **out, const isoq_params *p, int m, const double *S_host,
+                             uint64_t seed);
+isoq_status isoq_sketch_destroy(isoq_sketch *sk);
+/* m and the projection S as used (fp32, [m][d]); any output may be NULL. */
+isoq_status isoq_sketch_export(const isoq_sketch *sk, int *m, float *S_out);
+
+/*
+ * isoq_quantize_qjl -- isoq_quantize plus the stage-2 sketch of every row.
+ *   idx_packed, norms  as isoq_quantize (bitwise the same records and norms).
+ *   signs   device, [n][m/8] bytes (4-byte aligned): bit i of a row's record
+ *           (bit i mod 8 of byte i / 8) is z_i.  The projection runs in fp16
+ *           with fp32 accumulation, so a sign whose exact projection lies
+ *           within about 2^-9 sum_j |S'_ij| |e_j| rho of zero may differ from
+ *           an exact computation (S' = S T^{-1}, e the normalised rotated error).
+ *   gamma   device, [n] fp32 ||x - x_hat||.
+ * Needs one rotation set per block of rows: n_sets == 1, or rows_per_set a
+ * multiple of 64 rows at d = 128 (32 at d = 256); ISOQ_E_UNSUPPORTED otherwise.
+ */
+isoq_status isoq_quantize_qjl(const isoq_params *p, const isoq_sketch *sk, int dtype, const void *x,
+                              int64_t n, int64_t rows_per_set, uint8_t *idx_packed, float *norms,
+                              uint8_t *signs, float *gamma, void *stream);
+
 /* Sizes: bytes of one packed index record, ceil(d * bits / 8); raw draws per
  * set for rot_host (Full 8 g4, Fast 4 g4, 2-D g2); exported parameters per set
  * (Full 8 g4, Fast 4 g4, 2-D 2 g2), with g4 = ceil(d/4), g2 = ceil(d/2).

@@ -23,6 +23,14 @@ struct isoq_params {
     float levels[16], thresholds[15];
 };
 
+struct isoq_sketch {
+    int variant, d, n_sets, m;
+    int device;
+    uint16_t *dfrag;                // device, [n_sets][m/16][d/32][64][8] fp16 of S' = S T^{-1}
+    float *dS;                      // device, [m][d] fp32 of S (query side)
+    std::vector<float> S;           // host copy of S as used
+};
+
 namespace {
 
 using namespace isoq;
@@ -539,6 +547,164 @@ isoq_status isoq_kv_scores(const isoq_params *pk, int dtype, const void *q, int 
     if (e != hipSuccess)
         return hip_fail(e, "after hipLaunchKernel");
     return ISOQ_OK;
+}
+
+isoq_status isoq_sketch_init(isoq_sketch **out, const isoq_params *p, int m, const double *S_host,
+                             uint64_t seed)
+{
+    if (!out)
+        return ISOQ_E_NULL;
+    *out = nullptr;
+    if (!p)
+        return ISOQ_E_NULL;
+    if (m < 1)
+        return ISOQ_E_INVALID;
+    if (!((p->d == 128 && (m == 64 || m == 128)) || (p->d == 256 && m == 64)))
+        return ISOQ_E_UNSUPPORTED;
+    const int d = p->d;
+    std::vector<double> S((size_t)m * d), Sp((size_t)m * d);
+    if (S_host) {
+        for (size_t i = 0; i < S.size(); i++) {
+            if (!std::isfinite(S_host[i]))
+                return ISOQ_E_INVALID;
+            S[i] = S_host[i];
+        }
+    } else {
+        seeded_projection(m, d, seed, S.data());
+    }
+    isoq_sketch *sk = new (std::nothrow) isoq_sketch();
+    if (!sk)
+        return ISOQ_E_NOMEM;
+    sk->variant = p->variant;
+    sk->d = d;
+    sk->n_sets = p->n_sets;
+    sk->m = m;
+    sk->device = p->device;
+    sk->dfrag = nullptr;
+    sk->dS = nullptr;
+    // S' = S T^{-1}: row i of S' is T applied to row i of S (T orthogonal),
+    // with the handle's own fp32 rotation parameters; then fp16 in the order
+    // lane l of k-step ks of column tile nt reads: S'[16 nt + l % 16][32 ks + 8 (l / 16) + i]
+    const int KS = d / 32, NT = m / 16;
+    const size_t per_set = (size_t)m * d;
+    std::vector<uint16_t> frag;
+    try {
+        sk->S.assign(S.begin(), S.end());
+        frag.resize((size_t)p->n_sets * per_set);
+    } catch (const std::bad_alloc &) {
+        delete sk;
+        return ISOQ_E_NOMEM;
+    }
+    for (size_t i = 0; i < S.size(); i++)
+        sk->S[i] = (float)S[i];
+    const size_t ex_per_set = export_per_set(p->variant, d);
+    for (int set = 0; set < p->n_sets; set++) {
+        rotate_rows_forward(p->variant, d, p->exported.data() + set * ex_per_set, S.data(), m, Sp.data());
+        uint16_t *f = frag.data() + set * per_set;
+        for (int nt = 0; nt < NT; nt++)
+            for (int ks = 0; ks < KS; ks++)
+                for (int l = 0; l < 64; l++)
+                    for (int i = 0; i < 8; i++) {
+                        const _Float16 h = (_Float16)Sp[(size_t)(16 * nt + l % 16) * d + 32 * ks + 8 * (l / 16) + i];
+                        uint16_t bits;
+                        std::memcpy(&bits, &h, 2);
+                        f[((size_t)(nt * KS + ks) * 64 + l) * 8 + i] = bits;
+                    }
+    }
+    hipError_t e = hipMalloc(reinterpret_cast<void **>(&sk->dfrag), frag.size() * 2);
+    if (e == hipSuccess)
+        e = hipMalloc(reinterpret_cast<void **>(&sk->dS), sk->S.size() * sizeof(float));
+    if (e == hipSuccess)
+        e = hipMemcpy(sk->dfrag, frag.data(), frag.size() * 2, hipMemcpyHostToDevice);
+    if (e == hipSuccess)
+        e = hipMemcpy(sk->dS, sk->S.data(), sk->S.size() * sizeof(float), hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+        if (sk->dfrag)
+            (void)hipFree(sk->dfrag);
+        if (sk->dS)
+            (void)hipFree(sk->dS);
+        delete sk;
+        return hip_fail(e, "isoq_sketch_init", e == hipErrorOutOfMemory ? ISOQ_E_NOMEM : ISOQ_E_HIP);
+    }
+    *out = sk;
+    return ISOQ_OK;
+}
+
+isoq_status isoq_sketch_destroy(isoq_sketch *sk)
+{
+    if (!sk)
+        return ISOQ_OK;
+    isoq_status st = ISOQ_OK;
+    int prev = -1;
+    (void)hipGetDevice(&prev);
+    if (prev != sk->device)
+        (void)hipSetDevice(sk->device);
+    if (sk->dfrag && hipFree(sk->dfrag) != hipSuccess)
+        st = ISOQ_E_HIP;
+    if (sk->dS && hipFree(sk->dS) != hipSuccess)
+        st = ISOQ_E_HIP;
+    if (prev >= 0 && prev != sk->device)
+        (void)hipSetDevice(prev);
+    delete sk;
+    return st;
+}
+
+isoq_status isoq_sketch_export(const isoq_sketch *sk, int *m, float *S_out)
+{
+    if (!sk)
+        return ISOQ_E_NULL;
+    if (m)
+        *m = sk->m;
+    if (S_out)
+        std::memcpy(S_out, sk->S.data(), sk->S.size() * sizeof(float));
+    return ISOQ_OK;
+}
+
+isoq_status isoq_quantize_qjl(const isoq_params *p, const isoq_sketch *sk, int dtype, const void *x,
+                              int64_t n, int64_t rows_per_set, uint8_t *idx_packed, float *norms,
+                              uint8_t *signs, float *gamma, void *stream)
+{
+    isoq_status st = check_common(p, dtype, n, rows_per_set);
+    if (st != ISOQ_OK)
+        return st;
+    if (!sk)
+        return ISOQ_E_NULL;
+    if (sk->variant != p->variant || sk->d != p->d || sk->n_sets != p->n_sets || sk->device != p->device)
+        return ISOQ_E_INVALID;
+    const int64_t rpb = rows_per_block(p);
+    if (p->n_sets > 1 && rows_per_set % rpb != 0)
+        return ISOQ_E_UNSUPPORTED;
+    if (n == 0)
+        return ISOQ_OK;
+    if (!x || !idx_packed || !norms || !signs || !gamma)
+        return ISOQ_E_NULL;
+    if (!aligned(x, 16) || !aligned(idx_packed, 4) || !aligned(norms, 4) || !aligned(signs, 4) ||
+        !aligned(gamma, 4))
+        return ISOQ_E_ALIGN;
+    if ((st = check_device(p)) != ISOQ_OK)
+        return st;
+    const void *fn = qjl_kernel_for(p->variant, p->d, p->bits, dtype == ISOQ_F16, sk->m);
+    if (!fn)
+        return ISOQ_E_UNSUPPORTED;
+    const int64_t tiles = (n + rpb - 1) / rpb;
+    if (tiles > 0x7FFFFFFF)
+        return ISOQ_E_UNSUPPORTED;
+    // with one rotation set, blocks walk several tiles each (the projection is
+    // staged once per block); otherwise one block per tile keeps each block
+    // on its own set
+    const int64_t blocks = p->n_sets == 1 ? std::min<int64_t>(tiles, kQjlBlocks) : tiles;
+    KArgs a{};
+    fill_args(p, a);
+    a.x = x;
+    a.rec_out = idx_packed;
+    a.norms_out = norms;
+    a.n = n;
+    a.rows_per_set = rows_per_set;
+    a.qjl_frag = sk->dfrag;
+    a.qjl_signs = signs;
+    a.qjl_gamma = gamma;
+    void *args[] = {&a};
+    return launch(fn, dim3((unsigned)blocks), args, stream);
 }
 
 }  // extern "C"

@@ -159,6 +159,51 @@ bool unit4(const double *u, double q[4])
 }
 }  // namespace
 
+void seeded_projection(int m, int d, uint64_t seed, double *out)
+{
+    const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
+    const int g4 = (d + 3) / 4;
+    for (int i = 0; i < m; i++)
+        for (int g = 0; g < g4; g++) {
+            uint32_t c[4] = {(uint32_t)g, (uint32_t)i, 3u, 0u};
+            philox4x32_10(c, k0, k1);
+            double z[4];
+            normal_pair(c[0], c[1], z);
+            normal_pair(c[2], c[3], z + 2);
+            for (int k = 0; k < 4 && 4 * g + k < d; k++)
+                out[(size_t)i * d + 4 * g + k] = z[k];
+        }
+}
+
+void rotate_rows_forward(int variant, int d, const float *unit_set, const double *in, int rows, double *out)
+{
+    for (int r = 0; r < rows; r++) {
+        const double *v = in + (size_t)r * d;
+        double *y = out + (size_t)r * d;
+        if (variant == VAR_PLANAR2D) {
+            for (int j = 0; j < d / 2; j++) {
+                const double c = unit_set[2 * j], sn = unit_set[2 * j + 1];
+                y[2 * j] = c * v[2 * j] - sn * v[2 * j + 1];
+                y[2 * j + 1] = sn * v[2 * j] + c * v[2 * j + 1];
+            }
+            continue;
+        }
+        for (int i = 0; i < d / 4; i++) {
+            const float *q = unit_set + (variant == VAR_FULL ? 8 : 4) * i;
+            const double qL[4] = {q[0], q[1], q[2], q[3]};
+            double t[4];
+            hamilton(qL, v + 4 * i, t);
+            if (variant == VAR_FULL) {
+                const double qRc[4] = {q[4], -q[5], -q[6], -q[7]};
+                hamilton(t, qRc, y + 4 * i);
+            } else {
+                for (int k = 0; k < 4; k++)
+                    y[4 * i + k] = t[k];
+            }
+        }
+    }
+}
+
 bool build_rotation(int variant, int d, int n_sets, const double *raw, std::vector<float> &exported,
                     std::vector<float> &device_layout)
 {

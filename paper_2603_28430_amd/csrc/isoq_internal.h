@@ -9,7 +9,7 @@
 
 namespace isoq {
 
-enum Mode { MODE_ROUNDTRIP = 0, MODE_QUANTIZE = 1, MODE_DEQUANTIZE = 2, MODE_APPEND = 3 };
+enum Mode { MODE_ROUNDTRIP = 0, MODE_QUANTIZE = 1, MODE_DEQUANTIZE = 2, MODE_APPEND = 3, MODE_QJL = 4 };
 enum Variant { VAR_FULL = 0, VAR_FAST = 1, VAR_PLANAR2D = 2 };
 
 // Every lane owns 8 consecutive coordinates of a row (two quaternion blocks or
@@ -69,6 +69,10 @@ struct KArgs {
     int64_t n_slots;         // cache capacity in slots (n_blocks * block_size)
     uint32_t n_heads, block_size;
     FastDiv div_block;
+    // stage-2 residual sketch (quantize with QJL)
+    const uint16_t *qjl_frag;  // [n_sets][m/16][d/32][64][8] fp16: S' = S T^{-1}, B-fragment order
+    uint8_t *qjl_signs;        // [n][m/8] sign bits of S (x - x_hat)
+    float *qjl_gamma;          // [n] ||x - x_hat||
 };
 
 // Attention logits against a paged cache of quantized keys (isoq_scores.hip).
@@ -104,6 +108,11 @@ ScoreKernel score_kernel_for(int variant, int d, int bits, bool f16, int group);
 // or nullptr.  Generic set indexing is needed when there is more than one
 // set and rows_per_set is not a multiple of the rows of a block.
 const void *kernel_for(int variant, int d, int bits, bool f16, bool generic_sets, int mode);
+// Blocks of the stage-2 sketch kernel with a single rotation set (each walks
+// several tiles).
+constexpr int64_t kQjlBlocks = 1024;
+// Quantize with the stage-2 sketch of m bits (isoq_qjl.hip), or nullptr.
+const void *qjl_kernel_for(int variant, int d, int bits, bool f16, int m);
 
 // Magnitude lookup table, used for 4-bit codebooks.  The magnitude axis of
 // the normalised coordinate is cut into cells of width h, h smaller than every
@@ -130,6 +139,11 @@ bool lloyd_levels(int bits, double sigma, int iters, double *levels);
 void seeded_draws(int variant, int d, int n_sets, uint64_t seed, double *out);
 size_t raw_per_set(int variant, int d);
 size_t export_per_set(int variant, int d);
+// Seeded stage-2 projection S [m][d] (Philox4x32-10 stream 3 + Box-Muller).
+void seeded_projection(int m, int d, uint64_t seed, double *out);
+// The forward block rotation of one set (exported unit parameters, Table 1
+// layout) applied to `rows` vectors of length d.
+void rotate_rows_forward(int variant, int d, const float *unit_set, const double *in, int rows, double *out);
 // From raw draws to (a) the exported unit parameters and (b) the device
 // layout.  Returns false when a quaternion draw is zero or not finite.
 bool build_rotation(int variant, int d, int n_sets, const double *raw, std::vector<float> &exported,

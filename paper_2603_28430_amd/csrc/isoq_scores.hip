@@ -205,8 +205,12 @@ __global__ __launch_bounds__(256) void score_kernel(const SArgs a)
 #pragma unroll
         for (int u = 0; u < S::KPT; u++) {
             float *dst = a.scores + ((int64_t)s * a.n_q_heads + (int64_t)h * G) * a.max_len + k.t[u];
+            // compile-time group sizes unroll fully; a run-time one loops
+            constexpr int GU = GT > 0 ? GT : 1;
+            for (int g0 = 0; g0 < G; g0 += GU)
 #pragma unroll
-            for (int g = 0; g < (GT > 0 ? GT : G); g++) {
+            for (int gi = 0; gi < GU; gi++) {
+                const int g = g0 + gi;
                 // Empty asm statements keep the register footprint small: the
                 // record words look modified per query head, so the field
                 // offsets are not hoisted out of this loop (d/F registers),

@@ -1,0 +1,561 @@
+// The stage-1 kernel template shared by isoq_kernels.hip (round trip,
+// quantize, dequantize, append) and isoq_qjl.hip (quantize with the stage-2
+// residual sketch): packed index records, the Stage1 work split and compute.
+#pragma once
+
+#include "isoq_device.h"
+#include "isoq_internal.h"
+
+namespace isoq {
+namespace {
+
+// ---- packed index records --------------------------------------------------
+// Lane `sub` of a row owns coordinates 8 sub .. 8 sub + 7, i.e. bits
+// [8 sub * BITS, 8 (sub + 1) * BITS) of the row's record: a 16-bit half-word
+// (2 bits), a 32-bit word (4 bits), or 24 bits at byte 3 sub (3 bits), which
+// the four lanes of a DPP quad merge into three aligned words.
+template <int BITS>
+__device__ __forceinline__ void store_bits(uint8_t *rec, int sub, uint32_t p, bool ok)
+{
+    if constexpr (BITS == 2) {
+        if (ok)
+            reinterpret_cast<uint16_t *>(rec)[sub] = (uint16_t)p;
+    } else if constexpr (BITS == 4) {
+        if (ok)
+            reinterpret_cast<uint32_t *>(rec)[sub] = p;
+    } else {
+        // lane k of a quad holds bits [24 k, 24 k + 24) of 96; lanes 0..2
+        // write word k = p_k >> 8 k | p_(k+1) << (24 - 8 k)
+        const uint32_t nb = dpp_u<DPP_QUAD_1233>(p);  // bits of the next lane in the quad
+        const int k = sub & 3;
+        if (ok && k < 3)
+            reinterpret_cast<uint32_t *>(rec)[3 * (sub >> 2) + k] = (p >> (8 * k)) | (nb << (24 - 8 * k));
+    }
+}
+
+template <int BITS>
+__device__ __forceinline__ uint32_t load_bits(const uint8_t *rec, int sub)
+{
+    if constexpr (BITS == 2) {
+        return reinterpret_cast<const uint16_t *>(rec)[sub];
+    } else if constexpr (BITS == 4) {
+        return reinterpret_cast<const uint32_t *>(rec)[sub];
+    } else {
+        const uint32_t *q = reinterpret_cast<const uint32_t *>(rec + 12 * (sub >> 2));
+        const uint32_t w0 = q[0], w1 = q[1], w2 = q[2];
+        const int k = sub & 3;  // 24 k = 32 lo_word + shift
+        const uint32_t lo = k < 2 ? w0 : (k == 2 ? w1 : w2);
+        const uint32_t hi = k < 2 ? w1 : (k == 2 ? w2 : 0u);
+        const int sh = (24 * k) & 31;
+        return (uint32_t)((((uint64_t)hi << 32) | lo) >> sh) & 0xFFFFFFu;
+    }
+}
+
+// Append the lane's bit of each mask to p, first mask first (p = 2 p + bit):
+// v_addc_co_u32 with the mask as carry-in does the shift and the insert in one
+// instruction.  The masks are written by VALU compares; a VALU read of an SGPR
+// as carry-in needs wait states after such a write, which the compiler cannot
+// insert inside an asm statement, so the block starts with s_nop 4.
+__device__ __forceinline__ uint32_t push_bits8(uint32_t p, const uint64_t m[8])
+{
+    asm("s_nop 4\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %1\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %2\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %3\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %4\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %5\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %6\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %7\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %8"
+        : "+v"(p)
+        : "s"(m[0]), "s"(m[1]), "s"(m[2]), "s"(m[3]), "s"(m[4]), "s"(m[5]), "s"(m[6]), "s"(m[7])
+        : "vcc");
+    return p;
+}
+
+__device__ __forceinline__ uint32_t push_bits4(uint32_t p, const uint64_t m[4])
+{
+    asm("s_nop 4\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %1\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %2\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %3\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %4"
+        : "+v"(p)
+        : "s"(m[0]), "s"(m[1]), "s"(m[2]), "s"(m[3])
+        : "vcc");
+    return p;
+}
+
+__device__ __forceinline__ uint32_t push_bits6(uint32_t p, const uint64_t m[6])
+{
+    asm("s_nop 4\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %1\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %2\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %3\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %4\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %5\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %6"
+        : "+v"(p)
+        : "s"(m[0]), "s"(m[1]), "s"(m[2]), "s"(m[3]), "s"(m[4]), "s"(m[5])
+        : "vcc");
+    return p;
+}
+
+__device__ __forceinline__ uint32_t push_bits12(uint32_t p, const uint64_t m[12])
+{
+    asm("s_nop 4\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %1\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %2\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %3\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %4\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %5\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %6\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %7\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %8\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %9\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %10\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %11\n\t"
+        "v_addc_co_u32_e64 %0, vcc, %0, %0, %12"
+        : "+v"(p)
+        : "s"(m[0]), "s"(m[1]), "s"(m[2]), "s"(m[3]), "s"(m[4]), "s"(m[5]), "s"(m[6]), "s"(m[7]),
+          "s"(m[8]), "s"(m[9]), "s"(m[10]), "s"(m[11])
+        : "vcc");
+    return p;
+}
+
+// ---- the kernel ---------------------------------------------------------------
+// Work split.  A row group is the 512/d rows one wave holds.  Block b (four
+// waves) owns the kTileGroups * 4 consecutive groups starting at
+// b * kTileGroups * 4; wave w takes groups base + 4u + w, u < kTileGroups, so
+// that each load or store instruction of the block touches one contiguous
+// span.  Blocks are not persistent: the dispatcher streams them through the
+// chip in address order, which keeps HBM pages and channels evenly busy.
+// When there is one parameter set, or rows_per_set is a multiple of the rows
+// of a block, all rows of a block share a set and the block stages that set's
+// parameters once through LDS (GENERIC_SETS = false).  Otherwise each lane
+// finds the set of its row for every group and reads its parameters from
+// global memory.  Parameters are staged before the tile's loads are issued:
+// measured on MI355X, this order beats issuing the data loads first.
+// QM: sketch size m of the stage-2 residual sketch (MODE_QJL only).
+template <int VAR, int D, int BITS, bool F16, int MODE, bool GENERIC_SETS, int QM = 0>
+struct Stage1 {
+    static constexpr int LPV = D / kCoordsPerLane;      // lanes per row
+    static constexpr int VPW = 64 / LPV;                // rows per wave
+    static constexpr int H = 1 << (BITS - 1);           // positive levels
+    static constexpr int PL = VAR == VAR_FULL ? 32 : 8; // parameter floats per lane
+    static constexpr int64_t ROWB = (int64_t)D * (F16 ? 2 : 4);  // bytes per row
+    static constexpr int64_t RECB = (int64_t)D * BITS / 8;       // bytes per index record
+    static constexpr int LANEB = F16 ? 16 : 32;         // row bytes per lane
+    static constexpr bool kUseLut = BITS == 4;           // magnitude lookup table
+    static constexpr bool kQjl = MODE == MODE_QJL;
+    static constexpr bool kEncode = MODE == MODE_QUANTIZE || MODE == MODE_APPEND || kQjl;  // records out
+    static constexpr bool kLevels = MODE == MODE_ROUNDTRIP || kQjl;  // selected levels needed
+    // stage-2 sketch: a wave's tile of rows, its fp16 error rows in LDS
+    static constexpr int kTileRows = kTileGroups * VPW;   // 16 (d = 128) or 8 (d = 256)
+    static constexpr int kEStride = D + 8;                // halfs per LDS error row (padded)
+
+    struct In {
+        Raw<F16> raw;
+        uint32_t bits;
+        float rho;
+    };
+
+    // Row addressing.  The row of a lane is grow + lr: grow, the first row of
+    // the group, is wave-uniform, and lr < VPW is the lane's row slot, so
+    // addresses are a scalar base plus a loop-invariant lane offset.  In the
+    // last (tail) tile, lanes past the end take the last row: they recompute
+    // it and store the same bits to the same place, which keeps the loop free
+    // of divergent branches.
+    template <bool TAIL>
+    __device__ static __forceinline__ int lane_row(const KArgs &a, int64_t grow, int slot)
+    {
+        if constexpr (TAIL)
+            return (int)(min(grow + slot, a.n - 1) - grow);
+        return slot;
+    }
+
+    __device__ static __forceinline__ void fetch(const KArgs &a, int64_t grow, int lr, int sub, In &in)
+    {
+        if constexpr (MODE == MODE_DEQUANTIZE) {
+            in.bits = load_bits<BITS>(a.rec_in + grow * RECB + (uint32_t)(lr * RECB), sub);
+            in.rho = (a.norms_in + grow)[lr];
+        } else if constexpr (MODE == MODE_APPEND) {
+            // token grow + lr, head blockIdx.x of rows [n_tokens][n_heads][d]
+            const int64_t tstride = (int64_t)a.n_heads * ROWB;
+            load_row_chunk<F16>(static_cast<const char *>(a.x) + grow * tstride + (int64_t)blockIdx.x * ROWB +
+                                    (uint32_t)(lr * (uint32_t)tstride + sub * LANEB),
+                                in.raw);
+        } else {
+            load_row_chunk<F16>(static_cast<const char *>(a.x) + grow * ROWB + (uint32_t)(lr * ROWB + sub * LANEB),
+                                in.raw);
+        }
+    }
+
+    // erow, eq: row of this lane in the wave's tile and the wave's LDS error
+    // tile (MODE_QJL only).
+    __device__ static __forceinline__ void compute(const KArgs &a, const float *P, const float *lev,
+                                                   const float *thr, const float *lds_levels,
+                                                   const LutEntry *lut, const In &in, int64_t grow,
+                                                   int lr, int sub, int erow = 0, _Float16 *eq = nullptr)
+    {
+        float yq[8];
+        if constexpr (MODE == MODE_DEQUANTIZE) {
+#pragma unroll
+            for (int j = 0; j < 8; j++) {
+                const uint32_t idx = (in.bits >> (BITS * j)) & (2 * H - 1);
+                yq[j] = lds_levels[idx] * in.rho;
+            }
+        } else {
+            float x[8];
+            unpack<F16>(in.raw, x);
+            const float rho = __builtin_amdgcn_sqrtf(row_sum<LPV>(sum_squares<F16>(in.raw, x)));
+            const float rho_e = fmaxf(rho, kEps);
+            float y[8], m[8];
+            // selected levels are scaled by rho for the round trip (it then
+            // yields rho * rec directly) and left normalised for the sketch
+            const float lscale = kQjl ? 1.f : rho;
+            rotate_forward<VAR>(P, x, y);
+#pragma unroll
+            for (int j = 0; j < 8; j++)
+                m[j] = fabsf(y[j]);
+            if constexpr (kUseLut) {
+                // 4 bits: cell of the normalised magnitude, one compare against
+                // the cell's threshold (quantize and round trip use the same t)
+                const float s = a.lut_inv_h * __builtin_amdgcn_rcpf(rho_e);
+                const float last = (float)(a.lut_cells - 1);
+                uint32_t p = 0;
+#pragma unroll
+                for (int j = 0; j < 8; j++) {
+                    const float t = m[j] * s;
+                    const LutEntry e = lut[(uint32_t)fminf(t, last)];
+                    const bool above = t > e.t;
+                    if constexpr (kLevels) {
+                        const float L = above ? e.hi : e.lo;
+                        yq[j] = (y[j] > 0.f ? L : -L) * lscale;
+                    }
+                    if constexpr (kEncode) {
+                        const uint32_t q = e.m + (above ? 1u : 0u);
+                        p |= (q ^ (y[j] > 0.f ? (uint32_t)H : (uint32_t)(H - 1))) << (BITS * j);
+                    }
+                }
+                if constexpr (kEncode)
+                    emit(a, grow, lr, sub, p, rho);
+            } else {
+            float ths[H > 1 ? H - 1 : 1];
+#pragma unroll
+            for (int k = 0; k < H - 1; k++)
+                ths[k] = thr[k] * rho_e;
+            if constexpr (kLevels) {
+                float lvs[H];
+#pragma unroll
+                for (int k = 0; k < H; k++)
+                    lvs[k] = lev[k] * lscale;
+                float L[8];
+#pragma unroll
+                for (int j = 0; j < 8; j++)
+                    L[j] = lvs[0];
+                // thresholds outer, coordinates inner: independent compares
+                // fill the distance between each compare and its select
+#pragma unroll
+                for (int k = 0; k < H - 1; k++)
+#pragma unroll
+                    for (int j = 0; j < 8; j++)
+                        L[j] = m[j] > ths[k] ? lvs[k + 1] : L[j];
+#pragma unroll
+                for (int j = 0; j < 8; j++)
+                    yq[j] = y[j] > 0.f ? L[j] : -L[j];
+            }
+            if constexpr (kEncode) {
+                // For y > 0 the index is H + m, otherwise (H - 1) - m: its top
+                // bit is the sign decision and every lower bit is the matching
+                // bit of the magnitude index m, inverted when y <= 0.  The
+                // lane masks of those bits are pushed into the record word
+                // from its most significant end: coordinate 7's top bit first.
+                // m: 3 bits, binary search (compare with the middle positive
+                // threshold, then with the one it selects); 2 bits, one compare.
+                // 4 coordinates per asm block (2 with the stage-2 sketch,
+                // whose extra state would otherwise push the live masks past
+                // the scalar register file)
+                static_assert(BITS == 2 || BITS == 3, "2 or 3 bits on this branch");
+                constexpr int CPB = kQjl ? 2 : 4;   // coordinates per push block
+                uint32_t p = 0;
+#pragma unroll
+                for (int j0 = 7; j0 >= 0; j0 -= CPB) {
+                    uint64_t mk[CPB * BITS];  // BITS masks per coordinate
+#pragma unroll
+                    for (int c = 0; c < CPB; c++) {
+                        const int j = j0 - c;
+                        uint64_t *o = mk + c * BITS;
+                        const uint64_t pos = __builtin_amdgcn_ballot_w64(y[j] > 0.f);
+                        o[0] = pos;
+                        if constexpr (H == 4) {
+                            const bool hi = m[j] > ths[1];
+                            const bool lo = m[j] > (hi ? ths[2] : ths[0]);
+                            o[1] = ~(__builtin_amdgcn_ballot_w64(hi) ^ pos);
+                            o[2] = ~(__builtin_amdgcn_ballot_w64(lo) ^ pos);
+                        } else {
+                            o[1] = ~(__builtin_amdgcn_ballot_w64(m[j] > ths[0]) ^ pos);
+                        }
+                    }
+                    if constexpr (CPB * BITS == 12)
+                        p = push_bits12(p, mk);
+                    else if constexpr (CPB * BITS == 8)
+                        p = push_bits8(p, mk);
+                    else if constexpr (CPB * BITS == 6)
+                        p = push_bits6(p, mk);
+                    else
+                        p = push_bits4(p, mk);
+                }
+                emit(a, grow, lr, sub, p, rho);
+            }
+            }
+            if constexpr (kQjl) {
+                // stage 2: e = y / rho' - c[idx], the quantization error of the
+                // normalised rotated row (zero for a zero row); gamma =
+                // rho ||e|| = ||x - x_hat|| (T is orthogonal); e goes to the
+                // wave's LDS tile as fp16 for the projection
+                const float inv = rho > 0.f ? __builtin_amdgcn_rcpf(rho_e) : 0.f;
+                float e[8], s2 = 0.f;
+#pragma unroll
+                for (int j = 0; j < 8; j++) {
+                    e[j] = rho > 0.f ? fmaf(y[j], inv, -yq[j]) : 0.f;
+                    s2 = fmaf(e[j], e[j], s2);
+                }
+                const float gamma = rho * __builtin_amdgcn_sqrtf(row_sum<LPV>(s2));
+                if (sub == 0)
+                    (a.qjl_gamma + grow)[lr] = gamma;
+                u32x4 h;
+#pragma unroll
+                for (int k = 0; k < 4; k++) {
+                    uint32_t v;
+                    asm("v_cvt_pk_f16_f32 %0, %1, %2" : "=v"(v) : "v"(e[2 * k]), "v"(e[2 * k + 1]));
+                    h[k] = v;
+                }
+                *reinterpret_cast<u32x4 *>(eq + erow * kEStride + 8 * sub) = h;
+            }
+        }
+        if constexpr (!kEncode) {
+            float o[8];
+            rotate_inverse<VAR>(P, yq, o);
+            store_row_chunk<F16>(static_cast<char *>(a.y) + grow * ROWB + (uint32_t)(lr * ROWB + sub * LANEB), o);
+        }
+    }
+
+    // Write one row's index record and norm: to row grow + lr (quantize), or
+    // to the cache slot of token grow + lr for head blockIdx.x (append): slot
+    // s is position s mod block_size of cache block s / block_size, and a
+    // cache block holds [n_heads][block_size] records.  A skipped slot writes
+    // nothing; the quad exchange inside store_bits runs on every lane either
+    // way.
+    __device__ static __forceinline__ void emit(const KArgs &a, int64_t grow, int lr, int sub,
+                                                uint32_t p, float rho)
+    {
+        if constexpr (MODE == MODE_QUANTIZE || MODE == MODE_QJL) {
+            store_bits<BITS>(a.rec_out + grow * RECB + (uint32_t)(lr * RECB), sub, p, true);
+            if (sub == 0)
+                (a.norms_out + grow)[lr] = rho;
+        } else {
+            const uint32_t h = blockIdx.x;
+            const int64_t s = (a.slots + grow)[lr];
+            const bool ok = s >= 0 && s < a.n_slots;
+            const uint32_t su = ok ? (uint32_t)s : 0u;
+            const uint32_t blk = fast_div(su, a.div_block);
+            const int64_t crow = ((int64_t)blk * a.n_heads + h) * a.block_size + (su - blk * a.block_size);
+            store_bits<BITS>(a.rec_out + crow * RECB, sub, p, ok);
+            if (ok && sub == 0)
+                a.norms_out[crow] = rho;
+        }
+    }
+
+    // parameter set of `row` (GENERIC_SETS only)
+    __device__ static __forceinline__ int set_of(const KArgs &a, int64_t row)
+    {
+        return (int)((row / a.rows_per_set) % a.n_sets);
+    }
+
+    __device__ static void run(const KArgs &a, float *lds_levels, float *lds_params, LutEntry *lds_lut,
+                               _Float16 *lds_frag = nullptr, _Float16 *lds_e = nullptr)
+    {
+        const int lane = threadIdx.x & 63;
+        const int sub = lane % LPV;
+        const int slot = lane / LPV;
+        const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+        const int64_t groups = (a.n + VPW - 1) / VPW;
+        // append: blocks (head, token range) are dispatched head-fastest, so
+        // the blocks in flight read all heads of the same tokens, one span
+        const int64_t base = (int64_t)(MODE == MODE_APPEND ? blockIdx.y : blockIdx.x) * (kBlockThreads / 64) *
+                             kTileGroups;
+
+        // 1. block-wide tables: the codebook (dequantize) and the rotation
+        //    parameters of the block's set, staged through LDS
+        if constexpr (MODE == MODE_DEQUANTIZE) {
+            if (threadIdx.x < 2 * H)
+                lds_levels[threadIdx.x] = a.lev_all[threadIdx.x];
+        }
+        if constexpr (kUseLut && MODE != MODE_DEQUANTIZE) {
+            const u32x4 *s4 = reinterpret_cast<const u32x4 *>(a.lut);
+            u32x4 *d4 = reinterpret_cast<u32x4 *>(lds_lut);
+            for (int i = threadIdx.x; i < a.lut_cells; i += kBlockThreads)
+                d4[i] = s4[i];
+        }
+        float P[PL];
+        if constexpr (!GENERIC_SETS) {
+            // append: the block's head (every set is a head, or there is one)
+            const int64_t set = a.n_sets <= 1           ? 0
+                                : MODE == MODE_APPEND ? (int64_t)blockIdx.x
+                                                      : (base * VPW / a.rows_per_set) % a.n_sets;
+            const u32x4 *s4 = reinterpret_cast<const u32x4 *>(a.params + set * (LPV * PL));
+            u32x4 *d4 = reinterpret_cast<u32x4 *>(lds_params);
+            for (int i = threadIdx.x; i < LPV * PL / 4; i += kBlockThreads)
+                d4[i] = s4[i];
+            if constexpr (kQjl) {
+                // the set's projection S' = S T^{-1} in MFMA B-fragment order
+                const u32x4 *f4 = reinterpret_cast<const u32x4 *>(a.qjl_frag + set * (int64_t)(QM * D));
+                u32x4 *g4 = reinterpret_cast<u32x4 *>(lds_frag);
+                for (int i = threadIdx.x; i < QM * D / 8; i += kBlockThreads)
+                    g4[i] = f4[i];
+            }
+        }
+        if constexpr (MODE == MODE_DEQUANTIZE || !GENERIC_SETS || kUseLut)
+            __syncthreads();
+        if constexpr (!GENERIC_SETS)
+            load_params<PL>(lds_params + sub * PL, P);
+
+        float lev[H], thr[H > 1 ? H - 1 : 1];
+#pragma unroll
+        for (int k = 0; k < H; k++)
+            lev[k] = a.lev_pos[k];
+#pragma unroll
+        for (int k = 0; k < H - 1; k++)
+            thr[k] = a.thr_pos[k];
+
+        // With the stage-2 sketch a block may walk several tiles (stride
+        // gridDim.x) so that the staged projection serves them all; the host
+        // launches one block per tile when the tiles' sets differ.  No
+        // barrier follows, so each wave leaves on its own.
+        _Float16 *eq = kQjl ? lds_e + w * kTileRows * kEStride : nullptr;
+        for (int64_t tb = (int64_t)(MODE == MODE_APPEND ? blockIdx.y : blockIdx.x);;
+             tb += (kQjl ? (int64_t)gridDim.x : (int64_t)1 << 62)) {
+            const int64_t tbase = tb * (kBlockThreads / 64) * kTileGroups;
+            if (tbase + w >= groups)
+                return;
+            const int64_t row0 = tbase * VPW;  // first row of the tile
+            if ((tbase + (kBlockThreads / 64) * kTileGroups) * VPW <= a.n)
+                tile<false>(a, P, lev, thr, lds_levels, lds_lut, row0, groups, tbase, w, sub, slot, eq);
+            else
+                tile<true>(a, P, lev, thr, lds_levels, lds_lut, row0, groups, tbase, w, sub, slot, eq);
+            if constexpr (kQjl)
+                sketch(a, lds_frag, eq, row0, groups, tbase, w);
+            else
+                return;
+        }
+    }
+
+    // Stage-2 sketch of the wave's tile: P = E S'^T with E the tile's error
+    // rows (fp16, LDS) and S' = S T^{-1} (fp16, LDS, B-fragment order) on
+    // v_mfma_f32_16x16x32_f16: lane l supplies row l % 16 and k = 8 (l / 16)
+    // .. +7 of A, column l % 16 and the same k of B, and receives column
+    // l % 16 of rows 4 (l / 16) .. +3 of the 16 x 16 result.  The sign bits
+    // of rho * P (rho > 0 unless the row is zero, whose e is zero) are the
+    // sketch; a ballot per result register gathers them, 16 columns per row,
+    // and lane t < 16 assembles row t's 32-bit words (columns 32 w .. 32 w + 31,
+    // bit i = column 32 w + i).
+    __device__ static __forceinline__ void sketch(const KArgs &a, const _Float16 *frag, const _Float16 *eq,
+                                                  int64_t row0, int64_t groups, int64_t base, int w)
+    {
+        typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+        typedef float f32x4 __attribute__((ext_vector_type(4)));
+        constexpr int KS = D / 32, NT = QM / 16;
+        const int l = threadIdx.x & 63;
+        const int r16 = l & 15, kq = l >> 4;
+        half8 A[KS];
+#pragma unroll
+        for (int ks = 0; ks < KS; ks++) {
+            if (r16 < kTileRows) {
+                A[ks] = *reinterpret_cast<const half8 *>(eq + r16 * kEStride + 32 * ks + 8 * kq);
+            } else {
+#pragma unroll
+                for (int i = 0; i < 8; i++)
+                    A[ks][i] = (_Float16)0.f;
+            }
+        }
+        // this lane's output row (lanes 0 .. kTileRows-1): group u, slot
+        const int u = r16 / VPW, sl = r16 - u * VPW;
+        const int64_t gl = 4 * u + w;
+        const bool ok = l < kTileRows && base + gl < groups;
+        const int64_t row = min(row0 + gl * VPW + sl, a.n - 1);
+        uint32_t *dst = reinterpret_cast<uint32_t *>(a.qjl_signs + row * (QM / 8));
+        // k-step outer, column tile inner: the NT accumulations are
+        // independent, so consecutive MFMAs do not wait on each other
+        f32x4 acc[NT];
+#pragma unroll
+        for (int nt = 0; nt < NT; nt++)
+            acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < KS; ks++) {
+            half8 b[NT];
+#pragma unroll
+            for (int nt = 0; nt < NT; nt++)
+                b[nt] = *reinterpret_cast<const half8 *>(frag + ((nt * KS + ks) * 64 + l) * 8);
+#pragma unroll
+            for (int nt = 0; nt < NT; nt++)
+                acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(A[ks], b[nt], acc[nt], 0, 0, 0);
+        }
+        // row t = 4 g + i sits in bits [16 g, 16 g + 16) of the ballot of
+        // result register i
+        const int i = l & 3, g = (l >> 2) & 3;
+#pragma unroll
+        for (int w2 = 0; w2 < NT / 2; w2++) {
+            uint32_t word = 0;
+#pragma unroll
+            for (int h = 0; h < 2; h++) {
+                const f32x4 v = acc[2 * w2 + h];
+                const uint64_t m0 = __builtin_amdgcn_ballot_w64(v[0] > 0.f);
+                const uint64_t m1 = __builtin_amdgcn_ballot_w64(v[1] > 0.f);
+                const uint64_t m2 = __builtin_amdgcn_ballot_w64(v[2] > 0.f);
+                const uint64_t m3 = __builtin_amdgcn_ballot_w64(v[3] > 0.f);
+                const uint64_t sel = i == 0 ? m0 : (i == 1 ? m1 : (i == 2 ? m2 : m3));
+                word |= ((uint32_t)(sel >> (16 * g)) & 0xFFFFu) << (16 * h);
+            }
+            if (ok)
+                dst[w2] = word;
+            // one word's masks live at a time (scalar registers)
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+
+    // The wave's kTileGroups groups: every load first (a group past the end
+    // re-reads the last group and is neither computed nor stored), kept in
+    // flight together by the scheduling barrier; then compute and store group
+    // by group.
+    template <bool TAIL>
+    __device__ static __forceinline__ void tile(const KArgs &a, float *P, const float *lev,
+                                                const float *thr, const float *lds_levels,
+                                                const LutEntry *lut, int64_t row0, int64_t groups,
+                                                int64_t base, int w, int sub, int slot, _Float16 *eq)
+    {
+        In buf[kTileGroups];
+#pragma unroll
+        for (int u = 0; u < kTileGroups; u++) {
+            const int gl = TAIL ? (int)(min(base + 4 * u + w, groups - 1) - base) : 4 * u + w;
+            const int64_t grow = row0 + (int64_t)gl * VPW;
+            fetch(a, grow, lane_row<TAIL>(a, grow, slot), sub, buf[u]);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int u = 0; u < kTileGroups; u++) {
+            const int gl = 4 * u + w;
+            if (TAIL && base + gl >= groups)
+                break;
+            const int64_t grow = row0 + (int64_t)gl * VPW;
+            const int lr = lane_row<TAIL>(a, grow, slot);
+            if constexpr (GENERIC_SETS)
+                load_params<PL>(a.params + ((int64_t)set_of(a, grow + lr) * LPV + sub) * PL, P);
+            compute(a, P, lev, thr, lds_levels, lut, buf[u], grow, lr, sub, u * VPW + slot, eq);
+        }
+    }
+};
+
+
+}  // namespace
+}  // namespace isoq

@@ -53,6 +53,10 @@ def _load():
     L.isoq_dequantize.argtypes = [vp, c_int, vp, vp, i64, i64, vp, vp]
     L.isoq_roundtrip.argtypes = [vp, c_int, vp, i64, i64, vp, vp]
     L.isoq_kv_append.argtypes = [vp, vp, c_int, vp, vp, vp, i64, c_int, vp, vp, vp, vp, i64, c_int, vp]
+    L.isoq_sketch_init.argtypes = [ctypes.POINTER(vp), vp, c_int, dp, ctypes.c_uint64]
+    L.isoq_sketch_destroy.argtypes = [vp]
+    L.isoq_sketch_export.argtypes = [vp, ctypes.POINTER(c_int), fp]
+    L.isoq_quantize_qjl.argtypes = [vp, vp, c_int, vp, i64, i64, vp, vp, vp, vp, vp]
     L.isoq_kv_scores.argtypes = [vp, c_int, vp, c_int, c_int, c_int, vp, vp, i64, c_int, vp, c_int, vp,
                                  ctypes.c_float, vp, i64, vp]
     L.isoq_packed_bytes.argtypes = [c_int, c_int]
@@ -68,7 +72,8 @@ def _load():
     L.isoq_last_hip_error.argtypes = []
     L.isoq_last_hip_error.restype = ctypes.c_char_p
     for f in ("isoq_params_init", "isoq_params_destroy", "isoq_params_export", "isoq_params_info",
-              "isoq_quantize", "isoq_dequantize", "isoq_roundtrip", "isoq_kv_append", "isoq_kv_scores", "isoq_codebook_lloyd",
+              "isoq_quantize", "isoq_dequantize", "isoq_roundtrip", "isoq_kv_append", "isoq_kv_scores", "isoq_sketch_init",
+              "isoq_sketch_destroy", "isoq_sketch_export", "isoq_quantize_qjl", "isoq_codebook_lloyd",
               "isoq_rotation_draws"):
         getattr(L, f).restype = c_int
     return L
@@ -325,3 +330,68 @@ def isoq_kv_scores(pk: Params, q, k_idx, k_rho, block_table, seq_lens, scale: fl
                               _ptr(block_table), int(max_blocks), _ptr(seq_lens), float(scale),
                               _ptr(scores), int(max_len), _stream_ptr(stream)), "isoq_kv_scores")
     return scores
+
+
+class Sketch:
+    """Owner of an isoq_sketch handle (stage-2 projection of a quantizer)."""
+
+    def __init__(self, handle: int, p: Params, m: int):
+        self.handle = ctypes.c_void_p(handle)
+        self.params, self.m, self.d = p, int(m), p.d
+
+    def close(self):
+        if self.handle:
+            _check(lib.isoq_sketch_destroy(self.handle), "isoq_sketch_destroy")
+            self.handle = ctypes.c_void_p(None)
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def isoq_sketch_init(p: Params, m: int, S=None, seed: int = 7) -> Sketch:
+    """Stage-2 sketch of quantizer p: projection S [m, d] (given, or drawn from seed)."""
+    dp = ctypes.POINTER(ctypes.c_double)
+    S_a = None if S is None else np.ascontiguousarray(S, dtype=np.float64)
+    if S_a is not None and S_a.shape != (m, p.d):
+        raise ValueError("S must be [m, d]")
+    h = ctypes.c_void_p()
+    _check(lib.isoq_sketch_init(ctypes.byref(h), p.handle, int(m),
+                                None if S_a is None else S_a.ctypes.data_as(dp), int(seed)),
+           "isoq_sketch_init")
+    return Sketch(h.value, p, m)
+
+
+def isoq_sketch_destroy(sk: Sketch) -> None:
+    sk.close()
+
+
+def isoq_sketch_export(sk: Sketch):
+    """(m, S as used, float32 [m, d])."""
+    m = ctypes.c_int()
+    S = np.zeros((sk.m, sk.d), np.float32)
+    _check(lib.isoq_sketch_export(sk.handle, ctypes.byref(m), S.ctypes.data_as(ctypes.POINTER(ctypes.c_float))),
+           "isoq_sketch_export")
+    return m.value, S
+
+
+def isoq_quantize_qjl(p: Params, sk: Sketch, x, rows_per_set: int = 1, idx_packed=None, norms=None,
+                      signs=None, gamma=None, stream=None):
+    """(records [n, R] uint8, norms [n] fp32, sign sketch [n, m/8] uint8, gamma [n] fp32)."""
+    torch = _torch()
+    n = _rows(x, p.d)
+    dev = x.device
+    if idx_packed is None:
+        idx_packed = torch.empty((n, p.record_bytes), dtype=torch.uint8, device=dev)
+    if norms is None:
+        norms = torch.empty((n,), dtype=torch.float32, device=dev)
+    if signs is None:
+        signs = torch.empty((n, sk.m // 8), dtype=torch.uint8, device=dev)
+    if gamma is None:
+        gamma = torch.empty((n,), dtype=torch.float32, device=dev)
+    _check(lib.isoq_quantize_qjl(p.handle, sk.handle, _dtype_code(x.dtype), _ptr(x), n, int(rows_per_set),
+                                 _ptr(idx_packed), _ptr(norms), _ptr(signs), _ptr(gamma), _stream_ptr(stream)),
+           "isoq_quantize_qjl")
+    return idx_packed, norms, signs, gamma

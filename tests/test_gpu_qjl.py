@@ -1,0 +1,174 @@
+"""Quantize with the stage-2 residual sketch (isoq_quantize_qjl) against the
+oracle (oracle.qjl_encode: z_i = [(S (x - x_hat))_i > 0], gamma = ||x - x_hat||).
+
+- Records and norms equal isoq_quantize's bit for bit.
+- Signs: identical to the oracle's exact projection p = S r wherever
+  |p_i| > tau_i, the bound on the kernel's error: it projects the normalised
+  rotated error e through S' = S T^{-1} in fp16 with fp32 accumulation, so
+  |rho (S'e)_i - p_i| <= rho ((2^-10 + 8e-6) sum_j |S'_ij| |e_j| + 6e-7 sum_j |S'_ij|)
+  (fp16 rounding of S' and e, fp32 accumulation, and the fp32 stage-1 error of
+  e); tau is twice that.  Rows with a stage-1 coordinate within 1e-6 of a
+  threshold (either cell admissible there, so e may differ) are left out.
+- gamma within 2e-5 rho of the oracle's (fp32 rotation of a unit direction).
+- The library's seeded projection equals the workload generator's draw.
+Needs an MI355X."""
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+if not torch.cuda.is_available():
+    pytest.skip("no GPU", allow_module_level=True)
+
+import paper_2603_28430_amd as iq  # noqa: E402
+
+DT = {"f16": (torch.float16, np.float16), "f32": (torch.float32, np.float32)}
+
+
+def run_case(variant, d, bits, m, dtype, n, n_sets=1, rows_per_set=1, seed=0, x=None, seeded_S=False):
+    print(f"case {variant} d={d} b={bits} m={m} {dtype} n={n} sets={n_sets}/{rows_per_set}", flush=True)
+    tdt, ndt = DT[dtype]
+    rot = workloads.rotation_draws(variant, d, n_sets, seed=1)
+    levels = oracle.codebook(bits, d)
+    p = iq.isoq_params_init(variant, d, bits, n_sets, rot=rot, codebook=levels)
+    S = workloads.qjl_matrix(m, d, seed=7 + seed)
+    sk = iq.isoq_sketch_init(p, m, seed=7 + seed) if seeded_S else iq.isoq_sketch_init(p, m, S=S)
+    if x is None:
+        x = workloads.unit_gaussian_rows(n, d, seed=seed, dtype=ndt)
+    xg = torch.from_numpy(x).cuda()
+    idx, rho, sg, gam = iq.isoq_quantize_qjl(p, sk, xg, rows_per_set)
+    qi, qr = iq.isoq_quantize(p, xg, rows_per_set)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(idx.cpu().numpy(), qi.cpu().numpy())
+    np.testing.assert_array_equal(rho.cpu().numpy(), qr.cpu().numpy())
+    signs = oracle.unpack(sg.cpu().numpy(), m, 1)
+    gamma = gam.cpu().numpy().astype(np.float64)
+
+    z, g_o, p_o, idx_o, rho_o, xh_o = oracle.qjl_encode(variant, d, bits, rot, levels, S, x, n_sets=n_sets,
+                                                        rows_per_set=rows_per_set)
+    _, _, _, yt = oracle.stage1(variant, d, bits, rot, levels, x, n_sets=n_sets, rows_per_set=rows_per_set,
+                                want_ytil=True)
+    thr = oracle.thresholds(bits, levels)
+    near = (np.abs(yt[..., None] - thr).min(-1) <= 1e-6).any(1)
+    e = yt - levels[idx_o]
+    per = oracle.raw_params_per_set(variant, d)
+    sets = (np.arange(len(x)) // rows_per_set) % n_sets
+    tau = np.zeros_like(p_o)
+    for s_ in range(n_sets):
+        rows = np.flatnonzero(sets == s_)
+        Sp = np.stack([oracle.encode(variant, d, rot[s_ * per:(s_ + 1) * per], Si) for Si in S])  # S T^-1 rows
+        A = np.abs(e[rows]) @ np.abs(Sp).T
+        B = np.abs(Sp).sum(1)[None, :]
+        tau[rows] = 2 * rho_o[rows, None] * ((2.0 ** -10 + 8e-6) * A + 6e-7 * B)
+    keep = ~near
+    decided = (np.abs(p_o) > tau) & keep[:, None]
+    bad = decided & (signs != z)
+    assert not bad.any(), (f"{int(bad.sum())} sign mismatches outside the band, first rows "
+                           f"{np.unique(np.argwhere(bad)[:, 0])[:5].tolist()}")
+    agree = (signs == z)[keep].mean() if keep.any() else 1.0
+    assert agree >= 0.97, agree
+    err = np.abs(gamma - g_o)
+    assert np.all(err[keep] <= 2e-5 * rho_o[keep] + 1e-30), float((err[keep] / np.maximum(rho_o[keep], 1e-30)).max())
+    # a zero row has no residual: every sign 0 and gamma 0 (its y~ = 0 sits
+    # on the middle threshold, so the comparison above leaves it out)
+    zero = rho_o == 0
+    assert np.all(signs[zero] == 0) and np.all(gamma[zero] == 0)
+    assert keep[~zero].mean() >= 0.98
+    return sk, S
+
+
+@pytest.mark.parametrize("bits", [2, 3, 4])
+@pytest.mark.parametrize("variant", ["full", "fast", "2d"])
+def test_qjl_d128_m128_f16(variant, bits):
+    run_case(variant, 128, bits, 128, "f16", 777, seed=bits)
+
+
+@pytest.mark.parametrize("variant,d,m,dtype", [("full", 128, 64, "f32"), ("fast", 128, 64, "f16"),
+                                               ("full", 256, 64, "f16"), ("2d", 256, 64, "f32"),
+                                               ("fast", 128, 128, "f32")])
+def test_qjl_shapes(variant, d, m, dtype):
+    run_case(variant, d, 3, m, dtype, 501, seed=d + m)
+
+
+@pytest.mark.parametrize("n", [1, 5, 17, 64, 65, 1000])
+def test_qjl_sizes(n):
+    run_case("full", 128, 3, 128, "f16", n, seed=n)
+
+
+def test_qjl_sets_per_block():
+    run_case("fast", 128, 3, 128, "f16", 640, n_sets=3, rows_per_set=64, seed=3)
+
+
+def test_qjl_zero_rows_and_scales():
+    d = 128
+    x = workloads.unit_gaussian_rows(200, d, seed=9, dtype=np.float32)
+    x[::7] = 0.0
+    x[1::7] *= 1e3
+    x[2::7] *= 1e-3
+    run_case("full", d, 3, 128, "f32", 200, x=x, seed=9)
+
+
+def test_qjl_seeded_projection_matches_generator():
+    sk, S = run_case("fast", 128, 3, 128, "f16", 300, seeded_S=True, seed=4)
+    m, S_lib = iq.isoq_sketch_export(sk)
+    assert m == 128
+    np.testing.assert_allclose(S_lib, S.astype(np.float32), rtol=0, atol=0)
+
+
+def test_qjl_estimator_is_unbiased_over_rows():
+    """The two-stage inner-product estimate built from the GPU's records,
+    signs and gamma: over many rows its error against <q, x> averages to zero
+    (the stage-1 estimate alone is biased for a query aligned with the mean
+    residual direction) and its spread obeys the QJL variance bound."""
+    variant, d, bits, m, n = "fast", 128, 2, 128, 20000
+    rot = workloads.rotation_draws(variant, d, 1, seed=1)
+    levels = oracle.codebook(bits, d)
+    p = iq.isoq_params_init(variant, d, bits, 1, rot=rot, codebook=levels)
+    S = workloads.qjl_matrix(m, d, seed=11)
+    sk = iq.isoq_sketch_init(p, m, S=S)
+    x = workloads.unit_gaussian_rows(n, d, seed=5, dtype=np.float32)
+    xg = torch.from_numpy(x).cuda()
+    idx, rho, sg, gam = iq.isoq_quantize_qjl(p, sk, xg)
+    xh = iq.isoq_dequantize(p, idx, rho, dtype=torch.float32)
+    torch.cuda.synchronize()
+    xh = xh.cpu().numpy().astype(np.float64)
+    z = oracle.unpack(sg.cpu().numpy(), m, 1)
+    g = gam.cpu().numpy().astype(np.float64)
+    # each row is its own query: <x, r> ~ ||r||^2 > 0 (the Lloyd-Max
+    # reconstruction is nearly orthogonal to its error), so stage 1 alone
+    # underestimates <x, x> consistently
+    q = x.astype(np.float64)
+    est = np.array([oracle.qjl_inner_product(q[i], xh[i:i + 1], z[i:i + 1], g[i:i + 1], S)[0]
+                    for i in range(n)])
+    truth = np.einsum("nd,nd->n", q, x)
+    base = np.einsum("nd,nd->n", q, xh)
+    err = est - truth
+    se = err.std() / np.sqrt(n)
+    assert abs(err.mean()) < 4 * se, (err.mean(), se)
+    assert abs((base - truth).mean()) > 8 * se
+    r2 = ((x - xh) ** 2).sum(1)
+    bound = np.pi / (2 * m) * (q * q).sum(1) * r2
+    assert err.var() <= 1.1 * bound.mean()
+
+
+def test_qjl_argument_errors():
+    p = iq.isoq_params_init("fast", 128, 3, 2)
+    with pytest.raises(iq.IsoqError) as e:
+        iq.isoq_sketch_init(p, 96)
+    assert e.value.status == 2
+    sk = iq.isoq_sketch_init(p, 128)
+    x = torch.zeros((100, 128), dtype=torch.float16, device="cuda")
+    with pytest.raises(iq.IsoqError) as e:
+        iq.isoq_quantize_qjl(p, sk, x, rows_per_set=10)      # sets not block-uniform
+    assert e.value.status == 2
+    p1 = iq.isoq_params_init("fast", 128, 3, 1)
+    with pytest.raises(iq.IsoqError) as e:
+        iq.isoq_quantize_qjl(p1, sk, x)                      # sketch of another handle's shape
+    assert e.value.status == 1
+    p512 = iq.isoq_params_init("full", 512, 3, 1)
+    with pytest.raises(iq.IsoqError) as e:
+        iq.isoq_sketch_init(p512, 64)
+    assert e.value.status == 2
