@@ -256,6 +256,24 @@ isoq_status isoq_quantize_qjl(const isoq_params *p, const isoq_sketch *sk, int d
                               int64_t n, int64_t rows_per_set, uint8_t *idx_packed, float *norms,
                               uint8_t *signs, float *gamma, void *stream);
 
+/*
+ * isoq_kv_scores_qjl -- isoq_kv_scores with the stage-2 residual correction:
+ *   scores[s][hq][t] = scale * (rho <T q, c[idx]> + sqrt(pi/2) / m * gamma
+ *                               * <S q, 2 z - 1>)
+ * for keys stored with their sketch: k_signs device [n_blocks][n_kv_heads]
+ * [block_size][m/8] bytes and k_gamma device fp32 [n_blocks][n_kv_heads]
+ * [block_size] (4-byte aligned), in the layout of k_idx / k_rho (sign
+ * records as written by isoq_quantize_qjl).  sk is the keys' sketch (built
+ * from pk).  Other arguments and limits as isoq_kv_scores; S q is computed
+ * in fp32.
+ */
+isoq_status isoq_kv_scores_qjl(const isoq_params *pk, const isoq_sketch *sk, int dtype, const void *q,
+                               int n_seqs, int n_q_heads, int n_kv_heads, const uint8_t *k_idx,
+                               const float *k_rho, const uint8_t *k_signs, const float *k_gamma,
+                               int64_t n_blocks, int block_size, const int32_t *block_table,
+                               int max_blocks_per_seq, const int32_t *seq_lens, float scale, float *scores,
+                               int64_t max_len, void *stream);
+
 /* Sizes: bytes of one packed index record, ceil(d * bits / 8); raw draws per
  * set for rot_host (Full 8 g4, Fast 4 g4, 2-D g2); exported parameters per set
  * (Full 8 g4, Fast 4 g4, 2-D 2 g2), with g4 = ceil(d/4), g2 = ceil(d/2).

@@ -472,11 +472,16 @@ isoq_status isoq_kv_append(const isoq_params *pk, const isoq_params *pv, int dty
     return launch(fn, dim3((unsigned)n_heads, (unsigned)blocks, has_v ? 2 : 1), args, stream);
 }
 
-isoq_status isoq_kv_scores(const isoq_params *pk, int dtype, const void *q, int n_seqs,
-                           int n_q_heads, int n_kv_heads, const uint8_t *k_idx, const float *k_rho,
-                           int64_t n_blocks, int block_size, const int32_t *block_table,
-                           int max_blocks_per_seq, const int32_t *seq_lens, float scale,
-                           float *scores, int64_t max_len, void *stream)
+}  // extern "C"
+
+namespace {
+
+// isoq_kv_scores and isoq_kv_scores_qjl (sk, k_signs, k_gamma non-NULL).
+isoq_status kv_scores(const isoq_params *pk, const isoq_sketch *sk, int dtype, const void *q, int n_seqs,
+                      int n_q_heads, int n_kv_heads, const uint8_t *k_idx, const float *k_rho,
+                      const uint8_t *k_signs, const float *k_gamma, int64_t n_blocks, int block_size,
+                      const int32_t *block_table, int max_blocks_per_seq, const int32_t *seq_lens, float scale,
+                      float *scores, int64_t max_len, void *stream)
 {
     if (!pk)
         return ISOQ_E_NULL;
@@ -487,6 +492,9 @@ isoq_status isoq_kv_scores(const isoq_params *pk, int dtype, const void *q, int 
         return ISOQ_E_INVALID;
     if (pk->n_sets != 1 && pk->n_sets != n_kv_heads)
         return ISOQ_E_INVALID;
+    if (sk && (sk->variant != pk->variant || sk->d != pk->d || sk->n_sets != pk->n_sets ||
+               sk->device != pk->device))
+        return ISOQ_E_INVALID;
     const int64_t max_pos = std::min<int64_t>(max_len, (int64_t)max_blocks_per_seq * block_size);
     if (n_seqs > 65535 || (int64_t)max_blocks_per_seq * block_size > 0x7FFFFFFF ||
         (max_pos + kScoreChunk - 1) / kScoreChunk > 65535)
@@ -495,18 +503,23 @@ isoq_status isoq_kv_scores(const isoq_params *pk, int dtype, const void *q, int 
         return ISOQ_OK;
     if (!q || !k_idx || !k_rho || !block_table || !seq_lens || !scores)
         return ISOQ_E_NULL;
+    if (sk && (!k_signs || !k_gamma))
+        return ISOQ_E_NULL;
     if (!aligned(q, 16) || !aligned(k_idx, 16) || !aligned(k_rho, 4) || !aligned(block_table, 4) ||
         !aligned(seq_lens, 4) || !aligned(scores, 4))
+        return ISOQ_E_ALIGN;
+    if (sk && (!aligned(k_signs, 4) || !aligned(k_gamma, 4)))
         return ISOQ_E_ALIGN;
     isoq_status st = check_device(pk);
     if (st != ISOQ_OK)
         return st;
     const int group = n_q_heads / n_kv_heads;
-    const ScoreKernel sk = score_kernel_for(pk->variant, pk->d, pk->bits, dtype == ISOQ_F16, group);
-    if (!sk.fn)
+    const ScoreKernel kern = sk ? score_qjl_kernel_for(pk->variant, pk->d, pk->bits, dtype == ISOQ_F16, group, sk->m)
+                                : score_kernel_for(pk->variant, pk->d, pk->bits, dtype == ISOQ_F16, group);
+    if (!kern.fn)
         return ISOQ_E_UNSUPPORTED;
-    const void *fn = sk.fn;
-    const size_t lds = sk.dyn_lds;
+    const void *fn = kern.fn;
+    const size_t lds = kern.dyn_lds;
     int lds_max = 0;
     hipError_t e = hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, pk->device);
     if (e != hipSuccess)
@@ -538,6 +551,12 @@ isoq_status isoq_kv_scores(const isoq_params *pk, int dtype, const void *q, int 
     a.div_block = make_fastdiv((uint32_t)block_size);
     for (int k = 0; k < (1 << pk->bits); k++)
         a.lev_all[k] = pk->levels[k];
+    if (sk) {
+        a.qjl_S = sk->dS;
+        a.k_signs = k_signs;
+        a.k_gamma = k_gamma;
+        a.qjl_scale = (float)((double)scale * std::sqrt(M_PI / 2.0) / sk->m);
+    }
     void *args[] = {&a};
     const dim3 grid((unsigned)n_kv_heads, (unsigned)((max_pos + kScoreChunk - 1) / kScoreChunk), (unsigned)n_seqs);
     e = hipLaunchKernel(fn, grid, dim3(256), args, lds, static_cast<hipStream_t>(stream));
@@ -547,6 +566,34 @@ isoq_status isoq_kv_scores(const isoq_params *pk, int dtype, const void *q, int 
     if (e != hipSuccess)
         return hip_fail(e, "after hipLaunchKernel");
     return ISOQ_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+isoq_status isoq_kv_scores(const isoq_params *pk, int dtype, const void *q, int n_seqs,
+                           int n_q_heads, int n_kv_heads, const uint8_t *k_idx, const float *k_rho,
+                           int64_t n_blocks, int block_size, const int32_t *block_table,
+                           int max_blocks_per_seq, const int32_t *seq_lens, float scale,
+                           float *scores, int64_t max_len, void *stream)
+{
+    return kv_scores(pk, nullptr, dtype, q, n_seqs, n_q_heads, n_kv_heads, k_idx, k_rho, nullptr, nullptr,
+                     n_blocks, block_size, block_table, max_blocks_per_seq, seq_lens, scale, scores, max_len,
+                     stream);
+}
+
+isoq_status isoq_kv_scores_qjl(const isoq_params *pk, const isoq_sketch *sk, int dtype, const void *q,
+                               int n_seqs, int n_q_heads, int n_kv_heads, const uint8_t *k_idx,
+                               const float *k_rho, const uint8_t *k_signs, const float *k_gamma,
+                               int64_t n_blocks, int block_size, const int32_t *block_table,
+                               int max_blocks_per_seq, const int32_t *seq_lens, float scale, float *scores,
+                               int64_t max_len, void *stream)
+{
+    if (!sk)
+        return ISOQ_E_NULL;
+    return kv_scores(pk, sk, dtype, q, n_seqs, n_q_heads, n_kv_heads, k_idx, k_rho, k_signs, k_gamma, n_blocks,
+                     block_size, block_table, max_blocks_per_seq, seq_lens, scale, scores, max_len, stream);
 }
 
 isoq_status isoq_sketch_init(isoq_sketch **out, const isoq_params *p, int m, const double *S_host,

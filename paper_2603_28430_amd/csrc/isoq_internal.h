@@ -90,6 +90,12 @@ struct SArgs {
     int32_t pad0;
     FastDiv div_block;
     float lev_all[16];           // c_0 .. c_{K-1}
+    // stage-2 residual correction (kernels with a sketch only)
+    const float *qjl_S;          // [m][d] fp32 projection
+    const uint8_t *k_signs;      // [n_blocks][n_kv_heads][block_size][m/8]
+    const float *k_gamma;        // [n_blocks][n_kv_heads][block_size]
+    float qjl_scale;             // scale * sqrt(pi/2) / m
+    int32_t pad1;
 };
 
 // Keys per workgroup of the score kernel.
@@ -103,6 +109,8 @@ struct ScoreKernel {
     size_t dyn_lds;
 };
 ScoreKernel score_kernel_for(int variant, int d, int bits, bool f16, int group);
+// The same with the stage-2 residual correction of m sign bits (isoq_scores_qjl.hip).
+ScoreKernel score_qjl_kernel_for(int variant, int d, int bits, bool f16, int group, int m);
 
 // Kernel entry for (variant, d, bits, fp16 rows?, generic set indexing?, mode),
 // or nullptr.  Generic set indexing is needed when there is more than one

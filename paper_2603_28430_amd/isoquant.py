@@ -57,6 +57,8 @@ def _load():
     L.isoq_sketch_destroy.argtypes = [vp]
     L.isoq_sketch_export.argtypes = [vp, ctypes.POINTER(c_int), fp]
     L.isoq_quantize_qjl.argtypes = [vp, vp, c_int, vp, i64, i64, vp, vp, vp, vp, vp]
+    L.isoq_kv_scores_qjl.argtypes = [vp, vp, c_int, vp, c_int, c_int, c_int, vp, vp, vp, vp, i64, c_int, vp, c_int,
+                                     vp, ctypes.c_float, vp, i64, vp]
     L.isoq_kv_scores.argtypes = [vp, c_int, vp, c_int, c_int, c_int, vp, vp, i64, c_int, vp, c_int, vp,
                                  ctypes.c_float, vp, i64, vp]
     L.isoq_packed_bytes.argtypes = [c_int, c_int]
@@ -73,7 +75,8 @@ def _load():
     L.isoq_last_hip_error.restype = ctypes.c_char_p
     for f in ("isoq_params_init", "isoq_params_destroy", "isoq_params_export", "isoq_params_info",
               "isoq_quantize", "isoq_dequantize", "isoq_roundtrip", "isoq_kv_append", "isoq_kv_scores", "isoq_sketch_init",
-              "isoq_sketch_destroy", "isoq_sketch_export", "isoq_quantize_qjl", "isoq_codebook_lloyd",
+              "isoq_sketch_destroy", "isoq_sketch_export", "isoq_quantize_qjl", "isoq_kv_scores_qjl",
+              "isoq_codebook_lloyd",
               "isoq_rotation_draws"):
         getattr(L, f).restype = c_int
     return L
@@ -296,7 +299,7 @@ def isoq_kv_append(pk: Params, k_new, slot_mapping, k_idx, k_rho, pv: Params = N
 
 
 def isoq_kv_scores(pk: Params, q, k_idx, k_rho, block_table, seq_lens, scale: float = 1.0,
-                   max_len=None, scores=None, stream=None):
+                   max_len=None, scores=None, stream=None, sketch=None, k_signs=None, k_gamma=None):
     """Attention logits scale * <q, k_hat> of queries q [n_seqs, n_q_heads, d]
     against the paged key cache k_idx [n_blocks, n_kv_heads, block_size, R] /
     k_rho [n_blocks, n_kv_heads, block_size], with block_table int32
@@ -322,14 +325,36 @@ def isoq_kv_scores(pk: Params, q, k_idx, k_rho, block_table, seq_lens, scale: fl
         scores = torch.empty((n_seqs, n_q_heads, max_len), dtype=torch.float32, device=q.device)
     elif tuple(scores.shape) != (n_seqs, n_q_heads, max_len) or scores.dtype != torch.float32:
         raise ValueError("scores must be fp32 [n_seqs, n_q_heads, max_len]")
-    for t in (q, k_idx, k_rho, block_table, seq_lens, scores):
+    ts = [q, k_idx, k_rho, block_table, seq_lens, scores]
+    if sketch is not None:
+        if k_signs is None or k_gamma is None:
+            raise ValueError("a sketch needs k_signs and k_gamma")
+        if (tuple(k_signs.shape) != (n_blocks, n_kv_heads, block_size, sketch.m // 8) or k_signs.dtype != torch.uint8
+                or tuple(k_gamma.shape) != tuple(k_rho.shape) or k_gamma.dtype != torch.float32):
+            raise ValueError("k_signs [n_blocks, n_kv_heads, block_size, m/8] uint8, k_gamma like k_rho")
+        ts += [k_signs, k_gamma]
+    for t in ts:
         if not t.is_cuda or not t.is_contiguous():
             raise ValueError("tensors must be contiguous and on the GPU")
-    _check(lib.isoq_kv_scores(pk.handle, _dtype_code(q.dtype), _ptr(q), int(n_seqs), int(n_q_heads),
-                              int(n_kv_heads), _ptr(k_idx), _ptr(k_rho), int(n_blocks), int(block_size),
-                              _ptr(block_table), int(max_blocks), _ptr(seq_lens), float(scale),
-                              _ptr(scores), int(max_len), _stream_ptr(stream)), "isoq_kv_scores")
+    if sketch is None:
+        _check(lib.isoq_kv_scores(pk.handle, _dtype_code(q.dtype), _ptr(q), int(n_seqs), int(n_q_heads),
+                                  int(n_kv_heads), _ptr(k_idx), _ptr(k_rho), int(n_blocks), int(block_size),
+                                  _ptr(block_table), int(max_blocks), _ptr(seq_lens), float(scale),
+                                  _ptr(scores), int(max_len), _stream_ptr(stream)), "isoq_kv_scores")
+    else:
+        _check(lib.isoq_kv_scores_qjl(pk.handle, sketch.handle, _dtype_code(q.dtype), _ptr(q), int(n_seqs),
+                                      int(n_q_heads), int(n_kv_heads), _ptr(k_idx), _ptr(k_rho), _ptr(k_signs),
+                                      _ptr(k_gamma), int(n_blocks), int(block_size), _ptr(block_table),
+                                      int(max_blocks), _ptr(seq_lens), float(scale), _ptr(scores), int(max_len),
+                                      _stream_ptr(stream)), "isoq_kv_scores_qjl")
     return scores
+
+
+def isoq_kv_scores_qjl(pk: Params, sketch, q, k_idx, k_rho, k_signs, k_gamma, block_table, seq_lens,
+                       scale: float = 1.0, max_len=None, scores=None, stream=None):
+    """isoq_kv_scores with the stage-2 residual correction (see include/isoquant.h)."""
+    return isoq_kv_scores(pk, q, k_idx, k_rho, block_table, seq_lens, scale, max_len, scores, stream,
+                          sketch=sketch, k_signs=k_signs, k_gamma=k_gamma)
 
 
 class Sketch:

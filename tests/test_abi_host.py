@@ -117,6 +117,8 @@ def test_argument_validation_before_any_device_call():
     assert binding.lib.isoq_sketch_destroy(None) == 0
     assert binding.lib.isoq_sketch_export(None, None, None) == 3
     assert binding.lib.isoq_quantize_qjl(None, None, 1, None, 4, 1, None, None, None, None, None) == 3
+    assert binding.lib.isoq_kv_scores_qjl(None, None, 1, None, 1, 1, 1, None, None, None, None, 1, 16, None, 1,
+                                          None, 1.0, None, 16, None) == 3
     assert binding.lib.isoq_params_destroy(None) == 0
     assert binding.lib.isoq_params_export(None, None, None, None) == 3
 
