@@ -32,13 +32,18 @@ sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBPS = 8000.0          # MI355X HBM3E, vendor figure
 METRIC = "fused quant-dequant vectors/s + effective HBM GB/s (% peak), d=128 3-bit fp16"
-KERNEL_SRC = os.path.join(ROOT, "paper_2603_28430_amd", "csrc", "isoq_kernels.hip")
+# every source the round-trip kernel is compiled from
+KERNEL_SRCS = [os.path.join(ROOT, "paper_2603_28430_amd", "csrc", f)
+               for f in ("isoq_kernels.hip", "isoq_stage1.h", "isoq_device.h", "isoq_internal.h")]
 PROFILES = os.path.join(ROOT, "profiles")
 
 
 def kernel_source_hash() -> str:
-    with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for path in KERNEL_SRCS:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def algorithmic_bytes(mode: str, n: int, d: int, bits: int, esz: int) -> int:
@@ -206,6 +211,43 @@ def kv_scores_side(torch, workloads):
             "GBps": b / ms / 1e6, "frac": b / ms / 1e6 / PEAK_HBM_GBPS}
 
 
+def kv_scores_qjl_side(torch, workloads):
+    """isoq_kv_scores_qjl: the logits of kv_scores_side with the stage-2
+    correction, m = 128 and 64 sign bits per key (same cache shape, random
+    records, norms, signs and gammas).  Algorithmic bytes per key: record,
+    norm, m/8 sign bytes, gamma and the logit."""
+    import paper_2603_28430_amd as iq
+
+    B, H, T, d, bs, bits = 8, 32, 32768, 128, 16, 3
+    p = iq.isoq_params_init("fast", d, bits, H, rot=workloads.rotation_draws("fast", d, H, seed=1))
+    nb = B * T // bs
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(4)
+    rec = torch.randint(0, 256, (nb, H, bs, p.record_bytes), dtype=torch.uint8, device="cuda", generator=gen)
+    rho = torch.rand((nb, H, bs), device="cuda", generator=gen) + 0.5
+    gam = torch.rand((nb, H, bs), device="cuda", generator=gen) * 0.2
+    table = torch.randperm(nb, device="cuda", generator=gen).to(torch.int32).view(B, T // bs)
+    lens = torch.full((B,), T, dtype=torch.int32, device="cuda")
+    q = torch.randn((B, H, d), device="cuda", generator=gen).to(torch.float16)
+    out = torch.empty((B, H, T), dtype=torch.float32, device="cuda")
+    res = {}
+    for m in (128, 64):
+        print(f"# kv scores qjl m={m}", file=sys.stderr, flush=True)
+        sk = iq.isoq_sketch_init(p, m)
+        sg = torch.randint(0, 256, (nb, H, bs, m // 8), dtype=torch.uint8, device="cuda", generator=gen)
+        fn = lambda i: iq.isoq_kv_scores_qjl(p, sk, q, rec, rho, sg, gam, table, lens, 0.0884, max_len=T,
+                                             scores=out)
+        ms = time_launches(fn, 50, 5, torch, 0.2)
+        keys = B * H * T
+        b = keys * (p.record_bytes + 4 + m // 8 + 4 + 4)
+        res[f"m{m}"] = {"shape": [B, H, T, d], "us_per_call": ms * 1e3, "keys_per_s": keys / (ms / 1e3),
+                        "GBps": b / ms / 1e6, "frac": b / ms / 1e6 / PEAK_HBM_GBPS}
+        sk.close()
+        del sg
+    p.close()
+    return res
+
+
 def qjl_side(torch, workloads):
     """isoq_quantize_qjl: stage-1 quantize plus the stage-2 residual sketch,
     1,048,576 unit-norm fp16 rows, d = 128, 3 bits, m = 128 and 64 sign bits.
@@ -263,6 +305,7 @@ def other_configs(measure, entry, torch, np, workloads):
     out["kv_append"] = kv_append_side(torch, workloads)
     out["kv_scores"] = kv_scores_side(torch, workloads)
     out["qjl_quantize"] = qjl_side(torch, workloads)
+    out["kv_scores_qjl"] = kv_scores_qjl_side(torch, workloads)
     print("# config kv cache", file=sys.stderr, flush=True)
     B, H, T, d_ = 8, 32, 32768, 128
     kv = [workloads.kv_stream_torch(B, H, T, d_, seed, "cuda").view(B * H * T, d_) for seed in (2, 3)]
@@ -294,7 +337,7 @@ def main() -> int:
     ap.add_argument("--no-extras", action="store_true")
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the side measurements of the d=256, d=512 and KV-cache workloads")
-    ap.add_argument("--side", choices=["kv-append", "kv-scores", "qjl"],
+    ap.add_argument("--side", choices=["kv-append", "kv-scores", "kv-scores-qjl", "qjl"],
                     help="run only this side measurement and print its JSON")
     ap.add_argument("--copy-only", action="store_true",
                     help="only time a plain device copy of the input size (counter calibration)")
@@ -312,7 +355,8 @@ def main() -> int:
 
     torch.cuda.set_device(0)
     if args.side:
-        fn = {"kv-append": kv_append_side, "kv-scores": kv_scores_side, "qjl": qjl_side}[args.side]
+        fn = {"kv-append": kv_append_side, "kv-scores": kv_scores_side, "kv-scores-qjl": kv_scores_qjl_side,
+              "qjl": qjl_side}[args.side]
         print(json.dumps({"side": args.side, **fn(torch, workloads)}), flush=True)
         return 0
     tdt, ndt, esz = {"f16": (torch.float16, np.float16, 2), "f32": (torch.float32, np.float32, 4)}[args.dtype]

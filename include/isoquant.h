@@ -25,8 +25,15 @@
  *     isoq_roundtrip (x_hat == x exactly).
  *   - A parameter handle is immutable after init; concurrent calls that share
  *     it are safe.  Only init and destroy allocate or free device memory.
- *   - Supported shapes in this version: d in {128, 256, 512}, bits in
- *     {2, 3, 4}, fp16 or fp32 rows (arithmetic is fp32 in every case).
+ *   - Supported shapes in this version: bits in {2, 3, 4}, fp16 or fp32 rows
+ *     (arithmetic is fp32 in every case); d from 1 to 1024 for quantize,
+ *     dequantize and round trip (tuned kernels for d in {128, 256, 512}, one
+ *     generic kernel family for every other width), d in {128, 256, 512} for
+ *     the KV-cache, attention-score and stage-2 calls.
+ *   - Widths that are not a multiple of the block size (4; 2-D: 2) follow
+ *     Sec. 5.1: the last block is zero padded, all pw rotated coordinates are
+ *     quantized and stored (pw = 4 ceil(d/4); 2-D: 2 ceil(d/2)), and the
+ *     padded coordinates are dropped after the inverse rotation.
  *   - Rows must be finite.  The squared norm is accumulated in fp32, so an
  *     fp32 row must have 1e-18 <= ||x|| <= 1e18 or be exactly zero (every fp16
  *     row qualifies); a zero row gives rho = 0, x_hat = 0 and every index
@@ -120,9 +127,10 @@ isoq_status isoq_params_info(const isoq_params *p, int *variant, int *d, int *bi
  * isoq_quantize -- encoder half of Algorithm 1: norm split, blockwise rotation,
  * scalar quantization.
  *   x          device, [n][d] rows of `dtype`.
- *   idx_packed device, [n][isoq_packed_bytes(d, bits)] bytes: per row one record
- *              in which rotated coordinate j occupies bits [j*bits, (j+1)*bits),
- *              bit m being bit (m mod 8) of byte m/8 (least significant first).
+ *   idx_packed device, [n][isoq_record_bytes(variant, d, bits)] bytes: per row
+ *              one record of the pw rotated coordinates in which coordinate j
+ *              occupies bits [j*bits, (j+1)*bits), bit m being bit (m mod 8) of
+ *              byte m/8 (least significant first); bits past pw*bits are 0.
  *   norms      device, [n] fp32 rho = ||x||_2.
  * Index of a coordinate y: number of thresholds t_k with y > t_k applied to the
  * direction x / max(rho, 1e-12).
@@ -274,10 +282,13 @@ isoq_status isoq_kv_scores_qjl(const isoq_params *pk, const isoq_sketch *sk, int
                                int max_blocks_per_seq, const int32_t *seq_lens, float scale, float *scores,
                                int64_t max_len, void *stream);
 
-/* Sizes: bytes of one packed index record, ceil(d * bits / 8); raw draws per
- * set for rot_host (Full 8 g4, Fast 4 g4, 2-D g2); exported parameters per set
- * (Full 8 g4, Fast 4 g4, 2-D 2 g2), with g4 = ceil(d/4), g2 = ceil(d/2).
- * Return 0 for invalid arguments. */
+/* Sizes: bytes of one packed index record, ceil(pw * bits / 8) with the
+ * padded width pw = 4 g4 (Full, Fast) or 2 g2 (2-D); isoq_packed_bytes is
+ * ceil(d * bits / 8), the same number whenever d is a multiple of 4.  Raw
+ * draws per set for rot_host (Full 8 g4, Fast 4 g4, 2-D g2); exported
+ * parameters per set (Full 8 g4, Fast 4 g4, 2-D 2 g2), with g4 = ceil(d/4),
+ * g2 = ceil(d/2).  Return 0 for invalid arguments. */
+size_t isoq_record_bytes(int variant, int d, int bits);
 size_t isoq_packed_bytes(int d, int bits);
 size_t isoq_raw_params_per_set(int variant, int d);
 size_t isoq_export_params_per_set(int variant, int d);

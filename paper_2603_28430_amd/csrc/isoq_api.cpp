@@ -15,7 +15,7 @@
 struct isoq_params {
     int variant, d, bits, n_sets;
     int device;
-    float *dparams;                 // device, [n_sets][d/8][params_per_lane], then the LUT
+    float *dparams;                 // device, [n_sets][slots_per_set][params_per_slot], then the LUT
     size_t lut_offset;              // floats from dparams to the magnitude LUT (0: none)
     int lut_cells;
     float lut_inv_h;
@@ -46,7 +46,10 @@ isoq_status hip_fail(hipError_t e, const char *where, isoq_status st = ISOQ_E_HI
 }
 
 bool valid_variant(int v) { return v == ISOQ_FULL || v == ISOQ_FAST || v == ISOQ_PLANAR2D; }
-bool supported_d(int d) { return d == 128 || d == 256 || d == 512; }
+// Widths of the tuned kernels (every entry point); other widths up to
+// kGenericMaxD have quantize, dequantize and round trip only.
+bool tuned_d(int d) { return d == 128 || d == 256 || d == 512; }
+bool supported_d(int d) { return d >= 1 && d <= kGenericMaxD; }
 bool supported_bits(int b) { return b >= 2 && b <= 4; }
 bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
@@ -73,7 +76,14 @@ isoq_status check_device(const isoq_params *p)
 // Rows of one block of the stage-1 kernels (a wave holds 512/d rows).
 int64_t rows_per_block(const isoq_params *p)
 {
+    if (!tuned_d(p->d))
+        return (int64_t)generic_rows_per_wave(slots_per_set(p->variant, p->d)) * (kBlockThreads / 64);
     return (int64_t)(64 / (p->d / kCoordsPerLane)) * (kBlockThreads / 64) * kTileGroups;
+}
+
+size_t record_bytes(int variant, int d, int bits)
+{
+    return ((size_t)padded_width(variant, d) * bits + 7) / 8;
 }
 
 // Per-handle kernel arguments: codebook halves, parameters, lookup table.
@@ -104,8 +114,34 @@ isoq_status launch(const void *fn, dim3 grid, void **args, void *stream)
     return ISOQ_OK;
 }
 
+isoq_status run_generic(const isoq_params *p, int dtype, int mode, KArgs &a, void *stream)
+{
+    const int slots = slots_per_set(p->variant, p->d);
+    const bool f16 = dtype == ISOQ_F16;
+    const void *fn = p->variant == VAR_FULL   ? generic_kernel_full(slots, p->bits, f16, mode)
+                     : p->variant == VAR_FAST ? generic_kernel_fast(slots, p->bits, f16, mode)
+                                              : generic_kernel_2d(slots, p->bits, f16, mode);
+    if (!fn)
+        return ISOQ_E_UNSUPPORTED;
+    const int64_t rpb = rows_per_block(p);
+    const int64_t blocks = (a.n + rpb - 1) / rpb;
+    if (blocks > 0x7FFFFFFF)
+        return ISOQ_E_UNSUPPORTED;
+    fill_args(p, a);
+    a.g_d = p->d;
+    a.g_pw = padded_width(p->variant, p->d);
+    a.g_slots = slots;
+    a.g_rec = (int32_t)record_bytes(p->variant, p->d, p->bits);
+    a.g_vec = p->d % 4 == 0;
+    a.g_set_stride = (int64_t)slots * params_per_slot(p->variant);
+    void *args[] = {&a};
+    return launch(fn, dim3((unsigned)blocks), args, stream);
+}
+
 isoq_status run(const isoq_params *p, int dtype, int mode, KArgs &a, void *stream)
 {
+    if (!tuned_d(p->d))
+        return run_generic(p, dtype, mode, a, stream);
     const bool f16 = dtype == ISOQ_F16;
     const int64_t rpb = rows_per_block(p);
     const bool generic = p->n_sets > 1 && (a.rows_per_set % rpb) != 0;
@@ -131,7 +167,7 @@ const char *isoq_status_string(isoq_status s)
     switch (s) {
     case ISOQ_OK: return "ok";
     case ISOQ_E_INVALID: return "invalid argument";
-    case ISOQ_E_UNSUPPORTED: return "unsupported shape (d in {128,256,512}, bits in {2,3,4}) or size limit";
+    case ISOQ_E_UNSUPPORTED: return "unsupported shape (d in 1..1024, bits in {2,3,4}; the KV, score and sketch calls need d in {128,256,512}) or size limit";
     case ISOQ_E_NULL: return "null pointer";
     case ISOQ_E_ALIGN: return "misaligned pointer";
     case ISOQ_E_HIP: return "HIP runtime error";
@@ -146,6 +182,13 @@ size_t isoq_packed_bytes(int d, int bits)
     if (d < 1 || bits < 1 || bits > 8)
         return 0;
     return ((size_t)d * bits + 7) / 8;
+}
+
+size_t isoq_record_bytes(int variant, int d, int bits)
+{
+    if (!valid_variant(variant) || d < 1 || bits < 1 || bits > 8)
+        return 0;
+    return record_bytes(variant, d, bits);
 }
 
 size_t isoq_raw_params_per_set(int variant, int d)
@@ -431,6 +474,8 @@ isoq_status isoq_kv_append(const isoq_params *pk, const isoq_params *pv, int dty
     if (has_v && (pv->variant != pk->variant || pv->d != pk->d || pv->bits != pk->bits ||
                   pv->device != pk->device))
         return ISOQ_E_INVALID;
+    if (!tuned_d(pk->d))
+        return ISOQ_E_UNSUPPORTED;
     if ((pk->n_sets != 1 && pk->n_sets != n_heads) || (has_v && pv->n_sets != 1 && pv->n_sets != n_heads))
         return ISOQ_E_INVALID;
     if (n_tokens > 0x7FFFFFFF / n_heads || n_blocks > 0x7FFFFFFF / block_size)
@@ -495,6 +540,8 @@ isoq_status kv_scores(const isoq_params *pk, const isoq_sketch *sk, int dtype, c
     if (sk && (sk->variant != pk->variant || sk->d != pk->d || sk->n_sets != pk->n_sets ||
                sk->device != pk->device))
         return ISOQ_E_INVALID;
+    if (!tuned_d(pk->d))
+        return ISOQ_E_UNSUPPORTED;
     const int64_t max_pos = std::min<int64_t>(max_len, (int64_t)max_blocks_per_seq * block_size);
     if (n_seqs > 65535 || (int64_t)max_blocks_per_seq * block_size > 0x7FFFFFFF ||
         (max_pos + kScoreChunk - 1) / kScoreChunk > 65535)

@@ -45,10 +45,14 @@ __device__ __forceinline__ uint32_t fast_div(uint32_t n, const FastDiv &f)
 template <int LPV>
 __device__ __forceinline__ float row_sum(float v)
 {
+    static_assert(LPV >= 4 && LPV <= 64 && (LPV & (LPV - 1)) == 0, "4 to 64 lanes, a power of two");
     v += dpp_f<DPP_QUAD_1032>(v);
     v += dpp_f<DPP_QUAD_2301>(v);
-    v += dpp_f<DPP_ROW_HALF_MIRROR>(v);
-    v += dpp_f<DPP_ROW_MIRROR>(v);
+    // half mirror: lane i of an 8-lane half takes lane 7 - i (the other quad)
+    if constexpr (LPV >= 8)
+        v += dpp_f<DPP_ROW_HALF_MIRROR>(v);
+    if constexpr (LPV >= 16)
+        v += dpp_f<DPP_ROW_MIRROR>(v);
     // across 16-lane rows: v_permlane16_swap exchanges odd rows of its first
     // operand with even rows of its second, v_permlane32_swap the upper half
     // of the first with the lower half of the second; with both operands v,
@@ -159,78 +163,82 @@ __device__ __forceinline__ void store_row_chunk(char *p, const float o[8])
 // 4x4 orthogonal matrix, precomputed at init); inverse v = M^T y (Prop. 1).
 // Fast: y = q_L v through the left-multiplication matrix of q_L = (a,b,c,d);
 // inverse conj(q_L) y = L(q_L)^T y.  2-D: y = R(theta) u, inverse R(-theta).
+//
+// A slot is 4 consecutive coordinates: one quaternion block, or two planar
+// pairs.  Its parameters: Full the 16 floats of M (row-major), Fast q_L,
+// 2-D (cos, sin) of each pair.
 template <int VAR>
-__device__ __forceinline__ void rotate_forward(const float *P, const float x[8], float y[8])
+constexpr int kSlotParams = VAR == VAR_FULL ? 16 : 4;
+
+template <int VAR>
+__device__ __forceinline__ void rotate4_forward(const float *P, const float *v, float *y)
 {
     if constexpr (VAR == VAR_FULL) {
 #pragma unroll
-        for (int b = 0; b < 2; b++) {
-            const float *M = P + 16 * b;
-            const float *v = x + 4 * b;
-#pragma unroll
-            for (int r = 0; r < 4; r++) {
-                float acc = M[4 * r] * v[0];
-                acc = fmaf(M[4 * r + 1], v[1], acc);
-                acc = fmaf(M[4 * r + 2], v[2], acc);
-                acc = fmaf(M[4 * r + 3], v[3], acc);
-                y[4 * b + r] = acc;
-            }
+        for (int r = 0; r < 4; r++) {
+            float acc = P[4 * r] * v[0];
+            acc = fmaf(P[4 * r + 1], v[1], acc);
+            acc = fmaf(P[4 * r + 2], v[2], acc);
+            acc = fmaf(P[4 * r + 3], v[3], acc);
+            y[r] = acc;
         }
     } else if constexpr (VAR == VAR_FAST) {
-#pragma unroll
-        for (int b = 0; b < 2; b++) {
-            const float a = P[4 * b], bb = P[4 * b + 1], c = P[4 * b + 2], d = P[4 * b + 3];
-            const float *v = x + 4 * b;
-            y[4 * b + 0] = fmaf(-d, v[3], fmaf(-c, v[2], fmaf(-bb, v[1], a * v[0])));
-            y[4 * b + 1] = fmaf(c, v[3], fmaf(-d, v[2], fmaf(a, v[1], bb * v[0])));
-            y[4 * b + 2] = fmaf(-bb, v[3], fmaf(a, v[2], fmaf(d, v[1], c * v[0])));
-            y[4 * b + 3] = fmaf(a, v[3], fmaf(bb, v[2], fmaf(-c, v[1], d * v[0])));
-        }
+        const float a = P[0], b = P[1], c = P[2], d = P[3];
+        y[0] = fmaf(-d, v[3], fmaf(-c, v[2], fmaf(-b, v[1], a * v[0])));
+        y[1] = fmaf(c, v[3], fmaf(-d, v[2], fmaf(a, v[1], b * v[0])));
+        y[2] = fmaf(-b, v[3], fmaf(a, v[2], fmaf(d, v[1], c * v[0])));
+        y[3] = fmaf(a, v[3], fmaf(b, v[2], fmaf(-c, v[1], d * v[0])));
     } else {
 #pragma unroll
-        for (int p = 0; p < 4; p++) {
+        for (int p = 0; p < 2; p++) {
             const float c = P[2 * p], s = P[2 * p + 1];
-            y[2 * p] = fmaf(-s, x[2 * p + 1], c * x[2 * p]);
-            y[2 * p + 1] = fmaf(c, x[2 * p + 1], s * x[2 * p]);
+            y[2 * p] = fmaf(-s, v[2 * p + 1], c * v[2 * p]);
+            y[2 * p + 1] = fmaf(c, v[2 * p + 1], s * v[2 * p]);
         }
     }
 }
 
 template <int VAR>
-__device__ __forceinline__ void rotate_inverse(const float *P, const float y[8], float o[8])
+__device__ __forceinline__ void rotate4_inverse(const float *P, const float *y, float *o)
 {
     if constexpr (VAR == VAR_FULL) {
 #pragma unroll
-        for (int b = 0; b < 2; b++) {
-            const float *M = P + 16 * b;
-            const float *v = y + 4 * b;
-#pragma unroll
-            for (int c = 0; c < 4; c++) {
-                float acc = M[c] * v[0];
-                acc = fmaf(M[4 + c], v[1], acc);
-                acc = fmaf(M[8 + c], v[2], acc);
-                acc = fmaf(M[12 + c], v[3], acc);
-                o[4 * b + c] = acc;
-            }
+        for (int c = 0; c < 4; c++) {
+            float acc = P[c] * y[0];
+            acc = fmaf(P[4 + c], y[1], acc);
+            acc = fmaf(P[8 + c], y[2], acc);
+            acc = fmaf(P[12 + c], y[3], acc);
+            o[c] = acc;
         }
     } else if constexpr (VAR == VAR_FAST) {
-#pragma unroll
-        for (int b = 0; b < 2; b++) {
-            const float a = P[4 * b], bb = P[4 * b + 1], c = P[4 * b + 2], d = P[4 * b + 3];
-            const float *v = y + 4 * b;
-            o[4 * b + 0] = fmaf(d, v[3], fmaf(c, v[2], fmaf(bb, v[1], a * v[0])));
-            o[4 * b + 1] = fmaf(-c, v[3], fmaf(d, v[2], fmaf(a, v[1], -bb * v[0])));
-            o[4 * b + 2] = fmaf(bb, v[3], fmaf(a, v[2], fmaf(-d, v[1], -c * v[0])));
-            o[4 * b + 3] = fmaf(a, v[3], fmaf(-bb, v[2], fmaf(c, v[1], -d * v[0])));
-        }
+        const float a = P[0], b = P[1], c = P[2], d = P[3];
+        o[0] = fmaf(d, y[3], fmaf(c, y[2], fmaf(b, y[1], a * y[0])));
+        o[1] = fmaf(-c, y[3], fmaf(d, y[2], fmaf(a, y[1], -b * y[0])));
+        o[2] = fmaf(b, y[3], fmaf(a, y[2], fmaf(-d, y[1], -c * y[0])));
+        o[3] = fmaf(a, y[3], fmaf(-b, y[2], fmaf(c, y[1], -d * y[0])));
     } else {
 #pragma unroll
-        for (int p = 0; p < 4; p++) {
+        for (int p = 0; p < 2; p++) {
             const float c = P[2 * p], s = P[2 * p + 1];
             o[2 * p] = fmaf(s, y[2 * p + 1], c * y[2 * p]);
             o[2 * p + 1] = fmaf(c, y[2 * p + 1], -s * y[2 * p]);
         }
     }
+}
+
+// A lane's 8 coordinates: two slots.
+template <int VAR>
+__device__ __forceinline__ void rotate_forward(const float *P, const float x[8], float y[8])
+{
+    rotate4_forward<VAR>(P, x, y);
+    rotate4_forward<VAR>(P + kSlotParams<VAR>, x + 4, y + 4);
+}
+
+template <int VAR>
+__device__ __forceinline__ void rotate_inverse(const float *P, const float y[8], float o[8])
+{
+    rotate4_inverse<VAR>(P, y, o);
+    rotate4_inverse<VAR>(P + kSlotParams<VAR>, y + 4, o + 4);
 }
 
 template <int PL>

@@ -1,0 +1,317 @@
+// Stage-1 kernels for vector widths outside {128, 256, 512}: any d from 1 to
+// 1024.  Algorithm 1 on the zero-padded vector of Sec. 5.1: when d is not a
+// multiple of the block size the last block is filled with zeros, all of its
+// rotated coordinates (4g in all, 2-D: 2 g2) are quantized and stored, and
+// the padded coordinates are dropped after the inverse rotation.
+//
+// Layout.  A row spans G lanes (G = 8 .. 64, a power of two) and lane s of
+// the row owns the 4-coordinate slots s, s + G, ..., s + (BPL - 1) G (a slot
+// is one quaternion block or two planar pairs), so consecutive lanes touch
+// consecutive slots.  A wave holds 64 / G rows per group and walks
+// kGenGroups groups, issuing every group's loads before computing.  The
+// record of a row is written and read bytewise: slot j's 4b index bits start
+// at bit 4b j.  Rows of a width that is a multiple of 4 move in one 8-byte
+// (fp16) or 16-byte (fp32) access per slot, other widths element by element.
+#pragma once
+
+#include "isoq_device.h"
+
+namespace isoq {
+namespace {
+
+constexpr int kGenGroups = 4;
+
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+
+template <bool F16>
+__device__ __forceinline__ void gen_load(const char *row, int j, int d, bool vec, float v[4])
+{
+    if (vec) {
+        if constexpr (F16) {
+            const f16x4 h = *reinterpret_cast<const f16x4 *>(row + 8 * j);
+#pragma unroll
+            for (int c = 0; c < 4; c++)
+                v[c] = (float)h[c];
+        } else {
+            const float4 f = *reinterpret_cast<const float4 *>(row + 16 * j);
+            v[0] = f.x;
+            v[1] = f.y;
+            v[2] = f.z;
+            v[3] = f.w;
+        }
+        return;
+    }
+#pragma unroll
+    for (int c = 0; c < 4; c++) {
+        const int i = 4 * j + c;
+        if constexpr (F16)
+            v[c] = i < d ? (float)reinterpret_cast<const _Float16 *>(row)[i] : 0.f;
+        else
+            v[c] = i < d ? reinterpret_cast<const float *>(row)[i] : 0.f;
+    }
+}
+
+template <bool F16>
+__device__ __forceinline__ void gen_store(char *row, int j, int d, bool vec, const float o[4])
+{
+    if (vec) {
+        if constexpr (F16) {
+            const f16x4 h = {(_Float16)o[0], (_Float16)o[1], (_Float16)o[2], (_Float16)o[3]};
+            *reinterpret_cast<f16x4 *>(row + 8 * j) = h;
+        } else {
+            *reinterpret_cast<float4 *>(row + 16 * j) = make_float4(o[0], o[1], o[2], o[3]);
+        }
+        return;
+    }
+#pragma unroll
+    for (int c = 0; c < 4; c++) {
+        const int i = 4 * j + c;
+        if (i < d) {
+            if constexpr (F16)
+                reinterpret_cast<_Float16 *>(row)[i] = (_Float16)o[c];
+            else
+                reinterpret_cast<float *>(row)[i] = o[c];
+        }
+    }
+}
+
+// Index bits of slot j (4 coordinates, BITS each) from a record of nb bytes.
+template <int BITS>
+__device__ __forceinline__ uint32_t gen_read_slot(const uint8_t *rec, int j, int nb)
+{
+    auto byte = [&](int k) -> uint32_t { return k < nb ? (uint32_t)rec[k] : 0u; };
+    if constexpr (BITS == 2)
+        return byte(j);
+    else if constexpr (BITS == 4)
+        return byte(2 * j) | (byte(2 * j + 1) << 8);
+    else if ((j & 1) == 0)   // bits 12 j .. 12 j + 11 start on a byte boundary
+        return byte(3 * j / 2) | ((byte(3 * j / 2 + 1) & 0xFu) << 8);
+    else                     // ... or in the middle of byte (3 j - 1) / 2
+        return (byte((3 * j - 1) / 2) >> 4) | (byte((3 * j + 1) / 2) << 4);
+}
+
+// Write the bytes whose first bit lies in slot j's bit range; `next` is the
+// next slot's index bits (only 3 bits per coordinate share a byte between
+// slots: the even slot owns it).
+template <int BITS>
+__device__ __forceinline__ void gen_write_slot(uint8_t *rec, int j, int nb, uint32_t p, uint32_t next)
+{
+    auto put = [&](int k, uint32_t v) {
+        if (k < nb)
+            rec[k] = (uint8_t)v;
+    };
+    if constexpr (BITS == 2) {
+        put(j, p);
+    } else if constexpr (BITS == 4) {
+        put(2 * j, p);
+        put(2 * j + 1, p >> 8);
+    } else if ((j & 1) == 0) {
+        put(3 * j / 2, p);
+        put(3 * j / 2 + 1, (p >> 8) | ((next & 0xFu) << 4));
+    } else {
+        put((3 * j + 1) / 2, p >> 4);
+    }
+}
+
+template <int VAR, int BITS, bool F16, int MODE, int G, int BPL>
+__global__ __launch_bounds__(kBlockThreads) void generic_kernel(const KArgs a)
+{
+    constexpr int R = 64 / G;                // rows per wave and group
+    constexpr int PS = kSlotParams<VAR>;
+    constexpr int H = 1 << (BITS - 1);
+    constexpr int ESZ = F16 ? 2 : 4;
+    constexpr bool kLoadX = MODE != MODE_DEQUANTIZE;
+    static_assert(MODE == MODE_ROUNDTRIP || MODE == MODE_QUANTIZE || MODE == MODE_DEQUANTIZE, "mode");
+
+    __shared__ float lev_s[16];
+    if constexpr (MODE == MODE_DEQUANTIZE) {
+        if (threadIdx.x == 0) {
+#pragma unroll
+            for (int k = 0; k < 2 * H; k++)
+                lev_s[k] = a.lev_all[k];
+        }
+        __syncthreads();
+    }
+
+    const int lane = threadIdx.x & 63;
+    const int sub = lane & (G - 1);
+    const int64_t row0 = ((int64_t)blockIdx.x * (kBlockThreads / 64) + (threadIdx.x >> 6)) * (kGenGroups * R) +
+                         lane / G;
+    const int d = a.g_d, slots = a.g_slots, nb = a.g_rec;
+    const bool vec = a.g_vec != 0;
+    const int64_t row_bytes = (int64_t)d * ESZ;
+
+    // ---- loads of every group first
+    float xv[kLoadX ? kGenGroups : 1][BPL][4];
+    uint32_t pin[kLoadX ? 1 : kGenGroups][BPL];
+    float rin[kLoadX ? 1 : kGenGroups];
+#pragma unroll
+    for (int t = 0; t < kGenGroups; t++) {
+        const int64_t row = row0 + (int64_t)t * R;
+        const bool ok = row < a.n;
+#pragma unroll
+        for (int k = 0; k < BPL; k++) {
+            const int j = sub + G * k;
+            const bool on = ok && j < slots;
+            if constexpr (kLoadX) {
+                if (on)
+                    gen_load<F16>(static_cast<const char *>(a.x) + row * row_bytes, j, d, vec, xv[t][k]);
+                else
+                    xv[t][k][0] = xv[t][k][1] = xv[t][k][2] = xv[t][k][3] = 0.f;
+            } else {
+                pin[t][k] = on ? gen_read_slot<BITS>(a.rec_in + row * nb, j, nb) : 0u;
+            }
+        }
+        if constexpr (!kLoadX)
+            rin[t] = ok ? a.norms_in[row] : 0.f;
+    }
+
+    // ---- rotation parameters of the lane's slots (reloaded when the set changes)
+    float P[BPL][PS];
+    int64_t pset = -1;
+    auto load_set = [&](int64_t set) {
+#pragma unroll
+        for (int k = 0; k < BPL; k++) {
+            const int j = min(sub + G * k, slots - 1);
+            load_params<PS>(a.params + set * a.g_set_stride + (int64_t)j * PS, P[k]);
+        }
+        pset = set;
+    };
+    if (a.n_sets == 1)
+        load_set(0);
+
+#pragma unroll
+    for (int t = 0; t < kGenGroups; t++) {
+        const int64_t row = row0 + (int64_t)t * R;
+        const bool ok = row < a.n;
+        if (a.n_sets > 1) {
+            const int64_t set = ok ? (row / a.rows_per_set) % a.n_sets : 0;
+            if (set != pset)
+                load_set(set);
+        }
+        float yq[BPL][4];
+        uint32_t pk[BPL];
+        float rho;
+        if constexpr (kLoadX) {
+            float s = 0.f;
+#pragma unroll
+            for (int k = 0; k < BPL; k++)
+#pragma unroll
+                for (int c = 0; c < 4; c++)
+                    s = fmaf(xv[t][k][c], xv[t][k][c], s);
+            rho = __builtin_amdgcn_sqrtf(row_sum<G>(s));
+            const float rho_e = fmaxf(rho, kEps);
+            // thresholds scaled by rho (the rotation is linear, so comparing
+            // |T x| with rho t equals comparing |T x / rho| with t); levels
+            // scaled by rho give rho * rec directly
+            float ths[H > 1 ? H - 1 : 1], lvs[H];
+#pragma unroll
+            for (int k = 0; k + 1 < H; k++)
+                ths[k] = a.thr_pos[k] * rho_e;
+#pragma unroll
+            for (int k = 0; k < H; k++)
+                lvs[k] = a.lev_pos[k] * rho;
+#pragma unroll
+            for (int k = 0; k < BPL; k++) {
+                const int j = sub + G * k;
+                float y[4];
+                rotate4_forward<VAR>(P[k], xv[t][k], y);
+                uint32_t p = 0;
+#pragma unroll
+                for (int c = 0; c < 4; c++) {
+                    const float m = fabsf(y[c]);
+                    float L = lvs[0];
+                    uint32_t cnt = 0;
+#pragma unroll
+                    for (int q = 0; q + 1 < H; q++) {
+                        const bool above = m > ths[q];
+                        L = above ? lvs[q + 1] : L;
+                        cnt += above ? 1u : 0u;
+                    }
+                    yq[k][c] = y[c] > 0.f ? L : -L;
+                    const uint32_t idx = y[c] > 0.f ? (uint32_t)H + cnt : (uint32_t)(H - 1) - cnt;
+                    p |= idx << (BITS * c);
+                }
+                // a planar slot past the padded width (its second pair is not
+                // a coordinate of the record) and slots past the row carry no bits
+                if (VAR == VAR_PLANAR2D && 4 * j + 2 >= a.g_pw)
+                    p &= (1u << (2 * BITS)) - 1u;
+                pk[k] = (ok && j < slots) ? p : 0u;
+            }
+        } else {
+            rho = rin[t];
+#pragma unroll
+            for (int k = 0; k < BPL; k++)
+#pragma unroll
+                for (int c = 0; c < 4; c++)
+                    yq[k][c] = lev_s[(pin[t][k] >> (BITS * c)) & (2 * H - 1)] * rho;
+        }
+
+        if constexpr (MODE == MODE_QUANTIZE) {
+#pragma unroll
+            for (int k = 0; k < BPL; k++) {
+                // the next slot of an even slot sits on the next lane (G is even)
+                const uint32_t next = BITS == 3 ? (uint32_t)__shfl_down((int)pk[k], 1, 64) : 0u;
+                const int j = sub + G * k;
+                if (ok && j < slots)
+                    gen_write_slot<BITS>(a.rec_out + row * nb, j, nb, pk[k], next);
+            }
+            if (ok && sub == 0)
+                a.norms_out[row] = rho;
+        } else {
+#pragma unroll
+            for (int k = 0; k < BPL; k++) {
+                const int j = sub + G * k;
+                if (ok && j < slots) {
+                    float o[4];
+                    rotate4_inverse<VAR>(P[k], yq[k], o);
+                    gen_store<F16>(static_cast<char *>(a.y) + row * row_bytes, j, d, vec, o);
+                }
+            }
+        }
+    }
+}
+
+// Row shape for a padded width of `slots` 4-coordinate slots: (G, BPL).
+template <int VAR, int BITS, bool F16, int MODE>
+const void *gen_pick_shape(int slots)
+{
+    if (slots <= 8)
+        return reinterpret_cast<const void *>(&generic_kernel<VAR, BITS, F16, MODE, 8, 1>);
+    if (slots <= 16)
+        return reinterpret_cast<const void *>(&generic_kernel<VAR, BITS, F16, MODE, 16, 1>);
+    if (slots <= 32)
+        return reinterpret_cast<const void *>(&generic_kernel<VAR, BITS, F16, MODE, 32, 1>);
+    if (slots <= 64)
+        return reinterpret_cast<const void *>(&generic_kernel<VAR, BITS, F16, MODE, 64, 1>);
+    if (slots <= 128)
+        return reinterpret_cast<const void *>(&generic_kernel<VAR, BITS, F16, MODE, 64, 2>);
+    if (slots <= 256)
+        return reinterpret_cast<const void *>(&generic_kernel<VAR, BITS, F16, MODE, 64, 4>);
+    return nullptr;
+}
+
+template <int VAR, int BITS, bool F16>
+const void *gen_pick_mode(int slots, int mode)
+{
+    switch (mode) {
+    case MODE_ROUNDTRIP: return gen_pick_shape<VAR, BITS, F16, MODE_ROUNDTRIP>(slots);
+    case MODE_QUANTIZE: return gen_pick_shape<VAR, BITS, F16, MODE_QUANTIZE>(slots);
+    case MODE_DEQUANTIZE: return gen_pick_shape<VAR, BITS, F16, MODE_DEQUANTIZE>(slots);
+    }
+    return nullptr;
+}
+
+template <int VAR>
+const void *gen_pick(int slots, int bits, bool f16, int mode)
+{
+    switch (bits) {
+    case 2: return f16 ? gen_pick_mode<VAR, 2, true>(slots, mode) : gen_pick_mode<VAR, 2, false>(slots, mode);
+    case 3: return f16 ? gen_pick_mode<VAR, 3, true>(slots, mode) : gen_pick_mode<VAR, 3, false>(slots, mode);
+    case 4: return f16 ? gen_pick_mode<VAR, 4, true>(slots, mode) : gen_pick_mode<VAR, 4, false>(slots, mode);
+    }
+    return nullptr;
+}
+
+}  // namespace
+}  // namespace isoq

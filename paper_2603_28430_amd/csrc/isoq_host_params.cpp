@@ -207,18 +207,20 @@ void rotate_rows_forward(int variant, int d, const float *unit_set, const double
 bool build_rotation(int variant, int d, int n_sets, const double *raw, std::vector<float> &exported,
                     std::vector<float> &device_layout)
 {
-    const int lpv = d / kCoordsPerLane;
-    const int pl = params_per_lane(variant);
+    // device layout: per set, slots_per_set slots of params_per_slot floats
+    // (a lane of the tuned kernels owns two consecutive slots)
+    const size_t per_set = (size_t)slots_per_set(variant, d) * params_per_slot(variant);
     const size_t rp = raw_per_set(variant, d);
     exported.assign((size_t)n_sets * export_per_set(variant, d), 0.f);
-    device_layout.assign((size_t)n_sets * lpv * pl, 0.f);
+    device_layout.assign((size_t)n_sets * per_set, 0.f);
     for (int s = 0; s < n_sets; s++) {
         const double *rs = raw + s * rp;
         float *ex = exported.data() + s * export_per_set(variant, d);
-        float *dv = device_layout.data() + (size_t)s * lpv * pl;
+        float *dv = device_layout.data() + (size_t)s * per_set;
         if (variant == VAR_PLANAR2D) {
-            // lane l owns pairs 4l .. 4l+3: (cos, sin) each
-            for (int j = 0; j < d / 2; j++) {
+            // slot l holds pairs 2l and 2l+1: (cos, sin) each
+            const int g2 = (d + 1) / 2;
+            for (int j = 0; j < g2; j++) {
                 if (!std::isfinite(rs[j]))
                     return false;
                 const double c = std::cos(rs[j]), sn = std::sin(rs[j]);
@@ -227,9 +229,12 @@ bool build_rotation(int variant, int d, int n_sets, const double *raw, std::vect
                 dv[2 * j] = (float)c;
                 dv[2 * j + 1] = (float)sn;
             }
+            if (g2 & 1)
+                dv[2 * g2] = 1.f;   // identity for the pair past the padded width
             continue;
         }
-        for (int i = 0; i < d / 4; i++) {
+        const int g = (d + 3) / 4;
+        for (int i = 0; i < g; i++) {
             double qL[4], qR[4] = {1, 0, 0, 0};
             if (!unit4(rs + (variant == VAR_FULL ? 8 : 4) * i, qL))
                 return false;
@@ -238,7 +243,7 @@ bool build_rotation(int variant, int d, int n_sets, const double *raw, std::vect
             if (variant == VAR_FAST) {
                 for (int c = 0; c < 4; c++) {
                     ex[4 * i + c] = (float)qL[c];
-                    dv[4 * i + c] = (float)qL[c];  // lane l: blocks 2l, 2l+1 -> floats 8l..8l+7
+                    dv[4 * i + c] = (float)qL[c];
                 }
                 continue;
             }
@@ -257,7 +262,6 @@ bool build_rotation(int variant, int d, int n_sets, const double *raw, std::vect
                 for (int r = 0; r < 4; r++)
                     M[r][c] = col[r];
             }
-            // lane l: blocks 2l, 2l+1 -> 16 floats each, row-major
             for (int r = 0; r < 4; r++)
                 for (int c = 0; c < 4; c++)
                     dv[16 * i + 4 * r + c] = (float)M[r][c];

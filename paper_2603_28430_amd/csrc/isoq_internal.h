@@ -26,6 +26,13 @@ constexpr int kTileGroups = 4;
 // 2-D (cos, sin) of the four pairs.
 inline int params_per_lane(int variant) { return variant == VAR_FULL ? 32 : 8; }
 
+// The same per 4-coordinate slot (one quaternion block or two planar pairs),
+// and the slots of a set: ceil(d/4) for Full and Fast, ceil(ceil(d/2) / 2)
+// for 2-D (an odd pair count leaves an identity pair in the last slot).
+inline int params_per_slot(int variant) { return variant == VAR_FULL ? 16 : 4; }
+inline int padded_width(int variant, int d) { return variant == VAR_PLANAR2D ? 2 * ((d + 1) / 2) : 4 * ((d + 3) / 4); }
+inline int slots_per_set(int variant, int d) { return (padded_width(variant, d) + 3) / 4; }
+
 // Division of 32-bit unsigned integers by a run-time constant d >= 1 through
 // one multiply-high, two shifts and two adds (Granlund and Montgomery,
 // "Division by invariant integers using multiplication", PLDI 1994, Fig. 4.1):
@@ -73,6 +80,14 @@ struct KArgs {
     const uint16_t *qjl_frag;  // [n_sets][m/16][d/32][64][8] fp16: S' = S T^{-1}, B-fragment order
     uint8_t *qjl_signs;        // [n][m/8] sign bits of S (x - x_hat)
     float *qjl_gamma;          // [n] ||x - x_hat||
+    // widths outside {128, 256, 512} (isoq_generic.h)
+    int32_t g_d;               // coordinates per row
+    int32_t g_pw;              // padded width: 4 ceil(d/4), 2-D 2 ceil(d/2)
+    int32_t g_slots;           // 4-coordinate slots per row, ceil(g_pw / 4)
+    int32_t g_rec;             // record bytes, ceil(g_pw * bits / 8)
+    int32_t g_vec;             // rows move in whole slots (d a multiple of 4)
+    int32_t pad2;
+    int64_t g_set_stride;      // floats per parameter set, kSlotParams * g_slots
 };
 
 // Attention logits against a paged cache of quantized keys (isoq_scores.hip).
@@ -116,6 +131,16 @@ ScoreKernel score_qjl_kernel_for(int variant, int d, int bits, bool f16, int gro
 // or nullptr.  Generic set indexing is needed when there is more than one
 // set and rows_per_set is not a multiple of the rows of a block.
 const void *kernel_for(int variant, int d, int bits, bool f16, bool generic_sets, int mode);
+// Stage-1 kernels for the other widths (d = 1 .. 1024) with `slots`
+// 4-coordinate slots per padded row, one per variant (isoq_generic_*.hip);
+// nullptr when no kernel fits.  Rows of one block: 4 waves x kGenRowsPerWave.
+const void *generic_kernel_full(int slots, int bits, bool f16, int mode);
+const void *generic_kernel_fast(int slots, int bits, bool f16, int mode);
+const void *generic_kernel_2d(int slots, int bits, bool f16, int mode);
+// Rows per wave of the generic kernels for a row of `slots` slots (64 / G
+// rows per group, 4 groups).
+inline int generic_rows_per_wave(int slots) { return 4 * (slots <= 8 ? 8 : slots <= 16 ? 4 : slots <= 32 ? 2 : 1); }
+constexpr int kGenericMaxD = 1024;
 // Blocks of the stage-2 sketch kernel with a single rotation set (each walks
 // several tiles).
 constexpr int64_t kQjlBlocks = 1024;

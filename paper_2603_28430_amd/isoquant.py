@@ -63,6 +63,8 @@ def _load():
                                  ctypes.c_float, vp, i64, vp]
     L.isoq_packed_bytes.argtypes = [c_int, c_int]
     L.isoq_packed_bytes.restype = ctypes.c_size_t
+    L.isoq_record_bytes.argtypes = [c_int, c_int, c_int]
+    L.isoq_record_bytes.restype = ctypes.c_size_t
     L.isoq_raw_params_per_set.argtypes = [c_int, c_int]
     L.isoq_raw_params_per_set.restype = ctypes.c_size_t
     L.isoq_export_params_per_set.argtypes = [c_int, c_int]
@@ -100,6 +102,10 @@ def isoq_status_string(status: int) -> str:
 
 def isoq_packed_bytes(d: int, bits: int) -> int:
     return int(lib.isoq_packed_bytes(int(d), int(bits)))
+
+
+def isoq_record_bytes(variant, d: int, bits: int) -> int:
+    return int(lib.isoq_record_bytes(_variant(variant), int(d), int(bits)))
 
 
 def isoq_raw_params_per_set(variant, d: int) -> int:
@@ -147,7 +153,7 @@ class Params:
 
     @property
     def record_bytes(self) -> int:
-        return isoq_packed_bytes(self.d, self.bits)
+        return isoq_record_bytes(self.variant, self.d, self.bits)
 
 
 def isoq_params_init(variant, d: int, bits: int, n_sets: int = 1, rot=None, codebook=None,
@@ -233,13 +239,15 @@ def isoq_roundtrip(p: Params, x, rows_per_set: int = 1, x_hat=None, stream=None)
 
 
 def isoq_quantize(p: Params, x, rows_per_set: int = 1, idx_packed=None, norms=None, stream=None):
-    """(packed index records [n, isoq_packed_bytes] uint8, norms [n] fp32)."""
+    """(packed index records [n, isoq_record_bytes] uint8, norms [n] fp32)."""
     torch = _torch()
     n = _rows(x, p.d)
     if idx_packed is None:
         idx_packed = torch.empty((n, p.record_bytes), dtype=torch.uint8, device=x.device)
     if norms is None:
         norms = torch.empty((n,), dtype=torch.float32, device=x.device)
+    if idx_packed.dtype != torch.uint8 or idx_packed.numel() != n * p.record_bytes or norms.numel() != n:
+        raise ValueError("idx_packed must hold n records of record_bytes bytes and norms n floats")
     _check(lib.isoq_quantize(p.handle, _dtype_code(x.dtype), ctypes.c_void_p(x.data_ptr()), n,
                              int(rows_per_set), ctypes.c_void_p(idx_packed.data_ptr()),
                              ctypes.c_void_p(norms.data_ptr()), _stream_ptr(stream)), "isoq_quantize")
@@ -253,6 +261,8 @@ def isoq_dequantize(p: Params, idx_packed, norms, dtype=None, rows_per_set: int 
     n = norms.numel()
     if x_hat is None:
         x_hat = torch.empty((n, p.d), dtype=dtype or torch.float16, device=norms.device)
+    if idx_packed.dtype != torch.uint8 or idx_packed.numel() != n * p.record_bytes or x_hat.numel() != n * p.d:
+        raise ValueError("idx_packed must hold one record per norm and x_hat one row of d per norm")
     _check(lib.isoq_dequantize(p.handle, _dtype_code(x_hat.dtype), ctypes.c_void_p(idx_packed.data_ptr()),
                                ctypes.c_void_p(norms.data_ptr()), n, int(rows_per_set),
                                ctypes.c_void_p(x_hat.data_ptr()), _stream_ptr(stream)), "isoq_dequantize")

@@ -29,7 +29,7 @@ def test_header_declares_the_boundary():
     names = _declared()
     for required in ("isoq_params_init", "isoq_params_destroy", "isoq_params_export",
                      "isoq_quantize", "isoq_dequantize", "isoq_roundtrip", "isoq_kv_append",
-                     "isoq_kv_scores", "isoq_packed_bytes",
+                     "isoq_kv_scores", "isoq_packed_bytes", "isoq_record_bytes",
                      "isoq_status_string"):
         assert required in names
 
@@ -52,6 +52,16 @@ def test_sizes():
             assert iq.isoq_raw_params_per_set(v, d) == workloads.raw_params_per_set(v, d)
             assert iq.isoq_export_params_per_set(v, d) == oracle.table1_params(v, d)
     assert iq.isoq_raw_params_per_set(7, 128) == 0
+    # records hold the padded width: 4 ceil(d/4) coordinates, 2-D 2 ceil(d/2)
+    for v in ("full", "fast", "2d"):
+        for d in (1, 2, 3, 5, 6, 7, 90, 91, 96, 128, 1000, 1023):
+            for b in (2, 3, 4):
+                pw = oracle.padded_width(v, d)
+                assert iq.isoq_record_bytes(v, d, b) == oracle.record_bytes(pw, b)
+                if d % 4 == 0:
+                    assert iq.isoq_record_bytes(v, d, b) == iq.isoq_packed_bytes(d, b)
+    assert iq.isoq_record_bytes("full", 0, 3) == 0
+    assert iq.isoq_record_bytes("2d", 9, 3) == 4 and iq.isoq_record_bytes("full", 9, 3) == 5
 
 
 def test_status_strings():
@@ -61,7 +71,7 @@ def test_status_strings():
 
 
 @pytest.mark.parametrize("bits", [2, 3, 4])
-@pytest.mark.parametrize("d", [128, 256, 512])
+@pytest.mark.parametrize("d", [128, 256, 512, 5, 90, 1000])
 def test_library_codebook_matches_oracle(bits, d):
     lib_levels = iq.isoq_codebook_lloyd(bits, d, 200)
     ref = oracle.codebook(bits, d, 200)
@@ -91,7 +101,7 @@ def test_argument_validation_before_any_device_call():
     assert init(None, 0, 128, 3, 1, None, None, 1) == 3            # NULL out
     assert init(ctypes.byref(h), 5, 128, 3, 1, None, None, 1) == 1  # bad variant
     assert init(ctypes.byref(h), 0, 128, 3, 0, None, None, 1) == 1  # n_sets < 1
-    assert init(ctypes.byref(h), 0, 96, 3, 1, None, None, 1) == 2   # d outside {128,256,512}
+    assert init(ctypes.byref(h), 0, 1025, 3, 1, None, None, 1) == 2  # d outside 1..1024
     assert init(ctypes.byref(h), 0, 128, 5, 1, None, None, 1) == 2  # bits outside {2,3,4}
     assert h.value is None
     bad = np.array([-1.0, -0.5, 0.2, 1.0])                          # not symmetric

@@ -1,0 +1,137 @@
+"""Parity of the generic-width stage-1 kernels (any d from 1 to 1024 outside
+{128, 256, 512}; Sec. 5.1 zero padding when d is not a multiple of the block
+size) with the oracle, through the C ABI.
+
+Per case: isoq_quantize, isoq_dequantize and isoq_roundtrip on the same rows;
+the fused path equals quantize followed by dequantize bit for bit; indices,
+norms and reconstructions against the oracle under the rule of
+tests/parity.py; the raw record equals the packing of its own indices (all
+pw = padded-width coordinates, bits past pw * bits zero).  Needs an MI355X."""
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from parity import Oracle
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+if not torch.cuda.is_available():
+    pytest.skip("no GPU", allow_module_level=True)
+
+import paper_2603_28430_amd as iq  # noqa: E402
+
+DT = {"f16": (torch.float16, np.float16), "f32": (torch.float32, np.float32)}
+
+# widths below, between and above the tuned ones; odd, 2 mod 4 and
+# multiple-of-4 widths; every row shape of the generic kernels (8 to 64 lanes,
+# 1 to 4 slots per lane) and its largest width
+WIDTHS = [1, 2, 3, 5, 6, 7, 20, 32, 33, 64, 80, 90, 96, 100, 127, 130, 192, 250, 256 + 4, 320, 384, 511, 640,
+          1000, 1024]
+
+
+def check(variant, d, bits, dtype, n, n_sets=1, rows_per_set=1, x=None, sample=None, seed=0):
+    tdt, ndt = DT[dtype]
+    rot = workloads.rotation_draws(variant, d, n_sets, seed=1)
+    levels = oracle.codebook(bits, d)
+    p = iq.isoq_params_init(variant, d, bits, n_sets, rot=rot, codebook=levels)
+    if x is None:
+        x = workloads.unit_gaussian_rows(n, d, seed=seed, dtype=ndt)
+    xg = torch.from_numpy(x).cuda()
+    idx, rho = iq.isoq_quantize(p, xg, rows_per_set)
+    xdq = iq.isoq_dequantize(p, idx, rho, dtype=tdt, rows_per_set=rows_per_set)
+    xrt = iq.isoq_roundtrip(p, xg, rows_per_set)
+    torch.cuda.synchronize()
+    idx, rho, xdq, xrt = idx.cpu().numpy(), rho.cpu().numpy(), xdq.cpu().numpy(), xrt.cpu().numpy()
+    assert np.array_equal(xrt.view(np.uint8), xdq.view(np.uint8))
+    pw = oracle.padded_width(variant, d)
+    assert idx.shape[1] == oracle.record_bytes(pw, bits) == iq.isoq_record_bytes(variant, d, bits)
+    sel = slice(None) if sample is None else sample
+    idx_g = oracle.unpack(idx[sel], pw, bits)
+    np.testing.assert_array_equal(oracle.pack(idx_g, bits), idx[sel])
+    o = Oracle(variant, d, bits, rot, levels, x, n_sets, rows_per_set, rows=sample)
+    o.check_indices(idx_g)
+    o.check_norms(rho[sel])
+    o.check_xhat(xrt[sel], ndt)
+    p.close()
+
+
+@pytest.mark.parametrize("d", WIDTHS)
+@pytest.mark.parametrize("variant", ["full", "fast", "2d"])
+def test_widths_parity(variant, d):
+    # several blocks and a ragged last group for every row shape
+    n = 1037 if d <= 256 else 263
+    for bits in (2, 3, 4):
+        for dtype in ("f16", "f32"):
+            print(f"case {variant} d={d} b={bits} {dtype} n={n}", flush=True)
+            check(variant, d, bits, dtype, n, seed=d + bits)
+
+
+@pytest.mark.parametrize("rows_per_set", [1, 5, 64, 1000])
+@pytest.mark.parametrize("variant,d", [("full", 90), ("fast", 96), ("2d", 75)])
+def test_widths_multiple_sets(variant, d, rows_per_set):
+    print(f"case {variant} d={d} sets=3 rps={rows_per_set}", flush=True)
+    check(variant, d, 3, "f16", 2003, n_sets=3, rows_per_set=rows_per_set)
+
+
+@pytest.mark.parametrize("n", [1, 2, 3, 5, 33])
+def test_widths_tiny_batches(n):
+    for variant in ("full", "fast", "2d"):
+        for d in (3, 64, 90, 1000):
+            print(f"case {variant} d={d} n={n}", flush=True)
+            check(variant, d, 3, "f32", n, seed=n)
+
+
+def test_widths_zero_and_scaled_rows():
+    for variant, d in (("full", 90), ("fast", 64), ("2d", 91)):
+        x = workloads.unit_gaussian_rows(64, d, seed=3, dtype=np.float32)
+        x[0] = 0.0
+        x[1] *= 1e-15
+        x[2] *= 1e15
+        x[3, : d // 2] = 0.0
+        print(f"case {variant} d={d} zero and scaled rows", flush=True)
+        check(variant, d, 3, "f32", 64, x=x)
+        p = iq.isoq_params_init(variant, d, 3, 1)
+        xg = torch.from_numpy(x).cuda()
+        idx, rho = iq.isoq_quantize(p, xg)
+        xh = iq.isoq_roundtrip(p, xg)
+        pw = oracle.padded_width(variant, d)
+        assert np.all(oracle.unpack(idx[:1].cpu().numpy(), pw, 3) == 3)
+        assert float(rho[0]) == 0.0 and torch.count_nonzero(xh[0]).item() == 0
+
+
+@pytest.mark.parametrize("variant,d,dtype", [("full", 96, "f16"), ("fast", 80, "f16"), ("2d", 90, "f32"),
+                                             ("full", 1000, "f32")])
+def test_widths_large_sampled(variant, d, dtype):
+    """Many row groups per block and a grid of thousands of blocks: sampled
+    rows against the oracle, every row for the fused identity."""
+    n = 1_000_003 if d <= 128 else 100_003
+    rng = np.random.default_rng(6)
+    sample = np.unique(np.concatenate([np.arange(64), np.arange(n - 64, n), rng.integers(0, n, 3000)]))
+    print(f"case {variant} d={d} {dtype} n={n}", flush=True)
+    check(variant, d, 3, dtype, n, sample=sample)
+
+
+def test_widths_unsupported_calls():
+    """Widths outside the generic range, and the KV / score / sketch calls at
+    a generic width, return ISOQ_E_UNSUPPORTED before any launch."""
+    with pytest.raises(iq.IsoqError) as e:
+        iq.isoq_params_init("full", 1025, 3, 1)
+    assert e.value.status == 2
+    p = iq.isoq_params_init("fast", 96, 3, 1)
+    with pytest.raises(iq.IsoqError) as e:
+        iq.isoq_sketch_init(p, 64)
+    assert e.value.status == 2
+    z = lambda *s, dt=torch.uint8: torch.zeros(s, dtype=dt, device="cuda")
+    R = p.record_bytes
+    lib = iq.isoquant.lib
+    k = z(4, 1, 96, dt=torch.float16)
+    slots = torch.arange(4, dtype=torch.int64, device="cuda")
+    rec, rho = z(2, 1, 16, R), z(2, 1, 16, dt=torch.float32)
+    assert lib.isoq_kv_append(p.handle, None, 1, k.data_ptr(), None, slots.data_ptr(), 4, 1, rec.data_ptr(),
+                              rho.data_ptr(), None, None, 2, 16, None) == 2
+    q = z(1, 1, 96, dt=torch.float16)
+    tab, lens = z(1, 2, dt=torch.int32), torch.ones((1,), dtype=torch.int32, device="cuda")
+    out = z(1, 1, 32, dt=torch.float32)
+    assert lib.isoq_kv_scores(p.handle, 1, q.data_ptr(), 1, 1, 1, rec.data_ptr(), rho.data_ptr(), 2, 16,
+                              tab.data_ptr(), 2, lens.data_ptr(), 1.0, out.data_ptr(), 32, None) == 2

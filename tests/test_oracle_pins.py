@@ -402,6 +402,30 @@ def test_zero_padding_when_d_not_multiple_of_four():
         np.testing.assert_allclose(xh[r], rho[r] * rec[:d], rtol=1e-15, atol=1e-17)
 
 
+@pytest.mark.parametrize("variant,d,pw", [("2d", 5, 6), ("2d", 9, 10), ("fast", 7, 8), ("fast", 1, 4)])
+def test_zero_padding_other_variants(variant, d, pw):
+    """Odd widths in the 2-D case pad the last pair, widths below a multiple
+    of 4 pad the last quaternion block (Sec. 5.1, Algorithm 1): the result is
+    the pw-wide path on the zero-padded direction with the padded outputs
+    dropped, and the record holds all pw rotated coordinates."""
+    bits = 3
+    rng = _rng(18)
+    x = rng.standard_normal((40, d))
+    rot = workloads.rotation_draws(variant, pw, 1, seed=7)
+    assert len(rot) == workloads.raw_params_per_set(variant, d)
+    c = oracle.codebook(bits, d)
+    idx, rho, xh = oracle.stage1(variant, d, bits, rot, c, x)
+    assert idx.shape == (40, pw) and oracle.padded_width(variant, d) == pw
+    thr = oracle.thresholds(bits, c)
+    for r in range(40):
+        xb = np.zeros(pw)
+        xb[:d] = x[r] / np.linalg.norm(x[r])
+        y = oracle.encode(variant, pw, rot, xb)
+        np.testing.assert_array_equal(idx[r], np.searchsorted(thr, y))
+        rec = oracle.decode(variant, pw, rot, c[idx[r]])
+        np.testing.assert_allclose(xh[r], rho[r] * rec[:d], rtol=1e-15, atol=1e-17)
+
+
 def test_multiple_parameter_sets():
     d, bits, n_sets, rps = 16, 3, 3, 2
     rng = _rng(17)
