@@ -280,6 +280,47 @@ def qjl_side(torch, workloads):
     return out
 
 
+def widths_side(torch, workloads):
+    """Generic-width kernels (widths outside {128, 256, 512}, Sec. 5.1 zero
+    padding): round trip and quantize of 1,048,576 unit-norm rows (262,144 for
+    d = 1000), Full and Fast, 3 bits.  Algorithmic bytes per row as for the
+    tuned widths: 2 d s for the round trip, d s + record + 4 for quantize (s =
+    bytes per element, record = ceil(pw * 3 / 8))."""
+    import numpy as np
+
+    import paper_2603_28430_amd as iq
+
+    out = {}
+    for d, dtype, n in ((64, "f16", 1 << 20), (80, "f16", 1 << 20), (96, "f16", 1 << 20), (90, "f16", 1 << 20),
+                        (192, "f16", 1 << 20), (1000, "f32", 1 << 18)):
+        tdt, ndt, esz = (torch.float16, np.float16, 2) if dtype == "f16" else (torch.float32, np.float32, 4)
+        name = f"d{d}_{dtype}_n{n}"
+        print(f"# widths {name}", file=sys.stderr, flush=True)
+        x0 = torch.from_numpy(workloads.unit_gaussian_rows(n, d, seed=0, dtype=ndt)).cuda()
+        xs = [x0] + [x0.clone() for _ in range(2)]
+        ys = [torch.empty_like(x0) for _ in range(3)]
+        res = {}
+        for variant in ("full", "fast"):
+            p = iq.isoq_params_init(variant, d, 3, 1, rot=workloads.rotation_draws(variant, d, 1, seed=1))
+            R = p.record_bytes
+            recs = [iq.isoq_quantize(p, xs[i]) for i in range(3)]
+            for mode in ("roundtrip", "quantize"):
+                if mode == "roundtrip":
+                    fn = lambda i: iq.isoq_roundtrip(p, xs[i % 3], x_hat=ys[i % 3])
+                    b = n * 2 * d * esz
+                else:
+                    fn = lambda i: iq.isoq_quantize(p, xs[i % 3], idx_packed=recs[i % 3][0], norms=recs[i % 3][1])
+                    b = n * (d * esz + R + 4)
+                ms = time_launches(fn, 50, 5, torch, 0.2)
+                res[f"{variant}_{mode}"] = {"us": ms * 1e3, "vectors_per_s": n / (ms / 1e3), "GBps": b / ms / 1e6,
+                                            "frac": b / ms / 1e6 / PEAK_HBM_GBPS}
+            p.close()
+        out[name] = res
+        del x0, xs, ys
+        torch.cuda.empty_cache()
+    return out
+
+
 def other_configs(measure, entry, torch, np, workloads):
     """Side measurements of the other workloads (their parity is tested in
     tests/test_gpu_full_sizes.py): d = 256 fp16 and d = 512 fp32 round trips
@@ -306,6 +347,7 @@ def other_configs(measure, entry, torch, np, workloads):
     out["kv_scores"] = kv_scores_side(torch, workloads)
     out["qjl_quantize"] = qjl_side(torch, workloads)
     out["kv_scores_qjl"] = kv_scores_qjl_side(torch, workloads)
+    out["widths"] = widths_side(torch, workloads)
     print("# config kv cache", file=sys.stderr, flush=True)
     B, H, T, d_ = 8, 32, 32768, 128
     kv = [workloads.kv_stream_torch(B, H, T, d_, seed, "cuda").view(B * H * T, d_) for seed in (2, 3)]
@@ -337,7 +379,7 @@ def main() -> int:
     ap.add_argument("--no-extras", action="store_true")
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the side measurements of the d=256, d=512 and KV-cache workloads")
-    ap.add_argument("--side", choices=["kv-append", "kv-scores", "kv-scores-qjl", "qjl"],
+    ap.add_argument("--side", choices=["kv-append", "kv-scores", "kv-scores-qjl", "qjl", "widths"],
                     help="run only this side measurement and print its JSON")
     ap.add_argument("--copy-only", action="store_true",
                     help="only time a plain device copy of the input size (counter calibration)")
@@ -356,7 +398,7 @@ def main() -> int:
     torch.cuda.set_device(0)
     if args.side:
         fn = {"kv-append": kv_append_side, "kv-scores": kv_scores_side, "kv-scores-qjl": kv_scores_qjl_side,
-              "qjl": qjl_side}[args.side]
+              "qjl": qjl_side, "widths": widths_side}[args.side]
         print(json.dumps({"side": args.side, **fn(torch, workloads)}), flush=True)
         return 0
     tdt, ndt, esz = {"f16": (torch.float16, np.float16, 2), "f32": (torch.float32, np.float32, 4)}[args.dtype]
