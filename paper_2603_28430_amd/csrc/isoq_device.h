@@ -74,13 +74,14 @@ struct Raw {
     u32x4 w[F16 ? 1 : 2];
 };
 
+// A lane's 8 coordinates: one 16-byte piece (fp16), or two (fp32), the
+// second `step` bytes after the first.
 template <bool F16>
-__device__ __forceinline__ void load_row_chunk(const char *p, Raw<F16> &r)
+__device__ __forceinline__ void load_row_chunk(const char *p, Raw<F16> &r, int step = 16)
 {
-    const u32x4 *q = reinterpret_cast<const u32x4 *>(p);
-    r.w[0] = __builtin_nontemporal_load(q);
+    r.w[0] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
     if constexpr (!F16)
-        r.w[1] = __builtin_nontemporal_load(q + 1);
+        r.w[1] = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p + step));
 }
 
 template <bool F16>
@@ -106,27 +107,39 @@ __device__ __forceinline__ void unpack(const Raw<F16> &r, float x[8])
     }
 }
 
+// Squared norm of one 4-coordinate slot (fp32 rows).
+__device__ __forceinline__ float slot_squares(const float *x)
+{
+    float s = x[0] * x[0];
+    s = fmaf(x[1], x[1], s);
+    s = fmaf(x[2], x[2], s);
+    return fmaf(x[3], x[3], s);
+}
+
+// A lane's part of the squared norm.  fp32 rows: the sum of its two slots'
+// squared norms, so that a row's total is one balanced tree over its slots in
+// order whether a lane owns adjacent slots (added here, then reduced across
+// lanes) or slots half a row apart (each half reduced across lanes, then the
+// halves added).
 template <bool F16>
 __device__ __forceinline__ float sum_squares(const Raw<F16> &r, const float x[8])
 {
-    float s = 0.f;
     if constexpr (F16) {
+        float s = 0.f;
 #pragma unroll
         for (int k = 0; k < 4; k++) {
             const uint32_t e = r.w[0][k];
             const f16x2 h = __builtin_bit_cast(f16x2, e);
             s = __builtin_amdgcn_fdot2(h, h, s, false);
         }
+        return s;
     } else {
-#pragma unroll
-        for (int k = 0; k < 8; k++)
-            s = fmaf(x[k], x[k], s);
+        return slot_squares(x) + slot_squares(x + 4);
     }
-    return s;
 }
 
 template <bool F16>
-__device__ __forceinline__ void store_row_chunk(char *p, const float o[8])
+__device__ __forceinline__ void store_row_chunk(char *p, const float o[8], int step = 16)
 {
     u32x4 *q = reinterpret_cast<u32x4 *>(p);
     if constexpr (F16) {
@@ -150,11 +163,12 @@ __device__ __forceinline__ void store_row_chunk(char *p, const float o[8])
             a[k] = __float_as_uint(o[k]);
             b[k] = __float_as_uint(o[4 + k]);
         }
-        // plain (write-back) stores: each instruction covers half of every
-        // 32-byte span of the wave's rows; L2 merges the two halves before the
-        // line goes out (streaming stores wrote such lines out twice)
+        // plain (write-back) stores: with adjacent pieces each instruction
+        // covers half of every 32-byte span of the wave's rows, and L2 merges
+        // the two halves before the line goes out (streaming stores wrote such
+        // lines out twice)
         q[0] = a;
-        q[1] = b;
+        *reinterpret_cast<u32x4 *>(p + step) = b;
     }
 }
 

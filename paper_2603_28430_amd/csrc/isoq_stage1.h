@@ -146,6 +146,13 @@ struct Stage1 {
     static constexpr int64_t ROWB = (int64_t)D * (F16 ? 2 : 4);  // bytes per row
     static constexpr int64_t RECB = (int64_t)D * BITS / 8;       // bytes per index record
     static constexpr int LANEB = F16 ? 16 : 32;         // row bytes per lane
+    // fp32 round trip: lane `sub` owns slots sub and sub + LPV (coordinates
+    // 4 sub .. +3 and D/2 + 4 sub .. +3), so each 16-byte access instruction
+    // of a wave covers one contiguous span; elsewhere it owns slots 2 sub and
+    // 2 sub + 1 (the record layout of the index bits follows that order)
+    static constexpr bool kSplit = !F16 && MODE == MODE_ROUNDTRIP;
+    static constexpr int kLaneOff = kSplit ? 16 : LANEB;       // bytes to lane sub's first piece
+    static constexpr int kStep = kSplit ? (int)(ROWB / 2) : 16;  // bytes to its second piece
     static constexpr bool kUseLut = BITS == 4;           // magnitude lookup table
     static constexpr bool kQjl = MODE == MODE_QJL;
     static constexpr bool kEncode = MODE == MODE_QUANTIZE || MODE == MODE_APPEND || kQjl;  // records out
@@ -153,6 +160,17 @@ struct Stage1 {
     // stage-2 sketch: a wave's tile of rows, its fp16 error rows in LDS
     static constexpr int kTileRows = kTileGroups * VPW;   // 16 (d = 128) or 8 (d = 256)
     static constexpr int kEStride = D + 8;                // halfs per LDS error row (padded)
+
+    // The lane's two slots' rotation parameters from a set's [2 LPV][PL / 2].
+    __device__ static __forceinline__ void lane_params(const float *set, int sub, float P[PL])
+    {
+        if constexpr (kSplit) {
+            load_params<PL / 2>(set + sub * (PL / 2), P);
+            load_params<PL / 2>(set + (sub + LPV) * (PL / 2), P + PL / 2);
+        } else {
+            load_params<PL>(set + sub * PL, P);
+        }
+    }
 
     struct In {
         Raw<F16> raw;
@@ -186,8 +204,8 @@ struct Stage1 {
                                     (uint32_t)(lr * (uint32_t)tstride + sub * LANEB),
                                 in.raw);
         } else {
-            load_row_chunk<F16>(static_cast<const char *>(a.x) + grow * ROWB + (uint32_t)(lr * ROWB + sub * LANEB),
-                                in.raw);
+            load_row_chunk<F16>(static_cast<const char *>(a.x) + grow * ROWB + (uint32_t)(lr * ROWB + sub * kLaneOff),
+                                in.raw, kStep);
         }
     }
 
@@ -208,7 +226,9 @@ struct Stage1 {
         } else {
             float x[8];
             unpack<F16>(in.raw, x);
-            const float rho = __builtin_amdgcn_sqrtf(row_sum<LPV>(sum_squares<F16>(in.raw, x)));
+            const float ss = kSplit ? row_sum<LPV>(slot_squares(x)) + row_sum<LPV>(slot_squares(x + 4))
+                                    : row_sum<LPV>(sum_squares<F16>(in.raw, x));
+            const float rho = __builtin_amdgcn_sqrtf(ss);
             const float rho_e = fmaxf(rho, kEps);
             float y[8], m[8];
             // selected levels are scaled by rho for the round trip (it then
@@ -245,7 +265,9 @@ struct Stage1 {
 #pragma unroll
             for (int k = 0; k < H - 1; k++)
                 ths[k] = thr[k] * rho_e;
-            if constexpr (kLevels) {
+            // with the sketch the levels come from the encoder's own
+            // compares (below); the round trip runs the compare chain
+            if constexpr (kLevels && !kQjl) {
                 float lvs[H];
 #pragma unroll
                 for (int k = 0; k < H; k++)
@@ -293,8 +315,20 @@ struct Stage1 {
                             const bool lo = m[j] > (hi ? ths[2] : ths[0]);
                             o[1] = ~(__builtin_amdgcn_ballot_w64(hi) ^ pos);
                             o[2] = ~(__builtin_amdgcn_ballot_w64(lo) ^ pos);
+                            if constexpr (kQjl) {
+                                // normalised level of magnitude index 2 hi + lo
+                                const float La = lo ? lev[1] : lev[0];
+                                const float Lb = lo ? lev[3] : lev[2];
+                                const float L = hi ? Lb : La;
+                                yq[j] = y[j] > 0.f ? L : -L;
+                            }
                         } else {
-                            o[1] = ~(__builtin_amdgcn_ballot_w64(m[j] > ths[0]) ^ pos);
+                            const bool above = m[j] > ths[0];
+                            o[1] = ~(__builtin_amdgcn_ballot_w64(above) ^ pos);
+                            if constexpr (kQjl) {
+                                const float L = above ? lev[1] : lev[0];
+                                yq[j] = y[j] > 0.f ? L : -L;
+                            }
                         }
                     }
                     if constexpr (CPB * BITS == 12)
@@ -337,7 +371,8 @@ struct Stage1 {
         if constexpr (!kEncode) {
             float o[8];
             rotate_inverse<VAR>(P, yq, o);
-            store_row_chunk<F16>(static_cast<char *>(a.y) + grow * ROWB + (uint32_t)(lr * ROWB + sub * LANEB), o);
+            store_row_chunk<F16>(static_cast<char *>(a.y) + grow * ROWB + (uint32_t)(lr * ROWB + sub * kLaneOff), o,
+                                 kStep);
         }
     }
 
@@ -419,7 +454,7 @@ struct Stage1 {
         if constexpr (MODE == MODE_DEQUANTIZE || !GENERIC_SETS || kUseLut)
             __syncthreads();
         if constexpr (!GENERIC_SETS)
-            load_params<PL>(lds_params + sub * PL, P);
+            lane_params(lds_params, sub, P);
 
         float lev[H], thr[H > 1 ? H - 1 : 1];
 #pragma unroll
@@ -550,7 +585,7 @@ struct Stage1 {
             const int64_t grow = row0 + (int64_t)gl * VPW;
             const int lr = lane_row<TAIL>(a, grow, slot);
             if constexpr (GENERIC_SETS)
-                load_params<PL>(a.params + ((int64_t)set_of(a, grow + lr) * LPV + sub) * PL, P);
+                lane_params(a.params + (int64_t)set_of(a, grow + lr) * LPV * PL, sub, P);
             compute(a, P, lev, thr, lds_levels, lut, buf[u], grow, lr, sub, u * VPW + slot, eq);
         }
     }
