@@ -48,7 +48,7 @@ isoq_status hip_fail(hipError_t e, const char *where, isoq_status st = ISOQ_E_HI
 bool valid_variant(int v) { return v == ISOQ_FULL || v == ISOQ_FAST || v == ISOQ_PLANAR2D; }
 // Widths of the tuned kernels (every entry point); other widths up to
 // kGenericMaxD have quantize, dequantize and round trip only.
-bool tuned_d(int d) { return d == 128 || d == 256 || d == 512; }
+bool tuned_d(int d) { return d == 64 || d == 128 || d == 256 || d == 512; }
 bool supported_d(int d) { return d >= 1 && d <= kGenericMaxD; }
 bool supported_bits(int b) { return b >= 2 && b <= 4; }
 bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
@@ -167,7 +167,7 @@ const char *isoq_status_string(isoq_status s)
     switch (s) {
     case ISOQ_OK: return "ok";
     case ISOQ_E_INVALID: return "invalid argument";
-    case ISOQ_E_UNSUPPORTED: return "unsupported shape (d in 1..1024, bits in {2,3,4}; the KV, score and sketch calls need d in {128,256,512}) or size limit";
+    case ISOQ_E_UNSUPPORTED: return "unsupported shape (d in 1..1024, bits in {2,3,4}; the KV and score calls need d in {64,128,256,512}, the sketch d in {128,256}) or size limit";
     case ISOQ_E_NULL: return "null pointer";
     case ISOQ_E_ALIGN: return "misaligned pointer";
     case ISOQ_E_HIP: return "HIP runtime error";

@@ -1,4 +1,4 @@
-// Stage-1 kernels for vector widths outside {128, 256, 512}: any d from 1 to
+// Stage-1 kernels for vector widths outside {64, 128, 256, 512}: any d from 1 to
 // 1024.  Algorithm 1 on the zero-padded vector of Sec. 5.1: when d is not a
 // multiple of the block size the last block is filled with zeros, all of its
 // rotated coordinates (4g in all, 2-D: 2 g2) are quantized and stored, and

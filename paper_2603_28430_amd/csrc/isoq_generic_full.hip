@@ -1,4 +1,4 @@
-// Stage-1 kernels of IsoQuant-Full for widths outside {128, 256, 512} (the
+// Stage-1 kernels of IsoQuant-Full for widths outside {64, 128, 256, 512} (the
 // template is in isoq_generic.h; one file per variant so they build in parallel).
 #include "isoq_generic.h"
 

@@ -80,7 +80,7 @@ struct KArgs {
     const uint16_t *qjl_frag;  // [n_sets][m/16][d/32][64][8] fp16: S' = S T^{-1}, B-fragment order
     uint8_t *qjl_signs;        // [n][m/8] sign bits of S (x - x_hat)
     float *qjl_gamma;          // [n] ||x - x_hat||
-    // widths outside {128, 256, 512} (isoq_generic.h)
+    // widths outside {64, 128, 256, 512} (isoq_generic.h)
     int32_t g_d;               // coordinates per row
     int32_t g_pw;              // padded width: 4 ceil(d/4), 2-D 2 ceil(d/2)
     int32_t g_slots;           // 4-coordinate slots per row, ceil(g_pw / 4)

@@ -93,6 +93,7 @@ template <int VAR>
 const void *pick_d(int d, int bits, bool f16, bool gen, int mode)
 {
     switch (d) {
+    case 64: return pick_bits<VAR, 64>(bits, f16, gen, mode);
     case 128: return pick_bits<VAR, 128>(bits, f16, gen, mode);
     case 256: return pick_bits<VAR, 256>(bits, f16, gen, mode);
     case 512: return pick_bits<VAR, 512>(bits, f16, gen, mode);

@@ -42,10 +42,11 @@ struct ScoreShape {
     static constexpr int E = 1 << FB;             // entries per table
     static constexpr int NF = D / F;              // fields (tables) per key
     static constexpr int RW = D * BITS / 32;      // record words
-    static constexpr int RV = RW / 4;             // 16-byte loads per record
+    static constexpr int LW = RW % 4 == 0 ? 4 : 2;  // words per record load (16 or 8 bytes)
+    static constexpr int RV = RW / LW;            // loads per record
     // keys per lane and batch
     static constexpr int KPT = RW <= 12 ? 2 : 1;
-    static_assert(RW % 4 == 0, "records are a whole number of 16-byte vectors");
+    static_assert(RW % LW == 0, "records are a whole number of 8-byte vectors");
     static constexpr int SW = QM / 32;             // sketch words per key
     static constexpr int NQ = QM / 4;              // 4-sign groups (16-entry tables) per key
     // LDS floats for g query heads: tables, codebook, rotated queries; with
@@ -241,14 +242,26 @@ __global__ __launch_bounds__(256) void score_kernel(const SArgs a)
             // an invalid key reads record 0 of block 0 (always present) and is not stored
             const int64_t krow =
                 k.ok[u] ? ((int64_t)blk * a.n_kv_heads + h) * a.block_size + (tt - bi * a.block_size) : 0;
-            const u32x4 *rp = reinterpret_cast<const u32x4 *>(a.k_idx + krow * RB);
+            if constexpr (S::LW == 4) {
+                const u32x4 *rp = reinterpret_cast<const u32x4 *>(a.k_idx + krow * RB);
 #pragma unroll
-            for (int v = 0; v < S::RV; v++) {
-                const u32x4 q4 = __builtin_nontemporal_load(rp + v);
+                for (int v = 0; v < S::RV; v++) {
+                    const u32x4 q4 = __builtin_nontemporal_load(rp + v);
 #pragma unroll
-                for (int c = 0; c < 4; c++) {
-                    const uint32_t e = q4[c];
-                    k.w[u][4 * v + c] = e;
+                    for (int c = 0; c < 4; c++) {
+                        const uint32_t e = q4[c];
+                        k.w[u][4 * v + c] = e;
+                    }
+                }
+            } else {
+                // records of 8 (mod 16) bytes: 8-byte loads
+                const u32x2 *rp = reinterpret_cast<const u32x2 *>(a.k_idx + krow * RB);
+#pragma unroll
+                for (int v = 0; v < S::RV; v++) {
+                    const u32x2 q2 = __builtin_nontemporal_load(rp + v);
+                    const uint32_t e0 = q2[0], e1 = q2[1];
+                    k.w[u][2 * v] = e0;
+                    k.w[u][2 * v + 1] = e1;
                 }
             }
             k.rho[u] = a.k_rho[krow];

@@ -120,7 +120,7 @@ def test_append_d128_sets_per_head(variant, bits, dtype):
              sets_k=8, sets_v=8, seed=bits)
 
 
-@pytest.mark.parametrize("d", [256, 512])
+@pytest.mark.parametrize("d", [64, 256, 512])
 @pytest.mark.parametrize("variant", ["full", "fast"])
 def test_append_wide_rows(variant, d):
     run_case(variant, d, 3, "f16", n_tokens=41, n_heads=4, block_size=32, n_blocks=3, sets_k=4,

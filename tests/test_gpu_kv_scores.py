@@ -130,7 +130,8 @@ def test_scores_d128(variant, bits, dtype):
              seed=bits)
 
 
-@pytest.mark.parametrize("d,bits", [(256, 2), (256, 3), (256, 4), (512, 2), (512, 3), (512, 4)])
+@pytest.mark.parametrize("d,bits", [(64, 2), (64, 3), (64, 4), (256, 2), (256, 3), (256, 4), (512, 2), (512, 3),
+                                    (512, 4)])
 def test_scores_wide(d, bits):
     run_case("full", d, bits, "f16", n_seqs=2, n_q=2, n_kv=2, bs=32, seq_lens=[1500, 70], seed=d + bits)
 

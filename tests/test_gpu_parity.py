@@ -54,17 +54,18 @@ def check(variant, d, bits, dtype, n, n_sets=1, rows_per_set=1, sample=None, see
 
 @pytest.mark.parametrize("dtype", ["f16", "f32"])
 @pytest.mark.parametrize("bits", [2, 3, 4])
-@pytest.mark.parametrize("d", [128, 256, 512])
+@pytest.mark.parametrize("d", [64, 128, 256, 512])
 @pytest.mark.parametrize("variant", ["full", "fast", "2d"])
 def test_parity_small_ragged(variant, d, bits, dtype):
     # a few hundred row groups: several waves, a ragged last group
-    n = {128: 1037, 256: 521, 512: 263}[d]
+    n = {64: 2075, 128: 1037, 256: 521, 512: 263}[d]
     print(f"case {variant} d={d} b={bits} {dtype} n={n}", flush=True)
     check(variant, d, bits, dtype, n)
 
 
 @pytest.mark.parametrize("variant,d,bits,dtype", [("full", 128, 3, "f16"), ("fast", 256, 2, "f16"),
-                                                  ("2d", 128, 4, "f32"), ("full", 512, 3, "f32")])
+                                                  ("2d", 128, 4, "f32"), ("full", 512, 3, "f32"),
+                                                  ("fast", 64, 3, "f16"), ("full", 64, 4, "f32")])
 def test_parity_many_groups_per_wave(variant, d, bits, dtype):
     """Large enough that every wave walks several row groups (prefetch loop and
     its odd tail); sampled rows against the oracle, every row for the
@@ -84,7 +85,7 @@ def test_parity_multiple_sets(variant, rows_per_set):
     """Parameter set of row r = (r / rows_per_set) mod n_sets; both the
     segment schedule (rows_per_set a multiple of the rows per wave) and the
     generic per-lane path."""
-    for d in (128, 256):
+    for d in (64, 128, 256):
         print(f"case {variant} d={d} rps={rows_per_set}", flush=True)
         check(variant, d, 3, "f16", 2003, n_sets=3, rows_per_set=rows_per_set)
 
@@ -92,7 +93,7 @@ def test_parity_multiple_sets(variant, rows_per_set):
 @pytest.mark.parametrize("n", [1, 2, 3, 4, 5, 17])
 def test_tiny_batches(n):
     for variant in ("full", "fast", "2d"):
-        for d in (128, 256, 512):
+        for d in (64, 128, 256, 512):
             check(variant, d, 3, "f16", n)
 
 

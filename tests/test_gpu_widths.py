@@ -1,6 +1,6 @@
 """Parity of the generic-width stage-1 kernels (any d from 1 to 1024 outside
-{128, 256, 512}; Sec. 5.1 zero padding when d is not a multiple of the block
-size) with the oracle, through the C ABI.
+{64, 128, 256, 512}; Sec. 5.1 zero padding when d is not a multiple of the
+block size) with the oracle, through the C ABI.
 
 Per case: isoq_quantize, isoq_dequantize and isoq_roundtrip on the same rows;
 the fused path equals quantize followed by dequantize bit for bit; indices,
@@ -26,8 +26,8 @@ DT = {"f16": (torch.float16, np.float16), "f32": (torch.float32, np.float32)}
 # widths below, between and above the tuned ones; odd, 2 mod 4 and
 # multiple-of-4 widths; every row shape of the generic kernels (8 to 64 lanes,
 # 1 to 4 slots per lane) and its largest width
-WIDTHS = [1, 2, 3, 5, 6, 7, 20, 32, 33, 64, 80, 90, 96, 100, 127, 130, 192, 250, 256 + 4, 320, 384, 511, 640,
-          1000, 1024]
+WIDTHS = [1, 2, 3, 5, 6, 7, 20, 32, 33, 60, 63, 80, 90, 96, 100, 127, 130, 192, 250, 256 + 4, 320, 384, 511,
+          640, 1000, 1024]
 
 
 def check(variant, d, bits, dtype, n, n_sets=1, rows_per_set=1, x=None, sample=None, seed=0):
@@ -77,13 +77,13 @@ def test_widths_multiple_sets(variant, d, rows_per_set):
 @pytest.mark.parametrize("n", [1, 2, 3, 5, 33])
 def test_widths_tiny_batches(n):
     for variant in ("full", "fast", "2d"):
-        for d in (3, 64, 90, 1000):
+        for d in (3, 60, 90, 1000):
             print(f"case {variant} d={d} n={n}", flush=True)
             check(variant, d, 3, "f32", n, seed=n)
 
 
 def test_widths_zero_and_scaled_rows():
-    for variant, d in (("full", 90), ("fast", 64), ("2d", 91)):
+    for variant, d in (("full", 90), ("fast", 60), ("2d", 91)):
         x = workloads.unit_gaussian_rows(64, d, seed=3, dtype=np.float32)
         x[0] = 0.0
         x[1] *= 1e-15
@@ -121,6 +121,9 @@ def test_widths_unsupported_calls():
     p = iq.isoq_params_init("fast", 96, 3, 1)
     with pytest.raises(iq.IsoqError) as e:
         iq.isoq_sketch_init(p, 64)
+    assert e.value.status == 2
+    with pytest.raises(iq.IsoqError) as e:               # the sketch needs d in {128, 256}
+        iq.isoq_sketch_init(iq.isoq_params_init("fast", 64, 3, 1), 64)
     assert e.value.status == 2
     z = lambda *s, dt=torch.uint8: torch.zeros(s, dtype=dt, device="cuda")
     R = p.record_bytes
