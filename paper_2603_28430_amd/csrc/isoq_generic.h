@@ -8,46 +8,70 @@
 // the row owns the 4-coordinate slots s, s + G, ..., s + (BPL - 1) G (a slot
 // is one quaternion block or two planar pairs), so consecutive lanes touch
 // consecutive slots.  A wave holds 64 / G rows per group and walks
-// kGenGroups groups, issuing every group's loads before computing.  The
+// generic_groups(BPL) groups, issuing every group's loads before computing.  The
 // record of a row is written and read bytewise: slot j's 4b index bits start
 // at bit 4b j.  Rows of a width that is a multiple of 4 move in one 8-byte
 // (fp16) or 16-byte (fp32) access per slot, other widths element by element.
 #pragma once
+
+#include <type_traits>
 
 #include "isoq_device.h"
 
 namespace isoq {
 namespace {
 
-constexpr int kGenGroups = 4;
-
 typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
 
+// A slot as loaded: 4 fp16 (kept packed until computed, two registers) or
+// 4 fp32 values.
 template <bool F16>
-__device__ __forceinline__ void gen_load(const char *row, int j, int d, bool vec, float v[4])
+using GenRaw = std::conditional_t<F16, f16x4, float4>;
+
+template <bool F16>
+__device__ __forceinline__ GenRaw<F16> gen_zero()
 {
-    if (vec) {
-        if constexpr (F16) {
-            const f16x4 h = *reinterpret_cast<const f16x4 *>(row + 8 * j);
-#pragma unroll
-            for (int c = 0; c < 4; c++)
-                v[c] = (float)h[c];
-        } else {
-            const float4 f = *reinterpret_cast<const float4 *>(row + 16 * j);
-            v[0] = f.x;
-            v[1] = f.y;
-            v[2] = f.z;
-            v[3] = f.w;
-        }
-        return;
+    if constexpr (F16)
+        return f16x4{(_Float16)0.f, (_Float16)0.f, (_Float16)0.f, (_Float16)0.f};
+    else
+        return make_float4(0.f, 0.f, 0.f, 0.f);
+}
+
+template <bool F16>
+__device__ __forceinline__ GenRaw<F16> gen_load(const char *row, int j, int d, bool vec)
+{
+    using T = std::conditional_t<F16, _Float16, float>;
+    if (vec)
+        return *reinterpret_cast<const GenRaw<F16> *>(row + 4 * sizeof(T) * j);
+    GenRaw<F16> v = gen_zero<F16>();
+    const T *e = reinterpret_cast<const T *>(row);
+    const int i = 4 * j;
+    if constexpr (F16) {
+        if (i < d) v[0] = e[i];
+        if (i + 1 < d) v[1] = e[i + 1];
+        if (i + 2 < d) v[2] = e[i + 2];
+        if (i + 3 < d) v[3] = e[i + 3];
+    } else {
+        if (i < d) v.x = e[i];
+        if (i + 1 < d) v.y = e[i + 1];
+        if (i + 2 < d) v.z = e[i + 2];
+        if (i + 3 < d) v.w = e[i + 3];
     }
+    return v;
+}
+
+template <bool F16>
+__device__ __forceinline__ void gen_unpack(const GenRaw<F16> &r, float v[4])
+{
+    if constexpr (F16) {
 #pragma unroll
-    for (int c = 0; c < 4; c++) {
-        const int i = 4 * j + c;
-        if constexpr (F16)
-            v[c] = i < d ? (float)reinterpret_cast<const _Float16 *>(row)[i] : 0.f;
-        else
-            v[c] = i < d ? reinterpret_cast<const float *>(row)[i] : 0.f;
+        for (int c = 0; c < 4; c++)
+            v[c] = (float)r[c];
+    } else {
+        v[0] = r.x;
+        v[1] = r.y;
+        v[2] = r.z;
+        v[3] = r.w;
     }
 }
 
@@ -117,6 +141,7 @@ template <int VAR, int BITS, bool F16, int MODE, int G, int BPL>
 __global__ __launch_bounds__(kBlockThreads) void generic_kernel(const KArgs a)
 {
     constexpr int R = 64 / G;                // rows per wave and group
+    constexpr int kGenGroups = generic_groups(BPL);
     constexpr int PS = kSlotParams<VAR>;
     constexpr int H = 1 << (BITS - 1);
     constexpr int ESZ = F16 ? 2 : 4;
@@ -142,7 +167,7 @@ __global__ __launch_bounds__(kBlockThreads) void generic_kernel(const KArgs a)
     const int64_t row_bytes = (int64_t)d * ESZ;
 
     // ---- loads of every group first
-    float xv[kLoadX ? kGenGroups : 1][BPL][4];
+    GenRaw<F16> xr[kLoadX ? kGenGroups : 1][BPL];
     uint32_t pin[kLoadX ? 1 : kGenGroups][BPL];
     float rin[kLoadX ? 1 : kGenGroups];
 #pragma unroll
@@ -154,10 +179,8 @@ __global__ __launch_bounds__(kBlockThreads) void generic_kernel(const KArgs a)
             const int j = sub + G * k;
             const bool on = ok && j < slots;
             if constexpr (kLoadX) {
-                if (on)
-                    gen_load<F16>(static_cast<const char *>(a.x) + row * row_bytes, j, d, vec, xv[t][k]);
-                else
-                    xv[t][k][0] = xv[t][k][1] = xv[t][k][2] = xv[t][k][3] = 0.f;
+                xr[t][k] = on ? gen_load<F16>(static_cast<const char *>(a.x) + row * row_bytes, j, d, vec)
+                              : gen_zero<F16>();
             } else {
                 pin[t][k] = on ? gen_read_slot<BITS>(a.rec_in + row * nb, j, nb) : 0u;
             }
@@ -193,12 +216,15 @@ __global__ __launch_bounds__(kBlockThreads) void generic_kernel(const KArgs a)
         uint32_t pk[BPL];
         float rho;
         if constexpr (kLoadX) {
+            float xv[BPL][4];
             float s = 0.f;
 #pragma unroll
-            for (int k = 0; k < BPL; k++)
+            for (int k = 0; k < BPL; k++) {
+                gen_unpack<F16>(xr[t][k], xv[k]);
 #pragma unroll
                 for (int c = 0; c < 4; c++)
-                    s = fmaf(xv[t][k][c], xv[t][k][c], s);
+                    s = fmaf(xv[k][c], xv[k][c], s);
+            }
             rho = __builtin_amdgcn_sqrtf(row_sum<G>(s));
             const float rho_e = fmaxf(rho, kEps);
             // thresholds scaled by rho (the rotation is linear, so comparing
@@ -215,7 +241,7 @@ __global__ __launch_bounds__(kBlockThreads) void generic_kernel(const KArgs a)
             for (int k = 0; k < BPL; k++) {
                 const int j = sub + G * k;
                 float y[4];
-                rotate4_forward<VAR>(P[k], xv[t][k], y);
+                rotate4_forward<VAR>(P[k], xv[k], y);
                 uint32_t p = 0;
 #pragma unroll
                 for (int c = 0; c < 4; c++) {

@@ -137,9 +137,16 @@ const void *kernel_for(int variant, int d, int bits, bool f16, bool generic_sets
 const void *generic_kernel_full(int slots, int bits, bool f16, int mode);
 const void *generic_kernel_fast(int slots, int bits, bool f16, int mode);
 const void *generic_kernel_2d(int slots, int bits, bool f16, int mode);
-// Rows per wave of the generic kernels for a row of `slots` slots (64 / G
-// rows per group, 4 groups).
-inline int generic_rows_per_wave(int slots) { return 4 * (slots <= 8 ? 8 : slots <= 16 ? 4 : slots <= 32 ? 2 : 1); }
+// Row shape of the generic kernels for a row of `slots` slots: G lanes per
+// row, BPL slots per lane, and row groups per wave (every group's loads are
+// in flight together: 8 groups of one slot, 4 groups of several).
+inline int generic_lanes(int slots) { return slots <= 8 ? 8 : slots <= 16 ? 16 : slots <= 32 ? 32 : 64; }
+inline int generic_bpl(int slots) { return slots <= 64 ? 1 : slots <= 128 ? 2 : 4; }
+constexpr int generic_groups(int bpl) { return bpl == 1 ? 8 : 4; }
+inline int generic_rows_per_wave(int slots)
+{
+    return generic_groups(generic_bpl(slots)) * (64 / generic_lanes(slots));
+}
 constexpr int kGenericMaxD = 1024;
 // Blocks of the stage-2 sketch kernel with a single rotation set (each walks
 // several tiles).
