@@ -165,6 +165,13 @@ __global__ __launch_bounds__(kBlockThreads) void generic_kernel(const KArgs a)
     const int d = a.g_d, slots = a.g_slots, nb = a.g_rec;
     const bool vec = a.g_vec != 0;
     const int64_t row_bytes = (int64_t)d * ESZ;
+    // the lane's row of group 0; group t is t R rows further (wave-uniform
+    // strides, so per-group addresses are one add)
+    const char *x0 = kLoadX ? static_cast<const char *>(a.x) + row0 * row_bytes : nullptr;
+    char *y0 = MODE != MODE_QUANTIZE ? static_cast<char *>(a.y) + row0 * row_bytes : nullptr;
+    const uint8_t *ri0 = MODE == MODE_DEQUANTIZE ? a.rec_in + row0 * nb : nullptr;
+    uint8_t *ro0 = MODE == MODE_QUANTIZE ? a.rec_out + row0 * nb : nullptr;
+    const int64_t xstep = (int64_t)R * row_bytes, rstep = (int64_t)R * nb;
 
     // ---- loads of every group first
     GenRaw<F16> xr[kLoadX ? kGenGroups : 1][BPL];
@@ -179,10 +186,10 @@ __global__ __launch_bounds__(kBlockThreads) void generic_kernel(const KArgs a)
             const int j = sub + G * k;
             const bool on = ok && j < slots;
             if constexpr (kLoadX) {
-                xr[t][k] = on ? gen_load<F16>(static_cast<const char *>(a.x) + row * row_bytes, j, d, vec)
+                xr[t][k] = on ? gen_load<F16>(x0 + t * xstep, j, d, vec)
                               : gen_zero<F16>();
             } else {
-                pin[t][k] = on ? gen_read_slot<BITS>(a.rec_in + row * nb, j, nb) : 0u;
+                pin[t][k] = on ? gen_read_slot<BITS>(ri0 + t * rstep, j, nb) : 0u;
             }
         }
         if constexpr (!kLoadX)
@@ -280,7 +287,7 @@ __global__ __launch_bounds__(kBlockThreads) void generic_kernel(const KArgs a)
                 const uint32_t next = BITS == 3 ? (uint32_t)__shfl_down((int)pk[k], 1, 64) : 0u;
                 const int j = sub + G * k;
                 if (ok && j < slots)
-                    gen_write_slot<BITS>(a.rec_out + row * nb, j, nb, pk[k], next);
+                    gen_write_slot<BITS>(ro0 + t * rstep, j, nb, pk[k], next);
             }
             if (ok && sub == 0)
                 a.norms_out[row] = rho;
@@ -291,7 +298,7 @@ __global__ __launch_bounds__(kBlockThreads) void generic_kernel(const KArgs a)
                 if (ok && j < slots) {
                     float o[4];
                     rotate4_inverse<VAR>(P[k], yq[k], o);
-                    gen_store<F16>(static_cast<char *>(a.y) + row * row_bytes, j, d, vec, o);
+                    gen_store<F16>(y0 + t * xstep, j, d, vec, o);
                 }
             }
         }
