@@ -10,6 +10,12 @@ namespace isoq {
 namespace {
 
 // ---- packed index records --------------------------------------------------
+// Two lane layouts write the same record (coordinate j at bits [j b, j b + b)):
+// a lane owning coordinates 8 sub .. 8 sub + 7 (store_bits / load_bits), or,
+// for fp32 rows, a lane owning slots sub and sub + LPV, whose 4b-bit pieces lie
+// in the first and the second half of the record (the _split variants).  In
+// both, the lane's index word p holds coordinate j of its 8 at bits
+// [j b, j b + b).
 // Lane `sub` of a row owns coordinates 8 sub .. 8 sub + 7, i.e. bits
 // [8 sub * BITS, 8 (sub + 1) * BITS) of the row's record: a 16-bit half-word
 // (2 bits), a 32-bit word (4 bits), or 24 bits at byte 3 sub (3 bits), which
@@ -31,6 +37,64 @@ __device__ __forceinline__ void store_bits(uint8_t *rec, int sub, uint32_t p, bo
         if (ok && k < 3)
             reinterpret_cast<uint32_t *>(rec)[3 * (sub >> 2) + k] = (p >> (8 * k)) | (nb << (24 - 8 * k));
     }
+}
+
+template <int BITS, int LPV>
+__device__ __forceinline__ void store_bits_split(uint8_t *rec, int sub, uint32_t p, bool ok)
+{
+    constexpr int PB = 4 * BITS;        // bits per piece
+    constexpr int HALF = LPV * PB / 8;  // bytes per half record
+    const uint32_t pa = p & ((1u << PB) - 1u), pb = p >> PB;
+    if constexpr (BITS == 2) {
+        if (ok) {
+            rec[sub] = (uint8_t)pa;
+            rec[HALF + sub] = (uint8_t)pb;
+        }
+    } else if constexpr (BITS == 4) {
+        if (ok) {
+            reinterpret_cast<uint16_t *>(rec)[sub] = (uint16_t)pa;
+            reinterpret_cast<uint16_t *>(rec + HALF)[sub] = (uint16_t)pb;
+        }
+    } else {
+        // 12-bit pieces: lanes 2q and 2q + 1 form the 24-bit unit q of a half,
+        // and the even lanes of an octet merge its four units into three
+        // words as store_bits merges a quad's (unit q + 1 is two lanes on;
+        // the last unit of a row, which would read past it, writes nothing)
+#pragma unroll
+        for (int h = 0; h < 2; h++) {
+            const uint32_t v = h ? pb : pa;
+            const uint32_t u = v | ((uint32_t)__shfl_down((int)v, 1, 64) << 12);
+            const uint32_t nu = (uint32_t)__shfl_down((int)u, 2, 64);
+            const int q = sub >> 1, k = q & 3;
+            if (ok && (sub & 1) == 0 && k < 3)
+                reinterpret_cast<uint32_t *>(rec + h * HALF)[3 * (q >> 2) + k] = (u >> (8 * k)) | (nu << (24 - 8 * k));
+        }
+    }
+}
+
+template <int BITS, int LPV>
+__device__ __forceinline__ uint32_t load_bits_split(const uint8_t *rec, int sub)
+{
+    constexpr int PB = 4 * BITS;
+    constexpr int HALF = LPV * PB / 8;
+    uint32_t pa, pb;
+    if constexpr (BITS == 2) {
+        pa = rec[sub];
+        pb = rec[HALF + sub];
+    } else if constexpr (BITS == 4) {
+        pa = reinterpret_cast<const uint16_t *>(rec)[sub];
+        pb = reinterpret_cast<const uint16_t *>(rec + HALF)[sub];
+    } else {
+        // the piece at bit 12 sub of a half: word k, and word k + 1 when the
+        // piece straddles it (then that word still belongs to the half)
+        const int o = 12 * sub, k = o >> 5, sh = o & 31;
+        const int k1 = sh > 20 ? k + 1 : k;
+        const uint32_t *wa = reinterpret_cast<const uint32_t *>(rec);
+        const uint32_t *wb = reinterpret_cast<const uint32_t *>(rec + HALF);
+        pa = (uint32_t)((((uint64_t)wa[k1] << 32) | wa[k]) >> sh) & 0xFFFu;
+        pb = (uint32_t)((((uint64_t)wb[k1] << 32) | wb[k]) >> sh) & 0xFFFu;
+    }
+    return pa | (pb << PB);
 }
 
 template <int BITS>
@@ -146,11 +210,13 @@ struct Stage1 {
     static constexpr int64_t ROWB = (int64_t)D * (F16 ? 2 : 4);  // bytes per row
     static constexpr int64_t RECB = (int64_t)D * BITS / 8;       // bytes per index record
     static constexpr int LANEB = F16 ? 16 : 32;         // row bytes per lane
-    // fp32 round trip: lane `sub` owns slots sub and sub + LPV (coordinates
-    // 4 sub .. +3 and D/2 + 4 sub .. +3), so each 16-byte access instruction
-    // of a wave covers one contiguous span; elsewhere it owns slots 2 sub and
-    // 2 sub + 1 (the record layout of the index bits follows that order)
-    static constexpr bool kSplit = !F16 && MODE == MODE_ROUNDTRIP;
+    // fp32 round trip, quantize and dequantize: lane `sub` owns slots sub and
+    // sub + LPV (coordinates 4 sub .. +3 and D/2 + 4 sub .. +3), so each
+    // 16-byte access instruction of a wave covers one contiguous span (its
+    // index pieces go to the two halves of the record); elsewhere it owns
+    // slots 2 sub and 2 sub + 1
+    static constexpr bool kSplit =
+        !F16 && (MODE == MODE_ROUNDTRIP || MODE == MODE_QUANTIZE || MODE == MODE_DEQUANTIZE);
     static constexpr int kLaneOff = kSplit ? 16 : LANEB;       // bytes to lane sub's first piece
     static constexpr int kStep = kSplit ? (int)(ROWB / 2) : 16;  // bytes to its second piece
     static constexpr bool kUseLut = BITS == 4;           // magnitude lookup table
@@ -195,7 +261,11 @@ struct Stage1 {
     __device__ static __forceinline__ void fetch(const KArgs &a, int64_t grow, int lr, int sub, In &in)
     {
         if constexpr (MODE == MODE_DEQUANTIZE) {
-            in.bits = load_bits<BITS>(a.rec_in + grow * RECB + (uint32_t)(lr * RECB), sub);
+            const uint8_t *rec = a.rec_in + grow * RECB + (uint32_t)(lr * RECB);
+            if constexpr (kSplit)
+                in.bits = load_bits_split<BITS, LPV>(rec, sub);
+            else
+                in.bits = load_bits<BITS>(rec, sub);
             in.rho = (a.norms_in + grow)[lr];
         } else if constexpr (MODE == MODE_APPEND) {
             // token grow + lr, head blockIdx.x of rows [n_tokens][n_heads][d]
@@ -386,7 +456,11 @@ struct Stage1 {
                                                 uint32_t p, float rho)
     {
         if constexpr (MODE == MODE_QUANTIZE || MODE == MODE_QJL) {
-            store_bits<BITS>(a.rec_out + grow * RECB + (uint32_t)(lr * RECB), sub, p, true);
+            uint8_t *rec = a.rec_out + grow * RECB + (uint32_t)(lr * RECB);
+            if constexpr (kSplit)
+                store_bits_split<BITS, LPV>(rec, sub, p, true);
+            else
+                store_bits<BITS>(rec, sub, p, true);
             if (sub == 0)
                 (a.norms_out + grow)[lr] = rho;
         } else {
