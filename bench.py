@@ -181,6 +181,44 @@ def kv_append_side(torch, workloads):
     return res
 
 
+def kv_append_qjl_side(torch, workloads):
+    """isoq_kv_append_qjl (key rows with the stage-2 sketch into a paged
+    cache, one launch): the decode step and the prefill-sized append of
+    kv_append_side, keys only, m = 128.  Algorithmic bytes per (token, head)
+    row: the fp16 row, the 48-byte record, the 4-byte norm, 16 sign bytes and
+    the 4-byte gamma (plus 8 bytes of slot per token)."""
+    import paper_2603_28430_amd as iq
+
+    H, d, bs, bits, m = 32, 128, 16, 3, 128
+    res = {}
+    for name, n_seq, per_seq in (("decode_32x1", 32, 1), ("prefill_8x4096", 8, 4096)):
+        n_tok = n_seq * per_seq
+        n_blocks = max(4096, 2 * n_tok // bs)
+        print(f"# kv append qjl {name}", file=sys.stderr, flush=True)
+        pk = iq.isoq_params_init("fast", d, bits, H, rot=workloads.rotation_draws("fast", d, H, seed=1))
+        sk = iq.isoq_sketch_init(pk, m)
+        k = workloads.kv_stream_torch(1, H, n_tok, d, 2, "cuda")[0].transpose(0, 1).contiguous()
+        blocks_per_seq = (per_seq + 1000 + bs - 1) // bs + 1
+        tables = torch.randperm(n_blocks, device="cuda")[: n_seq * blocks_per_seq].view(n_seq, -1)
+        pos = torch.arange(per_seq, device="cuda") + (1000 if per_seq == 1 else 0)
+        slots = (tables[:, pos // bs] * bs + pos % bs).reshape(-1).to(torch.int64)
+        R = pk.record_bytes
+        rec = torch.empty((n_blocks, H, bs, R), dtype=torch.uint8, device="cuda")
+        sg = torch.empty((n_blocks, H, bs, m // 8), dtype=torch.uint8, device="cuda")
+        rho = torch.empty((n_blocks, H, bs), dtype=torch.float32, device="cuda")
+        gam = torch.empty((n_blocks, H, bs), dtype=torch.float32, device="cuda")
+        fn = lambda i: iq.isoq_kv_append_qjl(pk, sk, k, slots, rec, rho, sg, gam)
+        steps = 200 if n_tok < 1000 else 50
+        ms = time_launches(fn, steps, 10, torch, 0.2)
+        b = n_tok * (H * (d * 2 + R + 4 + m // 8 + 4) + 8)
+        res[name] = {"tokens": n_tok, "heads": H, "us_per_call": ms * 1e3, "GBps": b / ms / 1e6,
+                     "frac": b / ms / 1e6 / PEAK_HBM_GBPS}
+        sk.close()
+        pk.close()
+        del k, rec, sg, rho, gam
+    return res
+
+
 def kv_scores_side(torch, workloads):
     """isoq_kv_scores: attention logits of one decoding query per head against
     a paged cache of quantized keys, 8 sequences x 32,768 positions x 32 heads,
@@ -345,6 +383,7 @@ def other_configs(measure, entry, torch, np, workloads):
         del x0, ins, outs_
         torch.cuda.empty_cache()
     out["kv_append"] = kv_append_side(torch, workloads)
+    out["kv_append_qjl"] = kv_append_qjl_side(torch, workloads)
     out["kv_scores"] = kv_scores_side(torch, workloads)
     out["qjl_quantize"] = qjl_side(torch, workloads)
     out["kv_scores_qjl"] = kv_scores_qjl_side(torch, workloads)
@@ -380,7 +419,7 @@ def main() -> int:
     ap.add_argument("--no-extras", action="store_true")
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the side measurements of the d=256, d=512 and KV-cache workloads")
-    ap.add_argument("--side", choices=["kv-append", "kv-scores", "kv-scores-qjl", "qjl", "widths"],
+    ap.add_argument("--side", choices=["kv-append", "kv-append-qjl", "kv-scores", "kv-scores-qjl", "qjl", "widths"],
                     help="run only this side measurement and print its JSON")
     ap.add_argument("--copy-only", action="store_true",
                     help="only time a plain device copy of the input size (counter calibration)")
@@ -398,7 +437,8 @@ def main() -> int:
 
     torch.cuda.set_device(0)
     if args.side:
-        fn = {"kv-append": kv_append_side, "kv-scores": kv_scores_side, "kv-scores-qjl": kv_scores_qjl_side,
+        fn = {"kv-append": kv_append_side, "kv-append-qjl": kv_append_qjl_side, "kv-scores": kv_scores_side,
+              "kv-scores-qjl": kv_scores_qjl_side,
               "qjl": qjl_side, "widths": widths_side}[args.side]
         print(json.dumps({"side": args.side, **fn(torch, workloads)}), flush=True)
         return 0

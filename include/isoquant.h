@@ -179,8 +179,8 @@ isoq_status isoq_roundtrip(const isoq_params *p, int dtype, const void *x, int64
  *   k_rho, v_rho  device, fp32 [n_blocks][n_heads][block_size].
  * Limits: n_tokens * n_heads < 2^31, n_blocks * block_size < 2^31, n_heads and
  * block_size >= 1, and at most 65,535 launch blocks of tokens (n_tokens up to
- * 4,194,240 at d = 128, 2,097,120 at d = 256, 1,048,560 at d = 512); beyond
- * that ISOQ_E_UNSUPPORTED.  Distinct tokens must map to distinct slots (a repeated slot
+ * 8,388,480 at d = 64, 4,194,240 at d = 128, 2,097,120 at d = 256, 1,048,560
+ * at d = 512); beyond that ISOQ_E_UNSUPPORTED.  Distinct tokens must map to distinct slots (a repeated slot
  * is written by both rows in an unspecified order).  Slots not named are left
  * untouched.  n_tokens = 0 is a no-op.
  */
@@ -264,6 +264,30 @@ isoq_status isoq_sketch_export(const isoq_sketch *sk, int *m, float *S_out);
 isoq_status isoq_quantize_qjl(const isoq_params *p, const isoq_sketch *sk, int dtype, const void *x,
                               int64_t n, int64_t rows_per_set, uint8_t *idx_packed, float *norms,
                               uint8_t *signs, float *gamma, void *stream);
+
+/*
+ * isoq_kv_append_qjl -- quantize-on-append of key rows with the stage-2
+ * residual sketch (Sec. 8): each new key row is encoded as by
+ * isoq_quantize_qjl (records, norms, m sign bits and gamma, bit for bit the
+ * same) and all four go straight into the cache slot of its token, in one
+ * launch.  Values need no sketch: append them with isoq_kv_append.
+ *
+ *   pk, sk      the K quantizer and its sketch (same variant, d, sets and
+ *               device); pk->n_sets == 1 or n_heads (head h uses set h).
+ *   dtype, k_new, slot_mapping, n_tokens, n_heads, k_idx, k_rho, n_blocks,
+ *   block_size  as in isoq_kv_append.
+ *   k_signs     device, [n_blocks][n_heads][block_size][m/8] bytes (4-byte
+ *               aligned), the sign sketch of each slot, bit i of byte i/8 =
+ *               [(S (x - x_hat))_i > 0].
+ *   k_gamma     device, fp32 [n_blocks][n_heads][block_size], ||x - x_hat||.
+ * Skipped slots (< 0 or >= n_blocks * block_size) are not written; other
+ * slots not named are untouched.  Limits as in isoq_kv_append; the widths and
+ * sketch sizes are those of isoq_sketch_init.
+ */
+isoq_status isoq_kv_append_qjl(const isoq_params *pk, const isoq_sketch *sk, int dtype, const void *k_new,
+                               const int64_t *slot_mapping, int64_t n_tokens, int n_heads, uint8_t *k_idx,
+                               float *k_rho, uint8_t *k_signs, float *k_gamma, int64_t n_blocks, int block_size,
+                               void *stream);
 
 /*
  * isoq_kv_scores_qjl -- isoq_kv_scores with the stage-2 residual correction:

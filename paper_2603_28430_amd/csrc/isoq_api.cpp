@@ -801,4 +801,59 @@ isoq_status isoq_quantize_qjl(const isoq_params *p, const isoq_sketch *sk, int d
     return launch(fn, dim3((unsigned)blocks), args, stream);
 }
 
+isoq_status isoq_kv_append_qjl(const isoq_params *pk, const isoq_sketch *sk, int dtype, const void *k_new,
+                               const int64_t *slot_mapping, int64_t n_tokens, int n_heads, uint8_t *k_idx,
+                               float *k_rho, uint8_t *k_signs, float *k_gamma, int64_t n_blocks, int block_size,
+                               void *stream)
+{
+    if (!pk || !sk)
+        return ISOQ_E_NULL;
+    if (dtype != ISOQ_F32 && dtype != ISOQ_F16)
+        return ISOQ_E_INVALID;
+    if (n_tokens < 0 || n_heads < 1 || block_size < 1 || n_blocks < 0)
+        return ISOQ_E_INVALID;
+    if (sk->variant != pk->variant || sk->d != pk->d || sk->n_sets != pk->n_sets || sk->device != pk->device)
+        return ISOQ_E_INVALID;
+    if (pk->n_sets != 1 && pk->n_sets != n_heads)
+        return ISOQ_E_INVALID;
+    if (n_tokens > 0x7FFFFFFF / n_heads || n_blocks > 0x7FFFFFFF / block_size)
+        return ISOQ_E_UNSUPPORTED;
+    if (n_tokens == 0 || n_blocks == 0)
+        return ISOQ_OK;
+    if (!k_new || !slot_mapping || !k_idx || !k_rho || !k_signs || !k_gamma)
+        return ISOQ_E_NULL;
+    if (!aligned(k_new, 16) || !aligned(slot_mapping, 8) || !aligned(k_idx, 4) || !aligned(k_rho, 4) ||
+        !aligned(k_signs, 4) || !aligned(k_gamma, 4))
+        return ISOQ_E_ALIGN;
+    isoq_status st = check_device(pk);
+    if (st != ISOQ_OK)
+        return st;
+    const void *fn = qjl_kernel_for(pk->variant, pk->d, pk->bits, dtype == ISOQ_F16, sk->m, true);
+    if (!fn)
+        return ISOQ_E_UNSUPPORTED;
+    // block (x, y) = (head, token range); a block stages its head's projection
+    // once and walks token ranges y, y + gridDim.y, ... of that head
+    const int64_t ranges = (n_tokens + rows_per_block(pk) - 1) / rows_per_block(pk);
+    const int64_t by = std::max<int64_t>(1, std::min<int64_t>(ranges, kQjlBlocks / n_heads));
+    if (by > 65535)
+        return ISOQ_E_UNSUPPORTED;
+    KArgs a{};
+    fill_args(pk, a);
+    a.x = k_new;
+    a.rec_out = k_idx;
+    a.norms_out = k_rho;
+    a.n = n_tokens;
+    a.rows_per_set = 1;
+    a.slots = slot_mapping;
+    a.n_slots = n_blocks * block_size;
+    a.n_heads = (uint32_t)n_heads;
+    a.block_size = (uint32_t)block_size;
+    a.div_block = make_fastdiv((uint32_t)block_size);
+    a.qjl_frag = sk->dfrag;
+    a.qjl_signs = k_signs;
+    a.qjl_gamma = k_gamma;
+    void *args[] = {&a};
+    return launch(fn, dim3((unsigned)n_heads, (unsigned)by, 1), args, stream);
+}
+
 }  // extern "C"

@@ -9,7 +9,14 @@
 
 namespace isoq {
 
-enum Mode { MODE_ROUNDTRIP = 0, MODE_QUANTIZE = 1, MODE_DEQUANTIZE = 2, MODE_APPEND = 3, MODE_QJL = 4 };
+enum Mode {
+    MODE_ROUNDTRIP = 0,
+    MODE_QUANTIZE = 1,
+    MODE_DEQUANTIZE = 2,
+    MODE_APPEND = 3,      // quantize into the slots of a paged cache
+    MODE_QJL = 4,         // quantize with the stage-2 sketch
+    MODE_APPEND_QJL = 5   // both: records, norms, signs and gamma into cache slots
+};
 enum Variant { VAR_FULL = 0, VAR_FAST = 1, VAR_PLANAR2D = 2 };
 
 // Every lane owns 8 consecutive coordinates of a row (two quaternion blocks or
@@ -151,8 +158,9 @@ constexpr int kGenericMaxD = 1024;
 // Blocks of the stage-2 sketch kernel with a single rotation set (each walks
 // several tiles).
 constexpr int64_t kQjlBlocks = 1024;
-// Quantize with the stage-2 sketch of m bits (isoq_qjl.hip), or nullptr.
-const void *qjl_kernel_for(int variant, int d, int bits, bool f16, int m);
+// Quantize with the stage-2 sketch of m bits (isoq_qjl.hip), or nullptr;
+// with `append`, the kernel that writes into the slots of a paged cache.
+const void *qjl_kernel_for(int variant, int d, int bits, bool f16, int m, bool append = false);
 
 // Magnitude lookup table, used for 4-bit codebooks.  The magnitude axis of
 // the normalised coordinate is cut into cells of width h, h smaller than every

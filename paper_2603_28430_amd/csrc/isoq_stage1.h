@@ -200,7 +200,8 @@ __device__ __forceinline__ uint32_t push_bits12(uint32_t p, const uint64_t m[12]
 // finds the set of its row for every group and reads its parameters from
 // global memory.  Parameters are staged before the tile's loads are issued:
 // measured on MI355X, this order beats issuing the data loads first.
-// QM: sketch size m of the stage-2 residual sketch (MODE_QJL only).
+// QM: sketch size m of the stage-2 residual sketch (MODE_QJL and
+// MODE_APPEND_QJL only).
 template <int VAR, int D, int BITS, bool F16, int MODE, bool GENERIC_SETS, int QM = 0>
 struct Stage1 {
     static constexpr int LPV = D / kCoordsPerLane;      // lanes per row
@@ -220,7 +221,8 @@ struct Stage1 {
     static constexpr int kLaneOff = kSplit ? 16 : LANEB;       // bytes to lane sub's first piece
     static constexpr int kStep = kSplit ? (int)(ROWB / 2) : 16;  // bytes to its second piece
     static constexpr bool kUseLut = BITS == 4;           // magnitude lookup table
-    static constexpr bool kQjl = MODE == MODE_QJL;
+    static constexpr bool kQjl = MODE == MODE_QJL || MODE == MODE_APPEND_QJL;
+    static constexpr bool kAppend = MODE == MODE_APPEND || MODE == MODE_APPEND_QJL;  // rows go to cache slots
     static constexpr bool kEncode = MODE == MODE_QUANTIZE || MODE == MODE_APPEND || kQjl;  // records out
     static constexpr bool kLevels = MODE == MODE_ROUNDTRIP || kQjl;  // selected levels needed
     // stage-2 sketch: a wave's tile of rows, its fp16 error rows in LDS
@@ -267,7 +269,7 @@ struct Stage1 {
             else
                 in.bits = load_bits<BITS>(rec, sub);
             in.rho = (a.norms_in + grow)[lr];
-        } else if constexpr (MODE == MODE_APPEND) {
+        } else if constexpr (kAppend) {
             // token grow + lr, head blockIdx.x of rows [n_tokens][n_heads][d]
             const int64_t tstride = (int64_t)a.n_heads * ROWB;
             load_row_chunk<F16>(static_cast<const char *>(a.x) + grow * tstride + (int64_t)blockIdx.x * ROWB +
@@ -426,8 +428,14 @@ struct Stage1 {
                     s2 = fmaf(e[j], e[j], s2);
                 }
                 const float gamma = rho * __builtin_amdgcn_sqrtf(row_sum<LPV>(s2));
-                if (sub == 0)
+                if constexpr (kAppend) {
+                    bool ok;
+                    const int64_t r = cache_row(a, grow, lr, ok);
+                    if (ok && sub == 0)
+                        a.qjl_gamma[r] = gamma;
+                } else if (sub == 0) {
                     (a.qjl_gamma + grow)[lr] = gamma;
+                }
                 u32x4 h;
 #pragma unroll
                 for (int k = 0; k < 4; k++) {
@@ -452,10 +460,22 @@ struct Stage1 {
     // cache block holds [n_heads][block_size] records.  A skipped slot writes
     // nothing; the quad exchange inside store_bits runs on every lane either
     // way.
+    // Cache row of token grow + lr for head blockIdx.x (append modes); ok is
+    // false for a skipped slot (then the row returned is 0 and must not be
+    // written).
+    __device__ static __forceinline__ int64_t cache_row(const KArgs &a, int64_t grow, int lr, bool &ok)
+    {
+        const int64_t s = (a.slots + grow)[lr];
+        ok = s >= 0 && s < a.n_slots;
+        const uint32_t su = ok ? (uint32_t)s : 0u;
+        const uint32_t blk = fast_div(su, a.div_block);
+        return ((int64_t)blk * a.n_heads + blockIdx.x) * a.block_size + (su - blk * a.block_size);
+    }
+
     __device__ static __forceinline__ void emit(const KArgs &a, int64_t grow, int lr, int sub,
                                                 uint32_t p, float rho)
     {
-        if constexpr (MODE == MODE_QUANTIZE || MODE == MODE_QJL) {
+        if constexpr (!kAppend) {
             uint8_t *rec = a.rec_out + grow * RECB + (uint32_t)(lr * RECB);
             if constexpr (kSplit)
                 store_bits_split<BITS, LPV>(rec, sub, p, true);
@@ -464,12 +484,8 @@ struct Stage1 {
             if (sub == 0)
                 (a.norms_out + grow)[lr] = rho;
         } else {
-            const uint32_t h = blockIdx.x;
-            const int64_t s = (a.slots + grow)[lr];
-            const bool ok = s >= 0 && s < a.n_slots;
-            const uint32_t su = ok ? (uint32_t)s : 0u;
-            const uint32_t blk = fast_div(su, a.div_block);
-            const int64_t crow = ((int64_t)blk * a.n_heads + h) * a.block_size + (su - blk * a.block_size);
+            bool ok;
+            const int64_t crow = cache_row(a, grow, lr, ok);
             store_bits<BITS>(a.rec_out + crow * RECB, sub, p, ok);
             if (ok && sub == 0)
                 a.norms_out[crow] = rho;
@@ -492,8 +508,7 @@ struct Stage1 {
         const int64_t groups = (a.n + VPW - 1) / VPW;
         // append: blocks (head, token range) are dispatched head-fastest, so
         // the blocks in flight read all heads of the same tokens, one span
-        const int64_t base = (int64_t)(MODE == MODE_APPEND ? blockIdx.y : blockIdx.x) * (kBlockThreads / 64) *
-                             kTileGroups;
+        const int64_t base = (int64_t)(kAppend ? blockIdx.y : blockIdx.x) * (kBlockThreads / 64) * kTileGroups;
 
         // 1. block-wide tables: the codebook (dequantize) and the rotation
         //    parameters of the block's set, staged through LDS
@@ -511,7 +526,7 @@ struct Stage1 {
         if constexpr (!GENERIC_SETS) {
             // append: the block's head (every set is a head, or there is one)
             const int64_t set = a.n_sets <= 1           ? 0
-                                : MODE == MODE_APPEND ? (int64_t)blockIdx.x
+                                : kAppend             ? (int64_t)blockIdx.x
                                                       : (base * VPW / a.rows_per_set) % a.n_sets;
             const u32x4 *s4 = reinterpret_cast<const u32x4 *>(a.params + set * (LPV * PL));
             u32x4 *d4 = reinterpret_cast<u32x4 *>(lds_params);
@@ -539,12 +554,13 @@ struct Stage1 {
             thr[k] = a.thr_pos[k];
 
         // With the stage-2 sketch a block may walk several tiles (stride
-        // gridDim.x) so that the staged projection serves them all; the host
-        // launches one block per tile when the tiles' sets differ.  No
-        // barrier follows, so each wave leaves on its own.
+        // gridDim.x, or gridDim.y over one head's tokens when appending) so
+        // that the staged projection serves them all; the host launches one
+        // block per tile when the tiles' sets differ.  No barrier follows, so
+        // each wave leaves on its own.
         _Float16 *eq = kQjl ? lds_e + w * kTileRows * kEStride : nullptr;
-        for (int64_t tb = (int64_t)(MODE == MODE_APPEND ? blockIdx.y : blockIdx.x);;
-             tb += (kQjl ? (int64_t)gridDim.x : (int64_t)1 << 62)) {
+        const int64_t tstride = kQjl ? (int64_t)(kAppend ? gridDim.y : gridDim.x) : (int64_t)1 << 62;
+        for (int64_t tb = (int64_t)(kAppend ? blockIdx.y : blockIdx.x);; tb += tstride) {
             const int64_t tbase = tb * (kBlockThreads / 64) * kTileGroups;
             if (tbase + w >= groups)
                 return;
@@ -591,8 +607,14 @@ struct Stage1 {
         // this lane's output row (lanes 0 .. kTileRows-1): group u, slot
         const int u = r16 / VPW, sl = r16 - u * VPW;
         const int64_t gl = 4 * u + w;
-        const bool ok = l < kTileRows && base + gl < groups;
-        const int64_t row = min(row0 + gl * VPW + sl, a.n - 1);
+        bool ok = l < kTileRows && base + gl < groups;
+        int64_t row = min(row0 + gl * VPW + sl, a.n - 1);
+        if constexpr (kAppend) {
+            // the token's cache row (a skipped slot writes nothing)
+            bool in_cache;
+            row = cache_row(a, row, 0, in_cache);
+            ok = ok && in_cache;
+        }
         uint32_t *dst = reinterpret_cast<uint32_t *>(a.qjl_signs + row * (QM / 8));
         // k-step outer, column tile inner: the NT accumulations are
         // independent, so consecutive MFMAs do not wait on each other

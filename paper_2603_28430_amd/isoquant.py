@@ -57,6 +57,7 @@ def _load():
     L.isoq_sketch_destroy.argtypes = [vp]
     L.isoq_sketch_export.argtypes = [vp, ctypes.POINTER(c_int), fp]
     L.isoq_quantize_qjl.argtypes = [vp, vp, c_int, vp, i64, i64, vp, vp, vp, vp, vp]
+    L.isoq_kv_append_qjl.argtypes = [vp, vp, c_int, vp, vp, i64, c_int, vp, vp, vp, vp, i64, c_int, vp]
     L.isoq_kv_scores_qjl.argtypes = [vp, vp, c_int, vp, c_int, c_int, c_int, vp, vp, vp, vp, i64, c_int, vp, c_int,
                                      vp, ctypes.c_float, vp, i64, vp]
     L.isoq_kv_scores.argtypes = [vp, c_int, vp, c_int, c_int, c_int, vp, vp, i64, c_int, vp, c_int, vp,
@@ -426,7 +427,42 @@ def isoq_quantize_qjl(p: Params, sk: Sketch, x, rows_per_set: int = 1, idx_packe
         signs = torch.empty((n, sk.m // 8), dtype=torch.uint8, device=dev)
     if gamma is None:
         gamma = torch.empty((n,), dtype=torch.float32, device=dev)
+    if (idx_packed.numel() != n * p.record_bytes or norms.numel() != n or signs.numel() != n * (sk.m // 8)
+            or gamma.numel() != n):
+        raise ValueError("outputs must hold n records, norms, sign sketches of m/8 bytes and gammas")
     _check(lib.isoq_quantize_qjl(p.handle, sk.handle, _dtype_code(x.dtype), _ptr(x), n, int(rows_per_set),
                                  _ptr(idx_packed), _ptr(norms), _ptr(signs), _ptr(gamma), _stream_ptr(stream)),
            "isoq_quantize_qjl")
     return idx_packed, norms, signs, gamma
+
+
+def isoq_kv_append_qjl(pk: Params, sk: Sketch, k_new, slot_mapping, k_idx, k_rho, k_signs, k_gamma,
+                       stream=None):
+    """Quantize new key rows k_new [n_tokens, n_heads, d] with the stage-2
+    sketch into the paged caches k_idx [n_blocks, n_heads, block_size, R],
+    k_rho and k_gamma [n_blocks, n_heads, block_size] fp32 and k_signs
+    [n_blocks, n_heads, block_size, m/8] uint8 at the slots slot_mapping
+    [n_tokens] int64 (see include/isoquant.h)."""
+    torch = _torch()
+    if k_new.dim() != 3 or k_idx.dim() != 4 or k_rho.dim() != 3 or k_signs.dim() != 4 or k_gamma.dim() != 3:
+        raise ValueError("k_new [n_tokens, n_heads, d], k_idx [n_blocks, n_heads, block_size, R], "
+                         "k_signs [n_blocks, n_heads, block_size, m/8], k_rho and k_gamma [n_blocks, n_heads, "
+                         "block_size]")
+    n_tokens, n_heads, d = k_new.shape
+    n_blocks, nh, block_size, rb = k_idx.shape
+    cache = (n_blocks, nh, block_size)
+    if (d != pk.d or nh != n_heads or rb != pk.record_bytes or tuple(k_rho.shape) != cache
+            or tuple(k_gamma.shape) != cache or tuple(k_signs.shape) != cache + (sk.m // 8,)):
+        raise ValueError("cache shapes do not match the rows, the handle and the sketch")
+    if slot_mapping.dtype != torch.int64 or slot_mapping.numel() != n_tokens:
+        raise ValueError("slot_mapping must be int64 [n_tokens]")
+    if (k_idx.dtype != torch.uint8 or k_signs.dtype != torch.uint8 or k_rho.dtype != torch.float32
+            or k_gamma.dtype != torch.float32):
+        raise TypeError("k_idx and k_signs uint8, k_rho and k_gamma float32")
+    for t in (k_new, slot_mapping, k_idx, k_rho, k_signs, k_gamma):
+        if not t.is_cuda or not t.is_contiguous():
+            raise ValueError("tensors must be contiguous and on the GPU")
+    _check(lib.isoq_kv_append_qjl(pk.handle, sk.handle, _dtype_code(k_new.dtype), _ptr(k_new), _ptr(slot_mapping),
+                                  int(n_tokens), int(n_heads), _ptr(k_idx), _ptr(k_rho), _ptr(k_signs),
+                                  _ptr(k_gamma), int(n_blocks), int(block_size), _stream_ptr(stream)),
+           "isoq_kv_append_qjl")

@@ -129,6 +129,8 @@ def test_argument_validation_before_any_device_call():
     assert binding.lib.isoq_quantize_qjl(None, None, 1, None, 4, 1, None, None, None, None, None) == 3
     assert binding.lib.isoq_kv_scores_qjl(None, None, 1, None, 1, 1, 1, None, None, None, None, 1, 16, None, 1,
                                           None, 1.0, None, 16, None) == 3
+    assert binding.lib.isoq_kv_append_qjl(None, None, 1, None, None, 4, 2, None, None, None, None, 8, 16,
+                                          None) == 3
     assert binding.lib.isoq_params_destroy(None) == 0
     assert binding.lib.isoq_params_export(None, None, None, None) == 3
 
