@@ -29,8 +29,8 @@
  *     (arithmetic is fp32 in every case); d from 1 to 1024 for quantize,
  *     dequantize and round trip (tuned kernels for d in {64, 128, 256, 512}, one
  *     generic kernel family for every other width), d in {64, 128, 256, 512} for
- *     the KV-cache and attention-score calls, d in {128, 256} for the stage-2
- *     sketch.
+ *     the KV-cache and attention-score calls, d in {64, 128, 256} for the
+ *     stage-2 sketch.
  *   - Widths that are not a multiple of the block size (4; 2-D: 2) follow
  *     Sec. 5.1: the last block is zero padded, all pw rotated coordinates are
  *     quantized and stored (pw = 4 ceil(d/4); 2-D: 2 ceil(d/2)), and the
@@ -234,7 +234,7 @@ isoq_status isoq_kv_scores(const isoq_params *pk, int dtype, const void *q, int 
  *     <q, x_hat> + sqrt(pi/2) / m * gamma * <S q, 2 z - 1>.
  *
  * isoq_sketch_init -- build the sketch of quantizer p on the current device.
- *   m       sketch bits per row: 64 or 128 at d = 128, 64 at d = 256.
+ *   m       sketch bits per row: 64 or 128 at d = 64 and 128, 64 at d = 256.
  *   S_host  NULL, or host array [m][d] of doubles (row-major).  NULL: S is
  *           drawn from `seed`: S[i][4g .. 4g+3] is the Box-Muller quadruple of
  *           Philox4x32-10 with key = seed and counter (g, i, 3, 0) (the

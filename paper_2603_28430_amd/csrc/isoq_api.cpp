@@ -167,7 +167,7 @@ const char *isoq_status_string(isoq_status s)
     switch (s) {
     case ISOQ_OK: return "ok";
     case ISOQ_E_INVALID: return "invalid argument";
-    case ISOQ_E_UNSUPPORTED: return "unsupported shape (d in 1..1024, bits in {2,3,4}; the KV and score calls need d in {64,128,256,512}, the sketch d in {128,256}) or size limit";
+    case ISOQ_E_UNSUPPORTED: return "unsupported shape (d in 1..1024, bits in {2,3,4}; the KV and score calls need d in {64,128,256,512}, the sketch d in {64,128,256}) or size limit";
     case ISOQ_E_NULL: return "null pointer";
     case ISOQ_E_ALIGN: return "misaligned pointer";
     case ISOQ_E_HIP: return "HIP runtime error";
@@ -653,7 +653,7 @@ isoq_status isoq_sketch_init(isoq_sketch **out, const isoq_params *p, int m, con
         return ISOQ_E_NULL;
     if (m < 1)
         return ISOQ_E_INVALID;
-    if (!((p->d == 128 && (m == 64 || m == 128)) || (p->d == 256 && m == 64)))
+    if (!(((p->d == 64 || p->d == 128) && (m == 64 || m == 128)) || (p->d == 256 && m == 64)))
         return ISOQ_E_UNSUPPORTED;
     const int d = p->d;
     std::vector<double> S((size_t)m * d), Sp((size_t)m * d);

@@ -31,7 +31,7 @@ __global__ __launch_bounds__(kBlockThreads) void qjl_kernel(const KArgs a)
 template <int VAR, int D, int BITS, bool F16, int MODE>
 const void *qjl_pick_m(int m)
 {
-    if constexpr (D == 128) {
+    if constexpr (D <= 128) {
         if (m == 64)
             return reinterpret_cast<const void *>(&qjl_kernel<VAR, D, BITS, F16, 64, MODE>);
         if (m == 128)
@@ -60,6 +60,7 @@ const void *qjl_pick(int variant, int d, int bits, bool f16, int m)
     auto by_d = [&](auto var) -> const void * {
         constexpr int V = decltype(var)::value;
         switch (d) {
+        case 64: return qjl_pick_bits<V, 64, MODE>(bits, f16, m);
         case 128: return qjl_pick_bits<V, 128, MODE>(bits, f16, m);
         case 256: return qjl_pick_bits<V, 256, MODE>(bits, f16, m);
         }

@@ -19,7 +19,7 @@ ScoreKernel entry_qjl(int group)
 template <int VAR, int D, int BITS, bool F16>
 ScoreKernel pick_m(int group, int m)
 {
-    if constexpr (D == 128) {
+    if constexpr (D <= 128) {
         if (m == 64)
             return entry_qjl<VAR, D, BITS, F16, 64>(group);
         if (m == 128)
@@ -46,6 +46,7 @@ template <int VAR>
 ScoreKernel pick_d(int d, int bits, bool f16, int group, int m)
 {
     switch (d) {
+    case 64: return pick_bits<VAR, 64>(bits, f16, group, m);
     case 128: return pick_bits<VAR, 128>(bits, f16, group, m);
     case 256: return pick_bits<VAR, 256>(bits, f16, group, m);
     }

@@ -74,7 +74,8 @@ def test_append_qjl_matches_row_encoder(variant, bits):
              seed=bits)
 
 
-@pytest.mark.parametrize("d,m,dtype,n_sets", [(128, 64, "f32", 1), (256, 64, "f16", 2), (256, 64, "f32", 1)])
+@pytest.mark.parametrize("d,m,dtype,n_sets", [(128, 64, "f32", 1), (256, 64, "f16", 2), (256, 64, "f32", 1),
+                                              (64, 128, "f16", 2), (64, 64, "f32", 1)])
 def test_append_qjl_shapes(d, m, dtype, n_sets):
     run_case("full", d, 3, m, dtype, n_tokens=70, n_heads=2, block_size=8, n_blocks=10, n_sets=n_sets, seed=d)
 

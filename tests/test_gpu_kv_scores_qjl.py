@@ -106,7 +106,8 @@ def test_scores_qjl_d128_m128(variant, bits):
     run_case(variant, 128, bits, 128, "f16", n_seqs=2, n_q=2, n_kv=2, bs=16, seq_lens=[1100, 45], seed=bits)
 
 
-@pytest.mark.parametrize("d,m,dtype", [(128, 64, "f32"), (256, 64, "f16"), (256, 64, "f32")])
+@pytest.mark.parametrize("d,m,dtype", [(128, 64, "f32"), (256, 64, "f16"), (256, 64, "f32"), (64, 64, "f16"),
+                                       (64, 128, "f32")])
 def test_scores_qjl_shapes(d, m, dtype):
     run_case("full", d, 3, m, dtype, n_seqs=2, n_q=2, n_kv=2, bs=16, seq_lens=[700, 31], seed=d + m)
 

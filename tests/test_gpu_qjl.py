@@ -88,7 +88,8 @@ def test_qjl_d128_m128_f16(variant, bits):
 
 @pytest.mark.parametrize("variant,d,m,dtype", [("full", 128, 64, "f32"), ("fast", 128, 64, "f16"),
                                                ("full", 256, 64, "f16"), ("2d", 256, 64, "f32"),
-                                               ("fast", 128, 128, "f32")])
+                                               ("fast", 128, 128, "f32"), ("full", 64, 64, "f16"),
+                                               ("fast", 64, 128, "f32"), ("2d", 64, 128, "f16")])
 def test_qjl_shapes(variant, d, m, dtype):
     run_case(variant, d, 3, m, dtype, 501, seed=d + m)
 
@@ -171,4 +172,7 @@ def test_qjl_argument_errors():
     p512 = iq.isoq_params_init("full", 512, 3, 1)
     with pytest.raises(iq.IsoqError) as e:
         iq.isoq_sketch_init(p512, 64)
+    assert e.value.status == 2
+    with pytest.raises(iq.IsoqError) as e:                   # 128 sign bits need d <= 128
+        iq.isoq_sketch_init(iq.isoq_params_init("full", 256, 3, 1), 128)
     assert e.value.status == 2
