@@ -229,7 +229,57 @@ struct Stage1 {
     static constexpr int kTileRows = kTileGroups * VPW;   // 32 (d = 64), 16 (d = 128) or 8 (d = 256)
     static constexpr int kEStride = D + 8;                // halfs per LDS error row (padded)
 
-    // The lane's two slots' rotation parameters from a set's [2 LPV][PL / 2].
+    // Staged parameters in LDS.  With the 4-bit lookup table (whose reads
+    // compete for LDS) chunk k (16 bytes) of lane sub goes to word k LPV + sub,
+    // the lane's chunks in the order it uses them, so the lanes of a row read
+    // consecutive words: a plain copy of the slot-major set puts every lane
+    // of the row on the same four banks (Full's 128 bytes per lane: a 16-way
+    // conflict), which cost the 4-bit kernels about 5%.  Without the table the
+    // plain copy measured about 1% faster, so those kernels keep it.
+    static constexpr bool kChunkMajor = kUseLut;
+
+    __device__ static __forceinline__ void stage_params(const float *set, float *lds)
+    {
+        if constexpr (!kChunkMajor) {
+            const u32x4 *s4 = reinterpret_cast<const u32x4 *>(set);
+            u32x4 *d4 = reinterpret_cast<u32x4 *>(lds);
+            for (int i = threadIdx.x; i < LPV * PL / 4; i += kBlockThreads)
+                d4[i] = s4[i];
+            return;
+        }
+        constexpr int CPS = PL / 8;  // 16-byte chunks per slot
+        const u32x4 *s4 = reinterpret_cast<const u32x4 *>(set);
+        u32x4 *d4 = reinterpret_cast<u32x4 *>(lds);
+        // LDS word j = k LPV + ln is written in order (no bank conflicts);
+        // its chunk is gathered from the set (a few KB, cached)
+        for (int j = threadIdx.x; j < LPV * PL / 4; j += kBlockThreads) {
+            const int k = j / LPV, ln = j - k * LPV;
+            const int half = k / CPS, c = k - half * CPS;
+            const int slot = kSplit ? half * LPV + ln : 2 * ln + half;
+            d4[j] = s4[slot * CPS + c];
+        }
+    }
+
+    __device__ static __forceinline__ void lds_lane_params(const float *lds, int sub, float P[PL])
+    {
+        if constexpr (!kChunkMajor) {
+            lane_params(lds, sub, P);
+            return;
+        }
+        const u32x4 *q = reinterpret_cast<const u32x4 *>(lds);
+#pragma unroll
+        for (int k = 0; k < PL / 4; k++) {
+            const u32x4 w = q[k * LPV + sub];
+            const uint32_t e0 = w[0], e1 = w[1], e2 = w[2], e3 = w[3];
+            P[4 * k] = __uint_as_float(e0);
+            P[4 * k + 1] = __uint_as_float(e1);
+            P[4 * k + 2] = __uint_as_float(e2);
+            P[4 * k + 3] = __uint_as_float(e3);
+        }
+    }
+
+    // The lane's two slots' rotation parameters from a set's [2 LPV][PL / 2]
+    // in global memory.
     __device__ static __forceinline__ void lane_params(const float *set, int sub, float P[PL])
     {
         if constexpr (kSplit) {
@@ -528,10 +578,7 @@ struct Stage1 {
             const int64_t set = a.n_sets <= 1           ? 0
                                 : kAppend             ? (int64_t)blockIdx.x
                                                       : (base * VPW / a.rows_per_set) % a.n_sets;
-            const u32x4 *s4 = reinterpret_cast<const u32x4 *>(a.params + set * (LPV * PL));
-            u32x4 *d4 = reinterpret_cast<u32x4 *>(lds_params);
-            for (int i = threadIdx.x; i < LPV * PL / 4; i += kBlockThreads)
-                d4[i] = s4[i];
+            stage_params(a.params + set * (LPV * PL), lds_params);
             if constexpr (kQjl) {
                 // the set's projection S' = S T^{-1} in MFMA B-fragment order
                 const u32x4 *f4 = reinterpret_cast<const u32x4 *>(a.qjl_frag + set * (int64_t)(QM * D));
@@ -543,7 +590,7 @@ struct Stage1 {
         if constexpr (MODE == MODE_DEQUANTIZE || !GENERIC_SETS || kUseLut)
             __syncthreads();
         if constexpr (!GENERIC_SETS)
-            lane_params(lds_params, sub, P);
+            lds_lane_params(lds_params, sub, P);
 
         float lev[H], thr[H > 1 ? H - 1 : 1];
 #pragma unroll
