@@ -140,3 +140,18 @@ def test_append_qjl_argument_errors():
     lib = iq.isoquant.lib
     assert lib.isoq_kv_append_qjl(p.handle, sk.handle, 1, x.data_ptr(), slots.data_ptr(), 4, 2, rec.data_ptr(),
                                   rho.data_ptr(), None, gam.data_ptr(), 2, 16, None) == 3
+
+
+def test_append_qjl_empty_is_a_noop():
+    p = iq.isoq_params_init("fast", 128, 3, 1)
+    sk = iq.isoq_sketch_init(p, 64)
+    x = torch.empty((0, 2, 128), dtype=torch.float16, device="cuda")
+    slots = torch.empty((0,), dtype=torch.int64, device="cuda")
+    rec = torch.full((2, 2, 16, 48), CANARY_B, dtype=torch.uint8, device="cuda")
+    sg = torch.full((2, 2, 16, 8), CANARY_B, dtype=torch.uint8, device="cuda")
+    rho = torch.full((2, 2, 16), CANARY_F, dtype=torch.float32, device="cuda")
+    gam = torch.full((2, 2, 16), CANARY_F, dtype=torch.float32, device="cuda")
+    iq.isoq_kv_append_qjl(p, sk, x, slots, rec, rho, sg, gam)
+    torch.cuda.synchronize()
+    assert torch.all(rec == CANARY_B) and torch.all(sg == CANARY_B)
+    assert torch.all(rho == CANARY_F) and torch.all(gam == CANARY_F)

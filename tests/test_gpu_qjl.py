@@ -176,3 +176,33 @@ def test_qjl_argument_errors():
     with pytest.raises(iq.IsoqError) as e:                   # 128 sign bits need d <= 128
         iq.isoq_sketch_init(iq.isoq_params_init("full", 256, 3, 1), 128)
     assert e.value.status == 2
+
+
+def test_qjl_guard_bands_determinism_stream_empty():
+    """Canary bytes around every output of isoq_quantize_qjl survive; a second
+    call and a call on a non-default stream write the same bytes; n = 0 is a
+    no-op."""
+    d, m, n, G = 128, 128, 777, 64
+    p = iq.isoq_params_init("full", d, 3, 1, rot=workloads.rotation_draws("full", d, 1, seed=1))
+    sk = iq.isoq_sketch_init(p, m)
+    x = torch.from_numpy(workloads.unit_gaussian_rows(n, d, seed=6, dtype=np.float16)).cuda()
+    R, mb = p.record_bytes, m // 8
+    bufs = [torch.full((n * w + 2 * G,), 0xA5, dtype=torch.uint8, device="cuda") for w in (R, 4, mb, 4)]
+    rec, nrm, sg, gm = (bufs[0][G:G + n * R].view(n, R), bufs[1][G:G + 4 * n].view(torch.float32),
+                        bufs[2][G:G + n * mb].view(n, mb), bufs[3][G:G + 4 * n].view(torch.float32))
+    iq.isoq_quantize_qjl(p, sk, x, idx_packed=rec, norms=nrm, signs=sg, gamma=gm)
+    torch.cuda.synchronize()
+    for b in bufs:
+        assert torch.all(b[:G] == 0xA5) and torch.all(b[-G:] == 0xA5)
+    again = iq.isoq_quantize_qjl(p, sk, x)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        other = iq.isoq_quantize_qjl(p, sk, x, stream=s)
+    s.synchronize()
+    torch.cuda.synchronize()
+    for a, b, c in zip((rec, nrm, sg, gm), again, other):
+        assert torch.equal(a, b) and torch.equal(a, c)
+    e = torch.empty((0, d), dtype=torch.float16, device="cuda")
+    out = iq.isoq_quantize_qjl(p, sk, e)
+    torch.cuda.synchronize()
+    assert all(t.numel() == 0 for t in out)

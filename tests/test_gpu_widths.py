@@ -135,3 +135,53 @@ def test_widths_unsupported_calls():
     out = z(1, 1, 32, dt=torch.float32)
     assert lib.isoq_kv_scores(p.handle, 1, q.data_ptr(), 1, 1, 1, rec.data_ptr(), rho.data_ptr(), 2, 16,
                               tab.data_ptr(), 2, lens.data_ptr(), 1.0, out.data_ptr(), 32, None) == 2
+
+
+@pytest.mark.parametrize("variant,d,dtype", [("full", 90, "f16"), ("fast", 96, "f32"), ("2d", 1000, "f16"),
+                                             ("fast", 7, "f32")])
+def test_widths_guard_bands_determinism_stream_in_place(variant, d, dtype):
+    """Canary bytes around every output survive; a second call writes the
+    same bytes; a non-default stream gives the same result; the round trip
+    may overwrite its input; n = 0 writes nothing."""
+    tdt, ndt = DT[dtype]
+    n, G = 517, 64
+    p = iq.isoq_params_init(variant, d, 3, 1, rot=workloads.rotation_draws(variant, d, 1, seed=1))
+    x = torch.from_numpy(workloads.unit_gaussian_rows(n, d, seed=4, dtype=ndt)).cuda()
+    R = p.record_bytes
+    big_y = torch.full((n * d + 2 * G,), -3.0, dtype=tdt, device="cuda")
+    big_r = torch.full((n * R + 2 * G,), 0xA5, dtype=torch.uint8, device="cuda")
+    big_n = torch.full((n + 2 * G,), -5.0, dtype=torch.float32, device="cuda")
+    big_d = torch.full((n * d + 2 * G,), -3.0, dtype=tdt, device="cuda")
+    y, rec, nrm, dq = (big_y[G:G + n * d].view(n, d), big_r[G:G + n * R].view(n, R), big_n[G:G + n],
+                       big_d[G:G + n * d].view(n, d))
+    iq.isoq_roundtrip(p, x, x_hat=y)
+    iq.isoq_quantize(p, x, idx_packed=rec, norms=nrm)
+    iq.isoq_dequantize(p, rec, nrm, x_hat=dq)
+    torch.cuda.synchronize()
+    for big, val in ((big_y, -3.0), (big_r, 0xA5), (big_n, -5.0), (big_d, -3.0)):
+        assert torch.all(big[:G] == val) and torch.all(big[-G:] == val)
+    assert torch.equal(y, dq)
+    # determinism
+    y2 = iq.isoq_roundtrip(p, x)
+    rec2, nrm2 = iq.isoq_quantize(p, x)
+    torch.cuda.synchronize()
+    assert torch.equal(y2, y) and torch.equal(rec2, rec) and torch.equal(nrm2, nrm)
+    # non-default stream
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        y3 = torch.empty_like(x)
+        iq.isoq_roundtrip(p, x, x_hat=y3, stream=s)
+    s.synchronize()
+    assert torch.equal(y3, y)
+    # in place
+    xi = x.clone()
+    iq.isoq_roundtrip(p, xi, x_hat=xi)
+    torch.cuda.synchronize()
+    assert torch.equal(xi, y)
+    # empty batch
+    e = torch.empty((0, d), dtype=tdt, device="cuda")
+    canary = torch.full((4,), 7.0, dtype=torch.float32, device="cuda")
+    out = iq.isoq_roundtrip(p, e)
+    idx0, _ = iq.isoq_quantize(p, e, norms=canary[:0])
+    torch.cuda.synchronize()
+    assert out.numel() == 0 and idx0.numel() == 0 and torch.all(canary == 7.0)
