@@ -294,6 +294,7 @@ struct Stage1 {
         Raw<F16> raw;
         uint32_t bits;
         float rho;
+        int64_t slot;  // append modes: the token's cache slot
     };
 
     // Row addressing.  The row of a lane is grow + lr: grow, the first row of
@@ -320,7 +321,10 @@ struct Stage1 {
                 in.bits = load_bits<BITS>(rec, sub);
             in.rho = (a.norms_in + grow)[lr];
         } else if constexpr (kAppend) {
-            // token grow + lr, head blockIdx.x of rows [n_tokens][n_heads][d]
+            // token grow + lr, head blockIdx.x of rows [n_tokens][n_heads][d];
+            // its slot is loaded with the row, so that the write-out does not
+            // wait for it
+            in.slot = (a.slots + grow)[lr];
             const int64_t tstride = (int64_t)a.n_heads * ROWB;
             load_row_chunk<F16>(static_cast<const char *>(a.x) + grow * tstride + (int64_t)blockIdx.x * ROWB +
                                     (uint32_t)(lr * (uint32_t)tstride + sub * LANEB),
@@ -381,7 +385,7 @@ struct Stage1 {
                     }
                 }
                 if constexpr (kEncode)
-                    emit(a, grow, lr, sub, p, rho);
+                    emit(a, grow, lr, sub, p, rho, in.slot);
             } else {
             float ths[H > 1 ? H - 1 : 1];
 #pragma unroll
@@ -462,7 +466,7 @@ struct Stage1 {
                     else
                         p = push_bits4(p, mk);
                 }
-                emit(a, grow, lr, sub, p, rho);
+                emit(a, grow, lr, sub, p, rho, in.slot);
             }
             }
             if constexpr (kQjl) {
@@ -480,7 +484,7 @@ struct Stage1 {
                 const float gamma = rho * __builtin_amdgcn_sqrtf(row_sum<LPV>(s2));
                 if constexpr (kAppend) {
                     bool ok;
-                    const int64_t r = cache_row(a, grow, lr, ok);
+                    const int64_t r = cache_row_of(a, in.slot, ok);
                     if (ok && sub == 0)
                         a.qjl_gamma[r] = gamma;
                 } else if (sub == 0) {
@@ -504,26 +508,31 @@ struct Stage1 {
         }
     }
 
-    // Write one row's index record and norm: to row grow + lr (quantize), or
-    // to the cache slot of token grow + lr for head blockIdx.x (append): slot
-    // s is position s mod block_size of cache block s / block_size, and a
-    // cache block holds [n_heads][block_size] records.  A skipped slot writes
-    // nothing; the quad exchange inside store_bits runs on every lane either
-    // way.
-    // Cache row of token grow + lr for head blockIdx.x (append modes); ok is
-    // false for a skipped slot (then the row returned is 0 and must not be
-    // written).
-    __device__ static __forceinline__ int64_t cache_row(const KArgs &a, int64_t grow, int lr, bool &ok)
+    // Cache row of slot s for head blockIdx.x (append modes): slot s is
+    // position s mod block_size of cache block s / block_size, and a cache
+    // block holds [n_heads][block_size] records.  ok is false for a skipped
+    // slot (s < 0 or past the cache; the row returned is then 0 and must not
+    // be written).
+    __device__ static __forceinline__ int64_t cache_row_of(const KArgs &a, int64_t s, bool &ok)
     {
-        const int64_t s = (a.slots + grow)[lr];
         ok = s >= 0 && s < a.n_slots;
         const uint32_t su = ok ? (uint32_t)s : 0u;
         const uint32_t blk = fast_div(su, a.div_block);
         return ((int64_t)blk * a.n_heads + blockIdx.x) * a.block_size + (su - blk * a.block_size);
     }
 
+    // The same for token grow + lr, its slot read from the slot mapping.
+    __device__ static __forceinline__ int64_t cache_row(const KArgs &a, int64_t grow, int lr, bool &ok)
+    {
+        return cache_row_of(a, (a.slots + grow)[lr], ok);
+    }
+
+    // Write one row's index record and norm: to row grow + lr (quantize), or
+    // to the cache row of the token's slot (append; `slot` was loaded with
+    // the row).  A skipped slot writes nothing; the quad exchange inside
+    // store_bits runs on every lane either way.
     __device__ static __forceinline__ void emit(const KArgs &a, int64_t grow, int lr, int sub,
-                                                uint32_t p, float rho)
+                                                uint32_t p, float rho, int64_t slot)
     {
         if constexpr (!kAppend) {
             uint8_t *rec = a.rec_out + grow * RECB + (uint32_t)(lr * RECB);
@@ -535,7 +544,7 @@ struct Stage1 {
                 (a.norms_out + grow)[lr] = rho;
         } else {
             bool ok;
-            const int64_t crow = cache_row(a, grow, lr, ok);
+            const int64_t crow = cache_row_of(a, slot, ok);
             store_bits<BITS>(a.rec_out + crow * RECB, sub, p, ok);
             if (ok && sub == 0)
                 a.norms_out[crow] = rho;
