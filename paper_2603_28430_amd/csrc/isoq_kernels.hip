@@ -8,13 +8,15 @@
 //                    K/V cache: blockIdx.x is the head, blockIdx.y the token
 //                    range, blockIdx.z selects K or V
 //
-// Mapping.  A lane owns 8 consecutive coordinates of one row: 16 bytes of
-// fp16 (one global_load_dwordx4) or 32 bytes of fp32 (two).  Those 8
-// coordinates are two quaternion blocks (Full/Fast, Sec. 5.2-5.3) or four
-// planar pairs (Sec. 5.4), so the rotation never leaves the lane.  A row spans
-// d/8 lanes (16, 32 or 64) and a wave holds 512/d rows; the squared norm is
-// reduced with DPP row operations inside each 16-lane row and with permlane
-// swaps across rows.  Every lane keeps the parameters of its own blocks in
+// Mapping.  A lane owns 8 coordinates of one row: two 4-coordinate slots,
+// each a quaternion block (Full/Fast, Sec. 5.2-5.3) or two planar pairs
+// (Sec. 5.4), so the rotation never leaves the lane.  fp16 rows: slots 2s and
+// 2s + 1, 16 bytes (one global_load_dwordx4); fp32 rows: slots s and
+// s + d/8 in the round trip, quantize and dequantize (two 16-byte accesses
+// that each cover a dense span across the wave), adjacent slots in append.
+// A row spans d/8 lanes (8, 16, 32 or 64) and a wave holds 512/d rows; the
+// squared norm is reduced with DPP row operations inside each 16-lane row and
+// with permlane swaps across rows.  Every lane keeps the parameters of its own blocks in
 // VGPRs for the whole kernel; the codebook sits in kernel-argument SGPRs.
 //
 // Blocks are not persistent: each owns a tile of consecutive row groups,

@@ -1,6 +1,7 @@
 // The stage-1 kernel template shared by isoq_kernels.hip (round trip,
-// quantize, dequantize, append) and isoq_qjl.hip (quantize with the stage-2
-// residual sketch): packed index records, the Stage1 work split and compute.
+// quantize, dequantize, append) and isoq_qjl.h (quantize with the stage-2
+// residual sketch, into rows or into cache slots): packed index records, the
+// Stage1 work split and compute.
 #pragma once
 
 #include "isoq_device.h"
