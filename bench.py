@@ -321,8 +321,9 @@ def qjl_side(torch, workloads):
 def widths_side(torch, workloads):
     """Widths outside {128, 256, 512} (Sec. 5.1 zero padding where needed):
     round trip and quantize of 1,048,576 unit-norm rows (262,144 for d = 1000),
-    Full and Fast, 3 bits; d = 64 runs the tuned kernels, the others the
-    generic ones.  Algorithmic bytes per row as for the
+    Full and Fast, 3 bits; d = 64 runs the tuned kernels, fp16 d = 80, 96, 160
+    and 192 the packed-row kernels, d = 90 and the fp32 rows the generic ones.  Algorithmic
+    bytes per row as for the
     tuned widths: 2 d s for the round trip, d s + record + 4 for quantize (s =
     bytes per element, record = ceil(pw * 3 / 8))."""
     import numpy as np
@@ -331,7 +332,7 @@ def widths_side(torch, workloads):
 
     out = {}
     for d, dtype, n in ((64, "f16", 1 << 20), (80, "f16", 1 << 20), (96, "f16", 1 << 20), (90, "f16", 1 << 20),
-                        (192, "f16", 1 << 20), (96, "f32", 1 << 20), (1000, "f32", 1 << 18)):
+                        (160, "f16", 1 << 20), (192, "f16", 1 << 20), (96, "f32", 1 << 20), (1000, "f32", 1 << 18)):
         tdt, ndt, esz = (torch.float16, np.float16, 2) if dtype == "f16" else (torch.float32, np.float32, 4)
         name = f"d{d}_{dtype}_n{n}"
         print(f"# widths {name}", file=sys.stderr, flush=True)

@@ -43,7 +43,8 @@ def build(verbose: bool = False) -> str:
     inc = [f"-I{INCLUDE}", f"-I{CSRC}"]
     jobs = []
     for src in ("isoq_kernels.hip", "isoq_scores.hip", "isoq_scores_qjl.hip", "isoq_qjl.hip",
-                "isoq_generic_full.hip", "isoq_generic_fast.hip", "isoq_generic_2d.hip", "isoq_qjl_append.hip"):
+                "isoq_generic_full.hip", "isoq_generic_fast.hip", "isoq_generic_2d.hip", "isoq_qjl_append.hip",
+                "isoq_packed.hip"):
         jobs.append([HIPCC, *DEVICE_FLAGS, *inc, "-c", os.path.join(CSRC, src), "-o",
                      os.path.join(obj_dir, src + ".o")])
     for src in ("isoq_api.cpp", "isoq_host_params.cpp"):

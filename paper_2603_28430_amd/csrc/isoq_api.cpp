@@ -73,11 +73,9 @@ isoq_status check_device(const isoq_params *p)
     return dev == p->device ? ISOQ_OK : ISOQ_E_DEVICE;
 }
 
-// Rows of one block of the stage-1 kernels (a wave holds 512/d rows).
+// Rows of one block of the tuned stage-1 kernels (a wave holds 512/d rows).
 int64_t rows_per_block(const isoq_params *p)
 {
-    if (!tuned_d(p->d))
-        return (int64_t)generic_rows_per_wave(slots_per_set(p->variant, p->d)) * (kBlockThreads / 64);
     return (int64_t)(64 / (p->d / kCoordsPerLane)) * (kBlockThreads / 64) * kTileGroups;
 }
 
@@ -118,12 +116,19 @@ isoq_status run_generic(const isoq_params *p, int dtype, int mode, KArgs &a, voi
 {
     const int slots = slots_per_set(p->variant, p->d);
     const bool f16 = dtype == ISOQ_F16;
-    const void *fn = p->variant == VAR_FULL   ? generic_kernel_full(slots, p->bits, f16, mode)
+    const int v = packed_rows(p->d, p->bits, f16);
+    const void *fn = v > 0                    ? (p->variant == VAR_FULL   ? packed_kernel_full(p->bits, mode)
+                                                 : p->variant == VAR_FAST ? packed_kernel_fast(p->bits, mode)
+                                                                          : packed_kernel_2d(p->bits, mode))
+                     : p->variant == VAR_FULL ? generic_kernel_full(slots, p->bits, f16, mode)
                      : p->variant == VAR_FAST ? generic_kernel_fast(slots, p->bits, f16, mode)
                                               : generic_kernel_2d(slots, p->bits, f16, mode);
     if (!fn)
         return ISOQ_E_UNSUPPORTED;
-    const int64_t rpb = rows_per_block(p);
+    // rows per block: packed, 4 waves of kTileGroups groups of v rows;
+    // generic, 4 waves of their row groups
+    const int64_t rpb = v > 0 ? (int64_t)v * (kBlockThreads / 64) * kTileGroups
+                              : (int64_t)generic_rows_per_wave(slots) * (kBlockThreads / 64);
     const int64_t blocks = (a.n + rpb - 1) / rpb;
     if (blocks > 0x7FFFFFFF)
         return ISOQ_E_UNSUPPORTED;
@@ -133,6 +138,8 @@ isoq_status run_generic(const isoq_params *p, int dtype, int mode, KArgs &a, voi
     a.g_slots = slots;
     a.g_rec = (int32_t)record_bytes(p->variant, p->d, p->bits);
     a.g_vec = p->d % 4 == 0;
+    a.g_rows = v;
+    a.g_block_set = p->n_sets == 1 || (v > 0 && a.rows_per_set % rpb == 0);
     a.g_set_stride = (int64_t)slots * params_per_slot(p->variant);
     void *args[] = {&a};
     return launch(fn, dim3((unsigned)blocks), args, stream);

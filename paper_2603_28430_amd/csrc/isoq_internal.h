@@ -71,7 +71,7 @@ struct KArgs {
     int64_t n;               // rows
     int64_t rows_per_set;    // rows per parameter set (>= 1)
     int32_t n_sets;
-    int32_t pad0;
+    int32_t g_block_set;     // packed-row kernels: the rows of each block share one set
     const float *lut;        // magnitude lookup table (4-bit codebooks), [lut_cells][4]
     float lut_inv_h;         // 1 / cell width, in units of the normalised coordinate
     int32_t lut_cells;
@@ -93,7 +93,7 @@ struct KArgs {
     int32_t g_slots;           // 4-coordinate slots per row, ceil(g_pw / 4)
     int32_t g_rec;             // record bytes, ceil(g_pw * bits / 8)
     int32_t g_vec;             // rows move in whole slots (d a multiple of 4)
-    int32_t pad2;
+    int32_t g_rows;            // packed-row kernels (isoq_packed.h): rows per wave group
     int64_t g_set_stride;      // floats per parameter set, kSlotParams * g_slots
 };
 
@@ -155,6 +155,25 @@ inline int generic_rows_per_wave(int slots)
     return generic_groups(generic_bpl(slots)) * (64 / generic_lanes(slots));
 }
 constexpr int kGenericMaxD = 1024;
+// Packed-row kernels (isoq_packed.h) for fp16 rows of width d = 16 k up to
+// 512 outside the tuned widths: V = floor(64 / (d/8)) rows per wave group,
+// one fewer for 3 bits when V d/8 is not a multiple of 4 (a quad of lanes
+// writes whole words); 0 where the family does not apply (the generic
+// kernels take those widths and every fp32 row).
+constexpr int kPackedMaxLanes = 63;   // d/8 at d = 504
+inline int packed_rows(int d, int bits, bool f16)
+{
+    if (!f16 || d % 16 != 0 || d > 8 * kPackedMaxLanes || d == 64 || d == 128 || d == 256)
+        return 0;
+    const int L = d / 8;
+    int v = 64 / L;
+    if (bits == 3 && (v * L) % 4 != 0)
+        v--;
+    return v;
+}
+const void *packed_kernel_full(int bits, int mode);
+const void *packed_kernel_fast(int bits, int mode);
+const void *packed_kernel_2d(int bits, int mode);
 // Blocks of the stage-2 sketch kernel with a single rotation set (each walks
 // several tiles).
 constexpr int64_t kQjlBlocks = 1024;

@@ -188,6 +188,123 @@ __device__ __forceinline__ uint32_t push_bits12(uint32_t p, const uint64_t m[12]
     return p;
 }
 
+// ---- the quantizer of a lane's 8 rotated coordinates --------------------------
+// Shared by the tuned kernels and the packed-row kernels (isoq_packed.h).  y:
+// rotated coordinates (in units of rho when rho is folded into the thresholds),
+// m = |y|.
+
+// 4 bits: the cell of each normalised magnitude m s in the lookup table, then
+// one compare against the cell's threshold (quantize and round trip use the
+// same t).  Returns the index word (ENCODE); yq gets the signed selected levels
+// times lscale (LEVELS).
+template <int BITS, bool LEVELS, bool ENCODE>
+__device__ __forceinline__ uint32_t lut_quantize(const float y[8], const float m[8], float s, float last,
+                                                 const LutEntry *lut, float lscale, float yq[8])
+{
+    constexpr int H = 1 << (BITS - 1);
+    uint32_t p = 0;
+#pragma unroll
+    for (int j = 0; j < 8; j++) {
+        const float t = m[j] * s;
+        const LutEntry e = lut[(uint32_t)fminf(t, last)];
+        const bool above = t > e.t;
+        if constexpr (LEVELS) {
+            const float L = above ? e.hi : e.lo;
+            yq[j] = (y[j] > 0.f ? L : -L) * lscale;
+        }
+        if constexpr (ENCODE) {
+            const uint32_t q = e.m + (above ? 1u : 0u);
+            p |= (q ^ (y[j] > 0.f ? (uint32_t)H : (uint32_t)(H - 1))) << (BITS * j);
+        }
+    }
+    return p;
+}
+
+// 2 and 3 bits: the signed selected levels from the scaled positive
+// thresholds ths and levels lvs, thresholds outer and coordinates inner, so
+// that independent compares fill the distance between each compare and its
+// select.
+template <int H>
+__device__ __forceinline__ void chain_levels(const float y[8], const float m[8], const float *ths, const float *lvs,
+                                             float yq[8])
+{
+    float L[8];
+#pragma unroll
+    for (int j = 0; j < 8; j++)
+        L[j] = lvs[0];
+#pragma unroll
+    for (int k = 0; k < H - 1; k++)
+#pragma unroll
+        for (int j = 0; j < 8; j++)
+            L[j] = m[j] > ths[k] ? lvs[k + 1] : L[j];
+#pragma unroll
+    for (int j = 0; j < 8; j++)
+        yq[j] = y[j] > 0.f ? L[j] : -L[j];
+}
+
+// 2 and 3 bits: the index word of the 8 coordinates from lane masks.  With
+// QJL, yq also gets the signed normalised levels (from lev) that the
+// encoder's compares select.
+template <int BITS, bool QJL>
+__device__ __forceinline__ uint32_t ballot_encode(const float y[8], const float m[8], const float *ths,
+                                                  const float *lev, float yq[8])
+{
+    constexpr int H = 1 << (BITS - 1);
+    // For y > 0 the index is H + m, otherwise (H - 1) - m: its top
+    // bit is the sign decision and every lower bit is the matching
+    // bit of the magnitude index m, inverted when y <= 0.  The
+    // lane masks of those bits are pushed into the record word
+    // from its most significant end: coordinate 7's top bit first.
+    // m: 3 bits, binary search (compare with the middle positive
+    // threshold, then with the one it selects); 2 bits, one compare.
+    // 4 coordinates per asm block (2 with the stage-2 sketch,
+    // whose extra state would otherwise push the live masks past
+    // the scalar register file)
+    static_assert(BITS == 2 || BITS == 3, "2 or 3 bits on this branch");
+    constexpr int CPB = QJL ? 2 : 4;   // coordinates per push block
+    uint32_t p = 0;
+#pragma unroll
+    for (int j0 = 7; j0 >= 0; j0 -= CPB) {
+        uint64_t mk[CPB * BITS];  // BITS masks per coordinate
+#pragma unroll
+        for (int c = 0; c < CPB; c++) {
+            const int j = j0 - c;
+            uint64_t *o = mk + c * BITS;
+            const uint64_t pos = __builtin_amdgcn_ballot_w64(y[j] > 0.f);
+            o[0] = pos;
+            if constexpr (H == 4) {
+                const bool hi = m[j] > ths[1];
+                const bool lo = m[j] > (hi ? ths[2] : ths[0]);
+                o[1] = ~(__builtin_amdgcn_ballot_w64(hi) ^ pos);
+                o[2] = ~(__builtin_amdgcn_ballot_w64(lo) ^ pos);
+                if constexpr (QJL) {
+                    // normalised level of magnitude index 2 hi + lo
+                    const float La = lo ? lev[1] : lev[0];
+                    const float Lb = lo ? lev[3] : lev[2];
+                    const float L = hi ? Lb : La;
+                    yq[j] = y[j] > 0.f ? L : -L;
+                }
+            } else {
+                const bool above = m[j] > ths[0];
+                o[1] = ~(__builtin_amdgcn_ballot_w64(above) ^ pos);
+                if constexpr (QJL) {
+                    const float L = above ? lev[1] : lev[0];
+                    yq[j] = y[j] > 0.f ? L : -L;
+                }
+            }
+        }
+        if constexpr (CPB * BITS == 12)
+            p = push_bits12(p, mk);
+        else if constexpr (CPB * BITS == 8)
+            p = push_bits8(p, mk);
+        else if constexpr (CPB * BITS == 6)
+            p = push_bits6(p, mk);
+        else
+            p = push_bits4(p, mk);
+    }
+    return p;
+}
+
 // ---- the kernel ---------------------------------------------------------------
 // Work split.  A row group is the 512/d rows one wave holds.  Block b (four
 // waves) owns the kTileGroups * 4 consecutive groups starting at
@@ -366,25 +483,9 @@ struct Stage1 {
             for (int j = 0; j < 8; j++)
                 m[j] = fabsf(y[j]);
             if constexpr (kUseLut) {
-                // 4 bits: cell of the normalised magnitude, one compare against
-                // the cell's threshold (quantize and round trip use the same t)
                 const float s = a.lut_inv_h * __builtin_amdgcn_rcpf(rho_e);
-                const float last = (float)(a.lut_cells - 1);
-                uint32_t p = 0;
-#pragma unroll
-                for (int j = 0; j < 8; j++) {
-                    const float t = m[j] * s;
-                    const LutEntry e = lut[(uint32_t)fminf(t, last)];
-                    const bool above = t > e.t;
-                    if constexpr (kLevels) {
-                        const float L = above ? e.hi : e.lo;
-                        yq[j] = (y[j] > 0.f ? L : -L) * lscale;
-                    }
-                    if constexpr (kEncode) {
-                        const uint32_t q = e.m + (above ? 1u : 0u);
-                        p |= (q ^ (y[j] > 0.f ? (uint32_t)H : (uint32_t)(H - 1))) << (BITS * j);
-                    }
-                }
+                const uint32_t p =
+                    lut_quantize<BITS, kLevels, kEncode>(y, m, s, (float)(a.lut_cells - 1), lut, lscale, yq);
                 if constexpr (kEncode)
                     emit(a, grow, lr, sub, p, rho, in.slot);
             } else {
@@ -399,74 +500,10 @@ struct Stage1 {
 #pragma unroll
                 for (int k = 0; k < H; k++)
                     lvs[k] = lev[k] * lscale;
-                float L[8];
-#pragma unroll
-                for (int j = 0; j < 8; j++)
-                    L[j] = lvs[0];
-                // thresholds outer, coordinates inner: independent compares
-                // fill the distance between each compare and its select
-#pragma unroll
-                for (int k = 0; k < H - 1; k++)
-#pragma unroll
-                    for (int j = 0; j < 8; j++)
-                        L[j] = m[j] > ths[k] ? lvs[k + 1] : L[j];
-#pragma unroll
-                for (int j = 0; j < 8; j++)
-                    yq[j] = y[j] > 0.f ? L[j] : -L[j];
+                chain_levels<H>(y, m, ths, lvs, yq);
             }
             if constexpr (kEncode) {
-                // For y > 0 the index is H + m, otherwise (H - 1) - m: its top
-                // bit is the sign decision and every lower bit is the matching
-                // bit of the magnitude index m, inverted when y <= 0.  The
-                // lane masks of those bits are pushed into the record word
-                // from its most significant end: coordinate 7's top bit first.
-                // m: 3 bits, binary search (compare with the middle positive
-                // threshold, then with the one it selects); 2 bits, one compare.
-                // 4 coordinates per asm block (2 with the stage-2 sketch,
-                // whose extra state would otherwise push the live masks past
-                // the scalar register file)
-                static_assert(BITS == 2 || BITS == 3, "2 or 3 bits on this branch");
-                constexpr int CPB = kQjl ? 2 : 4;   // coordinates per push block
-                uint32_t p = 0;
-#pragma unroll
-                for (int j0 = 7; j0 >= 0; j0 -= CPB) {
-                    uint64_t mk[CPB * BITS];  // BITS masks per coordinate
-#pragma unroll
-                    for (int c = 0; c < CPB; c++) {
-                        const int j = j0 - c;
-                        uint64_t *o = mk + c * BITS;
-                        const uint64_t pos = __builtin_amdgcn_ballot_w64(y[j] > 0.f);
-                        o[0] = pos;
-                        if constexpr (H == 4) {
-                            const bool hi = m[j] > ths[1];
-                            const bool lo = m[j] > (hi ? ths[2] : ths[0]);
-                            o[1] = ~(__builtin_amdgcn_ballot_w64(hi) ^ pos);
-                            o[2] = ~(__builtin_amdgcn_ballot_w64(lo) ^ pos);
-                            if constexpr (kQjl) {
-                                // normalised level of magnitude index 2 hi + lo
-                                const float La = lo ? lev[1] : lev[0];
-                                const float Lb = lo ? lev[3] : lev[2];
-                                const float L = hi ? Lb : La;
-                                yq[j] = y[j] > 0.f ? L : -L;
-                            }
-                        } else {
-                            const bool above = m[j] > ths[0];
-                            o[1] = ~(__builtin_amdgcn_ballot_w64(above) ^ pos);
-                            if constexpr (kQjl) {
-                                const float L = above ? lev[1] : lev[0];
-                                yq[j] = y[j] > 0.f ? L : -L;
-                            }
-                        }
-                    }
-                    if constexpr (CPB * BITS == 12)
-                        p = push_bits12(p, mk);
-                    else if constexpr (CPB * BITS == 8)
-                        p = push_bits8(p, mk);
-                    else if constexpr (CPB * BITS == 6)
-                        p = push_bits6(p, mk);
-                    else
-                        p = push_bits4(p, mk);
-                }
+                const uint32_t p = ballot_encode<BITS, kQjl>(y, m, ths, lev, yq);
                 emit(a, grow, lr, sub, p, rho, in.slot);
             }
             }

@@ -1,6 +1,8 @@
-"""Parity of the generic-width stage-1 kernels (any d from 1 to 1024 outside
-{64, 128, 256, 512}; Sec. 5.1 zero padding when d is not a multiple of the
-block size) with the oracle, through the C ABI.
+"""Parity of the stage-1 kernels at widths outside {64, 128, 256, 512} with
+the oracle, through the C ABI: the packed-row kernels (fp16 rows,
+d = 16 k up to 504; 3 bits at d = 272, 304, ... 496 excepted) and the
+generic kernels (every other width and dtype up to d = 1024; Sec. 5.1 zero
+padding when d is not a multiple of the block size).
 
 Per case: isoq_quantize, isoq_dequantize and isoq_roundtrip on the same rows;
 the fused path equals quantize followed by dequantize bit for bit; indices,
@@ -25,9 +27,11 @@ DT = {"f16": (torch.float16, np.float16), "f32": (torch.float32, np.float32)}
 
 # widths below, between and above the tuned ones; odd, 2 mod 4 and
 # multiple-of-4 widths; every row shape of the generic kernels (8 to 64 lanes,
-# 1 to 4 slots per lane) and its largest width
-WIDTHS = [1, 2, 3, 5, 6, 7, 20, 32, 33, 60, 63, 80, 90, 96, 100, 127, 130, 192, 250, 256 + 4, 320, 384, 511,
-          640, 1000, 1024]
+# 1 to 4 slots per lane) and its largest width; packed rows of 2 to 62 lanes
+# (d = 16 .. 496: V d/8 a multiple of 4 or not, one row per wave), and widths
+# where 3 bits falls back to the generic kernels (272, 496)
+WIDTHS = [1, 2, 3, 5, 6, 7, 16, 20, 32, 33, 48, 60, 63, 80, 90, 96, 100, 112, 127, 130, 144, 160, 192, 208, 250,
+          256 + 4, 272, 320, 384, 496, 511, 640, 1000, 1024]
 
 
 def check(variant, d, bits, dtype, n, n_sets=1, rows_per_set=1, x=None, sample=None, seed=0):
@@ -68,7 +72,7 @@ def test_widths_parity(variant, d):
 
 
 @pytest.mark.parametrize("rows_per_set", [1, 5, 64, 1000])
-@pytest.mark.parametrize("variant,d", [("full", 90), ("fast", 96), ("2d", 75)])
+@pytest.mark.parametrize("variant,d", [("full", 90), ("fast", 96), ("2d", 75), ("full", 80), ("2d", 160)])
 def test_widths_multiple_sets(variant, d, rows_per_set):
     print(f"case {variant} d={d} sets=3 rps={rows_per_set}", flush=True)
     check(variant, d, 3, "f16", 2003, n_sets=3, rows_per_set=rows_per_set)
@@ -77,7 +81,7 @@ def test_widths_multiple_sets(variant, d, rows_per_set):
 @pytest.mark.parametrize("n", [1, 2, 3, 5, 33])
 def test_widths_tiny_batches(n):
     for variant in ("full", "fast", "2d"):
-        for d in (3, 60, 90, 1000):
+        for d in (3, 60, 80, 90, 96, 1000):
             print(f"case {variant} d={d} n={n}", flush=True)
             check(variant, d, 3, "f32", n, seed=n)
 
