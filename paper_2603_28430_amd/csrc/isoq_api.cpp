@@ -116,18 +116,19 @@ isoq_status run_generic(const isoq_params *p, int dtype, int mode, KArgs &a, voi
 {
     const int slots = slots_per_set(p->variant, p->d);
     const bool f16 = dtype == ISOQ_F16;
-    const int v = packed_rows(p->d, p->bits, f16);
-    const void *fn = v > 0                    ? (p->variant == VAR_FULL   ? packed_kernel_full(p->bits, mode)
-                                                 : p->variant == VAR_FAST ? packed_kernel_fast(p->bits, mode)
-                                                                          : packed_kernel_2d(p->bits, mode))
+    const PackedShape ps = packed_shape(p->d, p->bits, f16);
+    const int v = ps.rows;
+    const void *fn = v > 0 ? (p->variant == VAR_FULL   ? packed_kernel_full(p->bits, mode, ps.chunks)
+                              : p->variant == VAR_FAST ? packed_kernel_fast(p->bits, mode, ps.chunks)
+                                                       : packed_kernel_2d(p->bits, mode, ps.chunks))
                      : p->variant == VAR_FULL ? generic_kernel_full(slots, p->bits, f16, mode)
                      : p->variant == VAR_FAST ? generic_kernel_fast(slots, p->bits, f16, mode)
                                               : generic_kernel_2d(slots, p->bits, f16, mode);
     if (!fn)
         return ISOQ_E_UNSUPPORTED;
-    // rows per block: packed, 4 waves of kTileGroups groups of v rows;
-    // generic, 4 waves of their row groups
-    const int64_t rpb = v > 0 ? (int64_t)v * (kBlockThreads / 64) * kTileGroups
+    // rows per block: packed, 4 waves of kTileGroups / chunks groups of v
+    // rows; generic, 4 waves of their row groups
+    const int64_t rpb = v > 0 ? (int64_t)v * (kBlockThreads / 64) * (kTileGroups / ps.chunks)
                               : (int64_t)generic_rows_per_wave(slots) * (kBlockThreads / 64);
     const int64_t blocks = (a.n + rpb - 1) / rpb;
     if (blocks > 0x7FFFFFFF)

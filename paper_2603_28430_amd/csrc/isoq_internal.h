@@ -156,24 +156,37 @@ inline int generic_rows_per_wave(int slots)
 }
 constexpr int kGenericMaxD = 1024;
 // Packed-row kernels (isoq_packed.h) for fp16 rows of width d = 16 k up to
-// 512 outside the tuned widths: V = floor(64 / (d/8)) rows per wave group,
-// one fewer for 3 bits when V d/8 is not a multiple of 4 (a quad of lanes
-// writes whole words); 0 where the family does not apply (the generic
-// kernels take those widths and every fp32 row).
+// 504 outside the tuned widths.  One 8-coordinate chunk per lane: L = d/8
+// lanes per row, V = floor(64 / L) rows per wave group, one fewer for 3 bits
+// when V L is not a multiple of 4 (a quad of lanes writes whole words).  Two
+// chunks per lane (one in each half of the row, L = d/16 lanes per row, L
+// even and, for 3 bits, a multiple of 4) where that keeps more lanes busy:
+// d = 192 and 320 (and 288 at 2 and 4 bits).  rows = 0 where the family does
+// not apply (the generic kernels take those widths and every fp32 row).
 constexpr int kPackedMaxLanes = 63;   // d/8 at d = 504
-inline int packed_rows(int d, int bits, bool f16)
+struct PackedShape {
+    int rows;     // rows per wave group
+    int chunks;   // 8-coordinate chunks per lane
+};
+inline PackedShape packed_shape(int d, int bits, bool f16)
 {
     if (!f16 || d % 16 != 0 || d > 8 * kPackedMaxLanes || d == 64 || d == 128 || d == 256)
-        return 0;
-    const int L = d / 8;
-    int v = 64 / L;
-    if (bits == 3 && (v * L) % 4 != 0)
-        v--;
-    return v;
+        return {0, 0};
+    const int l1 = d / 8;
+    int v1 = 64 / l1;
+    if (bits == 3 && (v1 * l1) % 4 != 0)
+        v1--;
+    const int l2 = d / 16;
+    if (d % 32 == 0 && (bits != 3 || l2 % 4 == 0)) {
+        const int v2 = 64 / l2;
+        if (v2 * l2 > v1 * l1)
+            return {v2, 2};
+    }
+    return {v1, 1};
 }
-const void *packed_kernel_full(int bits, int mode);
-const void *packed_kernel_fast(int bits, int mode);
-const void *packed_kernel_2d(int bits, int mode);
+const void *packed_kernel_full(int bits, int mode, int chunks);
+const void *packed_kernel_fast(int bits, int mode, int chunks);
+const void *packed_kernel_2d(int bits, int mode, int chunks);
 // Blocks of the stage-2 sketch kernel with a single rotation set (each walks
 // several tiles).
 constexpr int64_t kQjlBlocks = 1024;

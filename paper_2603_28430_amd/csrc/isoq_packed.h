@@ -17,6 +17,14 @@
 // merge their 24-bit pieces into three words, so V L is kept a multiple of 4
 // (the host lowers V by one when it is not); in a ragged last group the
 // quad that ends the data writes its last word as a half word.
+//
+// Where it keeps more lanes busy (d = 192: 60 lanes instead of 48; d = 320,
+// and 288 at 2 and 4 bits) a lane owns two chunks instead, sub and sub + L of
+// its row with L = d/16 lanes per row: each 16-byte access instruction then
+// covers the first or the second halves of the wave's rows, its index bits go
+// to the two halves of the row's record (row-relative addressing; with 3 bits
+// L is a multiple of 4, so quads stay inside a row), and a wave walks half as
+// many groups so that the same bytes are in flight.
 #pragma once
 
 #include "isoq_stage1.h"
@@ -92,37 +100,38 @@ __device__ __forceinline__ float packed_pair_total(const float *rp, int n)
     return tot;
 }
 
-template <int VAR, int BITS, bool F16, int MODE>
+template <int VAR, int BITS, int MODE, int C>
 __global__ __launch_bounds__(kBlockThreads) void packed_kernel(const KArgs a)
 {
     constexpr int H = 1 << (BITS - 1);
-    constexpr int PL = VAR == VAR_FULL ? 32 : 8;   // parameter floats per lane
-    constexpr int LANEB = F16 ? 16 : 32;           // row bytes per lane
+    constexpr int PL = VAR == VAR_FULL ? 32 : 8;   // parameter floats per chunk
+    constexpr int GPW = kTileGroups / C;           // groups per wave (4 C chunks in flight per lane)
     constexpr bool kUseLut = BITS == 4;
     constexpr bool kEncode = MODE == MODE_QUANTIZE;
     constexpr bool kLoadX = MODE != MODE_DEQUANTIZE;
     static_assert(MODE == MODE_ROUNDTRIP || MODE == MODE_QUANTIZE || MODE == MODE_DEQUANTIZE, "mode");
+    static_assert(C == 1 || C == 2, "one or two chunks per lane");
 
     __shared__ float lds_levels[16];
     __shared__ __align__(16) LutEntry lds_lut[kUseLut && kLoadX ? kLutMaxCells : 1];
     __shared__ float lds_pairs[kBlockThreads / 2];   // 32 pair sums per wave
-    // Full's 128 bytes per lane are staged through LDS when the block has one
+    // Full's 128 bytes per chunk are staged through LDS when the block has one
     // set (per-lane global loads of them move more through the vector memory
     // pipe than the rows do); Fast and 2-D read their 32 bytes directly,
     // which measured faster than a staging barrier
     constexpr bool kStage = VAR == VAR_FULL;
     __shared__ __align__(16) float lds_params[kStage ? kPackedMaxLanes * PL : 4];
 
-    const int L = a.g_d >> 3;   // lanes per row (even)
-    const int V = a.g_rows;     // rows per group
+    const int L = a.g_d >> (C + 2);   // lanes per row (even): d / (8 C)
+    const int V = a.g_rows;           // rows per group
     const int lane = threadIdx.x & 63;
     const int q = lane / L;
-    const int sub = lane - q * L;         // chunk of the lane within its row
-    const int lr = min(q, V - 1);         // row of the lane in the group (idle lanes: the last)
+    const int sub = lane - q * L;     // the lane's chunks of its row: sub, sub + L (C = 2)
+    const int lr = min(q, V - 1);     // row of the lane in the group (idle lanes: the last)
     const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int64_t rowb = (int64_t)a.g_d * (F16 ? 2 : 4);
-    const int64_t recb = (int64_t)L * BITS;   // d b / 8
-    const int64_t base = (int64_t)blockIdx.x * (kBlockThreads / 64) * kTileGroups;
+    const int64_t rowb = (int64_t)a.g_d * 2;       // fp16 rows
+    const int64_t recb = (int64_t)L * C * BITS;    // d b / 8
+    const int64_t base = (int64_t)blockIdx.x * (kBlockThreads / 64) * GPW;
 
     if constexpr (MODE == MODE_DEQUANTIZE) {
         if (threadIdx.x < 2 * H)
@@ -134,29 +143,34 @@ __global__ __launch_bounds__(kBlockThreads) void packed_kernel(const KArgs a)
         for (int i = threadIdx.x; i < a.lut_cells; i += kBlockThreads)
             d4[i] = s4[i];
     }
-    // rotation parameters of the lane's two slots: once, when the whole block
+    // rotation parameters of the lane's chunks: once, when the whole block
     // has one set; otherwise per group, when the lane's set changes
     const bool uni = a.g_block_set != 0;
     const int64_t bset = a.n_sets == 1 || !uni ? 0 : (base * V / a.rows_per_set) % a.n_sets;
     if (kStage && uni) {
         const u32x4 *s4 = reinterpret_cast<const u32x4 *>(a.params + bset * a.g_set_stride);
         u32x4 *d4 = reinterpret_cast<u32x4 *>(lds_params);
-        for (int i = threadIdx.x; i < L * (PL / 4); i += kBlockThreads)
+        for (int i = threadIdx.x; i < C * L * (PL / 4); i += kBlockThreads)
             d4[i] = s4[i];
     }
     if (MODE == MODE_DEQUANTIZE || (kUseLut && kLoadX) || (kStage && uni))
         __syncthreads();
-    float P[PL];
+    float P[C][PL];
     int64_t pset = -1;
     auto load_set = [&](int64_t set) {
-        load_params<PL>(a.params + set * a.g_set_stride + (int64_t)sub * PL, P);
+#pragma unroll
+        for (int k = 0; k < C; k++)
+            load_params<PL>(a.params + set * a.g_set_stride + (int64_t)(sub + k * L) * PL, P[k]);
         pset = set;
     };
     if (uni) {
-        if constexpr (kStage)
-            load_params<PL>(lds_params + sub * PL, P);
-        else
+        if constexpr (kStage) {
+#pragma unroll
+            for (int k = 0; k < C; k++)
+                load_params<PL>(lds_params + (sub + k * L) * PL, P[k]);
+        } else {
             load_set(bset);
+        }
     }
     float lev[H], thr[H > 1 ? H - 1 : 1];
 #pragma unroll
@@ -166,47 +180,65 @@ __global__ __launch_bounds__(kBlockThreads) void packed_kernel(const KArgs a)
     for (int k = 0; k < H - 1; k++)
         thr[k] = a.thr_pos[k];
 
-    // ---- the wave's kTileGroups groups (4u + w of the block's): every load
-    //      first, then compute and store group by group
-    Raw<F16> raw[kLoadX ? kTileGroups : 1];
-    uint32_t bin[kLoadX ? 1 : kTileGroups];
-    float rin[kLoadX ? 1 : kTileGroups];
+    // ---- the wave's GPW groups (4u + w of the block's): every load first,
+    //      then compute and store group by group.  One chunk per lane: a
+    //      group is one stretch of V L chunks (flat addressing, chunk = lane);
+    //      two: lane sub of row q owns chunks sub and sub + L of that row.
+    Raw<true> raw[kLoadX ? GPW : 1][C];
+    uint32_t bin[kLoadX ? 1 : GPW][C];
+    float rin[kLoadX ? 1 : GPW];
 #pragma unroll
-    for (int u = 0; u < kTileGroups; u++) {
+    for (int u = 0; u < GPW; u++) {
         // a group past the end re-reads group 0 (and is neither computed nor stored)
         const int64_t g0 = (base + 4 * u + w) * V;
         const int64_t grow = g0 < a.n ? g0 : 0;
-        const int nv = (int)min((int64_t)V, a.n - grow) * L;   // chunks of data in the group
-        const int c = lane < nv ? lane : 0;                    // lanes past them read chunk 0
+        const int rows = (int)min((int64_t)V, a.n - grow);   // rows of data in the group
+        const int nv = rows * L;                               // lanes holding data
+        const int rq = q < rows ? q : 0;                       // lanes past them read row 0
         if constexpr (kLoadX) {
-            load_row_chunk<F16>(static_cast<const char *>(a.x) + grow * rowb + (uint32_t)(c * LANEB), raw[u]);
+            const char *row = static_cast<const char *>(a.x) + (grow + rq) * rowb;
+#pragma unroll
+            for (int k = 0; k < C; k++)
+                load_row_chunk<true>(row + (uint32_t)((sub + k * L) * 16), raw[u][k]);
         } else {
-            bin[u] = packed_load_bits<BITS>(a.rec_in + grow * recb, lane, nv);
-            rin[u] = (a.norms_in + grow)[lane < nv ? lr : 0];
+            if constexpr (C == 1) {
+                bin[u][0] = packed_load_bits<BITS>(a.rec_in + grow * recb, lane, nv);
+            } else {
+                const uint8_t *rec = a.rec_in + (grow + rq) * recb;
+#pragma unroll
+                for (int k = 0; k < C; k++)
+                    bin[u][k] = load_bits<BITS>(rec + k * L * BITS, sub);
+            }
+            rin[u] = (a.norms_in + grow)[rq];
         }
     }
     __builtin_amdgcn_sched_barrier(0);
 
     float *pairs = lds_pairs + w * 32;
 #pragma unroll
-    for (int u = 0; u < kTileGroups; u++) {
+    for (int u = 0; u < GPW; u++) {
         const int64_t grow = (base + 4 * u + w) * V;
         if (grow >= a.n)
             break;
-        const int nv = (int)min((int64_t)V, a.n - grow) * L;
+        const int rows = (int)min((int64_t)V, a.n - grow);
+        const int nv = rows * L;
         const bool on = lane < nv;
         if (!uni) {
             const int64_t set = ((grow + (on ? lr : 0)) / a.rows_per_set) % a.n_sets;
             if (set != pset)
                 load_set(set);
         }
-        float yq[8], rho;
+        float yq[C][8], rho;
         if constexpr (kLoadX) {
-            float x[8];
-            unpack<F16>(raw[u], x);
-            // squared norm: pair sums by DPP, then the row's L/2 pair sums
-            // through LDS, added in order by every lane of the row
-            float ss = sum_squares<F16>(raw[u], x);
+            float x[C][8];
+            // squared norm: the lane's chunks, pair sums by DPP, then the
+            // row's L/2 pair sums through LDS, added in order by every lane
+            float ss = 0.f;
+#pragma unroll
+            for (int k = 0; k < C; k++) {
+                unpack<true>(raw[u][k], x[k]);
+                ss += sum_squares<true>(raw[u][k], x[k]);
+            }
             ss += dpp_f<DPP_QUAD_1032>(ss);
             pairs[lane >> 1] = ss;
             __builtin_amdgcn_wave_barrier();
@@ -214,32 +246,42 @@ __global__ __launch_bounds__(kBlockThreads) void packed_kernel(const KArgs a)
             __builtin_amdgcn_wave_barrier();
             rho = __builtin_amdgcn_sqrtf(tot);
             const float rho_e = fmaxf(rho, kEps);
-            float y[8], m[8];
-            rotate_forward<VAR>(P, x, y);
+            float ths[H > 1 ? H - 1 : 1], lvs[H];
 #pragma unroll
-            for (int j = 0; j < 8; j++)
-                m[j] = fabsf(y[j]);
-            uint32_t p = 0;
-            if constexpr (kUseLut) {
-                const float s = a.lut_inv_h * __builtin_amdgcn_rcpf(rho_e);
-                p = lut_quantize<BITS, !kEncode, kEncode>(y, m, s, (float)(a.lut_cells - 1), lds_lut, rho, yq);
-            } else {
-                float ths[H > 1 ? H - 1 : 1];
+            for (int k = 0; k < H - 1; k++)
+                ths[k] = thr[k] * rho_e;
 #pragma unroll
-                for (int k = 0; k < H - 1; k++)
-                    ths[k] = thr[k] * rho_e;
-                if constexpr (kEncode) {
-                    p = ballot_encode<BITS, false>(y, m, ths, lev, yq);
+            for (int k = 0; k < H; k++)
+                lvs[k] = lev[k] * rho;
+            uint32_t p[C];
+#pragma unroll
+            for (int k = 0; k < C; k++) {
+                float y[8], m[8];
+                rotate_forward<VAR>(P[k], x[k], y);
+#pragma unroll
+                for (int j = 0; j < 8; j++)
+                    m[j] = fabsf(y[j]);
+                if constexpr (kUseLut) {
+                    const float s = a.lut_inv_h * __builtin_amdgcn_rcpf(rho_e);
+                    p[k] = lut_quantize<BITS, !kEncode, kEncode>(y, m, s, (float)(a.lut_cells - 1), lds_lut, rho,
+                                                                 yq[k]);
+                } else if constexpr (kEncode) {
+                    p[k] = ballot_encode<BITS, false>(y, m, ths, lev, yq[k]);
                 } else {
-                    float lvs[H];
-#pragma unroll
-                    for (int k = 0; k < H; k++)
-                        lvs[k] = lev[k] * rho;
-                    chain_levels<H>(y, m, ths, lvs, yq);
+                    chain_levels<H>(y, m, ths, lvs, yq[k]);
                 }
             }
             if constexpr (kEncode) {
-                packed_store_bits<BITS>(a.rec_out + grow * recb, lane, p, nv);
+                if constexpr (C == 1) {
+                    packed_store_bits<BITS>(a.rec_out + grow * recb, lane, p[0], nv);
+                } else {
+                    // row-relative: with 3 bits L is a multiple of 4, so quads
+                    // stay inside a row and each half record starts on a word
+                    uint8_t *rec = a.rec_out + (grow + lr) * recb;
+#pragma unroll
+                    for (int k = 0; k < C; k++)
+                        store_bits<BITS>(rec + k * L * BITS, sub, p[k], on);
+                }
                 if (on && sub == 0)
                     (a.norms_out + grow)[lr] = rho;
                 continue;
@@ -247,25 +289,31 @@ __global__ __launch_bounds__(kBlockThreads) void packed_kernel(const KArgs a)
         } else {
             rho = rin[u];
 #pragma unroll
-            for (int j = 0; j < 8; j++)
-                yq[j] = lds_levels[(bin[u] >> (BITS * j)) & (2 * H - 1)] * rho;
+            for (int k = 0; k < C; k++)
+#pragma unroll
+                for (int j = 0; j < 8; j++)
+                    yq[k][j] = lds_levels[(bin[u][k] >> (BITS * j)) & (2 * H - 1)] * rho;
         }
         if constexpr (!kEncode) {
-            float o[8];
-            rotate_inverse<VAR>(P, yq, o);
-            if (on)
-                store_row_chunk<F16>(static_cast<char *>(a.y) + grow * rowb + (uint32_t)(lane * LANEB), o);
+            char *row = static_cast<char *>(a.y) + (grow + lr) * rowb;
+#pragma unroll
+            for (int k = 0; k < C; k++) {
+                float o[8];
+                rotate_inverse<VAR>(P[k], yq[k], o);
+                if (on)
+                    store_row_chunk<true>(row + (uint32_t)((sub + k * L) * 16), o);
+            }
         }
     }
 }
 
-template <int VAR, int BITS>
+template <int VAR, int BITS, int C>
 const void *packed_pick_mode(int mode)
 {
     switch (mode) {
-    case MODE_ROUNDTRIP: return reinterpret_cast<const void *>(&packed_kernel<VAR, BITS, true, MODE_ROUNDTRIP>);
-    case MODE_QUANTIZE: return reinterpret_cast<const void *>(&packed_kernel<VAR, BITS, true, MODE_QUANTIZE>);
-    case MODE_DEQUANTIZE: return reinterpret_cast<const void *>(&packed_kernel<VAR, BITS, true, MODE_DEQUANTIZE>);
+    case MODE_ROUNDTRIP: return reinterpret_cast<const void *>(&packed_kernel<VAR, BITS, MODE_ROUNDTRIP, C>);
+    case MODE_QUANTIZE: return reinterpret_cast<const void *>(&packed_kernel<VAR, BITS, MODE_QUANTIZE, C>);
+    case MODE_DEQUANTIZE: return reinterpret_cast<const void *>(&packed_kernel<VAR, BITS, MODE_DEQUANTIZE, C>);
     }
     return nullptr;
 }
@@ -275,12 +323,15 @@ const void *packed_pick_mode(int mode)
 // (measured at d = 96: 0.71 of the HBM roofline for the round trip, against
 // 0.60-0.64 with a lane's 32 contiguous bytes)
 template <int VAR>
-const void *packed_pick(int bits, int mode)
+const void *packed_pick(int bits, int mode, int chunks)
 {
-    switch (bits) {
-    case 2: return packed_pick_mode<VAR, 2>(mode);
-    case 3: return packed_pick_mode<VAR, 3>(mode);
-    case 4: return packed_pick_mode<VAR, 4>(mode);
+    switch (bits * 4 + chunks) {
+    case 2 * 4 + 1: return packed_pick_mode<VAR, 2, 1>(mode);
+    case 2 * 4 + 2: return packed_pick_mode<VAR, 2, 2>(mode);
+    case 3 * 4 + 1: return packed_pick_mode<VAR, 3, 1>(mode);
+    case 3 * 4 + 2: return packed_pick_mode<VAR, 3, 2>(mode);
+    case 4 * 4 + 1: return packed_pick_mode<VAR, 4, 1>(mode);
+    case 4 * 4 + 2: return packed_pick_mode<VAR, 4, 2>(mode);
     }
     return nullptr;
 }

@@ -1,11 +1,11 @@
-// Stage-1 packed-row kernels for fp16 rows of width d = 16 k up to 512
+// Stage-1 packed-row kernels for fp16 rows of width d = 16 k up to 504
 // outside the tuned four (the template is in isoq_packed.h).
 #include "isoq_packed.h"
 
 namespace isoq {
 
-const void *packed_kernel_full(int bits, int mode) { return packed_pick<VAR_FULL>(bits, mode); }
-const void *packed_kernel_fast(int bits, int mode) { return packed_pick<VAR_FAST>(bits, mode); }
-const void *packed_kernel_2d(int bits, int mode) { return packed_pick<VAR_PLANAR2D>(bits, mode); }
+const void *packed_kernel_full(int bits, int mode, int chunks) { return packed_pick<VAR_FULL>(bits, mode, chunks); }
+const void *packed_kernel_fast(int bits, int mode, int chunks) { return packed_pick<VAR_FAST>(bits, mode, chunks); }
+const void *packed_kernel_2d(int bits, int mode, int chunks) { return packed_pick<VAR_PLANAR2D>(bits, mode, chunks); }
 
 }  // namespace isoq

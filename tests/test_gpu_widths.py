@@ -28,10 +28,11 @@ DT = {"f16": (torch.float16, np.float16), "f32": (torch.float32, np.float32)}
 # widths below, between and above the tuned ones; odd, 2 mod 4 and
 # multiple-of-4 widths; every row shape of the generic kernels (8 to 64 lanes,
 # 1 to 4 slots per lane) and its largest width; packed rows of 2 to 62 lanes
-# (d = 16 .. 496: V d/8 a multiple of 4 or not, one row per wave), and widths
-# where 3 bits falls back to the generic kernels (272, 496)
+# (d = 16 .. 496: V d/8 a multiple of 4 or not, one row per wave), two
+# chunks per lane (192, 288 at 2 and 4 bits, 320), and widths where 3 bits
+# falls back to the generic kernels (272, 496)
 WIDTHS = [1, 2, 3, 5, 6, 7, 16, 20, 32, 33, 48, 60, 63, 80, 90, 96, 100, 112, 127, 130, 144, 160, 192, 208, 250,
-          256 + 4, 272, 320, 384, 496, 511, 640, 1000, 1024]
+          256 + 4, 272, 288, 320, 384, 496, 511, 640, 1000, 1024]
 
 
 def check(variant, d, bits, dtype, n, n_sets=1, rows_per_set=1, x=None, sample=None, seed=0):
@@ -72,7 +73,8 @@ def test_widths_parity(variant, d):
 
 
 @pytest.mark.parametrize("rows_per_set", [1, 5, 64, 1000])
-@pytest.mark.parametrize("variant,d", [("full", 90), ("fast", 96), ("2d", 75), ("full", 80), ("2d", 160)])
+@pytest.mark.parametrize("variant,d", [("full", 90), ("fast", 96), ("2d", 75), ("full", 80), ("2d", 160),
+                                       ("full", 192)])
 def test_widths_multiple_sets(variant, d, rows_per_set):
     print(f"case {variant} d={d} sets=3 rps={rows_per_set}", flush=True)
     check(variant, d, 3, "f16", 2003, n_sets=3, rows_per_set=rows_per_set)
@@ -81,7 +83,7 @@ def test_widths_multiple_sets(variant, d, rows_per_set):
 @pytest.mark.parametrize("n", [1, 2, 3, 5, 33])
 def test_widths_tiny_batches(n):
     for variant in ("full", "fast", "2d"):
-        for d in (3, 60, 80, 90, 96, 1000):
+        for d in (3, 60, 80, 90, 96, 192, 1000):
             print(f"case {variant} d={d} n={n}", flush=True)
             check(variant, d, 3, "f32", n, seed=n)
 
@@ -105,7 +107,7 @@ def test_widths_zero_and_scaled_rows():
 
 
 @pytest.mark.parametrize("variant,d,dtype", [("full", 96, "f16"), ("fast", 80, "f16"), ("2d", 90, "f32"),
-                                             ("full", 1000, "f32")])
+                                             ("full", 1000, "f32"), ("fast", 192, "f16")])
 def test_widths_large_sampled(variant, d, dtype):
     """Many row groups per block and a grid of thousands of blocks: sampled
     rows against the oracle, every row for the fused identity."""
@@ -142,7 +144,7 @@ def test_widths_unsupported_calls():
 
 
 @pytest.mark.parametrize("variant,d,dtype", [("full", 90, "f16"), ("fast", 96, "f32"), ("2d", 1000, "f16"),
-                                             ("fast", 7, "f32")])
+                                             ("fast", 7, "f32"), ("fast", 80, "f16"), ("2d", 320, "f16")])
 def test_widths_guard_bands_determinism_stream_in_place(variant, d, dtype):
     """Canary bytes around every output survive; a second call writes the
     same bytes; a non-default stream gives the same result; the round trip
