@@ -131,7 +131,8 @@ __global__ __launch_bounds__(kBlockThreads) void packed_kernel(const KArgs a)
     const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int64_t rowb = (int64_t)a.g_d * 2;       // fp16 rows
     const int64_t recb = (int64_t)L * C * BITS;    // d b / 8
-    const int64_t base = (int64_t)blockIdx.x * (kBlockThreads / 64) * GPW;
+    constexpr int TPB = packed_tiles_per_block(VAR, C);   // row tiles per block
+    const int64_t base0 = (int64_t)blockIdx.x * TPB * (kBlockThreads / 64) * GPW;
 
     if constexpr (MODE == MODE_DEQUANTIZE) {
         if (threadIdx.x < 2 * H)
@@ -146,7 +147,7 @@ __global__ __launch_bounds__(kBlockThreads) void packed_kernel(const KArgs a)
     // rotation parameters of the lane's chunks: once, when the whole block
     // has one set; otherwise per group, when the lane's set changes
     const bool uni = a.g_block_set != 0;
-    const int64_t bset = a.n_sets == 1 || !uni ? 0 : (base * V / a.rows_per_set) % a.n_sets;
+    const int64_t bset = a.n_sets == 1 || !uni ? 0 : (base0 * V / a.rows_per_set) % a.n_sets;
     if (kStage && uni) {
         const u32x4 *s4 = reinterpret_cast<const u32x4 *>(a.params + bset * a.g_set_stride);
         u32x4 *d4 = reinterpret_cast<u32x4 *>(lds_params);
@@ -180,128 +181,134 @@ __global__ __launch_bounds__(kBlockThreads) void packed_kernel(const KArgs a)
     for (int k = 0; k < H - 1; k++)
         thr[k] = a.thr_pos[k];
 
-    // ---- the wave's GPW groups (4u + w of the block's): every load first,
-    //      then compute and store group by group.  One chunk per lane: a
-    //      group is one stretch of V L chunks (flat addressing, chunk = lane);
-    //      two: lane sub of row q owns chunks sub and sub + L of that row.
-    Raw<true> raw[kLoadX ? GPW : 1][C];
-    uint32_t bin[kLoadX ? 1 : GPW][C];
-    float rin[kLoadX ? 1 : GPW];
+    // ---- per tile, the wave's GPW groups (4u + w of the tile's): every load
+    //      first, then compute and store group by group.  One chunk per
+    //      lane: a group is one stretch of V L chunks (flat addressing, chunk
+    //      = lane); two: lane sub of row q owns chunks sub and sub + L of that
+    //      row.  The tile test is block-uniform (no barrier follows).
+    for (int tt = 0; tt < TPB; tt++) {
+        const int64_t base = base0 + (int64_t)tt * (kBlockThreads / 64) * GPW;
+        if (base * V >= a.n)
+            return;
+        Raw<true> raw[kLoadX ? GPW : 1][C];
+        uint32_t bin[kLoadX ? 1 : GPW][C];
+        float rin[kLoadX ? 1 : GPW];
 #pragma unroll
-    for (int u = 0; u < GPW; u++) {
-        // a group past the end re-reads group 0 (and is neither computed nor stored)
-        const int64_t g0 = (base + 4 * u + w) * V;
-        const int64_t grow = g0 < a.n ? g0 : 0;
-        const int rows = (int)min((int64_t)V, a.n - grow);   // rows of data in the group
-        const int nv = rows * L;                               // lanes holding data
-        const int rq = q < rows ? q : 0;                       // lanes past them read row 0
-        if constexpr (kLoadX) {
-            const char *row = static_cast<const char *>(a.x) + (grow + rq) * rowb;
-#pragma unroll
-            for (int k = 0; k < C; k++)
-                load_row_chunk<true>(row + (uint32_t)((sub + k * L) * 16), raw[u][k]);
-        } else {
-            if constexpr (C == 1) {
-                bin[u][0] = packed_load_bits<BITS>(a.rec_in + grow * recb, lane, nv);
-            } else {
-                const uint8_t *rec = a.rec_in + (grow + rq) * recb;
+        for (int u = 0; u < GPW; u++) {
+            // a group past the end re-reads group 0 (and is neither computed nor stored)
+            const int64_t g0 = (base + 4 * u + w) * V;
+            const int64_t grow = g0 < a.n ? g0 : 0;
+            const int rows = (int)min((int64_t)V, a.n - grow);   // rows of data in the group
+            const int nv = rows * L;                               // lanes holding data
+            const int rq = q < rows ? q : 0;                       // lanes past them read row 0
+            if constexpr (kLoadX) {
+                const char *row = static_cast<const char *>(a.x) + (grow + rq) * rowb;
 #pragma unroll
                 for (int k = 0; k < C; k++)
-                    bin[u][k] = load_bits<BITS>(rec + k * L * BITS, sub);
-            }
-            rin[u] = (a.norms_in + grow)[rq];
-        }
-    }
-    __builtin_amdgcn_sched_barrier(0);
-
-    float *pairs = lds_pairs + w * 32;
-#pragma unroll
-    for (int u = 0; u < GPW; u++) {
-        const int64_t grow = (base + 4 * u + w) * V;
-        if (grow >= a.n)
-            break;
-        const int rows = (int)min((int64_t)V, a.n - grow);
-        const int nv = rows * L;
-        const bool on = lane < nv;
-        if (!uni) {
-            const int64_t set = ((grow + (on ? lr : 0)) / a.rows_per_set) % a.n_sets;
-            if (set != pset)
-                load_set(set);
-        }
-        float yq[C][8], rho;
-        if constexpr (kLoadX) {
-            float x[C][8];
-            // squared norm: the lane's chunks, pair sums by DPP, then the
-            // row's L/2 pair sums through LDS, added in order by every lane
-            float ss = 0.f;
-#pragma unroll
-            for (int k = 0; k < C; k++) {
-                unpack<true>(raw[u][k], x[k]);
-                ss += sum_squares<true>(raw[u][k], x[k]);
-            }
-            ss += dpp_f<DPP_QUAD_1032>(ss);
-            pairs[lane >> 1] = ss;
-            __builtin_amdgcn_wave_barrier();
-            const float tot = packed_pair_total(pairs + lr * (L >> 1), L >> 1);
-            __builtin_amdgcn_wave_barrier();
-            rho = __builtin_amdgcn_sqrtf(tot);
-            const float rho_e = fmaxf(rho, kEps);
-            float ths[H > 1 ? H - 1 : 1], lvs[H];
-#pragma unroll
-            for (int k = 0; k < H - 1; k++)
-                ths[k] = thr[k] * rho_e;
-#pragma unroll
-            for (int k = 0; k < H; k++)
-                lvs[k] = lev[k] * rho;
-            uint32_t p[C];
-#pragma unroll
-            for (int k = 0; k < C; k++) {
-                float y[8], m[8];
-                rotate_forward<VAR>(P[k], x[k], y);
-#pragma unroll
-                for (int j = 0; j < 8; j++)
-                    m[j] = fabsf(y[j]);
-                if constexpr (kUseLut) {
-                    const float s = a.lut_inv_h * __builtin_amdgcn_rcpf(rho_e);
-                    p[k] = lut_quantize<BITS, !kEncode, kEncode>(y, m, s, (float)(a.lut_cells - 1), lds_lut, rho,
-                                                                 yq[k]);
-                } else if constexpr (kEncode) {
-                    p[k] = ballot_encode<BITS, false>(y, m, ths, lev, yq[k]);
-                } else {
-                    chain_levels<H>(y, m, ths, lvs, yq[k]);
-                }
-            }
-            if constexpr (kEncode) {
+                    load_row_chunk<true>(row + (uint32_t)((sub + k * L) * 16), raw[u][k]);
+            } else {
                 if constexpr (C == 1) {
-                    packed_store_bits<BITS>(a.rec_out + grow * recb, lane, p[0], nv);
+                    bin[u][0] = packed_load_bits<BITS>(a.rec_in + grow * recb, lane, nv);
                 } else {
-                    // row-relative: with 3 bits L is a multiple of 4, so quads
-                    // stay inside a row and each half record starts on a word
-                    uint8_t *rec = a.rec_out + (grow + lr) * recb;
+                    const uint8_t *rec = a.rec_in + (grow + rq) * recb;
 #pragma unroll
                     for (int k = 0; k < C; k++)
-                        store_bits<BITS>(rec + k * L * BITS, sub, p[k], on);
+                        bin[u][k] = load_bits<BITS>(rec + k * L * BITS, sub);
                 }
-                if (on && sub == 0)
-                    (a.norms_out + grow)[lr] = rho;
-                continue;
+                rin[u] = (a.norms_in + grow)[rq];
             }
-        } else {
-            rho = rin[u];
-#pragma unroll
-            for (int k = 0; k < C; k++)
-#pragma unroll
-                for (int j = 0; j < 8; j++)
-                    yq[k][j] = lds_levels[(bin[u][k] >> (BITS * j)) & (2 * H - 1)] * rho;
         }
-        if constexpr (!kEncode) {
-            char *row = static_cast<char *>(a.y) + (grow + lr) * rowb;
+        __builtin_amdgcn_sched_barrier(0);
+
+        float *pairs = lds_pairs + w * 32;
 #pragma unroll
-            for (int k = 0; k < C; k++) {
-                float o[8];
-                rotate_inverse<VAR>(P[k], yq[k], o);
-                if (on)
-                    store_row_chunk<true>(row + (uint32_t)((sub + k * L) * 16), o);
+        for (int u = 0; u < GPW; u++) {
+            const int64_t grow = (base + 4 * u + w) * V;
+            if (grow >= a.n)
+                break;
+            const int rows = (int)min((int64_t)V, a.n - grow);
+            const int nv = rows * L;
+            const bool on = lane < nv;
+            if (!uni) {
+                const int64_t set = ((grow + (on ? lr : 0)) / a.rows_per_set) % a.n_sets;
+                if (set != pset)
+                    load_set(set);
+            }
+            float yq[C][8], rho;
+            if constexpr (kLoadX) {
+                float x[C][8];
+                // squared norm: the lane's chunks, pair sums by DPP, then the
+                // row's L/2 pair sums through LDS, added in order by every lane
+                float ss = 0.f;
+#pragma unroll
+                for (int k = 0; k < C; k++) {
+                    unpack<true>(raw[u][k], x[k]);
+                    ss += sum_squares<true>(raw[u][k], x[k]);
+                }
+                ss += dpp_f<DPP_QUAD_1032>(ss);
+                pairs[lane >> 1] = ss;
+                __builtin_amdgcn_wave_barrier();
+                const float tot = packed_pair_total(pairs + lr * (L >> 1), L >> 1);
+                __builtin_amdgcn_wave_barrier();
+                rho = __builtin_amdgcn_sqrtf(tot);
+                const float rho_e = fmaxf(rho, kEps);
+                float ths[H > 1 ? H - 1 : 1], lvs[H];
+#pragma unroll
+                for (int k = 0; k < H - 1; k++)
+                    ths[k] = thr[k] * rho_e;
+#pragma unroll
+                for (int k = 0; k < H; k++)
+                    lvs[k] = lev[k] * rho;
+                uint32_t p[C];
+#pragma unroll
+                for (int k = 0; k < C; k++) {
+                    float y[8], m[8];
+                    rotate_forward<VAR>(P[k], x[k], y);
+#pragma unroll
+                    for (int j = 0; j < 8; j++)
+                        m[j] = fabsf(y[j]);
+                    if constexpr (kUseLut) {
+                        const float s = a.lut_inv_h * __builtin_amdgcn_rcpf(rho_e);
+                        p[k] = lut_quantize<BITS, !kEncode, kEncode>(y, m, s, (float)(a.lut_cells - 1), lds_lut, rho,
+                                                                     yq[k]);
+                    } else if constexpr (kEncode) {
+                        p[k] = ballot_encode<BITS, false>(y, m, ths, lev, yq[k]);
+                    } else {
+                        chain_levels<H>(y, m, ths, lvs, yq[k]);
+                    }
+                }
+                if constexpr (kEncode) {
+                    if constexpr (C == 1) {
+                        packed_store_bits<BITS>(a.rec_out + grow * recb, lane, p[0], nv);
+                    } else {
+                        // row-relative: with 3 bits L is a multiple of 4, so quads
+                        // stay inside a row and each half record starts on a word
+                        uint8_t *rec = a.rec_out + (grow + lr) * recb;
+#pragma unroll
+                        for (int k = 0; k < C; k++)
+                            store_bits<BITS>(rec + k * L * BITS, sub, p[k], on);
+                    }
+                    if (on && sub == 0)
+                        (a.norms_out + grow)[lr] = rho;
+                    continue;
+                }
+            } else {
+                rho = rin[u];
+#pragma unroll
+                for (int k = 0; k < C; k++)
+#pragma unroll
+                    for (int j = 0; j < 8; j++)
+                        yq[k][j] = lds_levels[(bin[u][k] >> (BITS * j)) & (2 * H - 1)] * rho;
+            }
+            if constexpr (!kEncode) {
+                char *row = static_cast<char *>(a.y) + (grow + lr) * rowb;
+#pragma unroll
+                for (int k = 0; k < C; k++) {
+                    float o[8];
+                    rotate_inverse<VAR>(P[k], yq[k], o);
+                    if (on)
+                        store_row_chunk<true>(row + (uint32_t)((sub + k * L) * 16), o);
+                }
             }
         }
     }

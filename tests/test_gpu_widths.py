@@ -72,7 +72,9 @@ def test_widths_parity(variant, d):
             check(variant, d, bits, dtype, n, seed=d + bits)
 
 
-@pytest.mark.parametrize("rows_per_set", [1, 5, 64, 1000])
+# 480 is a multiple of the packed kernels' block heights at d = 80, 96, 160
+# and 192 (96, 80, 48 and 40 rows), so each block there has one set
+@pytest.mark.parametrize("rows_per_set", [1, 5, 64, 480, 1000])
 @pytest.mark.parametrize("variant,d", [("full", 90), ("fast", 96), ("2d", 75), ("full", 80), ("2d", 160),
                                        ("full", 192)])
 def test_widths_multiple_sets(variant, d, rows_per_set):
