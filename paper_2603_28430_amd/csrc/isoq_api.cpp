@@ -117,13 +117,14 @@ isoq_status run_generic(const isoq_params *p, int dtype, int mode, KArgs &a, voi
     const int slots = slots_per_set(p->variant, p->d);
     const bool f16 = dtype == ISOQ_F16;
     const PackedShape ps = packed_shape(p->d, p->bits, f16);
+    const bool pairs = f16 && p->d % 4 == 2;
     const int v = ps.rows;
     const void *fn = v > 0 ? (p->variant == VAR_FULL   ? packed_kernel_full(p->bits, mode, ps.chunks)
                               : p->variant == VAR_FAST ? packed_kernel_fast(p->bits, mode, ps.chunks)
                                                        : packed_kernel_2d(p->bits, mode, ps.chunks))
-                     : p->variant == VAR_FULL ? generic_kernel_full(slots, p->bits, f16, mode)
-                     : p->variant == VAR_FAST ? generic_kernel_fast(slots, p->bits, f16, mode)
-                                              : generic_kernel_2d(slots, p->bits, f16, mode);
+                     : p->variant == VAR_FULL ? generic_kernel_full(slots, p->bits, f16, mode, pairs)
+                     : p->variant == VAR_FAST ? generic_kernel_fast(slots, p->bits, f16, mode, pairs)
+                                              : generic_kernel_2d(slots, p->bits, f16, mode, pairs);
     if (!fn)
         return ISOQ_E_UNSUPPORTED;
     // rows per block: packed, tiles of 4 waves of kTileGroups / chunks groups

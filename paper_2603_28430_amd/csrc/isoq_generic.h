@@ -11,7 +11,9 @@
 // generic_groups(BPL) groups, issuing every group's loads before computing.  The
 // record of a row is written and read bytewise: slot j's 4b index bits start
 // at bit 4b j.  Rows of a width that is a multiple of 4 move in one 8-byte
-// (fp16) or 16-byte (fp32) access per slot, other widths element by element.
+// (fp16) or 16-byte (fp32) access per slot; fp16 rows of other even widths in
+// coordinate pairs (4-byte accesses: such a row starts on a 4-byte boundary,
+// PAIRS instantiations); the rest element by element.
 #pragma once
 
 #include <type_traits>
@@ -58,6 +60,24 @@ __device__ __forceinline__ GenRaw<F16> gen_load(const char *row, int j, int d, b
         if (i + 3 < d) v.w = e[i + 3];
     }
     return v;
+}
+
+// fp16 rows of even width d, 2 mod 4: slot j's first pair is inside the row,
+// its second unless j is the last slot.
+__device__ __forceinline__ f16x4 gen_load_pairs(const char *row, int j, int d)
+{
+    const f16x2 *q = reinterpret_cast<const f16x2 *>(row) + 2 * j;
+    const f16x2 lo = q[0];
+    const f16x2 hi = 4 * j + 2 < d ? q[1] : f16x2{(_Float16)0.f, (_Float16)0.f};
+    return f16x4{lo[0], lo[1], hi[0], hi[1]};
+}
+
+__device__ __forceinline__ void gen_store_pairs(char *row, int j, int d, const float o[4])
+{
+    f16x2 *q = reinterpret_cast<f16x2 *>(row) + 2 * j;
+    q[0] = f16x2{(_Float16)o[0], (_Float16)o[1]};
+    if (4 * j + 2 < d)
+        q[1] = f16x2{(_Float16)o[2], (_Float16)o[3]};
 }
 
 template <bool F16>
@@ -137,9 +157,10 @@ __device__ __forceinline__ void gen_write_slot(uint8_t *rec, int j, int nb, uint
     }
 }
 
-template <int VAR, int BITS, bool F16, int MODE, int G, int BPL>
+template <int VAR, int BITS, bool F16, int MODE, int G, int BPL, bool PAIRS>
 __global__ __launch_bounds__(kBlockThreads) void generic_kernel(const KArgs a)
 {
+    static_assert(!PAIRS || F16, "pair accesses are for fp16 rows");
     constexpr int R = 64 / G;                // rows per wave and group
     constexpr int kGenGroups = generic_groups(BPL);
     constexpr int PS = kSlotParams<VAR>;
@@ -186,8 +207,10 @@ __global__ __launch_bounds__(kBlockThreads) void generic_kernel(const KArgs a)
             const int j = sub + G * k;
             const bool on = ok && j < slots;
             if constexpr (kLoadX) {
-                xr[t][k] = on ? gen_load<F16>(x0 + t * xstep, j, d, vec)
-                              : gen_zero<F16>();
+                if constexpr (PAIRS)
+                    xr[t][k] = on ? gen_load_pairs(x0 + t * xstep, j, d) : gen_zero<F16>();
+                else
+                    xr[t][k] = on ? gen_load<F16>(x0 + t * xstep, j, d, vec) : gen_zero<F16>();
             } else {
                 pin[t][k] = on ? gen_read_slot<BITS>(ri0 + t * rstep, j, nb) : 0u;
             }
@@ -298,7 +321,10 @@ __global__ __launch_bounds__(kBlockThreads) void generic_kernel(const KArgs a)
                 if (ok && j < slots) {
                     float o[4];
                     rotate4_inverse<VAR>(P[k], yq[k], o);
-                    gen_store<F16>(y0 + t * xstep, j, d, vec, o);
+                    if constexpr (PAIRS)
+                        gen_store_pairs(y0 + t * xstep, j, d, o);
+                    else
+                        gen_store<F16>(y0 + t * xstep, j, d, vec, o);
                 }
             }
         }
@@ -306,42 +332,51 @@ __global__ __launch_bounds__(kBlockThreads) void generic_kernel(const KArgs a)
 }
 
 // Row shape for a padded width of `slots` 4-coordinate slots: (G, BPL).
-template <int VAR, int BITS, bool F16, int MODE>
+template <int VAR, int BITS, bool F16, int MODE, bool PAIRS>
 const void *gen_pick_shape(int slots)
 {
     if (slots <= 8)
-        return reinterpret_cast<const void *>(&generic_kernel<VAR, BITS, F16, MODE, 8, 1>);
+        return reinterpret_cast<const void *>(&generic_kernel<VAR, BITS, F16, MODE, 8, 1, PAIRS>);
     if (slots <= 16)
-        return reinterpret_cast<const void *>(&generic_kernel<VAR, BITS, F16, MODE, 16, 1>);
+        return reinterpret_cast<const void *>(&generic_kernel<VAR, BITS, F16, MODE, 16, 1, PAIRS>);
     if (slots <= 32)
-        return reinterpret_cast<const void *>(&generic_kernel<VAR, BITS, F16, MODE, 32, 1>);
+        return reinterpret_cast<const void *>(&generic_kernel<VAR, BITS, F16, MODE, 32, 1, PAIRS>);
     if (slots <= 64)
-        return reinterpret_cast<const void *>(&generic_kernel<VAR, BITS, F16, MODE, 64, 1>);
+        return reinterpret_cast<const void *>(&generic_kernel<VAR, BITS, F16, MODE, 64, 1, PAIRS>);
     if (slots <= 128)
-        return reinterpret_cast<const void *>(&generic_kernel<VAR, BITS, F16, MODE, 64, 2>);
+        return reinterpret_cast<const void *>(&generic_kernel<VAR, BITS, F16, MODE, 64, 2, PAIRS>);
     if (slots <= 256)
-        return reinterpret_cast<const void *>(&generic_kernel<VAR, BITS, F16, MODE, 64, 4>);
+        return reinterpret_cast<const void *>(&generic_kernel<VAR, BITS, F16, MODE, 64, 4, PAIRS>);
     return nullptr;
 }
 
-template <int VAR, int BITS, bool F16>
+template <int VAR, int BITS, bool F16, bool PAIRS>
 const void *gen_pick_mode(int slots, int mode)
 {
     switch (mode) {
-    case MODE_ROUNDTRIP: return gen_pick_shape<VAR, BITS, F16, MODE_ROUNDTRIP>(slots);
-    case MODE_QUANTIZE: return gen_pick_shape<VAR, BITS, F16, MODE_QUANTIZE>(slots);
-    case MODE_DEQUANTIZE: return gen_pick_shape<VAR, BITS, F16, MODE_DEQUANTIZE>(slots);
+    case MODE_ROUNDTRIP: return gen_pick_shape<VAR, BITS, F16, MODE_ROUNDTRIP, PAIRS>(slots);
+    case MODE_QUANTIZE: return gen_pick_shape<VAR, BITS, F16, MODE_QUANTIZE, PAIRS>(slots);
+    case MODE_DEQUANTIZE: return gen_pick_shape<VAR, BITS, F16, MODE_DEQUANTIZE, PAIRS>(slots);
     }
     return nullptr;
 }
 
+// pairs: fp16 rows of even width 2 mod 4 (coordinate-pair accesses)
+template <int VAR, int BITS>
+const void *gen_pick_dtype(int slots, bool f16, int mode, bool pairs)
+{
+    if (!f16)
+        return gen_pick_mode<VAR, BITS, false, false>(slots, mode);
+    return pairs ? gen_pick_mode<VAR, BITS, true, true>(slots, mode) : gen_pick_mode<VAR, BITS, true, false>(slots, mode);
+}
+
 template <int VAR>
-const void *gen_pick(int slots, int bits, bool f16, int mode)
+const void *gen_pick(int slots, int bits, bool f16, int mode, bool pairs)
 {
     switch (bits) {
-    case 2: return f16 ? gen_pick_mode<VAR, 2, true>(slots, mode) : gen_pick_mode<VAR, 2, false>(slots, mode);
-    case 3: return f16 ? gen_pick_mode<VAR, 3, true>(slots, mode) : gen_pick_mode<VAR, 3, false>(slots, mode);
-    case 4: return f16 ? gen_pick_mode<VAR, 4, true>(slots, mode) : gen_pick_mode<VAR, 4, false>(slots, mode);
+    case 2: return gen_pick_dtype<VAR, 2>(slots, f16, mode, pairs);
+    case 3: return gen_pick_dtype<VAR, 3>(slots, f16, mode, pairs);
+    case 4: return gen_pick_dtype<VAR, 4>(slots, f16, mode, pairs);
     }
     return nullptr;
 }

@@ -4,9 +4,9 @@
 
 namespace isoq {
 
-const void *generic_kernel_2d(int slots, int bits, bool f16, int mode)
+const void *generic_kernel_2d(int slots, int bits, bool f16, int mode, bool pairs)
 {
-    return gen_pick<VAR_PLANAR2D>(slots, bits, f16, mode);
+    return gen_pick<VAR_PLANAR2D>(slots, bits, f16, mode, pairs);
 }
 
 }  // namespace isoq

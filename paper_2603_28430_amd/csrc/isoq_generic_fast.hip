@@ -4,9 +4,9 @@
 
 namespace isoq {
 
-const void *generic_kernel_fast(int slots, int bits, bool f16, int mode)
+const void *generic_kernel_fast(int slots, int bits, bool f16, int mode, bool pairs)
 {
-    return gen_pick<VAR_FAST>(slots, bits, f16, mode);
+    return gen_pick<VAR_FAST>(slots, bits, f16, mode, pairs);
 }
 
 }  // namespace isoq

@@ -141,9 +141,11 @@ const void *kernel_for(int variant, int d, int bits, bool f16, bool generic_sets
 // Stage-1 kernels for the other widths (d = 1 .. 1024) with `slots`
 // 4-coordinate slots per padded row, one per variant (isoq_generic_*.hip);
 // nullptr when no kernel fits.  Rows of one block: 4 waves x kGenRowsPerWave.
-const void *generic_kernel_full(int slots, int bits, bool f16, int mode);
-const void *generic_kernel_fast(int slots, int bits, bool f16, int mode);
-const void *generic_kernel_2d(int slots, int bits, bool f16, int mode);
+// pairs: fp16 rows whose width is even and not a multiple of 4 move in
+// coordinate pairs (separate instantiations)
+const void *generic_kernel_full(int slots, int bits, bool f16, int mode, bool pairs);
+const void *generic_kernel_fast(int slots, int bits, bool f16, int mode, bool pairs);
+const void *generic_kernel_2d(int slots, int bits, bool f16, int mode, bool pairs);
 // Row shape of the generic kernels for a row of `slots` slots: G lanes per
 // row, BPL slots per lane, and row groups per wave (every group's loads are
 // in flight together: 8 groups of one slot, 4 groups of several).

@@ -2,7 +2,8 @@
 the oracle, through the C ABI: the packed-row kernels (fp16 rows,
 d = 16 k up to 504; 3 bits at d = 272, 304, ... 496 excepted) and the
 generic kernels (every other width and dtype up to d = 1024; Sec. 5.1 zero
-padding when d is not a multiple of the block size).
+padding when d is not a multiple of the block size; fp16 rows of width 2 mod 4
+move in coordinate pairs).
 
 Per case: isoq_quantize, isoq_dequantize and isoq_roundtrip on the same rows;
 the fused path equals quantize followed by dequantize bit for bit; indices,
@@ -109,7 +110,7 @@ def test_widths_zero_and_scaled_rows():
 
 
 @pytest.mark.parametrize("variant,d,dtype", [("full", 96, "f16"), ("fast", 80, "f16"), ("2d", 90, "f32"),
-                                             ("full", 1000, "f32"), ("fast", 192, "f16")])
+                                             ("full", 1000, "f32"), ("fast", 192, "f16"), ("full", 90, "f16")])
 def test_widths_large_sampled(variant, d, dtype):
     """Many row groups per block and a grid of thousands of blocks: sampled
     rows against the oracle, every row for the fused identity."""
