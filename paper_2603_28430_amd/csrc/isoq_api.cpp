@@ -101,9 +101,9 @@ void fill_args(const isoq_params *p, KArgs &a)
     a.lut_cells = p->lut_cells;
 }
 
-isoq_status launch(const void *fn, dim3 grid, void **args, void *stream)
+isoq_status launch(const void *fn, dim3 grid, void **args, void *stream, int threads = kBlockThreads)
 {
-    hipError_t e = hipLaunchKernel(fn, grid, dim3(kBlockThreads), args, 0, static_cast<hipStream_t>(stream));
+    hipError_t e = hipLaunchKernel(fn, grid, dim3(threads), args, 0, static_cast<hipStream_t>(stream));
     if (e != hipSuccess)
         return hip_fail(e, "hipLaunchKernel");
     e = hipGetLastError();
@@ -775,7 +775,9 @@ isoq_status isoq_quantize_qjl(const isoq_params *p, const isoq_sketch *sk, int d
         return ISOQ_E_NULL;
     if (sk->variant != p->variant || sk->d != p->d || sk->n_sets != p->n_sets || sk->device != p->device)
         return ISOQ_E_INVALID;
-    const int64_t rpb = rows_per_block(p);
+    // rows of one tile (a block's waves, kTileGroups groups each)
+    const int waves = qjl_waves(sk->m, false, p->n_sets);
+    const int64_t rpb = rows_per_block(p) / 4 * waves;
     if (p->n_sets > 1 && rows_per_set % rpb != 0)
         return ISOQ_E_UNSUPPORTED;
     if (n == 0)
@@ -787,16 +789,16 @@ isoq_status isoq_quantize_qjl(const isoq_params *p, const isoq_sketch *sk, int d
         return ISOQ_E_ALIGN;
     if ((st = check_device(p)) != ISOQ_OK)
         return st;
-    const void *fn = qjl_kernel_for(p->variant, p->d, p->bits, dtype == ISOQ_F16, sk->m);
+    const void *fn = qjl_kernel_for(p->variant, p->d, p->bits, dtype == ISOQ_F16, sk->m, false, waves);
     if (!fn)
         return ISOQ_E_UNSUPPORTED;
     const int64_t tiles = (n + rpb - 1) / rpb;
     if (tiles > 0x7FFFFFFF)
         return ISOQ_E_UNSUPPORTED;
     // with one rotation set, blocks walk several tiles each (the projection is
-    // staged once per block); otherwise one block per tile keeps each block
-    // on its own set
-    const int64_t blocks = p->n_sets == 1 ? std::min<int64_t>(tiles, kQjlBlocks) : tiles;
+    // staged once per block; kQjlBlocks 4-wave blocks or half as many 8-wave
+    // ones); otherwise one block per tile keeps each block on its own set
+    const int64_t blocks = p->n_sets == 1 ? std::min<int64_t>(tiles, kQjlBlocks * 4 / waves) : tiles;
     KArgs a{};
     fill_args(p, a);
     a.x = x;
@@ -808,7 +810,7 @@ isoq_status isoq_quantize_qjl(const isoq_params *p, const isoq_sketch *sk, int d
     a.qjl_signs = signs;
     a.qjl_gamma = gamma;
     void *args[] = {&a};
-    return launch(fn, dim3((unsigned)blocks), args, stream);
+    return launch(fn, dim3((unsigned)blocks), args, stream, 64 * waves);
 }
 
 isoq_status isoq_kv_append_qjl(const isoq_params *pk, const isoq_sketch *sk, int dtype, const void *k_new,
@@ -838,13 +840,15 @@ isoq_status isoq_kv_append_qjl(const isoq_params *pk, const isoq_sketch *sk, int
     isoq_status st = check_device(pk);
     if (st != ISOQ_OK)
         return st;
-    const void *fn = qjl_kernel_for(pk->variant, pk->d, pk->bits, dtype == ISOQ_F16, sk->m, true);
+    const int waves = qjl_waves(sk->m, true, pk->n_sets);
+    const void *fn = qjl_kernel_for(pk->variant, pk->d, pk->bits, dtype == ISOQ_F16, sk->m, true, waves);
     if (!fn)
         return ISOQ_E_UNSUPPORTED;
     // block (x, y) = (head, token range); a block stages its head's projection
     // once and walks token ranges y, y + gridDim.y, ... of that head
-    const int64_t ranges = (n_tokens + rows_per_block(pk) - 1) / rows_per_block(pk);
-    const int64_t by = std::max<int64_t>(1, std::min<int64_t>(ranges, kQjlBlocks / n_heads));
+    const int64_t rpr = rows_per_block(pk) / 4 * waves;   // tokens per range
+    const int64_t ranges = (n_tokens + rpr - 1) / rpr;
+    const int64_t by = std::max<int64_t>(1, std::min<int64_t>(ranges, kQjlBlocks * 4 / waves / n_heads));
     if (by > 65535)
         return ISOQ_E_UNSUPPORTED;
     KArgs a{};
@@ -863,7 +867,7 @@ isoq_status isoq_kv_append_qjl(const isoq_params *pk, const isoq_sketch *sk, int
     a.qjl_signs = k_signs;
     a.qjl_gamma = k_gamma;
     void *args[] = {&a};
-    return launch(fn, dim3((unsigned)n_heads, (unsigned)by, 1), args, stream);
+    return launch(fn, dim3((unsigned)n_heads, (unsigned)by, 1), args, stream, 64 * waves);
 }
 
 }  // extern "C"

@@ -4,7 +4,10 @@
 // sign(S (x - x_hat)) as m bits and ||x - x_hat|| per row.  The projection is the path's one dense
 // contraction, P = E S'^T over a wave's tile of rows, on MFMA (fp16 inputs,
 // fp32 accumulation); S' = S T^{-1} per rotation set is staged in LDS once
-// per block.
+// per block.  Blocks have 4 or 8 waves (WAVES, chosen by qjl_waves): with
+// m = 128 the staged projection (32 KB at d = 128) and the waves' error tiles
+// let three 4-wave blocks (12 waves) or two 8-wave blocks (16 waves) share a
+// CU's LDS.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -16,53 +19,56 @@
 namespace isoq {
 namespace {
 
-template <int VAR, int D, int BITS, bool F16, int QM, int MODE>
-__global__ __launch_bounds__(kBlockThreads) void qjl_kernel(const KArgs a)
+template <int VAR, int D, int BITS, bool F16, int QM, int MODE, int WAVES>
+__global__ __launch_bounds__(WAVES * 64) void qjl_kernel(const KArgs a)
 {
-    using S = Stage1<VAR, D, BITS, F16, MODE, false, QM>;
+    using S = Stage1<VAR, D, BITS, F16, MODE, false, QM, WAVES>;
     __shared__ float lds_levels[16];
     __shared__ __align__(16) float lds_params[S::LPV * S::PL];
     __shared__ __align__(16) LutEntry lds_lut[S::kUseLut ? kLutMaxCells : 1];
     __shared__ __align__(16) _Float16 lds_frag[QM * D];
-    __shared__ __align__(16) _Float16 lds_e[(kBlockThreads / 64) * S::kTileRows * S::kEStride];
+    __shared__ __align__(16) _Float16 lds_e[WAVES * S::kTileRows * S::kEStride];
     S::run(a, lds_levels, lds_params, lds_lut, lds_frag, lds_e);
 }
 
+// Instantiated pairs (m, waves): m = 64 with 4 waves; m = 128 (d <= 128)
+// with 8 waves, and with 4 waves for quantize into rows (several sets).
 template <int VAR, int D, int BITS, bool F16, int MODE>
-const void *qjl_pick_m(int m)
+const void *qjl_pick_m(int m, int waves)
 {
+    if (m == 64 && waves == 4)
+        return reinterpret_cast<const void *>(&qjl_kernel<VAR, D, BITS, F16, 64, MODE, 4>);
     if constexpr (D <= 128) {
-        if (m == 64)
-            return reinterpret_cast<const void *>(&qjl_kernel<VAR, D, BITS, F16, 64, MODE>);
-        if (m == 128)
-            return reinterpret_cast<const void *>(&qjl_kernel<VAR, D, BITS, F16, 128, MODE>);
-    } else {
-        if (m == 64)
-            return reinterpret_cast<const void *>(&qjl_kernel<VAR, D, BITS, F16, 64, MODE>);
+        if (m == 128 && waves == 8)
+            return reinterpret_cast<const void *>(&qjl_kernel<VAR, D, BITS, F16, 128, MODE, 8>);
+        if constexpr (MODE == MODE_QJL) {
+            if (m == 128 && waves == 4)
+                return reinterpret_cast<const void *>(&qjl_kernel<VAR, D, BITS, F16, 128, MODE, 4>);
+        }
     }
     return nullptr;
 }
 
 template <int VAR, int D, int MODE>
-const void *qjl_pick_bits(int bits, bool f16, int m)
+const void *qjl_pick_bits(int bits, bool f16, int m, int waves)
 {
     switch (bits) {
-    case 2: return f16 ? qjl_pick_m<VAR, D, 2, true, MODE>(m) : qjl_pick_m<VAR, D, 2, false, MODE>(m);
-    case 3: return f16 ? qjl_pick_m<VAR, D, 3, true, MODE>(m) : qjl_pick_m<VAR, D, 3, false, MODE>(m);
-    case 4: return f16 ? qjl_pick_m<VAR, D, 4, true, MODE>(m) : qjl_pick_m<VAR, D, 4, false, MODE>(m);
+    case 2: return f16 ? qjl_pick_m<VAR, D, 2, true, MODE>(m, waves) : qjl_pick_m<VAR, D, 2, false, MODE>(m, waves);
+    case 3: return f16 ? qjl_pick_m<VAR, D, 3, true, MODE>(m, waves) : qjl_pick_m<VAR, D, 3, false, MODE>(m, waves);
+    case 4: return f16 ? qjl_pick_m<VAR, D, 4, true, MODE>(m, waves) : qjl_pick_m<VAR, D, 4, false, MODE>(m, waves);
     }
     return nullptr;
 }
 
 template <int MODE>
-const void *qjl_pick(int variant, int d, int bits, bool f16, int m)
+const void *qjl_pick(int variant, int d, int bits, bool f16, int m, int waves)
 {
     auto by_d = [&](auto var) -> const void * {
         constexpr int V = decltype(var)::value;
         switch (d) {
-        case 64: return qjl_pick_bits<V, 64, MODE>(bits, f16, m);
-        case 128: return qjl_pick_bits<V, 128, MODE>(bits, f16, m);
-        case 256: return qjl_pick_bits<V, 256, MODE>(bits, f16, m);
+        case 64: return qjl_pick_bits<V, 64, MODE>(bits, f16, m, waves);
+        case 128: return qjl_pick_bits<V, 128, MODE>(bits, f16, m, waves);
+        case 256: return qjl_pick_bits<V, 256, MODE>(bits, f16, m, waves);
         }
         return nullptr;
     };

@@ -4,9 +4,9 @@
 
 namespace isoq {
 
-const void *qjl_append_kernel_for(int variant, int d, int bits, bool f16, int m)
+const void *qjl_append_kernel_for(int variant, int d, int bits, bool f16, int m, int waves)
 {
-    return qjl_pick<MODE_APPEND_QJL>(variant, d, bits, f16, m);
+    return qjl_pick<MODE_APPEND_QJL>(variant, d, bits, f16, m, waves);
 }
 
 }  // namespace isoq

@@ -306,9 +306,10 @@ __device__ __forceinline__ uint32_t ballot_encode(const float y[8], const float 
 }
 
 // ---- the kernel ---------------------------------------------------------------
-// Work split.  A row group is the 512/d rows one wave holds.  Block b (four
-// waves) owns the kTileGroups * 4 consecutive groups starting at
-// b * kTileGroups * 4; wave w takes groups base + 4u + w, u < kTileGroups, so
+// Work split.  A row group is the 512/d rows one wave holds.  Block b (WAVES
+// waves, four except for some sketch kernels) owns the kTileGroups * WAVES
+// consecutive groups starting at b * kTileGroups * WAVES; wave w takes groups
+// base + WAVES u + w, u < kTileGroups, so
 // that each load or store instruction of the block touches one contiguous
 // span.  Blocks are not persistent: the dispatcher streams them through the
 // chip in address order, which keeps HBM pages and channels evenly busy.
@@ -319,9 +320,10 @@ __device__ __forceinline__ uint32_t ballot_encode(const float y[8], const float 
 // global memory.  Parameters are staged before the tile's loads are issued:
 // measured on MI355X, this order beats issuing the data loads first.
 // QM: sketch size m of the stage-2 residual sketch (MODE_QJL and
-// MODE_APPEND_QJL only).
-template <int VAR, int D, int BITS, bool F16, int MODE, bool GENERIC_SETS, int QM = 0>
+// MODE_APPEND_QJL only).  WAVES: waves per block (BT = 64 WAVES threads).
+template <int VAR, int D, int BITS, bool F16, int MODE, bool GENERIC_SETS, int QM = 0, int WAVES = 4>
 struct Stage1 {
+    static constexpr int BT = WAVES * 64;               // threads per block
     static constexpr int LPV = D / kCoordsPerLane;      // lanes per row
     static constexpr int VPW = 64 / LPV;                // rows per wave
     static constexpr int H = 1 << (BITS - 1);           // positive levels
@@ -361,7 +363,7 @@ struct Stage1 {
         if constexpr (!kChunkMajor) {
             const u32x4 *s4 = reinterpret_cast<const u32x4 *>(set);
             u32x4 *d4 = reinterpret_cast<u32x4 *>(lds);
-            for (int i = threadIdx.x; i < LPV * PL / 4; i += kBlockThreads)
+            for (int i = threadIdx.x; i < LPV * PL / 4; i += BT)
                 d4[i] = s4[i];
             return;
         }
@@ -370,7 +372,7 @@ struct Stage1 {
         u32x4 *d4 = reinterpret_cast<u32x4 *>(lds);
         // LDS word j = k LPV + ln is written in order (no bank conflicts);
         // its chunk is gathered from the set (a few KB, cached)
-        for (int j = threadIdx.x; j < LPV * PL / 4; j += kBlockThreads) {
+        for (int j = threadIdx.x; j < LPV * PL / 4; j += BT) {
             const int k = j / LPV, ln = j - k * LPV;
             const int half = k / CPS, c = k - half * CPS;
             const int slot = kSplit ? half * LPV + ln : 2 * ln + half;
@@ -605,7 +607,7 @@ struct Stage1 {
         const int64_t groups = (a.n + VPW - 1) / VPW;
         // append: blocks (head, token range) are dispatched head-fastest, so
         // the blocks in flight read all heads of the same tokens, one span
-        const int64_t base = (int64_t)(kAppend ? blockIdx.y : blockIdx.x) * (kBlockThreads / 64) * kTileGroups;
+        const int64_t base = (int64_t)(kAppend ? blockIdx.y : blockIdx.x) * WAVES * kTileGroups;
 
         // 1. block-wide tables: the codebook (dequantize) and the rotation
         //    parameters of the block's set, staged through LDS
@@ -616,7 +618,7 @@ struct Stage1 {
         if constexpr (kUseLut && MODE != MODE_DEQUANTIZE) {
             const u32x4 *s4 = reinterpret_cast<const u32x4 *>(a.lut);
             u32x4 *d4 = reinterpret_cast<u32x4 *>(lds_lut);
-            for (int i = threadIdx.x; i < a.lut_cells; i += kBlockThreads)
+            for (int i = threadIdx.x; i < a.lut_cells; i += BT)
                 d4[i] = s4[i];
         }
         float P[PL];
@@ -630,7 +632,7 @@ struct Stage1 {
                 // the set's projection S' = S T^{-1} in MFMA B-fragment order
                 const u32x4 *f4 = reinterpret_cast<const u32x4 *>(a.qjl_frag + set * (int64_t)(QM * D));
                 u32x4 *g4 = reinterpret_cast<u32x4 *>(lds_frag);
-                for (int i = threadIdx.x; i < QM * D / 8; i += kBlockThreads)
+                for (int i = threadIdx.x; i < QM * D / 8; i += BT)
                     g4[i] = f4[i];
             }
         }
@@ -655,11 +657,11 @@ struct Stage1 {
         _Float16 *eq = kQjl ? lds_e + w * kTileRows * kEStride : nullptr;
         const int64_t tstride = kQjl ? (int64_t)(kAppend ? gridDim.y : gridDim.x) : (int64_t)1 << 62;
         for (int64_t tb = (int64_t)(kAppend ? blockIdx.y : blockIdx.x);; tb += tstride) {
-            const int64_t tbase = tb * (kBlockThreads / 64) * kTileGroups;
+            const int64_t tbase = tb * WAVES * kTileGroups;
             if (tbase + w >= groups)
                 return;
             const int64_t row0 = tbase * VPW;  // first row of the tile
-            if ((tbase + (kBlockThreads / 64) * kTileGroups) * VPW <= a.n)
+            if ((tbase + WAVES * kTileGroups) * VPW <= a.n)
                 tile<false>(a, P, lev, thr, lds_levels, lds_lut, row0, groups, tbase, w, sub, slot, eq);
             else
                 tile<true>(a, P, lev, thr, lds_levels, lds_lut, row0, groups, tbase, w, sub, slot, eq);
@@ -705,7 +707,7 @@ struct Stage1 {
             }
             // this lane's output row (lanes 0 .. 15 of the block): group u, slot
             const int u = ar / VPW, sl = ar - u * VPW;
-            const int64_t gl = 4 * u + w;
+            const int64_t gl = WAVES * u + w;
             bool ok = l < 16 && ar < kTileRows && base + gl < groups;
             int64_t row = min(row0 + gl * VPW + sl, a.n - 1);
             if constexpr (kAppend) {
@@ -768,14 +770,14 @@ struct Stage1 {
         In buf[kTileGroups];
 #pragma unroll
         for (int u = 0; u < kTileGroups; u++) {
-            const int gl = TAIL ? (int)(min(base + 4 * u + w, groups - 1) - base) : 4 * u + w;
+            const int gl = TAIL ? (int)(min(base + WAVES * u + w, groups - 1) - base) : WAVES * u + w;
             const int64_t grow = row0 + (int64_t)gl * VPW;
             fetch(a, grow, lane_row<TAIL>(a, grow, slot), sub, buf[u]);
         }
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int u = 0; u < kTileGroups; u++) {
-            const int gl = 4 * u + w;
+            const int gl = WAVES * u + w;
             if (TAIL && base + gl >= groups)
                 break;
             const int64_t grow = row0 + (int64_t)gl * VPW;
