@@ -199,12 +199,13 @@ constexpr int64_t kQjlBlocks = 1024;
 // Quantize with the stage-2 sketch of m bits (isoq_qjl.hip), or nullptr;
 // with `append`, the kernel that writes into the slots of a paged cache.
 const void *qjl_kernel_for(int variant, int d, int bits, bool f16, int m, bool append, int waves);
-// Waves per block of the sketch kernels: 8 with m = 128, so that one staged
-// copy of the projection serves twice the waves (LDS admits 12 waves of
-// 4-wave blocks per CU at d = 128, 16 of 8-wave blocks); 4 with m = 64, and
-// for quantize into rows with several sets (a block's rows share one set, and
-// rows_per_set must stay a multiple of the smaller block).
-inline int qjl_waves(int m, bool append, int n_sets) { return m == 128 && (append || n_sets == 1) ? 8 : 4; }
+// Waves per block of the sketch kernels: 8, so that one staged copy of the
+// projection serves twice the waves (at d = 128, m = 128 LDS admits 12 waves
+// of 4-wave blocks per CU, 16 of 8-wave blocks; the 8-wave kernels also take
+// fewer registers); 4 for quantize into rows with several sets (a block's
+// rows share one set, and rows_per_set must stay a multiple of the smaller
+// block).
+inline int qjl_waves(int m, bool append, int n_sets) { return append || n_sets == 1 ? 8 : 4; }
 
 // Magnitude lookup table, used for 4-bit codebooks.  The magnitude axis of
 // the normalised coordinate is cut into cells of width h, h smaller than every

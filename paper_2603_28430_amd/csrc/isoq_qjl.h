@@ -4,10 +4,10 @@
 // sign(S (x - x_hat)) as m bits and ||x - x_hat|| per row.  The projection is the path's one dense
 // contraction, P = E S'^T over a wave's tile of rows, on MFMA (fp16 inputs,
 // fp32 accumulation); S' = S T^{-1} per rotation set is staged in LDS once
-// per block.  Blocks have 4 or 8 waves (WAVES, chosen by qjl_waves): with
-// m = 128 the staged projection (32 KB at d = 128) and the waves' error tiles
-// let three 4-wave blocks (12 waves) or two 8-wave blocks (16 waves) share a
-// CU's LDS.
+// per block.  Blocks have 8 waves, or 4 for quantize with several sets
+// (WAVES, chosen by qjl_waves): at d = 128, m = 128 the staged projection
+// (32 KB) and the waves' error tiles let three 4-wave blocks (12 waves) or
+// two 8-wave blocks (16 waves) share a CU's LDS.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -31,13 +31,17 @@ __global__ __launch_bounds__(WAVES * 64) void qjl_kernel(const KArgs a)
     S::run(a, lds_levels, lds_params, lds_lut, lds_frag, lds_e);
 }
 
-// Instantiated pairs (m, waves): m = 64 with 4 waves; m = 128 (d <= 128)
-// with 8 waves, and with 4 waves for quantize into rows (several sets).
+// Instantiated (m, waves): m = 64, and m = 128 at d <= 128, with 8 waves; with
+// 4 waves as well for quantize into rows (several sets).
 template <int VAR, int D, int BITS, bool F16, int MODE>
 const void *qjl_pick_m(int m, int waves)
 {
-    if (m == 64 && waves == 4)
-        return reinterpret_cast<const void *>(&qjl_kernel<VAR, D, BITS, F16, 64, MODE, 4>);
+    if (m == 64 && waves == 8)
+        return reinterpret_cast<const void *>(&qjl_kernel<VAR, D, BITS, F16, 64, MODE, 8>);
+    if constexpr (MODE == MODE_QJL) {
+        if (m == 64 && waves == 4)
+            return reinterpret_cast<const void *>(&qjl_kernel<VAR, D, BITS, F16, 64, MODE, 4>);
+    }
     if constexpr (D <= 128) {
         if (m == 128 && waves == 8)
             return reinterpret_cast<const void *>(&qjl_kernel<VAR, D, BITS, F16, 128, MODE, 8>);
