@@ -101,6 +101,8 @@ def test_qjl_sizes(n):
 
 def test_qjl_sets_per_block():
     run_case("fast", 128, 3, 128, "f16", 640, n_sets=3, rows_per_set=64, seed=3)
+    # m = 64 with several sets (4-wave blocks of 128 rows at d = 64)
+    run_case("full", 64, 2, 64, "f32", 1000, n_sets=2, rows_per_set=128, seed=4)
 
 
 def test_qjl_zero_rows_and_scales():
