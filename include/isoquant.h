@@ -27,10 +27,12 @@
  *     it are safe.  Only init and destroy allocate or free device memory.
  *   - Supported shapes in this version: bits in {2, 3, 4}, fp16 or fp32 rows
  *     (arithmetic is fp32 in every case); d from 1 to 1024 for quantize,
- *     dequantize and round trip (tuned kernels for d in {64, 128, 256, 512}, one
- *     generic kernel family for every other width), d in {64, 128, 256, 512} for
- *     the KV-cache and attention-score calls, d in {64, 128, 256} for the
- *     stage-2 sketch.
+ *     dequantize and round trip (tuned kernels for d in {64, 128, 256, 512},
+ *     packed-row kernels for fp16 rows at other multiples of 16 up to 504, a
+ *     generic kernel family for every other width), d in {64, 128, 256, 512}
+ *     for the KV-cache append, d in {64, 96, 128, 160, 192, 256, 512} for the
+ *     attention-score call without the sketch, d in {64, 128, 256} for the
+ *     stage-2 sketch and the calls that use it.
  *   - Widths that are not a multiple of the block size (4; 2-D: 2) follow
  *     Sec. 5.1: the last block is zero padded, all pw rotated coordinates are
  *     quantized and stored (pw = 4 ceil(d/4); 2-D: 2 ceil(d/2)), and the

@@ -49,6 +49,9 @@ bool valid_variant(int v) { return v == ISOQ_FULL || v == ISOQ_FAST || v == ISOQ
 // Widths of the tuned kernels (every entry point); other widths up to
 // kGenericMaxD have quantize, dequantize and round trip only.
 bool tuned_d(int d) { return d == 64 || d == 128 || d == 256 || d == 512; }
+// widths of the decoding calls (append, logits): the tuned ones and three
+// common attention head widths
+bool decode_d(int d) { return tuned_d(d) || d == 96 || d == 160 || d == 192; }
 bool supported_d(int d) { return d >= 1 && d <= kGenericMaxD; }
 bool supported_bits(int b) { return b >= 2 && b <= 4; }
 bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
@@ -177,7 +180,9 @@ const char *isoq_status_string(isoq_status s)
     switch (s) {
     case ISOQ_OK: return "ok";
     case ISOQ_E_INVALID: return "invalid argument";
-    case ISOQ_E_UNSUPPORTED: return "unsupported shape (d in 1..1024, bits in {2,3,4}; the KV and score calls need d in {64,128,256,512}, the sketch d in {64,128,256}) or size limit";
+    case ISOQ_E_UNSUPPORTED:
+        return "unsupported shape (d in 1..1024, bits in {2,3,4}; the KV append needs d in {64,128,256,512}, the score "
+               "call d in {64,96,128,160,192,256,512}, the sketch d in {64,128,256}) or size limit";
     case ISOQ_E_NULL: return "null pointer";
     case ISOQ_E_ALIGN: return "misaligned pointer";
     case ISOQ_E_HIP: return "HIP runtime error";
@@ -550,7 +555,7 @@ isoq_status kv_scores(const isoq_params *pk, const isoq_sketch *sk, int dtype, c
     if (sk && (sk->variant != pk->variant || sk->d != pk->d || sk->n_sets != pk->n_sets ||
                sk->device != pk->device))
         return ISOQ_E_INVALID;
-    if (!tuned_d(pk->d))
+    if (sk ? !tuned_d(pk->d) : !decode_d(pk->d))
         return ISOQ_E_UNSUPPORTED;
     const int64_t max_pos = std::min<int64_t>(max_len, (int64_t)max_blocks_per_seq * block_size);
     if (n_seqs > 65535 || (int64_t)max_blocks_per_seq * block_size > 0x7FFFFFFF ||

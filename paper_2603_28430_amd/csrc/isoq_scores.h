@@ -42,11 +42,13 @@ struct ScoreShape {
     static constexpr int E = 1 << FB;             // entries per table
     static constexpr int NF = D / F;              // fields (tables) per key
     static constexpr int RW = D * BITS / 32;      // record words
-    static constexpr int LW = RW % 4 == 0 ? 4 : 2;  // words per record load (16 or 8 bytes)
+    // words per record load: 16, 8 or 4 bytes, the largest that divides the
+    // record (a record of d b / 8 bytes starts on such a boundary)
+    static constexpr int LW = RW % 4 == 0 ? 4 : RW % 2 == 0 ? 2 : 1;
     static constexpr int RV = RW / LW;            // loads per record
     // keys per lane and batch
     static constexpr int KPT = RW <= 12 ? 2 : 1;
-    static_assert(RW % LW == 0, "records are a whole number of 8-byte vectors");
+    static_assert(RW * 32 == D * BITS, "records are a whole number of words");
     static constexpr int SW = QM / 32;             // sketch words per key
     static constexpr int NQ = QM / 4;              // 4-sign groups (16-entry tables) per key
     // LDS floats for g query heads: tables, codebook, rotated queries; with
@@ -253,6 +255,12 @@ __global__ __launch_bounds__(256) void score_kernel(const SArgs a)
                         k.w[u][4 * v + c] = e;
                     }
                 }
+            } else if constexpr (S::LW == 1) {
+                // records of an odd number of words: 4-byte loads
+                const uint32_t *rp = reinterpret_cast<const uint32_t *>(a.k_idx + krow * RB);
+#pragma unroll
+                for (int v = 0; v < S::RV; v++)
+                    k.w[u][v] = __builtin_nontemporal_load(rp + v);
             } else {
                 // records of 8 (mod 16) bytes: 8-byte loads
                 const u32x2 *rp = reinterpret_cast<const u32x2 *>(a.k_idx + krow * RB);

@@ -47,7 +47,10 @@ ScoreKernel pick_d(int d, int bits, bool f16, int group)
 {
     switch (d) {
     case 64: return pick_bits<VAR, 64>(bits, f16, group);
+    case 96: return pick_bits<VAR, 96>(bits, f16, group);
     case 128: return pick_bits<VAR, 128>(bits, f16, group);
+    case 160: return pick_bits<VAR, 160>(bits, f16, group);
+    case 192: return pick_bits<VAR, 192>(bits, f16, group);
     case 256: return pick_bits<VAR, 256>(bits, f16, group);
     case 512: return pick_bits<VAR, 512>(bits, f16, group);
     }

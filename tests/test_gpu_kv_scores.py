@@ -131,9 +131,18 @@ def test_scores_d128(variant, bits, dtype):
 
 
 @pytest.mark.parametrize("d,bits", [(64, 2), (64, 3), (64, 4), (256, 2), (256, 3), (256, 4), (512, 2), (512, 3),
-                                    (512, 4)])
+                                    (512, 4), (96, 2), (96, 3), (96, 4), (160, 2), (160, 3), (160, 4), (192, 2),
+                                    (192, 3), (192, 4)])
 def test_scores_wide(d, bits):
     run_case("full", d, bits, "f16", n_seqs=2, n_q=2, n_kv=2, bs=32, seq_lens=[1500, 70], seed=d + bits)
+
+
+@pytest.mark.parametrize("variant,d,bits,dtype", [("fast", 96, 3, "f32"), ("2d", 96, 3, "f16"), ("fast", 160, 3, "f16"),
+                                                  ("2d", 192, 2, "f32")])
+def test_scores_head_widths(variant, d, bits, dtype):
+    """Widths 96, 160 and 192: records of 9, 15 and 18 words at 3 bits (4- and
+    8-byte record loads), grouped query heads."""
+    run_case(variant, d, bits, dtype, n_seqs=2, n_q=8, n_kv=2, bs=16, seq_lens=[700, 33], seed=d + 3)
 
 
 @pytest.mark.parametrize("n_q,n_kv,n_sets", [(8, 2, 2), (8, 2, 1), (6, 1, 1), (32, 8, 8)])
