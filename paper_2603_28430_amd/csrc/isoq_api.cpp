@@ -181,8 +181,9 @@ const char *isoq_status_string(isoq_status s)
     case ISOQ_OK: return "ok";
     case ISOQ_E_INVALID: return "invalid argument";
     case ISOQ_E_UNSUPPORTED:
-        return "unsupported shape (d in 1..1024, bits in {2,3,4}; the KV append needs d in {64,128,256,512}, the score "
-               "call d in {64,96,128,160,192,256,512}, the sketch d in {64,128,256}) or size limit";
+        return "unsupported shape (d in 1..1024, bits in {2,3,4}; the KV append needs d in {64,128,256,512} or fp16 "
+               "rows at 96, 160, 192, the score call d in {64,96,128,160,192,256,512}, the sketch d in {64,128,256}) "
+               "or size limit";
     case ISOQ_E_NULL: return "null pointer";
     case ISOQ_E_ALIGN: return "misaligned pointer";
     case ISOQ_E_HIP: return "HIP runtime error";
@@ -489,7 +490,13 @@ isoq_status isoq_kv_append(const isoq_params *pk, const isoq_params *pv, int dty
     if (has_v && (pv->variant != pk->variant || pv->d != pk->d || pv->bits != pk->bits ||
                   pv->device != pk->device))
         return ISOQ_E_INVALID;
-    if (!tuned_d(pk->d))
+    // fp16 rows at d = 96, 160 and 192 use the packed-row kernels (rows of a
+    // group back to back across the wave; with 3 bits their rows must span a
+    // multiple of 4 lanes, which these widths do)
+    const PackedShape ps = packed_shape(pk->d, pk->bits, true);
+    const bool packed = !tuned_d(pk->d) && decode_d(pk->d) && dtype == ISOQ_F16 && ps.rows > 0 &&
+                        (pk->bits != 3 || (pk->d / (8 * ps.chunks)) % 4 == 0);
+    if (!tuned_d(pk->d) && !packed)
         return ISOQ_E_UNSUPPORTED;
     if ((pk->n_sets != 1 && pk->n_sets != n_heads) || (has_v && pv->n_sets != 1 && pv->n_sets != n_heads))
         return ISOQ_E_INVALID;
@@ -507,10 +514,17 @@ isoq_status isoq_kv_append(const isoq_params *pk, const isoq_params *pv, int dty
     if (st != ISOQ_OK)
         return st;
     // one kernel for both tensors; block (x, y, z) = (head, token range, K|V)
-    const void *fn = kernel_for(pk->variant, pk->d, pk->bits, dtype == ISOQ_F16, false, MODE_APPEND);
+    const void *fn = !packed ? kernel_for(pk->variant, pk->d, pk->bits, dtype == ISOQ_F16, false, MODE_APPEND)
+                     : pk->variant == VAR_FULL ? packed_kernel_full(pk->bits, MODE_APPEND, ps.chunks)
+                     : pk->variant == VAR_FAST ? packed_kernel_fast(pk->bits, MODE_APPEND, ps.chunks)
+                                               : packed_kernel_2d(pk->bits, MODE_APPEND, ps.chunks);
     if (!fn)
         return ISOQ_E_UNSUPPORTED;
-    const int64_t blocks = (n_tokens + rows_per_block(pk) - 1) / rows_per_block(pk);
+    // tokens per block: 4 waves of kTileGroups (packed: kTileGroups / chunks)
+    // row groups
+    const int64_t rpb = packed ? (int64_t)ps.rows * (kBlockThreads / 64) * (kTileGroups / ps.chunks)
+                               : rows_per_block(pk);
+    const int64_t blocks = (n_tokens + rpb - 1) / rpb;
     if (blocks > 65535)
         return ISOQ_E_UNSUPPORTED;
     KArgs ak{}, av{};
@@ -527,6 +541,11 @@ isoq_status isoq_kv_append(const isoq_params *pk, const isoq_params *pv, int dty
         a.n_heads = (uint32_t)n_heads;
         a.block_size = (uint32_t)block_size;
         a.div_block = make_fastdiv((uint32_t)block_size);
+        if (packed) {
+            a.g_d = pk->d;
+            a.g_rows = ps.rows;
+            a.g_set_stride = (int64_t)slots_per_set(pk->variant, pk->d) * params_per_slot(pk->variant);
+        }
     }
     void *args[] = {&ak, &av};
     return launch(fn, dim3((unsigned)n_heads, (unsigned)blocks, has_v ? 2 : 1), args, stream);

@@ -25,6 +25,13 @@
 // to the two halves of the row's record (row-relative addressing; with 3 bits
 // L is a multiple of 4, so quads stay inside a row), and a wave walks half as
 // many groups so that the same bytes are in flight.
+//
+// Append (MODE_APPEND, fp16 K/V rows into the slots of a paged cache, at
+// d = 96, 160 and 192): block (x, y, z) = (head, token range, K or V) as in
+// the tuned append, the rows of a group are consecutive tokens of one head
+// (row-relative addressing, input stride n_heads d), and each row's record
+// and norm go to its token's cache row.  With 3 bits L is a multiple of 4 at
+// these widths, so quads stay inside a row.
 #pragma once
 
 #include "isoq_stage1.h"
@@ -101,15 +108,16 @@ __device__ __forceinline__ float packed_pair_total(const float *rp, int n)
 }
 
 template <int VAR, int BITS, int MODE, int C>
-__global__ __launch_bounds__(kBlockThreads) void packed_kernel(const KArgs a)
+__device__ __forceinline__ void packed_body(const KArgs &a)
 {
     constexpr int H = 1 << (BITS - 1);
     constexpr int PL = VAR == VAR_FULL ? 32 : 8;   // parameter floats per chunk
     constexpr int GPW = kTileGroups / C;           // groups per wave (4 C chunks in flight per lane)
     constexpr bool kUseLut = BITS == 4;
-    constexpr bool kEncode = MODE == MODE_QUANTIZE;
+    constexpr bool kAppend = MODE == MODE_APPEND;
+    constexpr bool kEncode = MODE == MODE_QUANTIZE || kAppend;
     constexpr bool kLoadX = MODE != MODE_DEQUANTIZE;
-    static_assert(MODE == MODE_ROUNDTRIP || MODE == MODE_QUANTIZE || MODE == MODE_DEQUANTIZE, "mode");
+    static_assert(MODE == MODE_ROUNDTRIP || MODE == MODE_QUANTIZE || MODE == MODE_DEQUANTIZE || kAppend, "mode");
     static_assert(C == 1 || C == 2, "one or two chunks per lane");
 
     __shared__ float lds_levels[16];
@@ -131,8 +139,11 @@ __global__ __launch_bounds__(kBlockThreads) void packed_kernel(const KArgs a)
     const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int64_t rowb = (int64_t)a.g_d * 2;       // fp16 rows
     const int64_t recb = (int64_t)L * C * BITS;    // d b / 8
-    constexpr int TPB = packed_tiles_per_block(VAR, C);   // row tiles per block
-    const int64_t base0 = (int64_t)blockIdx.x * TPB * (kBlockThreads / 64) * GPW;
+    constexpr int TPB = kAppend ? 1 : packed_tiles_per_block(VAR, C);   // row tiles per block
+    const int64_t base0 = (int64_t)(kAppend ? blockIdx.y : blockIdx.x) * TPB * (kBlockThreads / 64) * GPW;
+    // append: the block's head, its input row stride and cache addressing
+    const int64_t head = kAppend ? (int64_t)blockIdx.x : 0;
+    const int64_t xstride = kAppend ? (int64_t)a.n_heads * rowb : rowb;
 
     if constexpr (MODE == MODE_DEQUANTIZE) {
         if (threadIdx.x < 2 * H)
@@ -146,8 +157,8 @@ __global__ __launch_bounds__(kBlockThreads) void packed_kernel(const KArgs a)
     }
     // rotation parameters of the lane's chunks: once, when the whole block
     // has one set; otherwise per group, when the lane's set changes
-    const bool uni = a.g_block_set != 0;
-    const int64_t bset = a.n_sets == 1 || !uni ? 0 : (base0 * V / a.rows_per_set) % a.n_sets;
+    const bool uni = kAppend || a.g_block_set != 0;
+    const int64_t bset = a.n_sets == 1 || !uni ? 0 : kAppend ? head : (base0 * V / a.rows_per_set) % a.n_sets;
     if (kStage && uni) {
         const u32x4 *s4 = reinterpret_cast<const u32x4 *>(a.params + bset * a.g_set_stride);
         u32x4 *d4 = reinterpret_cast<u32x4 *>(lds_params);
@@ -193,6 +204,7 @@ __global__ __launch_bounds__(kBlockThreads) void packed_kernel(const KArgs a)
         Raw<true> raw[kLoadX ? GPW : 1][C];
         uint32_t bin[kLoadX ? 1 : GPW][C];
         float rin[kLoadX ? 1 : GPW];
+        int64_t slot[kAppend ? GPW : 1];   // append: each row's cache slot, loaded with the row
 #pragma unroll
         for (int u = 0; u < GPW; u++) {
             // a group past the end re-reads group 0 (and is neither computed nor stored)
@@ -202,10 +214,12 @@ __global__ __launch_bounds__(kBlockThreads) void packed_kernel(const KArgs a)
             const int nv = rows * L;                               // lanes holding data
             const int rq = q < rows ? q : 0;                       // lanes past them read row 0
             if constexpr (kLoadX) {
-                const char *row = static_cast<const char *>(a.x) + (grow + rq) * rowb;
+                const char *row = static_cast<const char *>(a.x) + (grow + rq) * xstride + head * rowb;
 #pragma unroll
                 for (int k = 0; k < C; k++)
                     load_row_chunk<true>(row + (uint32_t)((sub + k * L) * 16), raw[u][k]);
+                if constexpr (kAppend)
+                    slot[u] = (a.slots + grow)[rq];
             } else {
                 if constexpr (C == 1) {
                     bin[u][0] = packed_load_bits<BITS>(a.rec_in + grow * recb, lane, nv);
@@ -277,7 +291,24 @@ __global__ __launch_bounds__(kBlockThreads) void packed_kernel(const KArgs a)
                         chain_levels<H>(y, m, ths, lvs, yq[k]);
                     }
                 }
-                if constexpr (kEncode) {
+                if constexpr (kAppend) {
+                    // the token's cache row: slot s is position s mod
+                    // block_size of cache block s / block_size, a block
+                    // holding [n_heads][block_size] records; a skipped slot
+                    // (s < 0 or past the cache) writes nothing
+                    const int64_t s = slot[u];
+                    const bool ok = s >= 0 && s < a.n_slots;
+                    const uint32_t su = ok ? (uint32_t)s : 0u;
+                    const uint32_t blk = fast_div(su, a.div_block);
+                    const int64_t cr = ((int64_t)blk * a.n_heads + head) * a.block_size + (su - blk * a.block_size);
+                    uint8_t *rec = a.rec_out + cr * recb;
+#pragma unroll
+                    for (int k = 0; k < C; k++)
+                        store_bits<BITS>(rec + k * L * BITS, sub, p[k], on && ok);
+                    if (on && ok && sub == 0)
+                        a.norms_out[cr] = rho;
+                    continue;
+                } else if constexpr (kEncode) {
                     if constexpr (C == 1) {
                         packed_store_bits<BITS>(a.rec_out + grow * recb, lane, p[0], nv);
                     } else {
@@ -314,6 +345,19 @@ __global__ __launch_bounds__(kBlockThreads) void packed_kernel(const KArgs a)
     }
 }
 
+template <int VAR, int BITS, int MODE, int C>
+__global__ __launch_bounds__(kBlockThreads) void packed_kernel(const KArgs a)
+{
+    packed_body<VAR, BITS, MODE, C>(a);
+}
+
+// K and V in one launch: blockIdx.z = 0 encodes the keys, 1 the values.
+template <int VAR, int BITS, int C>
+__global__ __launch_bounds__(kBlockThreads) void packed_append_kernel(const KArgs k, const KArgs v)
+{
+    packed_body<VAR, BITS, MODE_APPEND, C>(blockIdx.z == 0 ? k : v);
+}
+
 template <int VAR, int BITS, int C>
 const void *packed_pick_mode(int mode)
 {
@@ -321,6 +365,7 @@ const void *packed_pick_mode(int mode)
     case MODE_ROUNDTRIP: return reinterpret_cast<const void *>(&packed_kernel<VAR, BITS, MODE_ROUNDTRIP, C>);
     case MODE_QUANTIZE: return reinterpret_cast<const void *>(&packed_kernel<VAR, BITS, MODE_QUANTIZE, C>);
     case MODE_DEQUANTIZE: return reinterpret_cast<const void *>(&packed_kernel<VAR, BITS, MODE_DEQUANTIZE, C>);
+    case MODE_APPEND: return reinterpret_cast<const void *>(&packed_append_kernel<VAR, BITS, C>);
     }
     return nullptr;
 }

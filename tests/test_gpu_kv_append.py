@@ -127,6 +127,26 @@ def test_append_wide_rows(variant, d):
              sets_v=1, seed=d)
 
 
+@pytest.mark.parametrize("variant,d,bits", [("full", 96, 3), ("fast", 96, 2), ("2d", 96, 4), ("fast", 160, 3),
+                                            ("full", 160, 4), ("full", 192, 3), ("fast", 192, 2), ("2d", 192, 3)])
+def test_append_head_widths(variant, d, bits):
+    """fp16 rows at d = 96, 160 and 192 (packed-row kernels; two chunks per
+    lane at 192): sets per head for K, one set for V, skipped slots."""
+    run_case(variant, d, bits, "f16", n_tokens=97, n_heads=6, block_size=16, n_blocks=9, sets_k=6, sets_v=1,
+             seed=d + bits)
+
+
+def test_append_head_widths_fp32_unsupported():
+    pk = iq.isoq_params_init("fast", 96, 3, 1)
+    k = torch.zeros((4, 2, 96), dtype=torch.float32, device="cuda")
+    slots = torch.arange(4, dtype=torch.int64, device="cuda")
+    rec = torch.zeros((2, 2, 16, pk.record_bytes), dtype=torch.uint8, device="cuda")
+    rho = torch.zeros((2, 2, 16), dtype=torch.float32, device="cuda")
+    with pytest.raises(iq.IsoqError) as e:
+        iq.isoq_kv_append(pk, k, slots, rec, rho)
+    assert e.value.status == 2
+
+
 @pytest.mark.parametrize("n_heads,block_size,sets_k,sets_v", [(1, 1, 1, 1), (5, 48, 5, 1),
                                                                (3, 7, 1, 3), (32, 16, 32, 32),
                                                                (40, 64, 1, 1)])
