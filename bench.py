@@ -139,19 +139,19 @@ def cpu_baseline(variant, d, bits, x_np, rot, levels, seconds: float):
                       f"(Algorithm 1, indices not stored), {threads} threads, {dt:.1f} s"}
 
 
-def kv_append_side(torch, workloads):
+def kv_append_side(torch, workloads, d=128, cases=(("decode_32x1", 32, 1), ("prefill_8x4096", 8, 4096))):
     """isoq_kv_append (quantize K and V into a paged cache, one launch): a
     decode step (32 sequences x 1 token) and a prefill-sized append (8
-    sequences x 4,096 tokens), 32 heads, d = 128, Fast, 3 bits, fp16, block
-    size 16, one quaternion set per head; each sequence owns randomly placed
-    cache blocks and fills them in order.  Algorithmic bytes per row: the fp16
-    row, the 48-byte record and the 4-byte norm (plus 8 bytes of slot per
-    token)."""
+    sequences x 4,096 tokens), 32 heads, d = 128 (or d), Fast, 3 bits, fp16,
+    block size 16, one quaternion set per head; each sequence owns randomly
+    placed cache blocks and fills them in order.  Algorithmic bytes per row:
+    the fp16 row, the record (48 bytes at d = 128) and the 4-byte norm (plus 8
+    bytes of slot per token)."""
     import paper_2603_28430_amd as iq
 
-    H, d, bs, bits = 32, 128, 16, 3
+    H, bs, bits = 32, 16, 3
     res = {}
-    for name, n_seq, per_seq in (("decode_32x1", 32, 1), ("prefill_8x4096", 8, 4096)):
+    for name, n_seq, per_seq in cases:
         n_tok = n_seq * per_seq
         n_blocks = max(4096, 2 * n_tok // bs)
         print(f"# kv append {name}", file=sys.stderr, flush=True)
@@ -179,6 +179,14 @@ def kv_append_side(torch, workloads):
         pv.close()
         del k, v, caches, rhos
     return res
+
+
+def head_widths_side(torch, workloads):
+    """The decoding calls at the attention head widths 96 and 192 (packed-row
+    append, logits with 4- and 8-byte record loads): the prefill-sized append
+    and the logits of kv_append_side and kv_scores_side at those widths."""
+    return {f"d{d}": {"kv_append": kv_append_side(torch, workloads, d, (("prefill_8x4096", 8, 4096),)),
+                      "kv_scores": kv_scores_side(torch, workloads, d)} for d in (96, 192)}
 
 
 def kv_append_qjl_side(torch, workloads):
@@ -219,16 +227,16 @@ def kv_append_qjl_side(torch, workloads):
     return res
 
 
-def kv_scores_side(torch, workloads):
+def kv_scores_side(torch, workloads, d=128):
     """isoq_kv_scores: attention logits of one decoding query per head against
     a paged cache of quantized keys, 8 sequences x 32,768 positions x 32 heads,
-    d = 128, Fast, 3 bits, block size 16, blocks placed at random.  The cache
-    content is random index bytes and norms (the cost does not depend on it).
-    Algorithmic bytes per key: its 48-byte record, 4-byte norm and 4-byte
-    logit."""
+    d = 128 (or d), Fast, 3 bits, block size 16, blocks placed at random.  The
+    cache content is random index bytes and norms (the cost does not depend on
+    it).  Algorithmic bytes per key: its record (48 bytes at d = 128), 4-byte
+    norm and 4-byte logit."""
     import paper_2603_28430_amd as iq
 
-    B, H, T, d, bs, bits = 8, 32, 32768, 128, 16, 3
+    B, H, T, bs, bits = 8, 32, 32768, 16, 3
     print("# kv scores", file=sys.stderr, flush=True)
     p = iq.isoq_params_init("fast", d, bits, H, rot=workloads.rotation_draws("fast", d, H, seed=1))
     nb = B * T // bs
@@ -389,6 +397,7 @@ def other_configs(measure, entry, torch, np, workloads):
     out["qjl_quantize"] = qjl_side(torch, workloads)
     out["kv_scores_qjl"] = kv_scores_qjl_side(torch, workloads)
     out["widths"] = widths_side(torch, workloads)
+    out["head_widths"] = head_widths_side(torch, workloads)
     print("# config kv cache", file=sys.stderr, flush=True)
     B, H, T, d_ = 8, 32, 32768, 128
     kv = [workloads.kv_stream_torch(B, H, T, d_, seed, "cuda").view(B * H * T, d_) for seed in (2, 3)]
@@ -420,7 +429,8 @@ def main() -> int:
     ap.add_argument("--no-extras", action="store_true")
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the side measurements of the d=256, d=512 and KV-cache workloads")
-    ap.add_argument("--side", choices=["kv-append", "kv-append-qjl", "kv-scores", "kv-scores-qjl", "qjl", "widths"],
+    ap.add_argument("--side", choices=["kv-append", "kv-append-qjl", "kv-scores", "kv-scores-qjl", "qjl", "widths",
+                                       "head-widths"],
                     help="run only this side measurement and print its JSON")
     ap.add_argument("--copy-only", action="store_true",
                     help="only time a plain device copy of the input size (counter calibration)")
@@ -440,7 +450,7 @@ def main() -> int:
     if args.side:
         fn = {"kv-append": kv_append_side, "kv-append-qjl": kv_append_qjl_side, "kv-scores": kv_scores_side,
               "kv-scores-qjl": kv_scores_qjl_side,
-              "qjl": qjl_side, "widths": widths_side}[args.side]
+              "qjl": qjl_side, "widths": widths_side, "head-widths": head_widths_side}[args.side]
         print(json.dumps({"side": args.side, **fn(torch, workloads)}), flush=True)
         return 0
     tdt, ndt, esz = {"f16": (torch.float16, np.float16, 2), "f32": (torch.float32, np.float32, 4)}[args.dtype]

@@ -195,12 +195,13 @@ def test_scores_of_keys_quantized_by_the_oracle():
              seed=21)
 
 
-def test_append_then_scores_end_to_end():
+@pytest.mark.parametrize("variant,d", [("full", 128), ("full", 96), ("fast", 192)])
+def test_append_then_scores_end_to_end(variant, d):
     """Keys appended by isoq_kv_append, logits from isoq_kv_scores, against
     the oracle's logits of the oracle's quantization of the same key rows
     (keys with a coordinate within 1e-6 of a threshold, where either cell is
     admissible, are left out)."""
-    variant, d, bits, H, bs = "full", 128, 3, 4, 16
+    bits, H, bs = 3, 4, 16
     pk, rot, levels = make(variant, d, bits, H)
     n_tok = 900
     x = workloads.unit_gaussian_rows(n_tok * H, d, seed=31, dtype=np.float16)
@@ -228,7 +229,7 @@ def test_append_then_scores_end_to_end():
         near = (np.abs(yt[..., None] - thr).min(-1) <= 1e-6).any(1)
         qv = q.cpu().numpy()[0, h].astype(np.float64)
         ref = oracle.attention_scores(variant, d, bits, rot_h, levels, qv, idx, rho, 0.1)
-        bound = (64 + 8) * 2.0 ** -23 * 0.1 * rho * np.linalg.norm(qv) * np.linalg.norm(levels[idx], axis=1)
+        bound = (d // 2 + 8) * 2.0 ** -23 * 0.1 * rho * np.linalg.norm(qv) * np.linalg.norm(levels[idx], axis=1)
         ok = ~near
         kept += ok.sum()
         err = np.abs(got[h, :n_tok].astype(np.float64) - ref)
