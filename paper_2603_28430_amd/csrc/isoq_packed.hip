@@ -1,5 +1,6 @@
 // Stage-1 packed-row kernels for fp16 rows of width d = 16 k up to 504
-// outside the tuned four (the template is in isoq_packed.h).
+// outside the tuned four, and the K/V append at d = 96, 160 and 192 (the
+// template is in isoq_packed.h).
 #include "isoq_packed.h"
 
 namespace isoq {
