@@ -36,6 +36,18 @@ __device__ __forceinline__ uint32_t dpp_u(uint32_t v)
     return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
 }
 
+// The head a block with grid x index `x` works on, of n_heads.  The
+// dispatcher deals blocks to the 8 XCDs in turn (block i to XCD i mod 8, with
+// the grid's x index fastest), and each XCD has its own L2.  When a head's
+// span of rows or records does not end on a 128-byte line (`shared`),
+// adjacent heads share lines, which two XCDs would each fetch from HBM, so
+// adjacent heads are kept on one XCD: with n_heads a multiple of 8, block x
+// takes head (x mod 8) (n_heads / 8) + x / 8; otherwise head x.
+__device__ __forceinline__ uint32_t xcd_head(uint32_t x, uint32_t n_heads, bool shared)
+{
+    return shared && n_heads % 8 == 0 ? (x % 8) * (n_heads / 8) + x / 8 : x;
+}
+
 __device__ __forceinline__ uint32_t fast_div(uint32_t n, const FastDiv &f)
 {
     const uint32_t t = __umulhi(n, f.m);

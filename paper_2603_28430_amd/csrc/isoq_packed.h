@@ -142,7 +142,7 @@ __device__ __forceinline__ void packed_body(const KArgs &a)
     constexpr int TPB = kAppend ? 1 : packed_tiles_per_block(VAR, C);   // row tiles per block
     const int64_t base0 = (int64_t)(kAppend ? blockIdx.y : blockIdx.x) * TPB * (kBlockThreads / 64) * GPW;
     // append: the block's head, its input row stride and cache addressing
-    const int64_t head = kAppend ? (int64_t)blockIdx.x : 0;
+    const int64_t head = kAppend ? (int64_t)xcd_head(blockIdx.x, a.n_heads, rowb % 128 != 0) : 0;
     const int64_t xstride = kAppend ? (int64_t)a.n_heads * rowb : rowb;
 
     if constexpr (MODE == MODE_DEQUANTIZE) {

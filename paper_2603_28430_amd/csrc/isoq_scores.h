@@ -115,7 +115,9 @@ __global__ __launch_bounds__(256) void score_kernel(const SArgs a)
         extern __shared__ __align__(16) float dyn[];
         smem = dyn;
     }
-    const int h = blockIdx.x, s = blockIdx.z;
+    // a head's records of one cache block: block_size records of RB bytes
+    const int h = (int)xcd_head(blockIdx.x, (uint32_t)a.n_kv_heads, a.block_size * RB % 128 != 0);
+    const int s = blockIdx.z;
     const int G = GT > 0 ? GT : a.group;
     int64_t len = a.seq_lens[s];
     len = min(len, a.max_len);

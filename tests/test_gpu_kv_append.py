@@ -136,6 +136,15 @@ def test_append_head_widths(variant, d, bits):
              seed=d + bits)
 
 
+@pytest.mark.parametrize("variant,d,n_heads", [("fast", 96, 16), ("full", 160, 8)])
+def test_append_head_widths_xcd_head_order(variant, d, n_heads):
+    """Rows of 192 and 320 bytes share cache lines between heads, so with a
+    head count that is a multiple of 8 the blocks take heads in XCD order;
+    every (token, head) row must still land in its own cache row."""
+    run_case(variant, d, 3, "f16", n_tokens=150, n_heads=n_heads, block_size=16, n_blocks=12, sets_k=n_heads,
+             sets_v=1, seed=d + n_heads)
+
+
 def test_append_head_widths_fp32_unsupported():
     pk = iq.isoq_params_init("fast", 96, 3, 1)
     k = torch.zeros((4, 2, 96), dtype=torch.float32, device="cuda")

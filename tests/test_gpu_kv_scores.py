@@ -145,6 +145,14 @@ def test_scores_head_widths(variant, d, bits, dtype):
     run_case(variant, d, bits, dtype, n_seqs=2, n_q=8, n_kv=2, bs=16, seq_lens=[700, 33], seed=d + 3)
 
 
+@pytest.mark.parametrize("d,bs,n_kv", [(96, 16, 8), (128, 7, 16), (192, 5, 8)])
+def test_scores_xcd_head_order(d, bs, n_kv):
+    """A head's records of one cache block not ending on a 128-byte line
+    (16 x 36, 7 x 48, 5 x 72 bytes) with a multiple of 8 key heads: blocks take
+    heads in XCD order, each head's logits must still be its own."""
+    run_case("fast", d, 3, "f16", n_seqs=2, n_q=2 * n_kv, n_kv=n_kv, bs=bs, seq_lens=[300, 41], seed=d + bs)
+
+
 @pytest.mark.parametrize("n_q,n_kv,n_sets", [(8, 2, 2), (8, 2, 1), (6, 1, 1), (32, 8, 8)])
 def test_scores_grouped_query_heads(n_q, n_kv, n_sets):
     run_case("fast", 128, 3, "f16", n_seqs=2, n_q=n_q, n_kv=n_kv, bs=16, seq_lens=[600, 45],
