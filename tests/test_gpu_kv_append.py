@@ -136,13 +136,15 @@ def test_append_head_widths(variant, d, bits):
              seed=d + bits)
 
 
-@pytest.mark.parametrize("variant,d,n_heads", [("fast", 96, 16), ("full", 160, 8)])
-def test_append_head_widths_xcd_head_order(variant, d, n_heads):
+@pytest.mark.parametrize("variant,d,n_heads,bs", [("fast", 96, 16, 16), ("full", 160, 8, 16), ("2d", 96, 8, 5),
+                                                  ("fast", 192, 8, 1)])
+def test_append_head_widths_xcd_head_order(variant, d, n_heads, bs):
     """Rows of 192 and 320 bytes share cache lines between heads, so with a
     head count that is a multiple of 8 the blocks take heads in XCD order;
-    every (token, head) row must still land in its own cache row."""
-    run_case(variant, d, 3, "f16", n_tokens=150, n_heads=n_heads, block_size=16, n_blocks=12, sets_k=n_heads,
-             sets_v=1, seed=d + n_heads)
+    every (token, head) row must still land in its own cache row (odd block
+    sizes, one-slot blocks, and 384-byte rows that keep head order)."""
+    run_case(variant, d, 3, "f16", n_tokens=150, n_heads=n_heads, block_size=bs, n_blocks=(200 + bs - 1) // bs,
+             sets_k=n_heads, sets_v=1, seed=d + n_heads + bs)
 
 
 def test_append_head_widths_fp32_unsupported():

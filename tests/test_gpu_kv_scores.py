@@ -145,6 +145,13 @@ def test_scores_head_widths(variant, d, bits, dtype):
     run_case(variant, d, bits, dtype, n_seqs=2, n_q=8, n_kv=2, bs=16, seq_lens=[700, 33], seed=d + 3)
 
 
+def test_scores_head_widths_lengths():
+    """d = 96: empty, one-token and block-straddling sequences, and max_len
+    cutting a sequence short."""
+    run_case("full", 96, 3, "f16", n_seqs=5, n_q=8, n_kv=8, bs=7, seq_lens=[0, 1, 6, 1025, 2100], max_len=2000,
+             seed=5)
+
+
 @pytest.mark.parametrize("d,bs,n_kv", [(96, 16, 8), (128, 7, 16), (192, 5, 8)])
 def test_scores_xcd_head_order(d, bs, n_kv):
     """A head's records of one cache block not ending on a 128-byte line
