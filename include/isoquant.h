@@ -30,10 +30,10 @@
  *     dequantize and round trip (tuned kernels for d in {64, 128, 256, 512},
  *     packed-row kernels for fp16 rows at other multiples of 16 up to 504, a
  *     generic kernel family for every other width), d in {64, 128, 256, 512}
- *     for the KV-cache append (and, fp16 rows only, 96, 160 and 192), d in
- *     {64, 96, 128, 160, 192, 256, 512} for the attention-score call without
- *     the sketch, d in {64, 128, 256} for the stage-2 sketch and the calls that
- *     use it.
+ *     for the KV-cache append (and, fp16 rows only, 80, 96, 160 and 192), d in
+ *     {64, 80, 96, 128, 160, 192, 256, 512} for the attention-score call
+ *     without the sketch, d in {64, 128, 256} for the stage-2 sketch and the
+ *     calls that use it.
  *   - Widths that are not a multiple of the block size (4; 2-D: 2) follow
  *     Sec. 5.1: the last block is zero padded, all pw rotated coordinates are
  *     quantized and stored (pw = 4 ceil(d/4); 2-D: 2 ceil(d/2)), and the
@@ -183,8 +183,8 @@ isoq_status isoq_roundtrip(const isoq_params *p, int dtype, const void *x, int64
  * Limits: n_tokens * n_heads < 2^31, n_blocks * block_size < 2^31, n_heads and
  * block_size >= 1, and at most 65,535 launch blocks of tokens (n_tokens up to
  * 8,388,480 at d = 64, 4,194,240 at d = 128, 2,097,120 at d = 256, 1,048,560
- * at d = 512; fp16 rows: 5,242,800 at d = 96, 3,145,680 at d = 160, 2,621,400
- * at d = 192); beyond that ISOQ_E_UNSUPPORTED.  Distinct tokens must map to distinct slots (a repeated slot
+ * at d = 512; fp16 rows: 6,291,360 at d = 80, 5,242,800 at d = 96, 3,145,680
+ * at d = 160, 2,621,400 at d = 192); beyond that ISOQ_E_UNSUPPORTED.  Distinct tokens must map to distinct slots (a repeated slot
  * is written by both rows in an unspecified order).  Slots not named are left
  * untouched.  n_tokens = 0 is a no-op.
  */

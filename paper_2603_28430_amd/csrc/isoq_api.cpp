@@ -51,7 +51,7 @@ bool valid_variant(int v) { return v == ISOQ_FULL || v == ISOQ_FAST || v == ISOQ
 bool tuned_d(int d) { return d == 64 || d == 128 || d == 256 || d == 512; }
 // widths of the decoding calls (append, logits): the tuned ones and three
 // common attention head widths
-bool decode_d(int d) { return tuned_d(d) || d == 96 || d == 160 || d == 192; }
+bool decode_d(int d) { return tuned_d(d) || d == 80 || d == 96 || d == 160 || d == 192; }
 bool supported_d(int d) { return d >= 1 && d <= kGenericMaxD; }
 bool supported_bits(int b) { return b >= 2 && b <= 4; }
 bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
@@ -182,8 +182,8 @@ const char *isoq_status_string(isoq_status s)
     case ISOQ_E_INVALID: return "invalid argument";
     case ISOQ_E_UNSUPPORTED:
         return "unsupported shape (d in 1..1024, bits in {2,3,4}; the KV append needs d in {64,128,256,512} or fp16 "
-               "rows at 96, 160, 192, the score call d in {64,96,128,160,192,256,512}, the sketch d in {64,128,256}) "
-               "or size limit";
+               "rows at 80, 96, 160, 192, the score call d in {64,80,96,128,160,192,256,512}, the sketch d in "
+               "{64,128,256}) or size limit";
     case ISOQ_E_NULL: return "null pointer";
     case ISOQ_E_ALIGN: return "misaligned pointer";
     case ISOQ_E_HIP: return "HIP runtime error";
@@ -490,12 +490,13 @@ isoq_status isoq_kv_append(const isoq_params *pk, const isoq_params *pv, int dty
     if (has_v && (pv->variant != pk->variant || pv->d != pk->d || pv->bits != pk->bits ||
                   pv->device != pk->device))
         return ISOQ_E_INVALID;
-    // fp16 rows at d = 96, 160 and 192 use the packed-row kernels (rows of a
-    // group back to back across the wave; with 3 bits their rows must span a
-    // multiple of 4 lanes, which these widths do)
+    // fp16 rows at d = 80, 96, 160 and 192 use the packed-row kernels (rows
+    // of a group back to back across the wave; with 3 bits a row spans a
+    // multiple of 4 lanes, or 10 lanes at d = 80 with one chunk per lane)
     const PackedShape ps = packed_shape(pk->d, pk->bits, true);
+    const int lanes = ps.rows > 0 ? pk->d / (8 * ps.chunks) : 0;
     const bool packed = !tuned_d(pk->d) && decode_d(pk->d) && dtype == ISOQ_F16 && ps.rows > 0 &&
-                        (pk->bits != 3 || (pk->d / (8 * ps.chunks)) % 4 == 0);
+                        (pk->bits != 3 || lanes % 4 == 0 || (ps.chunks == 1 && lanes % 2 == 0));
     if (!tuned_d(pk->d) && !packed)
         return ISOQ_E_UNSUPPORTED;
     if ((pk->n_sets != 1 && pk->n_sets != n_heads) || (has_v && pv->n_sets != 1 && pv->n_sets != n_heads))

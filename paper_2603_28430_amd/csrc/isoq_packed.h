@@ -27,11 +27,12 @@
 // many groups so that the same bytes are in flight.
 //
 // Append (MODE_APPEND, fp16 K/V rows into the slots of a paged cache, at
-// d = 96, 160 and 192): block (x, y, z) = (head, token range, K or V) as in
-// the tuned append, the rows of a group are consecutive tokens of one head
+// d = 80, 96, 160 and 192): block (x, y, z) = (head, token range, K or V) as
+// in the tuned append, the rows of a group are consecutive tokens of one head
 // (row-relative addressing, input stride n_heads d), and each row's record
 // and norm go to its token's cache row.  With 3 bits L is a multiple of 4 at
-// these widths, so quads stay inside a row.
+// 96, 160 and 192, so quads stay inside a row; at 80 (L = 10) lane pairs
+// write the record in half-words.
 #pragma once
 
 #include "isoq_stage1.h"
@@ -80,6 +81,25 @@ __device__ __forceinline__ void packed_store_bits(uint8_t *rec, int c, uint32_t 
             reinterpret_cast<uint16_t *>(rec)[c] = (uint16_t)p;
         else
             reinterpret_cast<uint32_t *>(rec)[c] = p;
+    }
+}
+
+// 3 bits, rows of a lane count that is even but not a multiple of 4 (d = 80):
+// lane sub's 24 bits go to byte 3 sub of the row's record through lane pairs
+// (rows start on even lanes): the even lane writes bytes 6 i .. 6 i + 3 (its
+// bits and the odd lane's first 8) as two half-words, the odd lane bytes
+// 6 i + 4 .. 6 i + 5.  Every lane of the wave must call it (DPP exchange).
+__device__ __forceinline__ void store_bits3_pairs(uint8_t *rec, int sub, uint32_t p, bool ok)
+{
+    const uint32_t o = dpp_u<DPP_QUAD_1032>(p);   // the pair partner's bits
+    uint16_t *h = reinterpret_cast<uint16_t *>(rec + 6 * (sub >> 1));
+    if (ok) {
+        if ((sub & 1) == 0) {
+            h[0] = (uint16_t)p;
+            h[1] = (uint16_t)((p >> 16) | (o << 8));
+        } else {
+            h[2] = (uint16_t)(p >> 8);
+        }
     }
 }
 
@@ -302,9 +322,14 @@ __device__ __forceinline__ void packed_body(const KArgs &a)
                     const uint32_t blk = fast_div(su, a.div_block);
                     const int64_t cr = ((int64_t)blk * a.n_heads + head) * a.block_size + (su - blk * a.block_size);
                     uint8_t *rec = a.rec_out + cr * recb;
+                    if (BITS == 3 && L % 4 != 0) {
+                        // d = 80: quads would straddle rows
+                        store_bits3_pairs(rec, sub, p[0], on && ok);
+                    } else {
 #pragma unroll
-                    for (int k = 0; k < C; k++)
-                        store_bits<BITS>(rec + k * L * BITS, sub, p[k], on && ok);
+                        for (int k = 0; k < C; k++)
+                            store_bits<BITS>(rec + k * L * BITS, sub, p[k], on && ok);
+                    }
                     if (on && ok && sub == 0)
                         a.norms_out[cr] = rho;
                     continue;

@@ -41,14 +41,16 @@ struct ScoreShape {
     static constexpr int FB = F * BITS;           // bits per field
     static constexpr int E = 1 << FB;             // entries per table
     static constexpr int NF = D / F;              // fields (tables) per key
-    static constexpr int RW = D * BITS / 32;      // record words
+    static constexpr int RW = (D * BITS + 31) / 32;  // record words (the last one partial at 3 bits, d = 80)
+    static constexpr int RH = D * BITS / 16;         // record half-words
+    static_assert(RH * 16 == D * BITS, "records are a whole number of half-words");
     // words per record load: 16, 8 or 4 bytes, the largest that divides the
-    // record (a record of d b / 8 bytes starts on such a boundary)
-    static constexpr int LW = RW % 4 == 0 ? 4 : RW % 2 == 0 ? 2 : 1;
-    static constexpr int RV = RW / LW;            // loads per record
+    // record (a record of d b / 8 bytes starts on such a boundary); 0: a
+    // record of an odd number of half-words, read in 2-byte loads
+    static constexpr int LW = RW * 32 != D * BITS ? 0 : RW % 4 == 0 ? 4 : RW % 2 == 0 ? 2 : 1;
+    static constexpr int RV = LW ? RW / LW : RH;   // loads per record
     // keys per lane and batch
     static constexpr int KPT = RW <= 12 ? 2 : 1;
-    static_assert(RW * 32 == D * BITS, "records are a whole number of words");
     static constexpr int SW = QM / 32;             // sketch words per key
     static constexpr int NQ = QM / 4;              // 4-sign groups (16-entry tables) per key
     // LDS floats for g query heads: tables, codebook, rotated queries; with
@@ -256,6 +258,16 @@ __global__ __launch_bounds__(256) void score_kernel(const SArgs a)
                         const uint32_t e = q4[c];
                         k.w[u][4 * v + c] = e;
                     }
+                }
+            } else if constexpr (S::LW == 0) {
+                // records of an odd number of half-words: 2-byte loads, paired
+                // into words (the upper half of the last word is zero)
+                const uint16_t *hp = reinterpret_cast<const uint16_t *>(a.k_idx + krow * RB);
+#pragma unroll
+                for (int c = 0; c < S::RW; c++) {
+                    const uint32_t lo = hp[2 * c];
+                    const uint32_t hi = 2 * c + 1 < S::RH ? (uint32_t)hp[2 * c + 1] : 0u;
+                    k.w[u][c] = lo | (hi << 16);
                 }
             } else if constexpr (S::LW == 1) {
                 // records of an odd number of words: 4-byte loads

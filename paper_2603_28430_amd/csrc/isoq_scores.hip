@@ -47,6 +47,7 @@ ScoreKernel pick_d(int d, int bits, bool f16, int group)
 {
     switch (d) {
     case 64: return pick_bits<VAR, 64>(bits, f16, group);
+    case 80: return pick_bits<VAR, 80>(bits, f16, group);
     case 96: return pick_bits<VAR, 96>(bits, f16, group);
     case 128: return pick_bits<VAR, 128>(bits, f16, group);
     case 160: return pick_bits<VAR, 160>(bits, f16, group);

@@ -128,16 +128,18 @@ def test_append_wide_rows(variant, d):
 
 
 @pytest.mark.parametrize("variant,d,bits", [("full", 96, 3), ("fast", 96, 2), ("2d", 96, 4), ("fast", 160, 3),
-                                            ("full", 160, 4), ("full", 192, 3), ("fast", 192, 2), ("2d", 192, 3)])
+                                            ("full", 160, 4), ("full", 192, 3), ("fast", 192, 2), ("2d", 192, 3),
+                                            ("fast", 80, 3), ("full", 80, 2), ("2d", 80, 4), ("full", 80, 3)])
 def test_append_head_widths(variant, d, bits):
-    """fp16 rows at d = 96, 160 and 192 (packed-row kernels; two chunks per
-    lane at 192): sets per head for K, one set for V, skipped slots."""
+    """fp16 rows at d = 80, 96, 160 and 192 (packed-row kernels; two chunks
+    per lane at 192; at 80 and 3 bits lane pairs write the records): sets per
+    head for K, one set for V, skipped slots."""
     run_case(variant, d, bits, "f16", n_tokens=97, n_heads=6, block_size=16, n_blocks=9, sets_k=6, sets_v=1,
              seed=d + bits)
 
 
 @pytest.mark.parametrize("variant,d,n_heads,bs", [("fast", 96, 16, 16), ("full", 160, 8, 16), ("2d", 96, 8, 5),
-                                                  ("fast", 192, 8, 1)])
+                                                  ("fast", 192, 8, 1), ("full", 80, 8, 16)])
 def test_append_head_widths_xcd_head_order(variant, d, n_heads, bs):
     """Rows of 192 and 320 bytes share cache lines between heads, so with a
     head count that is a multiple of 8 the blocks take heads in XCD order;

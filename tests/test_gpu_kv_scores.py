@@ -131,17 +131,17 @@ def test_scores_d128(variant, bits, dtype):
 
 
 @pytest.mark.parametrize("d,bits", [(64, 2), (64, 3), (64, 4), (256, 2), (256, 3), (256, 4), (512, 2), (512, 3),
-                                    (512, 4), (96, 2), (96, 3), (96, 4), (160, 2), (160, 3), (160, 4), (192, 2),
-                                    (192, 3), (192, 4)])
+                                    (512, 4), (80, 2), (80, 3), (80, 4), (96, 2), (96, 3), (96, 4), (160, 2),
+                                    (160, 3), (160, 4), (192, 2), (192, 3), (192, 4)])
 def test_scores_wide(d, bits):
     run_case("full", d, bits, "f16", n_seqs=2, n_q=2, n_kv=2, bs=32, seq_lens=[1500, 70], seed=d + bits)
 
 
 @pytest.mark.parametrize("variant,d,bits,dtype", [("fast", 96, 3, "f32"), ("2d", 96, 3, "f16"), ("fast", 160, 3, "f16"),
-                                                  ("2d", 192, 2, "f32")])
+                                                  ("2d", 192, 2, "f32"), ("fast", 80, 3, "f16"), ("2d", 80, 3, "f32")])
 def test_scores_head_widths(variant, d, bits, dtype):
-    """Widths 96, 160 and 192: records of 9, 15 and 18 words at 3 bits (4- and
-    8-byte record loads), grouped query heads."""
+    """Widths 80, 96, 160 and 192: records of 7.5, 9, 15 and 18 words at 3 bits
+    (2-, 4- and 8-byte record loads), grouped query heads."""
     run_case(variant, d, bits, dtype, n_seqs=2, n_q=8, n_kv=2, bs=16, seq_lens=[700, 33], seed=d + 3)
 
 
@@ -152,7 +152,7 @@ def test_scores_head_widths_lengths():
              seed=5)
 
 
-@pytest.mark.parametrize("d,bs,n_kv", [(96, 16, 8), (128, 7, 16), (192, 5, 8)])
+@pytest.mark.parametrize("d,bs,n_kv", [(96, 16, 8), (128, 7, 16), (192, 5, 8), (80, 16, 8)])
 def test_scores_xcd_head_order(d, bs, n_kv):
     """A head's records of one cache block not ending on a 128-byte line
     (16 x 36, 7 x 48, 5 x 72 bytes) with a multiple of 8 key heads: blocks take
@@ -210,7 +210,7 @@ def test_scores_of_keys_quantized_by_the_oracle():
              seed=21)
 
 
-@pytest.mark.parametrize("variant,d", [("full", 128), ("full", 96), ("fast", 192)])
+@pytest.mark.parametrize("variant,d", [("full", 128), ("full", 96), ("fast", 192), ("2d", 80)])
 def test_append_then_scores_end_to_end(variant, d):
     """Keys appended by isoq_kv_append, logits from isoq_kv_scores, against
     the oracle's logits of the oracle's quantization of the same key rows

@@ -123,24 +123,24 @@ def test_widths_large_sampled(variant, d, dtype):
 
 def test_widths_unsupported_calls():
     """Widths outside the generic range, and the KV / score / sketch calls at
-    a width outside theirs (d = 80: a 30-byte 3-bit record), return
+    a width outside theirs (d = 100), return
     ISOQ_E_UNSUPPORTED before any launch."""
     with pytest.raises(iq.IsoqError) as e:
         iq.isoq_params_init("full", 1025, 3, 1)
     assert e.value.status == 2
-    p = iq.isoq_params_init("fast", 80, 3, 1)
+    p = iq.isoq_params_init("fast", 100, 3, 1)
     with pytest.raises(iq.IsoqError) as e:
         iq.isoq_sketch_init(p, 64)
     assert e.value.status == 2
     z = lambda *s, dt=torch.uint8: torch.zeros(s, dtype=dt, device="cuda")
     R = p.record_bytes
     lib = iq.isoquant.lib
-    k = z(4, 1, 80, dt=torch.float16)
+    k = z(4, 1, 100, dt=torch.float16)
     slots = torch.arange(4, dtype=torch.int64, device="cuda")
     rec, rho = z(2, 1, 16, R), z(2, 1, 16, dt=torch.float32)
     assert lib.isoq_kv_append(p.handle, None, 1, k.data_ptr(), None, slots.data_ptr(), 4, 1, rec.data_ptr(),
                               rho.data_ptr(), None, None, 2, 16, None) == 2
-    q = z(1, 1, 80, dt=torch.float16)
+    q = z(1, 1, 100, dt=torch.float16)
     tab, lens = z(1, 2, dt=torch.int32), torch.ones((1,), dtype=torch.int32, device="cuda")
     out = z(1, 1, 32, dt=torch.float32)
     assert lib.isoq_kv_scores(p.handle, 1, q.data_ptr(), 1, 1, 1, rec.data_ptr(), rho.data_ptr(), 2, 16,
