@@ -182,11 +182,12 @@ def kv_append_side(torch, workloads, d=128, cases=(("decode_32x1", 32, 1), ("pre
 
 
 def head_widths_side(torch, workloads):
-    """The decoding calls at the attention head widths 96 and 192 (packed-row
-    append, logits with 4- and 8-byte record loads): the prefill-sized append
-    and the logits of kv_append_side and kv_scores_side at those widths."""
+    """The decoding calls at the attention head widths 80, 96 and 192
+    (packed-row append, logits with 2-, 4- and 8-byte record loads): the
+    prefill-sized append and the logits of kv_append_side and kv_scores_side
+    at those widths."""
     return {f"d{d}": {"kv_append": kv_append_side(torch, workloads, d, (("prefill_8x4096", 8, 4096),)),
-                      "kv_scores": kv_scores_side(torch, workloads, d)} for d in (96, 192)}
+                      "kv_scores": kv_scores_side(torch, workloads, d)} for d in (80, 96, 192)}
 
 
 def kv_append_qjl_side(torch, workloads):
