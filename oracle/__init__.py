@@ -18,8 +18,8 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "isoq_oracle.c")
 _LIB = os.path.join(_HERE, "liboracle.so")
 
-FULL, FAST, PLANAR2D = 0, 1, 2
-VARIANTS = {"full": FULL, "fast": FAST, "2d": PLANAR2D}
+FULL, FAST, PLANAR2D, BLOCK8 = 0, 1, 2, 3
+VARIANTS = {"full": FULL, "fast": FAST, "2d": PLANAR2D, "8d": BLOCK8}
 
 
 def build() -> str:
@@ -53,6 +53,12 @@ def lib():
         L.orc_fast_inverse.argtypes = [dp, dp, dp]
         L.orc_planar_forward.argtypes = [ctypes.c_double, dp, dp]
         L.orc_planar_inverse.argtypes = [ctypes.c_double, dp, dp]
+        L.orc_det8.argtypes = [dp]
+        L.orc_det8.restype = ctypes.c_double
+        L.orc_orthonormalize8.argtypes = [dp, dp]
+        L.orc_orthonormalize8.restype = ctypes.c_int
+        L.orc_block8_forward.argtypes = [dp, dp, dp]
+        L.orc_block8_inverse.argtypes = [dp, dp, dp]
         L.orc_thresholds.argtypes = [ctypes.c_int, dp, dp]
         L.orc_lloyd_max_gaussian.argtypes = [ctypes.c_int, ctypes.c_double, ctypes.c_int, dp]
         L.orc_lloyd_max_gaussian.restype = ctypes.c_int
@@ -147,6 +153,35 @@ def planar_inverse(theta, u):
     return out
 
 
+# --- 8-D grouped blocks (Table 3; Sec. 5.7 with k = 8) ---------------------------
+def det8(M):
+    """Determinant of an 8x8 matrix (Gaussian elimination, partial pivoting)."""
+    M = _d(np.asarray(M).reshape(8, 8))
+    return float(lib().orc_det8(_p(M)))
+
+
+def orthonormalize8(G):
+    """The block rotation of a raw 8x8 draw G: Gram-Schmidt Q of G's columns
+    (G = QR, diag R > 0), with column 0 negated when det Q = -1.  [8, 8]."""
+    G = _d(np.asarray(G).reshape(8, 8))
+    Q = np.zeros((8, 8))
+    if lib().orc_orthonormalize8(_p(G), _p(Q)) != 0:
+        raise ValueError("linearly dependent columns")
+    return Q
+
+
+def block8_forward(G, v):
+    G, v, out = _d(np.asarray(G).reshape(8, 8)), _d(v), np.zeros(8)
+    lib().orc_block8_forward(_p(G), _p(v), _p(out))
+    return out
+
+
+def block8_inverse(G, y):
+    G, y, out = _d(np.asarray(G).reshape(8, 8)), _d(y), np.zeros(8)
+    lib().orc_block8_inverse(_p(G), _p(y), _p(out))
+    return out
+
+
 # --- codebook ------------------------------------------------------------------
 def lloyd_max_gaussian(bits: int, sigma: float, iters: int = 200) -> np.ndarray:
     out = np.zeros(1 << bits)
@@ -181,9 +216,13 @@ def table1_params(variant, d: int) -> int:
     return lib().orc_table1_params(_variant(variant), int(d))
 
 
-def padded_width(variant, d: int) -> int:
+def block_width(variant) -> int:
     v = _variant(variant)
-    return num_blocks(v, d) * (2 if v == PLANAR2D else 4)
+    return 2 if v == PLANAR2D else 8 if v == BLOCK8 else 4
+
+
+def padded_width(variant, d: int) -> int:
+    return num_blocks(variant, d) * block_width(variant)
 
 
 def mul_count_reset():

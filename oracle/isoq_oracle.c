@@ -23,7 +23,14 @@
  *   - quaternion block i holds coordinates 4i..4i+3 with coordinate 4i the
  *     real part; the 2-D case pairs coordinates (2j, 2j+1);
  *   - Full evaluates (q_L v) conj(q_R) left to right (associative, Prop. 1);
- *   - raw rotation draws are normalised here, u / ||u||  (Sec. 5.5).
+ *   - raw rotation draws are normalised here, u / ||u||  (Sec. 5.5);
+ *   - 8-D grouped blocks (the block-size axis of Table 3; Sec. 5.7 states the
+ *     law of a Haar block rotation for any block size k): coordinates 8i..8i+7
+ *     form block i, rotated by its own R_i ~ Haar(SO(8)).  A raw draw is an
+ *     8x8 matrix G of i.i.d. N(0,1) entries; R_i is the orthogonal factor Q of
+ *     G = QR with diag(R) > 0 (Haar on O(8)), with its first column negated
+ *     when det Q = -1 (a fixed reflection maps that coset onto SO(8) and
+ *     keeps the measure).
  *
  * Pins: every public function is checked in the CPU test suite against facts
  * that do not come from this file (defining relations of H, the textbook
@@ -38,6 +45,7 @@
 #define ORC_FULL 0
 #define ORC_FAST 1
 #define ORC_PLANAR2D 2
+#define ORC_BLOCK8 3
 
 static const double ORC_EPS = 1e-12;
 
@@ -156,6 +164,120 @@ void orc_planar_inverse(double theta, const double u[2], double out[2])
 }
 
 /* ---------------------------------------------------------------------------
+ * 8-D grouped blocks (Table 3; Sec. 5.7 with k = 8).
+ * ------------------------------------------------------------------------- */
+
+/* Determinant of a row-major 8x8 matrix by Gaussian elimination with partial
+ * pivoting (the product of the pivots, sign flipped once per row swap). */
+double orc_det8(const double M[64])
+{
+    double a[8][8];
+    for (int r = 0; r < 8; r++)
+        for (int c = 0; c < 8; c++)
+            a[r][c] = M[8 * r + c];
+    double det = 1.0;
+    for (int k = 0; k < 8; k++) {
+        int piv = k;
+        for (int r = k + 1; r < 8; r++)
+            if (fabs(a[r][k]) > fabs(a[piv][k]))
+                piv = r;
+        if (a[piv][k] == 0.0)
+            return 0.0;
+        if (piv != k) {
+            for (int c = 0; c < 8; c++) {
+                double t = a[k][c];
+                a[k][c] = a[piv][c];
+                a[piv][c] = t;
+            }
+            det = -det;
+        }
+        det *= a[k][k];
+        for (int r = k + 1; r < 8; r++) {
+            double f = a[r][k] / a[k][k];
+            for (int c = k; c < 8; c++)
+                a[r][c] -= f * a[k][c];
+        }
+    }
+    return det;
+}
+
+/*
+ * The rotation of one 8-D block from its raw draw G (row-major 8x8): the
+ * columns of G orthonormalised in order by Gram-Schmidt, which is the Q of
+ * G = QR with a positive diagonal in R (each column loses its components along
+ * the earlier ones, a second pass removing what rounding left, then is scaled
+ * to unit length); then det Q = +1 by negating column 0 when it is -1.
+ * Q is written row-major.  Returns 0, or -1 when the columns are linearly
+ * dependent.
+ */
+int orc_orthonormalize8(const double G[64], double Q[64])
+{
+    double col[8][8]; /* col[c][r] = entry (r, c) */
+    for (int r = 0; r < 8; r++)
+        for (int c = 0; c < 8; c++)
+            col[c][r] = G[8 * r + c];
+    for (int c = 0; c < 8; c++) {
+        for (int pass = 0; pass < 2; pass++)
+            for (int p = 0; p < c; p++) {
+                double dot = 0.0;
+                for (int r = 0; r < 8; r++)
+                    dot += col[p][r] * col[c][r];
+                for (int r = 0; r < 8; r++)
+                    col[c][r] -= dot * col[p][r];
+            }
+        double ss = 0.0;
+        for (int r = 0; r < 8; r++)
+            ss += col[c][r] * col[c][r];
+        double n = sqrt(ss);
+        if (!(n > 0.0) || !isfinite(n))
+            return -1;
+        for (int r = 0; r < 8; r++)
+            col[c][r] /= n;
+    }
+    for (int r = 0; r < 8; r++)
+        for (int c = 0; c < 8; c++)
+            Q[8 * r + c] = col[c][r];
+    if (orc_det8(Q) < 0.0)
+        for (int r = 0; r < 8; r++)
+            Q[8 * r] = -Q[8 * r];
+    return 0;
+}
+
+/* y = Q v for one 8-D block (64 multiplications, counted). */
+void orc_block8_forward(const double G[64], const double v[8], double out[8])
+{
+    double Q[64];
+    if (orc_orthonormalize8(G, Q) != 0) {
+        for (int r = 0; r < 8; r++)
+            out[r] = NAN;
+        return;
+    }
+    for (int r = 0; r < 8; r++) {
+        double acc = 0.0;
+        for (int c = 0; c < 8; c++)
+            acc += cmul(Q[8 * r + c], v[c]);
+        out[r] = acc;
+    }
+}
+
+/* v = Q^T y, the inverse of a block rotation (Q is orthogonal). */
+void orc_block8_inverse(const double G[64], const double y[8], double out[8])
+{
+    double Q[64];
+    if (orc_orthonormalize8(G, Q) != 0) {
+        for (int c = 0; c < 8; c++)
+            out[c] = NAN;
+        return;
+    }
+    for (int c = 0; c < 8; c++) {
+        double acc = 0.0;
+        for (int r = 0; r < 8; r++)
+            acc += cmul(Q[8 * r + c], y[r]);
+        out[c] = acc;
+    }
+}
+
+/* ---------------------------------------------------------------------------
  * Scalar Lloyd-Max quantizer Q (Sec. 1 and 7.2 name it; fit procedure is the
  * reading stated in the header).
  * ------------------------------------------------------------------------- */
@@ -237,29 +359,32 @@ static int quantize_index(int bits, const double *thr, double y)
  * Geometry of the partition (Sec. 4.1, Sec. 5.1, Sec. 6).
  * ------------------------------------------------------------------------- */
 
-/* number of local blocks: g4 = ceil(d/4) for Full/Fast, g2 = ceil(d/2) for 2-D */
+/* number of local blocks: g4 = ceil(d/4) for Full/Fast, g2 = ceil(d/2) for 2-D,
+ * g8 = ceil(d/8) for 8-D blocks */
 int orc_num_blocks(int variant, int d)
 {
-    return variant == ORC_PLANAR2D ? (d + 1) / 2 : (d + 3) / 4;
+    return variant == ORC_PLANAR2D ? (d + 1) / 2 : variant == ORC_BLOCK8 ? (d + 7) / 8 : (d + 3) / 4;
 }
 
-/* raw parameters per set: Full 8 g4 (u_L, u_R), Fast 4 g4 (u_L), 2-D g2 angles */
+/* raw parameters per set: Full 8 g4 (u_L, u_R), Fast 4 g4 (u_L), 2-D g2 angles,
+ * 8-D 64 g8 (one raw 8x8 matrix per block) */
 int orc_raw_params_per_set(int variant, int d)
 {
     int g = orc_num_blocks(variant, d);
-    return variant == ORC_FULL ? 8 * g : variant == ORC_FAST ? 4 * g : g;
+    return variant == ORC_FULL ? 8 * g : variant == ORC_FAST ? 4 * g : variant == ORC_BLOCK8 ? 64 * g : g;
 }
 
-/* rotation parameters counted as in Table 1: 8 g4 / 4 g4 / 2 g2 (cos, sin) */
+/* rotation parameters counted as in Table 1: 8 g4 / 4 g4 / 2 g2 (cos, sin);
+ * 8-D blocks (not in Table 1) store their 64 matrix entries per block */
 int orc_table1_params(int variant, int d)
 {
     int g = orc_num_blocks(variant, d);
-    return variant == ORC_FULL ? 8 * g : variant == ORC_FAST ? 4 * g : 2 * g;
+    return variant == ORC_FULL ? 8 * g : variant == ORC_FAST ? 4 * g : variant == ORC_BLOCK8 ? 64 * g : 2 * g;
 }
 
 /* ---------------------------------------------------------------------------
  * Encoder / decoder transforms on a whole normalised vector (Sec. 5.1: the
- * block-diagonal element of (SO(4))^g, or of (SO(2))^g2, applied block by
+ * block-diagonal element of (SO(4))^g, of (SO(2))^g2 or of (SO(8))^g8, applied block by
  * block on the zero-padded vector).  `pad` holds blk*g coordinates.
  * ------------------------------------------------------------------------- */
 static void block_forward(int variant, const double *rot, int i, const double *vin, double *vout)
@@ -273,6 +398,8 @@ static void block_forward(int variant, const double *rot, int i, const double *v
         double qL[4];
         orc_qnormalize(rot + 4 * i, qL);
         orc_fast_forward(qL, vin, vout);
+    } else if (variant == ORC_BLOCK8) {
+        orc_block8_forward(rot + 64 * i, vin, vout);
     } else {
         orc_planar_forward(rot[i], vin, vout);
     }
@@ -289,12 +416,14 @@ static void block_inverse(int variant, const double *rot, int i, const double *v
         double qL[4];
         orc_qnormalize(rot + 4 * i, qL);
         orc_fast_inverse(qL, vin, vout);
+    } else if (variant == ORC_BLOCK8) {
+        orc_block8_inverse(rot + 64 * i, vin, vout);
     } else {
         orc_planar_inverse(rot[i], vin, vout);
     }
 }
 
-static int block_width(int variant) { return variant == ORC_PLANAR2D ? 2 : 4; }
+static int block_width(int variant) { return variant == ORC_PLANAR2D ? 2 : variant == ORC_BLOCK8 ? 8 : 4; }
 
 /*
  * Encoder E on one normalised vector: out[0 .. blk*g) = blockwise rotation of
@@ -304,7 +433,7 @@ void orc_encode(int variant, int d, const double *rot, const double *xbar, doubl
 {
     int blk = block_width(variant), g = orc_num_blocks(variant, d);
     for (int i = 0; i < g; i++) {
-        double v[4] = {0, 0, 0, 0};
+        double v[8] = {0, 0, 0, 0, 0, 0, 0, 0};
         for (int c = 0; c < blk; c++)
             v[c] = (blk * i + c < d) ? xbar[blk * i + c] : 0.0;
         block_forward(variant, rot, i, v, out + blk * i);
@@ -316,7 +445,7 @@ void orc_decode(int variant, int d, const double *rot, const double *yhat, doubl
 {
     int blk = block_width(variant), g = orc_num_blocks(variant, d);
     for (int i = 0; i < g; i++) {
-        double r[4];
+        double r[8];
         block_inverse(variant, rot, i, yhat + blk * i, r);
         for (int c = 0; c < blk; c++)
             if (blk * i + c < d)
@@ -344,7 +473,7 @@ static int64_t set_of_row(int64_t row, int n_sets, int64_t rows_per_set)
  * ------------------------------------------------------------------------- */
 static int stage1_args_ok(int variant, int d, int bits, int n_sets, int64_t rows_per_set)
 {
-    return !(variant < 0 || variant > 2 || d < 1 || d > 4096 || bits < 1 || bits > 8 || n_sets < 1 ||
+    return !(variant < 0 || variant > 3 || d < 1 || d > 4096 || bits < 1 || bits > 8 || n_sets < 1 ||
              (n_sets > 1 && rows_per_set < 1));
 }
 

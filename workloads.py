@@ -2,7 +2,8 @@
 
 This module holds random draws and input recipes only, none of the method's
 arithmetic: it produces raw (unnormalised) quaternion draws u ~ N(0, I_4),
-raw planar angles theta ~ U[0, 2 pi), and unit-norm Gaussian input rows.  Both
+raw planar angles theta ~ U[0, 2 pi), raw 8x8 Gaussian matrices for 8-D
+blocks (not orthonormalised), and unit-norm Gaussian input rows.  Both
 the oracle and the HIP library normalise and use the draws on their own.
 
 Rotation draws use Philox4x32-10 (Salmon, Moraes, Dror and Shaw, "Parallel
@@ -12,7 +13,9 @@ initialisation implements the same definition independently):
 
     key     = (seed mod 2^32, seed div 2^32)
     counter = (block, set, stream, 0), stream 0 = u_L, 1 = u_R, 2 = angle
-              (and (column group, row, 3, 0) for the stage-2 projection)
+              (and (column group, row, 3, 0) for the stage-2 projection,
+              (block, set, 4, q) for entries 4q .. 4q + 3 of the raw
+              row-major 8x8 matrix of an 8-D block, q = 0 .. 15)
     u       = (z0, z1, z2, z3) with (z0, z1) = BM(w0, w1), (z2, z3) = BM(w2, w3)
     BM(a, b) = sqrt(-2 ln U1) * (cos 2 pi U2, sin 2 pi U2),
                U1 = (a + 0.5) / 2^32, U2 = b / 2^32
@@ -31,8 +34,8 @@ PHILOX_W0 = 0x9E3779B9
 PHILOX_W1 = 0xBB67AE85
 _MASK32 = np.uint64(0xFFFFFFFF)
 
-FULL, FAST, PLANAR2D = 0, 1, 2
-_VARIANTS = {"full": FULL, "fast": FAST, "2d": PLANAR2D}
+FULL, FAST, PLANAR2D, BLOCK8 = 0, 1, 2, 3
+_VARIANTS = {"full": FULL, "fast": FAST, "2d": PLANAR2D, "8d": BLOCK8}
 
 
 def variant_id(v) -> int:
@@ -71,10 +74,12 @@ def _box_muller(a, b):
     return r * np.cos(2.0 * np.pi * u2), r * np.sin(2.0 * np.pi * u2)
 
 
-def philox_gaussian4(blocks, sets, stream, seed):
-    """Four N(0,1) draws per (block, set) counter: array [..., 4] float64."""
-    blocks, sets = np.broadcast_arrays(np.asarray(blocks, np.uint64), np.asarray(sets, np.uint64))
-    ctr = np.stack([blocks, sets, np.full_like(blocks, stream), np.zeros_like(blocks)], axis=-1)
+def philox_gaussian4(blocks, sets, stream, seed, word3=0):
+    """Four N(0,1) draws per counter (block, set, stream, word3): array [..., 4]
+    float64."""
+    blocks, sets, word3 = np.broadcast_arrays(np.asarray(blocks, np.uint64), np.asarray(sets, np.uint64),
+                                              np.asarray(word3, np.uint64))
+    ctr = np.stack([blocks, sets, np.full_like(blocks, stream), word3], axis=-1)
     w = philox4x32_10(ctr, _key(seed))
     z0, z1 = _box_muller(w[..., 0], w[..., 1])
     z2, z3 = _box_muller(w[..., 2], w[..., 3])
@@ -85,6 +90,8 @@ def raw_params_per_set(variant, d: int) -> int:
     v = variant_id(variant)
     if v == PLANAR2D:
         return (d + 1) // 2
+    if v == BLOCK8:
+        return 64 * ((d + 7) // 8)
     g = (d + 3) // 4
     return 8 * g if v == FULL else 4 * g
 
@@ -93,9 +100,14 @@ def rotation_draws(variant, d: int, n_sets: int = 1, seed: int = 1) -> np.ndarra
     """Raw rotation draws, flat float64 array [n_sets * raw_params_per_set].
 
     Full: per set, per block i: (u_L[0..3], u_R[0..3]); Fast: u_L[0..3];
-    2-D: one angle theta per coordinate pair.
+    2-D: one angle theta per coordinate pair; 8-D: per set, per block of 8
+    coordinates, a raw 8x8 N(0, 1) matrix, row-major.
     """
     v = variant_id(variant)
+    if v == BLOCK8:
+        g8 = (d + 7) // 8
+        s, b, q = np.meshgrid(np.arange(n_sets), np.arange(g8), np.arange(16), indexing="ij")
+        return philox_gaussian4(b, s, 4, seed, q).reshape(-1)   # [n_sets, g8, 16 x 4]
     if v == PLANAR2D:
         g2 = (d + 1) // 2
         b, s = np.meshgrid(np.arange(g2), np.arange(n_sets))
