@@ -5,8 +5,9 @@
  * IsoQuant (arXiv 2603.28430) compresses a d-dimensional vector x in four
  * steps (Algorithm 1): split off the norm rho = ||x|| (Sec. 3); rotate the
  * direction block by block, with 4-D quaternion blocks v -> q_L v conj(q_R)
- * (IsoQuant-Full, Sec. 5.2), v -> q_L v (IsoQuant-Fast, Sec. 5.3) or 2-D
- * planar rotations (Sec. 5.4); quantize every rotated coordinate with one
+ * (IsoQuant-Full, Sec. 5.2), v -> q_L v (IsoQuant-Fast, Sec. 5.3), 2-D
+ * planar rotations (Sec. 5.4) or 8-D grouped blocks (Table 3's block-size
+ * axis, Haar(SO(8)) blocks as in Sec. 5.7); quantize every rotated coordinate with one
  * shared b-bit Lloyd-Max codebook; then dequantize, rotate back and multiply
  * by rho.
  *
@@ -14,7 +15,8 @@
  *   - Status codes are returned, never exceptions.  Arguments are validated
  *     before any device work; a call that returns an error launched nothing.
  *   - Rows are contiguous, row-major [n][d].  Coordinate 4i of a row is the
- *     real part of quaternion block i; the 2-D case pairs (2j, 2j+1).
+ *     real part of quaternion block i; the 2-D case pairs (2j, 2j+1); 8-D
+ *     block i holds coordinates 8i .. 8i+7.
  *   - Device buffers are owned by the caller and must live on the device that
  *     was current at isoq_params_init.  Row buffers (fp16/fp32) must be
  *     16-byte aligned, index records and norm arrays 4-byte aligned.
@@ -33,11 +35,13 @@
  *     for the KV-cache append (and, fp16 rows only, 80, 96, 160 and 192), d in
  *     {64, 80, 96, 128, 160, 192, 256, 512} for the attention-score call
  *     without the sketch, d in {64, 128, 256} for the stage-2 sketch and the
- *     calls that use it.
- *   - Widths that are not a multiple of the block size (4; 2-D: 2) follow
- *     Sec. 5.1: the last block is zero padded, all pw rotated coordinates are
- *     quantized and stored (pw = 4 ceil(d/4); 2-D: 2 ceil(d/2)), and the
- *     padded coordinates are dropped after the inverse rotation.
+ *     calls that use it (Full, Fast and 2-D handles; every other call takes
+ *     all four variants).
+ *   - Widths that are not a multiple of the block size (4; 2-D: 2; 8-D: 8)
+ *     follow Sec. 5.1: the last block is zero padded, all pw rotated
+ *     coordinates are quantized and stored (pw = 4 ceil(d/4); 2-D:
+ *     2 ceil(d/2); 8-D: 8 ceil(d/8)), and the padded coordinates are dropped
+ *     after the inverse rotation.
  *   - Rows must be finite.  The squared norm is accumulated in fp32, so an
  *     fp32 row must have 1e-18 <= ||x|| <= 1e18 or be exactly zero (every fp16
  *     row qualifies); a zero row gives rho = 0, x_hat = 0 and every index
@@ -64,8 +68,9 @@ typedef enum isoq_status {
     ISOQ_E_DEVICE = 7       /* called with a device other than the handle's            */
 } isoq_status;
 
-/* variants (Sec. 5.2, 5.3, 5.4) */
-enum { ISOQ_FULL = 0, ISOQ_FAST = 1, ISOQ_PLANAR2D = 2 };
+/* variants (Sec. 5.2, 5.3, 5.4; ISOQ_BLOCK8: 8-D grouped blocks, Table 3 and
+ * Sec. 5.7) */
+enum { ISOQ_FULL = 0, ISOQ_FAST = 1, ISOQ_PLANAR2D = 2, ISOQ_BLOCK8 = 3 };
 /* row element types */
 enum { ISOQ_F32 = 0, ISOQ_F16 = 1 };
 
@@ -75,7 +80,7 @@ typedef struct isoq_params isoq_params;
  * isoq_params_init -- build the rotation parameters and the codebook of one
  * quantizer and copy them to the current device.
  *
- *   variant   ISOQ_FULL, ISOQ_FAST or ISOQ_PLANAR2D.
+ *   variant   ISOQ_FULL, ISOQ_FAST, ISOQ_PLANAR2D or ISOQ_BLOCK8.
  *   d, bits   vector width and bits per coordinate.
  *   n_sets    number of independent rotation sets (e.g. one per attention
  *             head); row r of a later call uses set (r / rows_per_set) mod
@@ -84,12 +89,17 @@ typedef struct isoq_params isoq_params;
  *             vectors normalised on the fly), n_sets * isoq_raw_params_per_set
  *             doubles: Full, per set and block i, u_L[4] then u_R[4]; Fast,
  *             u_L[4] per block; 2-D, one angle theta (radians) per coordinate
- *             pair.  Quaternions are normalised here (u / ||u||); a zero u is
- *             ISOQ_E_INVALID.
+ *             pair; 8-D, a raw 8x8 matrix G per block of 8 coordinates
+ *             (row-major).  Quaternions are normalised here (u / ||u||); a zero
+ *             u is ISOQ_E_INVALID.  An 8-D block rotates by the orthogonal
+ *             factor Q of G = QR with a positive diagonal in R (Haar on O(8)
+ *             for Gaussian G), with column 0 negated when det Q = -1 (so Q is
+ *             in SO(8)); G with dependent columns is ISOQ_E_INVALID.
  *             NULL: draw them from `seed` (Haar sampling, Sec. 5.5): u ~ N(0,I4)
  *             and theta ~ U[0, 2 pi) from Philox4x32-10 with key = seed and
  *             counter (block, set, stream, 0), stream 0 for u_L, 1 for u_R, 2 for
- *             theta; Box-Muller maps the four 32-bit words (w0..w3) to
+ *             theta (8-D: G ~ N(0,1) entries 4q .. 4q+3 from counter
+ *             (block, set, 4, q), q = 0..15); Box-Muller maps the four 32-bit words (w0..w3) to
  *             (z0, z1) = sqrt(-2 ln U1) (cos 2 pi U2, sin 2 pi U2) with
  *             U1 = (w0 + 1/2) / 2^32, U2 = w1 / 2^32, likewise (z2, z3) from
  *             (w2, w3); theta = 2 pi w0 / 2^32.
@@ -98,8 +108,11 @@ typedef struct isoq_params isoq_params;
  *             then symmetrised exactly).  NULL: Lloyd-Max levels for N(0, 1/d)
  *             after 200 Lloyd iterations from levels evenly spaced on
  *             [-3/sqrt(d), 3/sqrt(d)].  Decision thresholds are the midpoints
- *             of adjacent levels; a value equal to a threshold goes to the
- *             lower level.
+ *             of adjacent levels.  The kernels take the sign of a rotated
+ *             value y (y > 0) and compare |y| with the positive thresholds
+ *             (|y| > t), so a value exactly on a threshold goes to the level
+ *             of smaller magnitude: the lower level for y > 0, the upper one
+ *             for y < 0 (0 itself goes to level 2^(bits-1) - 1).
  *   out       receives the handle (set to NULL on error).
  * Host arrays are only read during the call; the caller keeps ownership.
  */
@@ -116,8 +129,10 @@ isoq_status isoq_params_destroy(isoq_params *p);
  * output may be NULL.
  *   rot_out        n_sets * isoq_export_params_per_set floats: Full, per
  *                  block q_L[4] then q_R[4] (unit); Fast q_L[4]; 2-D
- *                  (cos theta, sin theta) per pair.  These are the parameter
- *                  counts of Table 1 (8 g4, 4 g4, 2 g2 per set).
+ *                  (cos theta, sin theta) per pair; 8-D the block's
+ *                  orthogonal Q (64 floats, row-major).  These are the
+ *                  parameter counts of Table 1 (8 g4, 4 g4, 2 g2 per set;
+ *                  8-D, not in Table 1: 64 g8).
  *   levels_out     2^bits levels, ascending.
  *   thresholds_out 2^bits - 1 decision thresholds, ascending.
  */

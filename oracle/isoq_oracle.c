@@ -208,14 +208,23 @@ double orc_det8(const double M[64])
  * the earlier ones, a second pass removing what rounding left, then is scaled
  * to unit length); then det Q = +1 by negating column 0 when it is -1.
  * Q is written row-major.  Returns 0, or -1 when the columns are linearly
- * dependent.
+ * dependent (a column left with less than 1e-12 of G's largest column norm
+ * after the projections: rounding leaves that in place of 0).
  */
 int orc_orthonormalize8(const double G[64], double Q[64])
 {
     double col[8][8]; /* col[c][r] = entry (r, c) */
+    double cmax = 0.0;
     for (int r = 0; r < 8; r++)
         for (int c = 0; c < 8; c++)
             col[c][r] = G[8 * r + c];
+    for (int c = 0; c < 8; c++) {
+        double ss = 0.0;
+        for (int r = 0; r < 8; r++)
+            ss += col[c][r] * col[c][r];
+        if (sqrt(ss) > cmax)
+            cmax = sqrt(ss);
+    }
     for (int c = 0; c < 8; c++) {
         for (int pass = 0; pass < 2; pass++)
             for (int p = 0; p < c; p++) {
@@ -229,7 +238,7 @@ int orc_orthonormalize8(const double G[64], double Q[64])
         for (int r = 0; r < 8; r++)
             ss += col[c][r] * col[c][r];
         double n = sqrt(ss);
-        if (!(n > 0.0) || !isfinite(n))
+        if (!(n > 1e-12 * cmax) || !isfinite(n))
             return -1;
         for (int r = 0; r < 8; r++)
             col[c][r] /= n;

@@ -3,7 +3,7 @@
 The computation runs in libisoquant.so (HIP kernels behind a C ABI, see
 include/isoquant.h); this package is its Python binding.
 """
-from .isoquant import (ISOQ_F16, ISOQ_F32, ISOQ_FAST, ISOQ_FULL, ISOQ_PLANAR2D, IsoqError,
+from .isoquant import (ISOQ_BLOCK8, ISOQ_F16, ISOQ_F32, ISOQ_FAST, ISOQ_FULL, ISOQ_PLANAR2D, IsoqError,
                        LIB_PATH, Params, isoq_codebook_lloyd, isoq_dequantize,
                        isoq_export_params_per_set, isoq_kv_append, isoq_kv_scores,
                        isoq_packed_bytes, isoq_record_bytes, Sketch, isoq_sketch_init, isoq_sketch_destroy,
@@ -14,7 +14,7 @@ from .isoquant import (ISOQ_F16, ISOQ_F32, ISOQ_FAST, ISOQ_FULL, ISOQ_PLANAR2D, 
                        isoq_status_string)
 
 __all__ = [
-    "ISOQ_F16", "ISOQ_F32", "ISOQ_FAST", "ISOQ_FULL", "ISOQ_PLANAR2D", "IsoqError", "LIB_PATH",
+    "ISOQ_BLOCK8", "ISOQ_F16", "ISOQ_F32", "ISOQ_FAST", "ISOQ_FULL", "ISOQ_PLANAR2D", "IsoqError", "LIB_PATH",
     "Params", "isoq_codebook_lloyd", "isoq_dequantize", "isoq_export_params_per_set", "isoq_kv_append",
     "isoq_kv_scores", "Sketch", "isoq_sketch_init", "isoq_sketch_destroy", "isoq_sketch_export",
     "isoq_quantize_qjl", "isoq_kv_scores_qjl", "isoq_kv_append_qjl",

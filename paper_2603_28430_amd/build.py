@@ -42,9 +42,10 @@ def build(verbose: bool = False) -> str:
     os.makedirs(obj_dir, exist_ok=True)
     inc = [f"-I{INCLUDE}", f"-I{CSRC}"]
     jobs = []
-    for src in ("isoq_kernels.hip", "isoq_scores.hip", "isoq_scores_qjl.hip", "isoq_qjl.hip",
-                "isoq_generic_full.hip", "isoq_generic_fast.hip", "isoq_generic_2d.hip", "isoq_qjl_append.hip",
-                "isoq_packed.hip"):
+    for src in ("isoq_kernels.hip", "isoq_kernels_8d.hip", "isoq_scores.hip", "isoq_scores_8d.hip",
+                "isoq_scores_qjl.hip", "isoq_qjl.hip", "isoq_generic_full.hip", "isoq_generic_fast.hip",
+                "isoq_generic_2d.hip", "isoq_generic_8d.hip", "isoq_qjl_append.hip", "isoq_packed.hip",
+                "isoq_packed_8d.hip"):
         jobs.append([HIPCC, *DEVICE_FLAGS, *inc, "-c", os.path.join(CSRC, src), "-o",
                      os.path.join(obj_dir, src + ".o")])
     for src in ("isoq_api.cpp", "isoq_host_params.cpp"):

@@ -45,7 +45,7 @@ isoq_status hip_fail(hipError_t e, const char *where, isoq_status st = ISOQ_E_HI
     return st;
 }
 
-bool valid_variant(int v) { return v == ISOQ_FULL || v == ISOQ_FAST || v == ISOQ_PLANAR2D; }
+bool valid_variant(int v) { return v == ISOQ_FULL || v == ISOQ_FAST || v == ISOQ_PLANAR2D || v == ISOQ_BLOCK8; }
 // Widths of the tuned kernels (every entry point); other widths up to
 // kGenericMaxD have quantize, dequantize and round trip only.
 bool tuned_d(int d) { return d == 64 || d == 128 || d == 256 || d == 512; }
@@ -115,26 +115,41 @@ isoq_status launch(const void *fn, dim3 grid, void **args, void *stream, int thr
     return ISOQ_OK;
 }
 
+const void *packed_kernel(int variant, int bits, int mode, int chunks)
+{
+    switch (variant) {
+    case VAR_FULL: return packed_kernel_full(bits, mode, chunks);
+    case VAR_FAST: return packed_kernel_fast(bits, mode, chunks);
+    case VAR_PLANAR2D: return packed_kernel_2d(bits, mode, chunks);
+    case VAR_BLOCK8: return packed_kernel_8d(bits, mode, chunks);
+    }
+    return nullptr;
+}
+
 isoq_status run_generic(const isoq_params *p, int dtype, int mode, KArgs &a, void *stream)
 {
-    const int slots = slots_per_set(p->variant, p->d);
+    // the generic kernels' slots: 4 coordinates (a 2-D row of 4k + 2
+    // coordinates ends in a half slot), or 8 for 8-D blocks
+    const int sw = p->variant == VAR_BLOCK8 ? 8 : 4;
+    const int slots = (padded_width(p->variant, p->d) + sw - 1) / sw;
+    if (slots < 1)
+        return ISOQ_E_UNSUPPORTED;
     const bool f16 = dtype == ISOQ_F16;
     const PackedShape ps = packed_shape(p->d, p->bits, f16);
-    const bool pairs = f16 && p->d % 4 == 2;
+    const bool pairs = sw == 4 && f16 && p->d % 4 == 2;
     const int v = ps.rows;
-    const void *fn = v > 0 ? (p->variant == VAR_FULL   ? packed_kernel_full(p->bits, mode, ps.chunks)
-                              : p->variant == VAR_FAST ? packed_kernel_fast(p->bits, mode, ps.chunks)
-                                                       : packed_kernel_2d(p->bits, mode, ps.chunks))
-                     : p->variant == VAR_FULL ? generic_kernel_full(slots, p->bits, f16, mode, pairs)
-                     : p->variant == VAR_FAST ? generic_kernel_fast(slots, p->bits, f16, mode, pairs)
-                                              : generic_kernel_2d(slots, p->bits, f16, mode, pairs);
+    const void *fn = v > 0 ? packed_kernel(p->variant, p->bits, mode, ps.chunks)
+                     : p->variant == VAR_FULL   ? generic_kernel_full(slots, p->bits, f16, mode, pairs)
+                     : p->variant == VAR_FAST   ? generic_kernel_fast(slots, p->bits, f16, mode, pairs)
+                     : p->variant == VAR_BLOCK8 ? generic_kernel_8d(slots, p->bits, f16, mode, pairs)
+                                                : generic_kernel_2d(slots, p->bits, f16, mode, pairs);
     if (!fn)
         return ISOQ_E_UNSUPPORTED;
     // rows per block: packed, tiles of 4 waves of kTileGroups / chunks groups
     // of v rows; generic, 4 waves of their row groups
     const int64_t rpb = v > 0 ? (int64_t)v * (kBlockThreads / 64) * (kTileGroups / ps.chunks) *
                                     packed_tiles_per_block(p->variant, ps.chunks)
-                              : (int64_t)generic_rows_per_wave(slots) * (kBlockThreads / 64);
+                              : (int64_t)generic_rows_per_wave(slots, sw) * (kBlockThreads / 64);
     const int64_t blocks = (a.n + rpb - 1) / rpb;
     if (blocks > 0x7FFFFFFF)
         return ISOQ_E_UNSUPPORTED;
@@ -143,10 +158,10 @@ isoq_status run_generic(const isoq_params *p, int dtype, int mode, KArgs &a, voi
     a.g_pw = padded_width(p->variant, p->d);
     a.g_slots = slots;
     a.g_rec = (int32_t)record_bytes(p->variant, p->d, p->bits);
-    a.g_vec = p->d % 4 == 0;
+    a.g_vec = p->d % sw == 0;
     a.g_rows = v;
     a.g_block_set = p->n_sets == 1 || (v > 0 && a.rows_per_set % rpb == 0);
-    a.g_set_stride = (int64_t)slots * params_per_slot(p->variant);
+    a.g_set_stride = (int64_t)slots_per_set(p->variant, p->d) * params_per_slot(p->variant);
     void *args[] = {&a};
     return launch(fn, dim3((unsigned)blocks), args, stream);
 }
@@ -516,9 +531,7 @@ isoq_status isoq_kv_append(const isoq_params *pk, const isoq_params *pv, int dty
         return st;
     // one kernel for both tensors; block (x, y, z) = (head, token range, K|V)
     const void *fn = !packed ? kernel_for(pk->variant, pk->d, pk->bits, dtype == ISOQ_F16, false, MODE_APPEND)
-                     : pk->variant == VAR_FULL ? packed_kernel_full(pk->bits, MODE_APPEND, ps.chunks)
-                     : pk->variant == VAR_FAST ? packed_kernel_fast(pk->bits, MODE_APPEND, ps.chunks)
-                                               : packed_kernel_2d(pk->bits, MODE_APPEND, ps.chunks);
+                             : packed_kernel(pk->variant, pk->bits, MODE_APPEND, ps.chunks);
     if (!fn)
         return ISOQ_E_UNSUPPORTED;
     // tokens per block: 4 waves of kTileGroups (packed: kTileGroups / chunks)
@@ -688,7 +701,8 @@ isoq_status isoq_sketch_init(isoq_sketch **out, const isoq_params *p, int m, con
         return ISOQ_E_NULL;
     if (m < 1)
         return ISOQ_E_INVALID;
-    if (!(((p->d == 64 || p->d == 128) && (m == 64 || m == 128)) || (p->d == 256 && m == 64)))
+    if (!(((p->d == 64 || p->d == 128) && (m == 64 || m == 128)) || (p->d == 256 && m == 64)) ||
+        p->variant == VAR_BLOCK8)
         return ISOQ_E_UNSUPPORTED;
     const int d = p->d;
     std::vector<double> S((size_t)m * d), Sp((size_t)m * d);

@@ -193,9 +193,15 @@ __device__ __forceinline__ void store_row_chunk(char *p, const float o[8], int s
 //
 // A slot is 4 consecutive coordinates: one quaternion block, or two planar
 // pairs.  Its parameters: Full the 16 floats of M (row-major), Fast q_L,
-// 2-D (cos, sin) of each pair.
+// 2-D (cos, sin) of each pair.  8-D blocks (VAR_BLOCK8) rotate a lane's 8
+// coordinates as one block: y = Q v with the block's 8x8 orthogonal matrix Q
+// (64 floats, row-major), inverse v = Q^T y.
 template <int VAR>
 constexpr int kSlotParams = VAR == VAR_FULL ? 16 : 4;
+
+// Parameter floats of a lane's 8 coordinates.
+template <int VAR>
+constexpr int kLanePL = VAR == VAR_FULL ? 32 : VAR == VAR_BLOCK8 ? 64 : 8;
 
 template <int VAR>
 __device__ __forceinline__ void rotate4_forward(const float *P, const float *v, float *y)
@@ -253,19 +259,41 @@ __device__ __forceinline__ void rotate4_inverse(const float *P, const float *y, 
     }
 }
 
-// A lane's 8 coordinates: two slots.
+// A lane's 8 coordinates: two slots, or one 8-D block.
 template <int VAR>
 __device__ __forceinline__ void rotate_forward(const float *P, const float x[8], float y[8])
 {
-    rotate4_forward<VAR>(P, x, y);
-    rotate4_forward<VAR>(P + kSlotParams<VAR>, x + 4, y + 4);
+    if constexpr (VAR == VAR_BLOCK8) {
+#pragma unroll
+        for (int r = 0; r < 8; r++) {
+            float acc = P[8 * r] * x[0];
+#pragma unroll
+            for (int c = 1; c < 8; c++)
+                acc = fmaf(P[8 * r + c], x[c], acc);
+            y[r] = acc;
+        }
+    } else {
+        rotate4_forward<VAR>(P, x, y);
+        rotate4_forward<VAR>(P + kSlotParams<VAR>, x + 4, y + 4);
+    }
 }
 
 template <int VAR>
 __device__ __forceinline__ void rotate_inverse(const float *P, const float y[8], float o[8])
 {
-    rotate4_inverse<VAR>(P, y, o);
-    rotate4_inverse<VAR>(P + kSlotParams<VAR>, y + 4, o + 4);
+    if constexpr (VAR == VAR_BLOCK8) {
+#pragma unroll
+        for (int c = 0; c < 8; c++) {
+            float acc = P[c] * y[0];
+#pragma unroll
+            for (int r = 1; r < 8; r++)
+                acc = fmaf(P[8 * r + c], y[r], acc);
+            o[c] = acc;
+        }
+    } else {
+        rotate4_inverse<VAR>(P, y, o);
+        rotate4_inverse<VAR>(P + kSlotParams<VAR>, y + 4, o + 4);
+    }
 }
 
 template <int PL>

@@ -5,12 +5,13 @@
 // the padded coordinates are dropped after the inverse rotation.
 //
 // Layout.  A row spans G lanes (G = 8 .. 64, a power of two) and lane s of
-// the row owns the 4-coordinate slots s, s + G, ..., s + (BPL - 1) G (a slot
-// is one quaternion block or two planar pairs), so consecutive lanes touch
-// consecutive slots.  A wave holds 64 / G rows per group and walks
-// generic_groups(BPL) groups, issuing every group's loads before computing.  The
-// record of a row is written and read bytewise: slot j's 4b index bits start
-// at bit 4b j.  Rows of a width that is a multiple of 4 move in one 8-byte
+// the row owns the slots s, s + G, ..., s + (BPL - 1) G (a slot is one
+// rotation block: 4 coordinates, a quaternion block or two planar pairs, or 8
+// coordinates for the 8-D blocks), so consecutive lanes touch consecutive
+// slots.  A wave holds 64 / G rows per group and walks
+// generic_groups(BPL, SW) groups, issuing every group's loads before computing.  The
+// record of a row is written and read bytewise: slot j's SW b index bits start
+// at bit SW b j (a whole byte for 8-coordinate slots).  Rows of a width that is a multiple of 4 move in one 8-byte
 // (fp16) or 16-byte (fp32) access per slot; fp16 rows of other even widths in
 // coordinate pairs (4-byte accesses: such a row starts on a 4-byte boundary,
 // PAIRS instantiations); the rest element by element.
@@ -24,41 +25,45 @@ namespace isoq {
 namespace {
 
 typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x8 __attribute__((ext_vector_type(8)));
 
-// A slot as loaded: 4 fp16 (kept packed until computed, two registers) or
-// 4 fp32 values.
-template <bool F16>
-using GenRaw = std::conditional_t<F16, f16x4, float4>;
+// Coordinates per slot: one rotation block (two planar pairs for 2-D).
+template <int VAR>
+constexpr int kGenSW = VAR == VAR_BLOCK8 ? 8 : 4;
 
-template <bool F16>
-__device__ __forceinline__ GenRaw<F16> gen_zero()
+// A slot as loaded: SW fp16 values (kept packed until computed) or SW fp32
+// values.
+template <bool F16, int SW>
+using GenRaw = std::conditional_t<F16, std::conditional_t<SW == 8, f16x8, f16x4>,
+                                  std::conditional_t<SW == 8, f32x8, f32x4>>;
+
+template <bool F16, int SW>
+__device__ __forceinline__ GenRaw<F16, SW> gen_zero()
 {
-    if constexpr (F16)
-        return f16x4{(_Float16)0.f, (_Float16)0.f, (_Float16)0.f, (_Float16)0.f};
-    else
-        return make_float4(0.f, 0.f, 0.f, 0.f);
+    GenRaw<F16, SW> v;
+#pragma unroll
+    for (int c = 0; c < SW; c++)
+        v[c] = 0;
+    return v;
 }
 
-template <bool F16>
-__device__ __forceinline__ GenRaw<F16> gen_load(const char *row, int j, int d, bool vec)
+// Slot j of a row: one vector access when the row's width is a multiple of
+// the slot width (vec), element by element (zero past d) otherwise.
+template <bool F16, int SW>
+__device__ __forceinline__ GenRaw<F16, SW> gen_load(const char *row, int j, int d, bool vec)
 {
     using T = std::conditional_t<F16, _Float16, float>;
     if (vec)
-        return *reinterpret_cast<const GenRaw<F16> *>(row + 4 * sizeof(T) * j);
-    GenRaw<F16> v = gen_zero<F16>();
+        return *reinterpret_cast<const GenRaw<F16, SW> *>(row + SW * sizeof(T) * j);
+    GenRaw<F16, SW> v = gen_zero<F16, SW>();
     const T *e = reinterpret_cast<const T *>(row);
-    const int i = 4 * j;
-    if constexpr (F16) {
-        if (i < d) v[0] = e[i];
-        if (i + 1 < d) v[1] = e[i + 1];
-        if (i + 2 < d) v[2] = e[i + 2];
-        if (i + 3 < d) v[3] = e[i + 3];
-    } else {
-        if (i < d) v.x = e[i];
-        if (i + 1 < d) v.y = e[i + 1];
-        if (i + 2 < d) v.z = e[i + 2];
-        if (i + 3 < d) v.w = e[i + 3];
-    }
+    const int i = SW * j;
+#pragma unroll
+    for (int c = 0; c < SW; c++)
+        if (i + c < d)
+            v[c] = e[i + c];
     return v;
 }
 
@@ -80,36 +85,29 @@ __device__ __forceinline__ void gen_store_pairs(char *row, int j, int d, const f
         q[1] = f16x2{(_Float16)o[2], (_Float16)o[3]};
 }
 
-template <bool F16>
-__device__ __forceinline__ void gen_unpack(const GenRaw<F16> &r, float v[4])
+template <bool F16, int SW>
+__device__ __forceinline__ void gen_unpack(const GenRaw<F16, SW> &r, float v[SW])
 {
-    if constexpr (F16) {
 #pragma unroll
-        for (int c = 0; c < 4; c++)
-            v[c] = (float)r[c];
-    } else {
-        v[0] = r.x;
-        v[1] = r.y;
-        v[2] = r.z;
-        v[3] = r.w;
-    }
+    for (int c = 0; c < SW; c++)
+        v[c] = (float)r[c];
 }
 
-template <bool F16>
-__device__ __forceinline__ void gen_store(char *row, int j, int d, bool vec, const float o[4])
+template <bool F16, int SW>
+__device__ __forceinline__ void gen_store(char *row, int j, int d, bool vec, const float o[SW])
 {
+    using T = std::conditional_t<F16, _Float16, float>;
     if (vec) {
-        if constexpr (F16) {
-            const f16x4 h = {(_Float16)o[0], (_Float16)o[1], (_Float16)o[2], (_Float16)o[3]};
-            *reinterpret_cast<f16x4 *>(row + 8 * j) = h;
-        } else {
-            *reinterpret_cast<float4 *>(row + 16 * j) = make_float4(o[0], o[1], o[2], o[3]);
-        }
+        GenRaw<F16, SW> h;
+#pragma unroll
+        for (int c = 0; c < SW; c++)
+            h[c] = (T)o[c];
+        *reinterpret_cast<GenRaw<F16, SW> *>(row + SW * sizeof(T) * j) = h;
         return;
     }
 #pragma unroll
-    for (int c = 0; c < 4; c++) {
-        const int i = 4 * j + c;
+    for (int c = 0; c < SW; c++) {
+        const int i = SW * j + c;
         if (i < d) {
             if constexpr (F16)
                 reinterpret_cast<_Float16 *>(row)[i] = (_Float16)o[c];
@@ -157,13 +155,41 @@ __device__ __forceinline__ void gen_write_slot(uint8_t *rec, int j, int nb, uint
     }
 }
 
+// 8-coordinate slots (8-D blocks): slot j's 8 b bits are bytes [b j, b j + b)
+// of the record, so every slot owns whole bytes.
+template <int BITS>
+__device__ __forceinline__ uint32_t gen_read_slot8(const uint8_t *rec, int j)
+{
+    if constexpr (BITS == 2)
+        return reinterpret_cast<const uint16_t *>(rec)[j];
+    else if constexpr (BITS == 4)
+        return reinterpret_cast<const uint32_t *>(rec)[j];
+    else
+        return (uint32_t)rec[3 * j] | ((uint32_t)rec[3 * j + 1] << 8) | ((uint32_t)rec[3 * j + 2] << 16);
+}
+
+template <int BITS>
+__device__ __forceinline__ void gen_write_slot8(uint8_t *rec, int j, uint32_t p)
+{
+    if constexpr (BITS == 2) {
+        reinterpret_cast<uint16_t *>(rec)[j] = (uint16_t)p;
+    } else if constexpr (BITS == 4) {
+        reinterpret_cast<uint32_t *>(rec)[j] = p;
+    } else {
+        rec[3 * j] = (uint8_t)p;
+        rec[3 * j + 1] = (uint8_t)(p >> 8);
+        rec[3 * j + 2] = (uint8_t)(p >> 16);
+    }
+}
+
 template <int VAR, int BITS, bool F16, int MODE, int G, int BPL, bool PAIRS>
 __global__ __launch_bounds__(kBlockThreads) void generic_kernel(const KArgs a)
 {
-    static_assert(!PAIRS || F16, "pair accesses are for fp16 rows");
+    constexpr int SW = kGenSW<VAR>;          // coordinates per slot
+    static_assert(!PAIRS || (F16 && SW == 4), "pair accesses are for fp16 rows of 4-coordinate slots");
     constexpr int R = 64 / G;                // rows per wave and group
-    constexpr int kGenGroups = generic_groups(BPL);
-    constexpr int PS = kSlotParams<VAR>;
+    constexpr int kGenGroups = generic_groups(BPL, SW);
+    constexpr int PS = SW == 8 ? 64 : kSlotParams<VAR>;
     constexpr int H = 1 << (BITS - 1);
     constexpr int ESZ = F16 ? 2 : 4;
     constexpr bool kLoadX = MODE != MODE_DEQUANTIZE;
@@ -195,7 +221,7 @@ __global__ __launch_bounds__(kBlockThreads) void generic_kernel(const KArgs a)
     const int64_t xstep = (int64_t)R * row_bytes, rstep = (int64_t)R * nb;
 
     // ---- loads of every group first
-    GenRaw<F16> xr[kLoadX ? kGenGroups : 1][BPL];
+    GenRaw<F16, SW> xr[kLoadX ? kGenGroups : 1][BPL];
     uint32_t pin[kLoadX ? 1 : kGenGroups][BPL];
     float rin[kLoadX ? 1 : kGenGroups];
 #pragma unroll
@@ -208,9 +234,11 @@ __global__ __launch_bounds__(kBlockThreads) void generic_kernel(const KArgs a)
             const bool on = ok && j < slots;
             if constexpr (kLoadX) {
                 if constexpr (PAIRS)
-                    xr[t][k] = on ? gen_load_pairs(x0 + t * xstep, j, d) : gen_zero<F16>();
+                    xr[t][k] = on ? gen_load_pairs(x0 + t * xstep, j, d) : gen_zero<F16, SW>();
                 else
-                    xr[t][k] = on ? gen_load<F16>(x0 + t * xstep, j, d, vec) : gen_zero<F16>();
+                    xr[t][k] = on ? gen_load<F16, SW>(x0 + t * xstep, j, d, vec) : gen_zero<F16, SW>();
+            } else if constexpr (SW == 8) {
+                pin[t][k] = on ? gen_read_slot8<BITS>(ri0 + t * rstep, j) : 0u;
             } else {
                 pin[t][k] = on ? gen_read_slot<BITS>(ri0 + t * rstep, j, nb) : 0u;
             }
@@ -242,17 +270,17 @@ __global__ __launch_bounds__(kBlockThreads) void generic_kernel(const KArgs a)
             if (set != pset)
                 load_set(set);
         }
-        float yq[BPL][4];
+        float yq[BPL][SW];
         uint32_t pk[BPL];
         float rho;
         if constexpr (kLoadX) {
-            float xv[BPL][4];
+            float xv[BPL][SW];
             float s = 0.f;
 #pragma unroll
             for (int k = 0; k < BPL; k++) {
-                gen_unpack<F16>(xr[t][k], xv[k]);
+                gen_unpack<F16, SW>(xr[t][k], xv[k]);
 #pragma unroll
-                for (int c = 0; c < 4; c++)
+                for (int c = 0; c < SW; c++)
                     s = fmaf(xv[k][c], xv[k][c], s);
             }
             rho = __builtin_amdgcn_sqrtf(row_sum<G>(s));
@@ -270,11 +298,14 @@ __global__ __launch_bounds__(kBlockThreads) void generic_kernel(const KArgs a)
 #pragma unroll
             for (int k = 0; k < BPL; k++) {
                 const int j = sub + G * k;
-                float y[4];
-                rotate4_forward<VAR>(P[k], xv[k], y);
+                float y[SW];
+                if constexpr (SW == 8)
+                    rotate_forward<VAR>(P[k], xv[k], y);
+                else
+                    rotate4_forward<VAR>(P[k], xv[k], y);
                 uint32_t p = 0;
 #pragma unroll
-                for (int c = 0; c < 4; c++) {
+                for (int c = 0; c < SW; c++) {
                     const float m = fabsf(y[c]);
                     float L = lvs[0];
                     uint32_t cnt = 0;
@@ -299,18 +330,23 @@ __global__ __launch_bounds__(kBlockThreads) void generic_kernel(const KArgs a)
 #pragma unroll
             for (int k = 0; k < BPL; k++)
 #pragma unroll
-                for (int c = 0; c < 4; c++)
+                for (int c = 0; c < SW; c++)
                     yq[k][c] = lev_s[(pin[t][k] >> (BITS * c)) & (2 * H - 1)] * rho;
         }
 
         if constexpr (MODE == MODE_QUANTIZE) {
 #pragma unroll
             for (int k = 0; k < BPL; k++) {
-                // the next slot of an even slot sits on the next lane (G is even)
-                const uint32_t next = BITS == 3 ? (uint32_t)__shfl_down((int)pk[k], 1, 64) : 0u;
                 const int j = sub + G * k;
-                if (ok && j < slots)
-                    gen_write_slot<BITS>(ro0 + t * rstep, j, nb, pk[k], next);
+                if constexpr (SW == 8) {
+                    if (ok && j < slots)
+                        gen_write_slot8<BITS>(ro0 + t * rstep, j, pk[k]);
+                } else {
+                    // the next slot of an even slot sits on the next lane (G is even)
+                    const uint32_t next = BITS == 3 ? (uint32_t)__shfl_down((int)pk[k], 1, 64) : 0u;
+                    if (ok && j < slots)
+                        gen_write_slot<BITS>(ro0 + t * rstep, j, nb, pk[k], next);
+                }
             }
             if (ok && sub == 0)
                 a.norms_out[row] = rho;
@@ -319,19 +355,22 @@ __global__ __launch_bounds__(kBlockThreads) void generic_kernel(const KArgs a)
             for (int k = 0; k < BPL; k++) {
                 const int j = sub + G * k;
                 if (ok && j < slots) {
-                    float o[4];
-                    rotate4_inverse<VAR>(P[k], yq[k], o);
+                    float o[SW];
+                    if constexpr (SW == 8)
+                        rotate_inverse<VAR>(P[k], yq[k], o);
+                    else
+                        rotate4_inverse<VAR>(P[k], yq[k], o);
                     if constexpr (PAIRS)
                         gen_store_pairs(y0 + t * xstep, j, d, o);
                     else
-                        gen_store<F16>(y0 + t * xstep, j, d, vec, o);
+                        gen_store<F16, SW>(y0 + t * xstep, j, d, vec, o);
                 }
             }
         }
     }
 }
 
-// Row shape for a padded width of `slots` 4-coordinate slots: (G, BPL).
+// Row shape for a padded width of `slots` slots: (G, BPL).
 template <int VAR, int BITS, bool F16, int MODE, bool PAIRS>
 const void *gen_pick_shape(int slots)
 {
@@ -345,8 +384,12 @@ const void *gen_pick_shape(int slots)
         return reinterpret_cast<const void *>(&generic_kernel<VAR, BITS, F16, MODE, 64, 1, PAIRS>);
     if (slots <= 128)
         return reinterpret_cast<const void *>(&generic_kernel<VAR, BITS, F16, MODE, 64, 2, PAIRS>);
-    if (slots <= 256)
-        return reinterpret_cast<const void *>(&generic_kernel<VAR, BITS, F16, MODE, 64, 4, PAIRS>);
+    // four slots per lane only with 4-coordinate slots (8-coordinate slots
+    // of d <= 1024 need at most two)
+    if constexpr (kGenSW<VAR> == 4) {
+        if (slots <= 256)
+            return reinterpret_cast<const void *>(&generic_kernel<VAR, BITS, F16, MODE, 64, 4, PAIRS>);
+    }
     return nullptr;
 }
 
@@ -361,13 +404,17 @@ const void *gen_pick_mode(int slots, int mode)
     return nullptr;
 }
 
-// pairs: fp16 rows of even width 2 mod 4 (coordinate-pair accesses)
+// pairs: fp16 rows of even width 2 mod 4 (coordinate-pair accesses; not for
+// 8-coordinate slots)
 template <int VAR, int BITS>
 const void *gen_pick_dtype(int slots, bool f16, int mode, bool pairs)
 {
     if (!f16)
         return gen_pick_mode<VAR, BITS, false, false>(slots, mode);
-    return pairs ? gen_pick_mode<VAR, BITS, true, true>(slots, mode) : gen_pick_mode<VAR, BITS, true, false>(slots, mode);
+    if constexpr (kGenSW<VAR> == 8)
+        return pairs ? nullptr : gen_pick_mode<VAR, BITS, true, false>(slots, mode);
+    else
+        return pairs ? gen_pick_mode<VAR, BITS, true, true>(slots, mode) : gen_pick_mode<VAR, BITS, true, false>(slots, mode);
 }
 
 template <int VAR>

@@ -64,6 +64,8 @@ size_t raw_per_set(int variant, int d)
 {
     if (variant == VAR_PLANAR2D)
         return (size_t)(d + 1) / 2;
+    if (variant == VAR_BLOCK8)
+        return 64 * ((size_t)(d + 7) / 8);
     const size_t g = (size_t)(d + 3) / 4;
     return variant == VAR_FULL ? 8 * g : 4 * g;
 }
@@ -72,6 +74,8 @@ size_t export_per_set(int variant, int d)
 {
     if (variant == VAR_PLANAR2D)
         return 2 * ((size_t)(d + 1) / 2);
+    if (variant == VAR_BLOCK8)
+        return 64 * ((size_t)(d + 7) / 8);
     const size_t g = (size_t)(d + 3) / 4;
     return variant == VAR_FULL ? 8 * g : 4 * g;
 }
@@ -124,6 +128,21 @@ void seeded_draws(int variant, int d, int n_sets, uint64_t seed, double *out)
             }
         return;
     }
+    if (variant == VAR_BLOCK8) {
+        // raw 8x8 matrix of block i, row-major: entries 4q .. 4q + 3 from
+        // counter (i, set, 4, q)
+        const int g8 = (d + 7) / 8;
+        for (int s = 0; s < n_sets; s++)
+            for (int i = 0; i < g8; i++)
+                for (int q = 0; q < 16; q++) {
+                    uint32_t c[4] = {(uint32_t)i, (uint32_t)s, 4u, (uint32_t)q};
+                    philox4x32_10(c, k0, k1);
+                    normal_pair(c[0], c[1], out + o);
+                    normal_pair(c[2], c[3], out + o + 2);
+                    o += 4;
+                }
+        return;
+    }
     const int g = (d + 3) / 4;
     const int sides = variant == VAR_FULL ? 2 : 1;
     for (int s = 0; s < n_sets; s++)
@@ -157,6 +176,86 @@ bool unit4(const double *u, double q[4])
         q[c] = u[c] / n;
     return true;
 }
+
+// The rotation of an 8-D block from its raw draw G (row-major 8x8): the
+// orthogonal factor Q of G = QR with a positive diagonal in R, by Householder
+// reflections (Golub and Van Loan, Matrix Computations, Sec. 5.2.2): H_k
+// zeroes column k of the working matrix below the diagonal, Q = H_0 ... H_6,
+// then column k of Q is negated wherever R_kk < 0.  det Q is -1 to the power
+// (reflections + negated columns); when it is -1, column 0 is negated once
+// more, which puts Q in SO(8).  False when G's columns are dependent (an R_kk
+// below 1e-12 of G's largest column norm, which rounding leaves in place of 0).
+bool haar_so8(const double *G, double Q[64])
+{
+    double A[8][8], W[8][8], cmax = 0;
+    for (int r = 0; r < 8; r++)
+        for (int c = 0; c < 8; c++) {
+            A[r][c] = G[8 * r + c];
+            W[r][c] = r == c ? 1.0 : 0.0;
+            if (!std::isfinite(A[r][c]))
+                return false;
+        }
+    for (int c = 0; c < 8; c++) {
+        double n = 0;
+        for (int r = 0; r < 8; r++)
+            n += A[r][c] * A[r][c];
+        cmax = std::max(cmax, std::sqrt(n));
+    }
+    if (!(cmax > 0))
+        return false;
+    int flips = 0;
+    for (int k = 0; k < 7; k++) {
+        double nx = 0;
+        for (int r = k; r < 8; r++)
+            nx += A[r][k] * A[r][k];
+        nx = std::sqrt(nx);
+        if (!(nx > 0))
+            return false;
+        // v = x - alpha e_k with alpha = -sign(x_k) ||x|| (no cancellation)
+        const double alpha = A[k][k] >= 0 ? -nx : nx;
+        double v[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+        for (int r = k; r < 8; r++)
+            v[r] = A[r][k];
+        v[k] -= alpha;
+        double vv = 0;
+        for (int r = k; r < 8; r++)
+            vv += v[r] * v[r];
+        // A <- H A on columns k.., W <- W H (W accumulates Q)
+        for (int c = k; c < 8; c++) {
+            double t = 0;
+            for (int r = k; r < 8; r++)
+                t += v[r] * A[r][c];
+            t *= 2.0 / vv;
+            for (int r = k; r < 8; r++)
+                A[r][c] -= t * v[r];
+        }
+        for (int r = 0; r < 8; r++) {
+            double t = 0;
+            for (int c = k; c < 8; c++)
+                t += W[r][c] * v[c];
+            t *= 2.0 / vv;
+            for (int c = k; c < 8; c++)
+                W[r][c] -= t * v[c];
+        }
+        flips++;   // det H_k = -1
+    }
+    for (int k = 0; k < 8; k++) {
+        if (!(std::fabs(A[k][k]) > 1e-12 * cmax) || !std::isfinite(A[k][k]))
+            return false;
+        if (A[k][k] < 0) {
+            for (int r = 0; r < 8; r++)
+                W[r][k] = -W[r][k];
+            flips++;
+        }
+    }
+    if (flips & 1)
+        for (int r = 0; r < 8; r++)
+            W[r][0] = -W[r][0];
+    for (int r = 0; r < 8; r++)
+        for (int c = 0; c < 8; c++)
+            Q[8 * r + c] = W[r][c];
+    return true;
+}
 }  // namespace
 
 void seeded_projection(int m, int d, uint64_t seed, double *out)
@@ -180,6 +279,16 @@ void rotate_rows_forward(int variant, int d, const float *unit_set, const double
     for (int r = 0; r < rows; r++) {
         const double *v = in + (size_t)r * d;
         double *y = out + (size_t)r * d;
+        if (variant == VAR_BLOCK8) {
+            for (int i = 0; i < d / 8; i++)
+                for (int a = 0; a < 8; a++) {
+                    double acc = 0;
+                    for (int c = 0; c < 8; c++)
+                        acc += (double)unit_set[64 * i + 8 * a + c] * v[8 * i + c];
+                    y[8 * i + a] = acc;
+                }
+            continue;
+        }
         if (variant == VAR_PLANAR2D) {
             for (int j = 0; j < d / 2; j++) {
                 const double c = unit_set[2 * j], sn = unit_set[2 * j + 1];
@@ -231,6 +340,20 @@ bool build_rotation(int variant, int d, int n_sets, const double *raw, std::vect
             }
             if (g2 & 1)
                 dv[2 * g2] = 1.f;   // identity for the pair past the padded width
+            continue;
+        }
+        if (variant == VAR_BLOCK8) {
+            // exported and device layouts alike: Q of each block, row-major
+            const int g8 = (d + 7) / 8;
+            for (int i = 0; i < g8; i++) {
+                double Q[64];
+                if (!haar_so8(rs + 64 * i, Q))
+                    return false;
+                for (int k = 0; k < 64; k++) {
+                    ex[64 * i + k] = (float)Q[k];
+                    dv[64 * i + k] = (float)Q[k];
+                }
+            }
             continue;
         }
         const int g = (d + 3) / 4;

@@ -17,7 +17,8 @@ enum Mode {
     MODE_QJL = 4,         // quantize with the stage-2 sketch
     MODE_APPEND_QJL = 5   // both: records, norms, signs and gamma into cache slots
 };
-enum Variant { VAR_FULL = 0, VAR_FAST = 1, VAR_PLANAR2D = 2 };
+// VAR_BLOCK8: 8-D grouped blocks, one 8x8 orthogonal matrix per 8 coordinates
+enum Variant { VAR_FULL = 0, VAR_FAST = 1, VAR_PLANAR2D = 2, VAR_BLOCK8 = 3 };
 
 // Every lane owns 8 consecutive coordinates of a row (two quaternion blocks or
 // four planar pairs), so a row spans d/8 lanes and a wave holds 512/d rows.
@@ -30,14 +31,18 @@ constexpr int kTileGroups = 4;
 
 // Device rotation parameters per lane, in floats: Full keeps the two 4x4
 // matrices M = L(q_L) R(conj q_R) row-major, Fast the two unit quaternions,
-// 2-D (cos, sin) of the four pairs.
-inline int params_per_lane(int variant) { return variant == VAR_FULL ? 32 : 8; }
+// 2-D (cos, sin) of the four pairs, 8-D the block's 8x8 matrix row-major.
+inline int params_per_lane(int variant) { return variant == VAR_FULL ? 32 : variant == VAR_BLOCK8 ? 64 : 8; }
 
-// The same per 4-coordinate slot (one quaternion block or two planar pairs),
-// and the slots of a set: ceil(d/4) for Full and Fast, ceil(ceil(d/2) / 2)
-// for 2-D (an odd pair count leaves an identity pair in the last slot).
-inline int params_per_slot(int variant) { return variant == VAR_FULL ? 16 : 4; }
-inline int padded_width(int variant, int d) { return variant == VAR_PLANAR2D ? 2 * ((d + 1) / 2) : 4 * ((d + 3) / 4); }
+// The same per 4-coordinate slot (one quaternion block, two planar pairs, or
+// half of an 8-D block: its matrix rows 0..3, then rows 4..7), and the slots
+// of a set: ceil(d/4) for Full and Fast, ceil(ceil(d/2) / 2) for 2-D (an odd
+// pair count leaves an identity pair in the last slot), 2 ceil(d/8) for 8-D.
+inline int params_per_slot(int variant) { return variant == VAR_FULL ? 16 : variant == VAR_BLOCK8 ? 32 : 4; }
+inline int padded_width(int variant, int d)
+{
+    return variant == VAR_PLANAR2D ? 2 * ((d + 1) / 2) : variant == VAR_BLOCK8 ? 8 * ((d + 7) / 8) : 4 * ((d + 3) / 4);
+}
 inline int slots_per_set(int variant, int d) { return (padded_width(variant, d) + 3) / 4; }
 
 // Division of 32-bit unsigned integers by a run-time constant d >= 1 through
@@ -131,6 +136,7 @@ struct ScoreKernel {
     size_t dyn_lds;
 };
 ScoreKernel score_kernel_for(int variant, int d, int bits, bool f16, int group);
+ScoreKernel score_kernel_for_block8(int d, int bits, bool f16, int group);
 // The same with the stage-2 residual correction of m sign bits (isoq_scores_qjl.hip).
 ScoreKernel score_qjl_kernel_for(int variant, int d, int bits, bool f16, int group, int m);
 
@@ -138,23 +144,29 @@ ScoreKernel score_qjl_kernel_for(int variant, int d, int bits, bool f16, int gro
 // or nullptr.  Generic set indexing is needed when there is more than one
 // set and rows_per_set is not a multiple of the rows of a block.
 const void *kernel_for(int variant, int d, int bits, bool f16, bool generic_sets, int mode);
-// Stage-1 kernels for the other widths (d = 1 .. 1024) with `slots`
-// 4-coordinate slots per padded row, one per variant (isoq_generic_*.hip);
-// nullptr when no kernel fits.  Rows of one block: 4 waves x kGenRowsPerWave.
+// The same for 8-D blocks (isoq_kernels_8d.hip).
+const void *kernel_for_block8(int d, int bits, bool f16, bool generic_sets, int mode);
+// Stage-1 kernels for the other widths (d = 1 .. 1024) with `slots` slots
+// per padded row (4 coordinates; 8 for 8-D blocks), one per variant
+// (isoq_generic_*.hip); nullptr when no kernel fits.  Rows of one block:
+// 4 waves x generic_rows_per_wave.
 // pairs: fp16 rows whose width is even and not a multiple of 4 move in
 // coordinate pairs (separate instantiations)
 const void *generic_kernel_full(int slots, int bits, bool f16, int mode, bool pairs);
 const void *generic_kernel_fast(int slots, int bits, bool f16, int mode, bool pairs);
 const void *generic_kernel_2d(int slots, int bits, bool f16, int mode, bool pairs);
-// Row shape of the generic kernels for a row of `slots` slots: G lanes per
-// row, BPL slots per lane, and row groups per wave (every group's loads are
-// in flight together: 8 groups of one slot, 4 groups of several).
+const void *generic_kernel_8d(int slots, int bits, bool f16, int mode, bool pairs);
+// Row shape of the generic kernels for a row of `slots` slots of sw
+// coordinates: G lanes per row, BPL slots per lane, and row groups per wave
+// (every group's loads are in flight together: 8 groups of one 4-coordinate
+// slot, 4 groups of several; half as many for 8-coordinate slots, whose 64
+// parameters per slot fill the registers).
 inline int generic_lanes(int slots) { return slots <= 8 ? 8 : slots <= 16 ? 16 : slots <= 32 ? 32 : 64; }
 inline int generic_bpl(int slots) { return slots <= 64 ? 1 : slots <= 128 ? 2 : 4; }
-constexpr int generic_groups(int bpl) { return bpl == 1 ? 8 : 4; }
-inline int generic_rows_per_wave(int slots)
+constexpr int generic_groups(int bpl, int sw) { return (bpl == 1 ? 8 : 4) / (sw == 8 ? 2 : 1); }
+inline int generic_rows_per_wave(int slots, int sw)
 {
-    return generic_groups(generic_bpl(slots)) * (64 / generic_lanes(slots));
+    return generic_groups(generic_bpl(slots), sw) * (64 / generic_lanes(slots));
 }
 constexpr int kGenericMaxD = 1024;
 // Packed-row kernels (isoq_packed.h) for fp16 rows of width d = 16 k up to
@@ -187,12 +199,16 @@ inline PackedShape packed_shape(int d, int bits, bool f16)
     return {v1, 1};
 }
 // Row tiles (4 waves x kTileGroups / chunks groups) per block: two for Full
-// with two chunks per lane, which halves its LDS staging per tile (measured
+// (and 8-D blocks) with two chunks per lane, which halves its LDS staging per tile (measured
 // 4% faster at d = 192; one chunk per lane measured 2-4% slower with two).
-constexpr int packed_tiles_per_block(int variant, int chunks) { return variant == VAR_FULL && chunks == 2 ? 2 : 1; }
+constexpr int packed_tiles_per_block(int variant, int chunks)
+{
+    return (variant == VAR_FULL || variant == VAR_BLOCK8) && chunks == 2 ? 2 : 1;
+}
 const void *packed_kernel_full(int bits, int mode, int chunks);
 const void *packed_kernel_fast(int bits, int mode, int chunks);
 const void *packed_kernel_2d(int bits, int mode, int chunks);
+const void *packed_kernel_8d(int bits, int mode, int chunks);
 // Blocks of the stage-2 sketch kernel with a single rotation set (each walks
 // several tiles).
 constexpr int64_t kQjlBlocks = 1024;

@@ -131,7 +131,7 @@ template <int VAR, int BITS, int MODE, int C>
 __device__ __forceinline__ void packed_body(const KArgs &a)
 {
     constexpr int H = 1 << (BITS - 1);
-    constexpr int PL = VAR == VAR_FULL ? 32 : 8;   // parameter floats per chunk
+    constexpr int PL = kLanePL<VAR>;               // parameter floats per chunk
     constexpr int GPW = kTileGroups / C;           // groups per wave (4 C chunks in flight per lane)
     constexpr bool kUseLut = BITS == 4;
     constexpr bool kAppend = MODE == MODE_APPEND;
@@ -143,11 +143,11 @@ __device__ __forceinline__ void packed_body(const KArgs &a)
     __shared__ float lds_levels[16];
     __shared__ __align__(16) LutEntry lds_lut[kUseLut && kLoadX ? kLutMaxCells : 1];
     __shared__ float lds_pairs[kBlockThreads / 2];   // 32 pair sums per wave
-    // Full's 128 bytes per chunk are staged through LDS when the block has one
-    // set (per-lane global loads of them move more through the vector memory
-    // pipe than the rows do); Fast and 2-D read their 32 bytes directly,
-    // which measured faster than a staging barrier
-    constexpr bool kStage = VAR == VAR_FULL;
+    // Full's 128 bytes per chunk (8-D: 256) are staged through LDS when the
+    // block has one set (per-lane global loads of them move more through the
+    // vector memory pipe than the rows do); Fast and 2-D read their 32 bytes
+    // directly, which measured faster than a staging barrier
+    constexpr bool kStage = VAR == VAR_FULL || VAR == VAR_BLOCK8;
     __shared__ __align__(16) float lds_params[kStage ? kPackedMaxLanes * PL : 4];
 
     const int L = a.g_d >> (C + 2);   // lanes per row (even): d / (8 C)

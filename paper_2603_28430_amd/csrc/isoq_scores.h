@@ -105,7 +105,7 @@ __global__ __launch_bounds__(256) void score_kernel(const SArgs a)
 {
     using S = ScoreShape<D, BITS, QM>;
     constexpr int LPQ = D / kCoordsPerLane;          // 8-coordinate chunks per query
-    constexpr int PL = VAR == VAR_FULL ? 32 : 8;
+    constexpr int PL = kLanePL<VAR>;
     constexpr int64_t RB = (int64_t)D * BITS / 8;    // record bytes
     // LDS: tables[G][NF][E] | levels[16] | q~[G][D] | (sketch) sign tables
     // [G][NQ][16] | S q [G][QM] | q [G][D]

@@ -327,17 +327,18 @@ struct Stage1 {
     static constexpr int LPV = D / kCoordsPerLane;      // lanes per row
     static constexpr int VPW = 64 / LPV;                // rows per wave
     static constexpr int H = 1 << (BITS - 1);           // positive levels
-    static constexpr int PL = VAR == VAR_FULL ? 32 : 8; // parameter floats per lane
+    static constexpr int PL = kLanePL<VAR>;              // parameter floats per lane
     static constexpr int64_t ROWB = (int64_t)D * (F16 ? 2 : 4);  // bytes per row
     static constexpr int64_t RECB = (int64_t)D * BITS / 8;       // bytes per index record
     static constexpr int LANEB = F16 ? 16 : 32;         // row bytes per lane
     // fp32 round trip, quantize and dequantize: lane `sub` owns slots sub and
     // sub + LPV (coordinates 4 sub .. +3 and D/2 + 4 sub .. +3), so each
     // 16-byte access instruction of a wave covers one contiguous span (its
-    // index pieces go to the two halves of the record); elsewhere it owns
-    // slots 2 sub and 2 sub + 1
-    static constexpr bool kSplit =
-        !F16 && (MODE == MODE_ROUNDTRIP || MODE == MODE_QUANTIZE || MODE == MODE_DEQUANTIZE);
+    // index pieces go to the two halves of the record); elsewhere, and for
+    // 8-D blocks (whose 8 coordinates must stay together), it owns slots
+    // 2 sub and 2 sub + 1
+    static constexpr bool kSplit = !F16 && VAR != VAR_BLOCK8 &&
+                                   (MODE == MODE_ROUNDTRIP || MODE == MODE_QUANTIZE || MODE == MODE_DEQUANTIZE);
     static constexpr int kLaneOff = kSplit ? 16 : LANEB;       // bytes to lane sub's first piece
     static constexpr int kStep = kSplit ? (int)(ROWB / 2) : 16;  // bytes to its second piece
     static constexpr bool kUseLut = BITS == 4;           // magnitude lookup table

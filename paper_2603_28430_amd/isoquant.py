@@ -16,9 +16,9 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libisoquant.so")
 
-ISOQ_FULL, ISOQ_FAST, ISOQ_PLANAR2D = 0, 1, 2
+ISOQ_FULL, ISOQ_FAST, ISOQ_PLANAR2D, ISOQ_BLOCK8 = 0, 1, 2, 3
 ISOQ_F32, ISOQ_F16 = 0, 1
-VARIANTS = {"full": ISOQ_FULL, "fast": ISOQ_FAST, "2d": ISOQ_PLANAR2D}
+VARIANTS = {"full": ISOQ_FULL, "fast": ISOQ_FAST, "2d": ISOQ_PLANAR2D, "8d": ISOQ_BLOCK8}
 
 STATUS = {0: "ISOQ_OK", 1: "ISOQ_E_INVALID", 2: "ISOQ_E_UNSUPPORTED", 3: "ISOQ_E_NULL",
           4: "ISOQ_E_ALIGN", 5: "ISOQ_E_HIP", 6: "ISOQ_E_NOMEM", 7: "ISOQ_E_DEVICE"}
@@ -218,21 +218,48 @@ def _dtype_code(t) -> int:
     raise TypeError(f"rows must be float16 or float32, got {t}")
 
 
+def _is_gpu(t) -> bool:
+    return t.is_cuda
+
+
 def _rows(x, d):
-    if not x.is_cuda:
-        raise ValueError("tensor must be on the GPU")
-    if not x.is_contiguous():
-        raise ValueError("tensor must be contiguous")
-    if x.shape[-1] != d:
-        raise ValueError(f"last dimension must be d={d}")
+    _device_tensors(x, x=x)
+    if x.dim() < 1 or x.shape[-1] != d:
+        raise ValueError(f"x: last dimension must be d={d}")
     return x.numel() // d
+
+
+def _like(name, t, dtypes, numel):
+    """Type and size of a tensor argument: one of `dtypes`, `numel` elements."""
+    torch = _torch()
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.dtype not in dtypes:
+        raise TypeError(f"{name} must be {' or '.join(str(d) for d in dtypes)}, got {t.dtype}")
+    if t.numel() != numel:
+        raise ValueError(f"{name} must hold {numel} elements, got {t.numel()}")
+
+
+def _device_tensors(ref, **ts):
+    """Every tensor a kernel touches: on the GPU, contiguous, on ref's device
+    (a pointer of the wrong kind or into the wrong memory would fault the GPU)."""
+    for name, t in ts.items():
+        if not _is_gpu(t):
+            raise ValueError(f"{name} must be on the GPU")
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+        if t.device != ref.device:
+            raise ValueError(f"{name} must be on {ref.device}, got {t.device}")
 
 
 def isoq_roundtrip(p: Params, x, rows_per_set: int = 1, x_hat=None, stream=None):
     """x_hat = stage-1 quantize->dequantize of x (same shape and dtype)."""
     n = _rows(x, p.d)
+    _dtype_code(x.dtype)
     if x_hat is None:
         x_hat = _torch().empty_like(x)
+    _like("x_hat", x_hat, (x.dtype,), n * p.d)
+    _device_tensors(x, x_hat=x_hat)
     _check(lib.isoq_roundtrip(p.handle, _dtype_code(x.dtype), ctypes.c_void_p(x.data_ptr()), n,
                               int(rows_per_set), ctypes.c_void_p(x_hat.data_ptr()), _stream_ptr(stream)),
            "isoq_roundtrip")
@@ -247,8 +274,10 @@ def isoq_quantize(p: Params, x, rows_per_set: int = 1, idx_packed=None, norms=No
         idx_packed = torch.empty((n, p.record_bytes), dtype=torch.uint8, device=x.device)
     if norms is None:
         norms = torch.empty((n,), dtype=torch.float32, device=x.device)
-    if idx_packed.dtype != torch.uint8 or idx_packed.numel() != n * p.record_bytes or norms.numel() != n:
-        raise ValueError("idx_packed must hold n records of record_bytes bytes and norms n floats")
+    _dtype_code(x.dtype)
+    _like("idx_packed", idx_packed, (torch.uint8,), n * p.record_bytes)
+    _like("norms", norms, (torch.float32,), n)
+    _device_tensors(x, idx_packed=idx_packed, norms=norms)
     _check(lib.isoq_quantize(p.handle, _dtype_code(x.dtype), ctypes.c_void_p(x.data_ptr()), n,
                              int(rows_per_set), ctypes.c_void_p(idx_packed.data_ptr()),
                              ctypes.c_void_p(norms.data_ptr()), _stream_ptr(stream)), "isoq_quantize")
@@ -259,11 +288,16 @@ def isoq_dequantize(p: Params, idx_packed, norms, dtype=None, rows_per_set: int 
                     stream=None):
     """Rows [n, d] of `dtype` (default float16) from packed records and norms."""
     torch = _torch()
+    _like("norms", norms, (torch.float32,), norms.numel() if isinstance(norms, torch.Tensor) else 0)
     n = norms.numel()
+    _device_tensors(norms, norms=norms)
     if x_hat is None:
         x_hat = torch.empty((n, p.d), dtype=dtype or torch.float16, device=norms.device)
-    if idx_packed.dtype != torch.uint8 or idx_packed.numel() != n * p.record_bytes or x_hat.numel() != n * p.d:
-        raise ValueError("idx_packed must hold one record per norm and x_hat one row of d per norm")
+    _like("idx_packed", idx_packed, (torch.uint8,), n * p.record_bytes)
+    _like("x_hat", x_hat, (torch.float16, torch.float32), n * p.d)
+    if dtype is not None and x_hat.dtype != dtype:
+        raise TypeError(f"x_hat is {x_hat.dtype}, dtype asks for {dtype}")
+    _device_tensors(norms, idx_packed=idx_packed, x_hat=x_hat)
     _check(lib.isoq_dequantize(p.handle, _dtype_code(x_hat.dtype), ctypes.c_void_p(idx_packed.data_ptr()),
                                ctypes.c_void_p(norms.data_ptr()), n, int(rows_per_set),
                                ctypes.c_void_p(x_hat.data_ptr()), _stream_ptr(stream)), "isoq_dequantize")
@@ -300,9 +334,7 @@ def isoq_kv_append(pk: Params, k_new, slot_mapping, k_idx, k_rho, pv: Params = N
                 or tuple(v_rho.shape) != tuple(k_rho.shape) or v_new.dtype != k_new.dtype):
             raise ValueError("V tensors must have the shapes and dtype of the K tensors")
         ts += [v_new, v_idx, v_rho]
-    for t in ts:
-        if not t.is_cuda or not t.is_contiguous():
-            raise ValueError("tensors must be contiguous and on the GPU")
+    _device_tensors(k_new, **{f"arg{i}": t for i, t in enumerate(ts)})
     _check(lib.isoq_kv_append(pk.handle, None if pv is None else pv.handle, _dtype_code(k_new.dtype),
                               _ptr(k_new), _ptr(v_new), _ptr(slot_mapping), int(n_tokens), int(n_heads),
                               _ptr(k_idx), _ptr(k_rho), _ptr(v_idx), _ptr(v_rho), int(n_blocks),
@@ -315,8 +347,10 @@ def isoq_kv_scores(pk: Params, q, k_idx, k_rho, block_table, seq_lens, scale: fl
     against the paged key cache k_idx [n_blocks, n_kv_heads, block_size, R] /
     k_rho [n_blocks, n_kv_heads, block_size], with block_table int32
     [n_seqs, max_blocks] and seq_lens int32 [n_seqs].  Returns fp32 scores
-    [n_seqs, n_q_heads, max_len]; positions at or past a sequence's length are
-    not written (see include/isoquant.h)."""
+    [n_seqs, n_q_heads, max_len]; the kernel does not write positions at or
+    past a sequence's length or behind an out-of-range block-table entry: a
+    `scores` tensor allocated here holds -inf there, a caller's keeps its
+    contents (see include/isoquant.h)."""
     torch = _torch()
     if q.dim() != 3 or k_idx.dim() != 4 or k_rho.dim() != 3 or block_table.dim() != 2:
         raise ValueError("q [n_seqs, n_q_heads, d], k_idx [n_blocks, n_kv_heads, block_size, R], "
@@ -333,7 +367,10 @@ def isoq_kv_scores(pk: Params, q, k_idx, k_rho, block_table, seq_lens, scale: fl
     if max_len is None:
         max_len = max_blocks * block_size
     if scores is None:
-        scores = torch.empty((n_seqs, n_q_heads, max_len), dtype=torch.float32, device=q.device)
+        # positions the kernel does not write (at or past a sequence's
+        # length, or behind an invalid block-table entry) read as -inf, so a
+        # softmax over max_len ignores them
+        scores = torch.full((n_seqs, n_q_heads, max_len), float("-inf"), dtype=torch.float32, device=q.device)
     elif tuple(scores.shape) != (n_seqs, n_q_heads, max_len) or scores.dtype != torch.float32:
         raise ValueError("scores must be fp32 [n_seqs, n_q_heads, max_len]")
     ts = [q, k_idx, k_rho, block_table, seq_lens, scores]
@@ -344,9 +381,7 @@ def isoq_kv_scores(pk: Params, q, k_idx, k_rho, block_table, seq_lens, scale: fl
                 or tuple(k_gamma.shape) != tuple(k_rho.shape) or k_gamma.dtype != torch.float32):
             raise ValueError("k_signs [n_blocks, n_kv_heads, block_size, m/8] uint8, k_gamma like k_rho")
         ts += [k_signs, k_gamma]
-    for t in ts:
-        if not t.is_cuda or not t.is_contiguous():
-            raise ValueError("tensors must be contiguous and on the GPU")
+    _device_tensors(q, **{f"arg{i}": t for i, t in enumerate(ts)})
     if sketch is None:
         _check(lib.isoq_kv_scores(pk.handle, _dtype_code(q.dtype), _ptr(q), int(n_seqs), int(n_q_heads),
                                   int(n_kv_heads), _ptr(k_idx), _ptr(k_rho), int(n_blocks), int(block_size),
@@ -427,9 +462,12 @@ def isoq_quantize_qjl(p: Params, sk: Sketch, x, rows_per_set: int = 1, idx_packe
         signs = torch.empty((n, sk.m // 8), dtype=torch.uint8, device=dev)
     if gamma is None:
         gamma = torch.empty((n,), dtype=torch.float32, device=dev)
-    if (idx_packed.numel() != n * p.record_bytes or norms.numel() != n or signs.numel() != n * (sk.m // 8)
-            or gamma.numel() != n):
-        raise ValueError("outputs must hold n records, norms, sign sketches of m/8 bytes and gammas")
+    _dtype_code(x.dtype)
+    _like("idx_packed", idx_packed, (torch.uint8,), n * p.record_bytes)
+    _like("norms", norms, (torch.float32,), n)
+    _like("signs", signs, (torch.uint8,), n * (sk.m // 8))
+    _like("gamma", gamma, (torch.float32,), n)
+    _device_tensors(x, idx_packed=idx_packed, norms=norms, signs=signs, gamma=gamma)
     _check(lib.isoq_quantize_qjl(p.handle, sk.handle, _dtype_code(x.dtype), _ptr(x), n, int(rows_per_set),
                                  _ptr(idx_packed), _ptr(norms), _ptr(signs), _ptr(gamma), _stream_ptr(stream)),
            "isoq_quantize_qjl")
@@ -459,9 +497,8 @@ def isoq_kv_append_qjl(pk: Params, sk: Sketch, k_new, slot_mapping, k_idx, k_rho
     if (k_idx.dtype != torch.uint8 or k_signs.dtype != torch.uint8 or k_rho.dtype != torch.float32
             or k_gamma.dtype != torch.float32):
         raise TypeError("k_idx and k_signs uint8, k_rho and k_gamma float32")
-    for t in (k_new, slot_mapping, k_idx, k_rho, k_signs, k_gamma):
-        if not t.is_cuda or not t.is_contiguous():
-            raise ValueError("tensors must be contiguous and on the GPU")
+    _device_tensors(k_new, k_new=k_new, slot_mapping=slot_mapping, k_idx=k_idx, k_rho=k_rho, k_signs=k_signs,
+                    k_gamma=k_gamma)
     _check(lib.isoq_kv_append_qjl(pk.handle, sk.handle, _dtype_code(k_new.dtype), _ptr(k_new), _ptr(slot_mapping),
                                   int(n_tokens), int(n_heads), _ptr(k_idx), _ptr(k_rho), _ptr(k_signs),
                                   _ptr(k_gamma), int(n_blocks), int(block_size), _stream_ptr(stream)),

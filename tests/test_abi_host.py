@@ -47,13 +47,15 @@ def test_sizes():
     assert iq.isoq_packed_bytes(256, 3) == 96
     assert iq.isoq_packed_bytes(5, 3) == 2
     assert iq.isoq_packed_bytes(0, 3) == 0
-    for v in ("full", "fast", "2d"):
-        for d in (128, 256, 512, 6):
+    for v in ("full", "fast", "2d", "8d"):
+        for d in (128, 256, 512, 6, 13):
             assert iq.isoq_raw_params_per_set(v, d) == workloads.raw_params_per_set(v, d)
+            assert iq.isoq_raw_params_per_set(v, d) == oracle.raw_params_per_set(v, d)
             assert iq.isoq_export_params_per_set(v, d) == oracle.table1_params(v, d)
     assert iq.isoq_raw_params_per_set(7, 128) == 0
-    # records hold the padded width: 4 ceil(d/4) coordinates, 2-D 2 ceil(d/2)
-    for v in ("full", "fast", "2d"):
+    # records hold the padded width: 4 ceil(d/4) coordinates, 2-D 2 ceil(d/2),
+    # 8-D 8 ceil(d/8)
+    for v in ("full", "fast", "2d", "8d"):
         for d in (1, 2, 3, 5, 6, 7, 90, 91, 96, 128, 1000, 1023):
             for b in (2, 3, 4):
                 pw = oracle.padded_width(v, d)
@@ -62,6 +64,7 @@ def test_sizes():
                     assert iq.isoq_record_bytes(v, d, b) == iq.isoq_packed_bytes(d, b)
     assert iq.isoq_record_bytes("full", 0, 3) == 0
     assert iq.isoq_record_bytes("2d", 9, 3) == 4 and iq.isoq_record_bytes("full", 9, 3) == 5
+    assert iq.isoq_record_bytes("8d", 9, 3) == 6 and iq.isoq_record_bytes("8d", 128, 3) == 48
 
 
 def test_status_strings():
@@ -86,7 +89,7 @@ def test_library_codebook_converges_to_max_table():
         np.testing.assert_allclose(lv[(1 << b) // 2:], g["levels_positive"][str(b)], atol=6e-4)
 
 
-@pytest.mark.parametrize("variant", ["full", "fast", "2d"])
+@pytest.mark.parametrize("variant", ["full", "fast", "2d", "8d"])
 def test_library_seeded_draws_match_workload_generator(variant):
     for seed in (0, 1, 2**40 + 7):
         a = iq.isoq_rotation_draws(variant, 128, 3, seed)
@@ -110,6 +113,13 @@ def test_argument_validation_before_any_device_call():
     assert init(ctypes.byref(h), 0, 128, 2, 1, None, unsorted.ctypes.data_as(dp), 1) == 1
     zero_q = np.zeros(8 * 32)
     assert init(ctypes.byref(h), 0, 128, 2, 1, zero_q.ctypes.data_as(dp), None, 1) == 1
+    # 8-D blocks: a raw matrix with dependent columns has no rotation
+    G = workloads.rotation_draws("8d", 128, 1, seed=1).reshape(16, 8, 8)
+    G[5, :, 3] = 2.0 * G[5, :, 1]
+    assert init(ctypes.byref(h), 3, 128, 3, 1, np.ascontiguousarray(G).ctypes.data_as(dp), None, 1) == 1
+    G[5] = 0.0
+    assert init(ctypes.byref(h), 3, 128, 3, 1, np.ascontiguousarray(G).ctypes.data_as(dp), None, 1) == 1
+    assert init(ctypes.byref(h), 4, 128, 3, 1, None, None, 1) == 1   # no variant 4
     for fn, args in ((binding.lib.isoq_roundtrip, (None, 1, None, 4, 1, None, None)),
                      (binding.lib.isoq_quantize, (None, 1, None, 4, 1, None, None, None)),
                      (binding.lib.isoq_dequantize, (None, 1, None, None, 4, 1, None, None))):

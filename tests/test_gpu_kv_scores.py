@@ -194,6 +194,31 @@ def test_scores_invalid_blocks_are_skipped():
     assert np.all(got[1, :, :32] != CANARY) and np.all(got[1, :, 48:64] != CANARY)
 
 
+def test_scores_allocated_by_the_binding_are_minus_inf_where_not_written():
+    """Positions the kernel leaves alone (past a sequence's length, behind an
+    invalid block-table entry) read as -inf in a scores tensor the binding
+    allocates, and every written logit equals the one written into a
+    caller's buffer."""
+    rng = np.random.default_rng(6)
+    d, bits, bs = 128, 3, 16
+    p, rot, levels = make("fast", d, bits, 2)
+    cache = Cache(rng, d, bits, 2, 2, bs, [100, 37])
+    cache.table[0, 2] = -1                       # positions 32..47 of sequence 0
+    rec, rho, table, lens = cache.device()
+    q = torch.from_numpy(workloads.unit_gaussian_rows(4, d, seed=8, dtype=np.float16)).cuda().view(2, 2, d)
+    ml = cache.table.shape[1] * bs
+    got = iq.isoq_kv_scores(p, q, rec, rho, table, lens, 0.5, max_len=ml)
+    ref = torch.full((2, 2, ml), CANARY, dtype=torch.float32, device="cuda")
+    iq.isoq_kv_scores(p, q, rec, rho, table, lens, 0.5, max_len=ml, scores=ref)
+    torch.cuda.synchronize()
+    got, ref = got.cpu().numpy(), ref.cpu().numpy()
+    written = ref != CANARY
+    assert np.all(np.isneginf(got[~written]))
+    np.testing.assert_array_equal(got[written], ref[written])
+    assert not written[0, :, 32:48].any() and not written[0, :, 100:].any() and not written[1, :, 37:].any()
+    assert written[0, :, :32].all() and written[1, :, :37].all()
+
+
 def test_scores_of_keys_quantized_by_the_oracle():
     """Realistic keys: the oracle's own quantization of unit Gaussian rows with
     the rotation of their head (AR(1)-free, seed-fixed)."""

@@ -71,7 +71,10 @@ def test_orthonormalize_leaves_a_rotation_alone():
 
 
 def test_dependent_columns_are_rejected():
-    G = np.ones((8, 8))
+    with pytest.raises(ValueError):
+        oracle.orthonormalize8(np.ones((8, 8)))
+    G = workloads.rotation_draws("8d", 8, 1, seed=30).reshape(8, 8)
+    G[:, 5] = 2.0 * G[:, 1] - G[:, 2]
     with pytest.raises(ValueError):
         oracle.orthonormalize8(G)
 
