@@ -95,9 +95,46 @@ def time_launches(fn, steps: int, warmup: int, torch, warm_seconds: float = 0.0)
     return s.elapsed_time(e) / steps
 
 
+# Host threads for the CPU baseline: the CPU share of one GPU on the GPU
+# boxes (16 cores per GPU), or fewer where fewer are available.
+CPU_SHARE = 16
+
+
+def graph_launch_us(fn, launches, torch, replays=20):
+    """Device time per launch of `fn` with the host out of the way: `launches`
+    calls captured in one HIP graph on a side stream (the binding launches on
+    the current stream, which is the capture stream inside the capture),
+    replayed `replays` times between HIP events.  None if capture fails."""
+    try:
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            fn(0)
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=side):
+            for i in range(launches):
+                fn(i)
+        g.replay()
+        torch.cuda.synchronize()
+        s = torch.cuda.Event(enable_timing=True)
+        e = torch.cuda.Event(enable_timing=True)
+        s.record()
+        for _ in range(replays):
+            g.replay()
+        e.record()
+        e.synchronize()
+        return s.elapsed_time(e) * 1e3 / (replays * launches)
+    except Exception as exc:  # capture unsupported: report the host-bound time only
+        print(f"# graph timing unavailable: {exc}", file=sys.stderr, flush=True)
+        return None
+
+
 def cpu_baseline(variant, d, bits, x_np, rot, levels, seconds: float):
     """The oracle (plain C, double precision) on the first rows of the same
-    workload, rows split across host threads.  Returns the JSON object."""
+    workload, rows split across host threads (all the cores of one GPU's CPU
+    share), and on one thread.  Returns the JSON object."""
     import numpy as np
 
     import oracle
@@ -106,7 +143,7 @@ def cpu_baseline(variant, d, bits, x_np, rot, levels, seconds: float):
         avail = len(os.sched_getaffinity(0))
     except AttributeError:
         avail = os.cpu_count() or 1
-    threads = max(1, min(16, avail))
+    threads = max(1, min(CPU_SHARE, avail))
     probe = 2000
     xd = np.ascontiguousarray(x_np[:probe], dtype=np.float64)
     rho = np.zeros(probe)
@@ -114,6 +151,13 @@ def cpu_baseline(variant, d, bits, x_np, rot, levels, seconds: float):
     t0 = time.perf_counter()
     oracle.stage1_range(variant, d, bits, rot, levels, xd, 0, probe, rho=rho, xh=xh)
     per_row = (time.perf_counter() - t0) / probe
+    # one thread: a bounded sample of about a quarter of the time budget
+    rows1 = int(min(len(x_np), max(1000, 0.25 * seconds / per_row)))
+    x1 = np.ascontiguousarray(x_np[:rows1], dtype=np.float64)
+    r1, h1 = np.zeros(rows1), np.zeros((rows1, d))
+    t0 = time.perf_counter()
+    oracle.stage1_range(variant, d, bits, rot, levels, x1, 0, rows1, rho=r1, xh=h1)
+    single = rows1 / (time.perf_counter() - t0)
     rows = int(min(len(x_np), max(threads * 1000, seconds * threads / per_row)))
     xd = np.ascontiguousarray(x_np[:rows], dtype=np.float64)
     rho = np.zeros(rows)
@@ -134,12 +178,62 @@ def cpu_baseline(variant, d, bits, x_np, rot, levels, seconds: float):
         dt = time.perf_counter() - t0
         if dt >= seconds or passes >= 100:
             break
-    return {"value": rows * passes / dt, "unit": "vectors/s", "cores": threads, "kind": "oracle",
+    return {"value": rows * passes / dt, "unit": "vectors/s", "cores": threads, "threads": threads,
+            "single_thread_value": single, "host_cpus": os.cpu_count(), "host_cpus_available": avail,
+            "kind": "oracle",
             "sample": f"first {rows} of the {len(x_np)} input rows x {passes} passes, fp64 C oracle "
-                      f"(Algorithm 1, indices not stored), {threads} threads, {dt:.1f} s"}
+                      f"(Algorithm 1, indices not stored), rows split over {threads} threads (one GPU's "
+                      f"CPU share of {CPU_SHARE} cores; {avail} available, {os.cpu_count()} on the host), "
+                      f"{dt:.1f} s; single_thread_value: the first {rows1} rows on one thread"}
 
 
-def kv_append_side(torch, workloads, d=128, cases=(("decode_32x1", 32, 1), ("prefill_8x4096", 8, 4096))):
+APPEND_CASES = (("decode_32x1", 32, 1), ("prefill_8x4096", 8, 4096))
+# --case: run one append workload only (a profile then covers one workload)
+CASE = None
+
+
+def _cases(cases):
+    return tuple(c for c in cases if CASE is None or c[0].startswith(CASE))
+
+
+def block8_side(torch, workloads):
+    """8-D grouped blocks (one 8x8 orthogonal matrix per 8 coordinates): round
+    trip and quantize of the headline rows (1,048,576 unit-norm fp16 vectors,
+    d = 128, 3 bits) and of 262,144 fp32 rows at d = 512.  Algorithmic bytes
+    per row as for the other variants."""
+    import numpy as np
+
+    import paper_2603_28430_amd as iq
+
+    out = {}
+    for d, n, tdt, ndt in ((128, 1 << 20, torch.float16, np.float16), (512, 1 << 18, torch.float32, np.float32)):
+        esz = 2 if tdt == torch.float16 else 4
+        print(f"# block8 d={d}", file=sys.stderr, flush=True)
+        x0 = torch.from_numpy(workloads.unit_gaussian_rows(n, d, seed=0, dtype=ndt)).cuda()
+        xs = [x0] + [x0.clone() for _ in range(2)]
+        ys = [torch.empty_like(x0) for _ in range(3)]
+        p = iq.isoq_params_init("8d", d, 3, 1, rot=workloads.rotation_draws("8d", d, 1, seed=1))
+        R = p.record_bytes
+        recs = [iq.isoq_quantize(p, xs[i]) for i in range(3)]
+        res = {}
+        for mode in ("roundtrip", "quantize"):
+            if mode == "roundtrip":
+                fn = lambda i: iq.isoq_roundtrip(p, xs[i % 3], x_hat=ys[i % 3])
+                b = n * 2 * d * esz
+            else:
+                fn = lambda i: iq.isoq_quantize(p, xs[i % 3], idx_packed=recs[i % 3][0], norms=recs[i % 3][1])
+                b = n * (d * esz + R + 4)
+            ms = time_launches(fn, 50, 5, torch, 0.2)
+            res[mode] = {"us": ms * 1e3, "vectors_per_s": n / (ms / 1e3), "GBps": b / ms / 1e6,
+                         "frac": b / ms / 1e6 / PEAK_HBM_GBPS}
+        p.close()
+        out[f"d{d}_{'f16' if esz == 2 else 'f32'}_n{n}_b3"] = res
+        del x0, xs, ys, recs
+        torch.cuda.empty_cache()
+    return out
+
+
+def kv_append_side(torch, workloads, d=128, cases=APPEND_CASES):
     """isoq_kv_append (quantize K and V into a paged cache, one launch): a
     decode step (32 sequences x 1 token) and a prefill-sized append (8
     sequences x 4,096 tokens), 32 heads, d = 128 (or d), Fast, 3 bits, fp16,
@@ -151,7 +245,7 @@ def kv_append_side(torch, workloads, d=128, cases=(("decode_32x1", 32, 1), ("pre
 
     H, bs, bits = 32, 16, 3
     res = {}
-    for name, n_seq, per_seq in cases:
+    for name, n_seq, per_seq in _cases(cases):
         n_tok = n_seq * per_seq
         n_blocks = max(4096, 2 * n_tok // bs)
         print(f"# kv append {name}", file=sys.stderr, flush=True)
@@ -173,12 +267,54 @@ def kv_append_side(torch, workloads, d=128, cases=(("decode_32x1", 32, 1), ("pre
         steps = 200 if n_tok < 1000 else 50
         ms = time_launches(fn, steps, 10, torch, 0.2)
         b = 2 * n_tok * (H * (d * 2 + R + 4) + 8)
-        res[name] = {"tokens": n_tok, "heads": H, "us_per_call": ms * 1e3, "GBps": b / ms / 1e6,
-                     "frac": b / ms / 1e6 / PEAK_HBM_GBPS}
+        res[name] = _append_entry(n_tok, H, ms, b, fn, torch)
         pk.close()
         pv.close()
         del k, v, caches, rhos
     return res
+
+
+def _append_entry(n_tok, H, ms, b, fn, torch):
+    """JSON entry of an append measurement.  A decode step (a few tokens) is
+    shorter than the host's per-call cost (~10 us through ctypes), so its
+    back-to-back event time measures the host: there the device time comes
+    from the same launches replayed from a HIP graph, and GBps / frac use it
+    (frac is null if graph capture is unavailable)."""
+    e = {"tokens": n_tok, "heads": H, "us_per_call": ms * 1e3}
+    if n_tok >= 1000:
+        e.update(GBps=b / ms / 1e6, frac=b / ms / 1e6 / PEAK_HBM_GBPS)
+        return e
+    us = graph_launch_us(fn, 50, torch)
+    e["us_per_launch_graph"] = us
+    e["GBps"] = None if us is None else b / us / 1e3
+    e["frac"] = None if us is None else b / us / 1e3 / PEAK_HBM_GBPS
+    return e
+
+
+def kv_cache_side(torch, workloads):
+    """The K/V cache stream [8, 32, 32768, 128] fp16, Fast 3-bit quantize only
+    (packed records and norms out), one quaternion set per head
+    (rows_per_set = 32,768): one step is the K tensor then the V tensor.
+    Algorithmic bytes per row: the fp16 row, the 48-byte record, the 4-byte
+    norm."""
+    import paper_2603_28430_amd as iq
+
+    B, H, T, d, bits = 8, 32, 32768, 128, 3
+    print("# config kv cache", file=sys.stderr, flush=True)
+    kv = [workloads.kv_stream_torch(B, H, T, d, seed, "cuda").view(B * H * T, d) for seed in (2, 3)]
+    p = iq.isoq_params_init("fast", d, bits, H, rot=workloads.rotation_draws("fast", d, H, seed=1))
+    n = B * H * T
+    recs = [torch.empty((n, p.record_bytes), dtype=torch.uint8, device="cuda") for _ in range(2)]
+    norms = [torch.empty((n,), dtype=torch.float32, device="cuda") for _ in range(2)]
+    fn = lambda i: iq.isoq_quantize(p, kv[i % 2], T, idx_packed=recs[i % 2], norms=norms[i % 2])
+    ms = time_launches(fn, 40, 4, torch, 0.2)
+    b = n * (d * 2 + p.record_bytes + 4)
+    step = 2 * ms  # K and V: two launches of the same size
+    p.close()
+    del kv, recs, norms
+    torch.cuda.empty_cache()
+    return {"shape": [B, H, T, d], "tensors": 2, "ms_per_step": step, "rows_per_s": 2 * n / (step / 1e3),
+            "GBps": 2 * b / step / 1e6, "frac": 2 * b / step / 1e6 / PEAK_HBM_GBPS}
 
 
 def head_widths_side(torch, workloads):
@@ -200,7 +336,7 @@ def kv_append_qjl_side(torch, workloads):
 
     H, d, bs, bits, m = 32, 128, 16, 3, 128
     res = {}
-    for name, n_seq, per_seq in (("decode_32x1", 32, 1), ("prefill_8x4096", 8, 4096)):
+    for name, n_seq, per_seq in _cases(APPEND_CASES):
         n_tok = n_seq * per_seq
         n_blocks = max(4096, 2 * n_tok // bs)
         print(f"# kv append qjl {name}", file=sys.stderr, flush=True)
@@ -220,8 +356,7 @@ def kv_append_qjl_side(torch, workloads):
         steps = 200 if n_tok < 1000 else 50
         ms = time_launches(fn, steps, 10, torch, 0.2)
         b = n_tok * (H * (d * 2 + R + 4 + m // 8 + 4) + 8)
-        res[name] = {"tokens": n_tok, "heads": H, "us_per_call": ms * 1e3, "GBps": b / ms / 1e6,
-                     "frac": b / ms / 1e6 / PEAK_HBM_GBPS}
+        res[name] = _append_entry(n_tok, H, ms, b, fn, torch)
         sk.close()
         pk.close()
         del k, rec, sg, rho, gam
@@ -399,16 +534,8 @@ def other_configs(measure, entry, torch, np, workloads):
     out["kv_scores_qjl"] = kv_scores_qjl_side(torch, workloads)
     out["widths"] = widths_side(torch, workloads)
     out["head_widths"] = head_widths_side(torch, workloads)
-    print("# config kv cache", file=sys.stderr, flush=True)
-    B, H, T, d_ = 8, 32, 32768, 128
-    kv = [workloads.kv_stream_torch(B, H, T, d_, seed, "cuda").view(B * H * T, d_) for seed in (2, 3)]
-    ms, b, n_ = measure("fast", 3, "quantize", 40, 4, 0.2, kv, kv, d_, n_sets=H, rows_per_set=T)
-    step = 2 * ms  # K and V: two launches of the same size
-    out["kv_cache_fast_b3_quantize"] = {
-        "shape": [B, H, T, d_], "tensors": 2, "ms_per_step": step, "rows_per_s": 2 * n_ / (step / 1e3),
-        "GBps": 2 * b / step / 1e6, "frac": 2 * b / step / 1e6 / PEAK_HBM_GBPS}
-    del kv
-    torch.cuda.empty_cache()
+    out["block8"] = block8_side(torch, workloads)
+    out["kv_cache_fast_b3_quantize"] = kv_cache_side(torch, workloads)
     return out
 
 
@@ -431,8 +558,10 @@ def main() -> int:
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the side measurements of the d=256, d=512 and KV-cache workloads")
     ap.add_argument("--side", choices=["kv-append", "kv-append-qjl", "kv-scores", "kv-scores-qjl", "qjl", "widths",
-                                       "head-widths"],
+                                       "head-widths", "kv-cache", "block8"],
                     help="run only this side measurement and print its JSON")
+    ap.add_argument("--case", choices=["decode", "prefill"],
+                    help="with --side kv-append or kv-append-qjl: that workload only")
     ap.add_argument("--copy-only", action="store_true",
                     help="only time a plain device copy of the input size (counter calibration)")
     args = ap.parse_args()
@@ -449,9 +578,11 @@ def main() -> int:
 
     torch.cuda.set_device(0)
     if args.side:
+        global CASE
+        CASE = args.case
         fn = {"kv-append": kv_append_side, "kv-append-qjl": kv_append_qjl_side, "kv-scores": kv_scores_side,
-              "kv-scores-qjl": kv_scores_qjl_side,
-              "qjl": qjl_side, "widths": widths_side, "head-widths": head_widths_side}[args.side]
+              "kv-scores-qjl": kv_scores_qjl_side, "qjl": qjl_side, "widths": widths_side,
+              "head-widths": head_widths_side, "kv-cache": kv_cache_side, "block8": block8_side}[args.side]
         print(json.dumps({"side": args.side, **fn(torch, workloads)}), flush=True)
         return 0
     tdt, ndt, esz = {"f16": (torch.float16, np.float16, 2), "f32": (torch.float32, np.float32, 4)}[args.dtype]
