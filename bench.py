@@ -32,9 +32,11 @@ sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBPS = 8000.0          # MI355X HBM3E, vendor figure
 METRIC = "fused quant-dequant vectors/s + effective HBM GB/s (% peak), d=128 3-bit fp16"
-# every source the round-trip kernel is compiled from
+# every source the round-trip kernels are compiled from (the VALU encoder and,
+# for fp16 rows at d = 64, 128 and 256, the matrix-core one)
 KERNEL_SRCS = [os.path.join(ROOT, "paper_2603_28430_amd", "csrc", f)
-               for f in ("isoq_kernels.hip", "isoq_stage1.h", "isoq_device.h", "isoq_internal.h")]
+               for f in ("isoq_kernels.hip", "isoq_kernels.h", "isoq_kernels_m.hip", "isoq_stage1.h",
+                         "isoq_stage1m.h", "isoq_device.h", "isoq_internal.h")]
 PROFILES = os.path.join(ROOT, "profiles")
 
 
@@ -55,6 +57,14 @@ def algorithmic_bytes(mode: str, n: int, d: int, bits: int, esz: int) -> int:
     if mode == "quantize":
         return n * (d * esz + rec + 4)
     return n * (rec + 4 + d * esz)
+
+
+def kernel_name(variant: str, d: int, bits: int, dtype: str, mode: str) -> str:
+    """The kernel a stage-1 launch runs: fp16 rows at d = 64, 128 and 256
+    (Full, Fast, 8-D) take the matrix-core encoder, everything else the VALU
+    one."""
+    quad = dtype == "f16" and variant != "2d" and d in (64, 128, 256) and mode != "dequantize"
+    return f"{'stage1m_kernel' if quad else 'stage1_kernel'}<{variant},{d},{bits},{dtype},{mode}>"
 
 
 def measured_traffic(tag: str):
@@ -662,7 +672,7 @@ def main() -> int:
         "roofline": {"bound": "hbm", "achieved": gbps, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                      "frac": gbps / PEAK_HBM_GBPS, "traffic": measured_traffic(tag),
                      "algorithmic_bytes_per_launch": abytes,
-                     "kernel": f"stage1_kernel<{args.variant},{d},{bits},{args.dtype},{args.mode}>",
+                     "kernel": kernel_name(args.variant, d, bits, args.dtype, args.mode),
                      "kernel_source_sha256": kernel_source_hash()},
     }
 

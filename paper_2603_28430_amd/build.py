@@ -21,9 +21,12 @@ ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 HIPCC = os.path.join(ROCM, "bin", "hipcc")
 ARCH = "gfx950"
 
-# Device code: gfx950 only; packed-FP32 VALU instructions are disabled.
+# Device code: gfx950 only; packed-FP32 VALU instructions are disabled; matrix
+# instructions read and write ordinary VGPRs (their results feed VALU code
+# directly, without accumulation-register copies and the waits they need).
 DEVICE_FLAGS = ["-x", "hip", f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
                 "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+                "-mllvm", "-amdgpu-mfma-vgpr-form",
                 "-Wall", "-Wno-unused-parameter"]
 HOST_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-D__HIP_PLATFORM_AMD__", f"-I{ROCM}/include",
               "-Wall", "-Wextra", "-Wno-unused-parameter"]
@@ -42,8 +45,8 @@ def build(verbose: bool = False) -> str:
     os.makedirs(obj_dir, exist_ok=True)
     inc = [f"-I{INCLUDE}", f"-I{CSRC}"]
     jobs = []
-    for src in ("isoq_kernels.hip", "isoq_kernels_8d.hip", "isoq_scores.hip", "isoq_scores_8d.hip",
-                "isoq_scores_qjl.hip", "isoq_qjl.hip", "isoq_generic_full.hip", "isoq_generic_fast.hip",
+    for src in ("isoq_kernels.hip", "isoq_kernels_8d.hip", "isoq_kernels_m.hip", "isoq_scores.hip",
+                "isoq_scores_8d.hip", "isoq_scores_qjl.hip", "isoq_qjl.hip", "isoq_generic_full.hip", "isoq_generic_fast.hip",
                 "isoq_generic_2d.hip", "isoq_generic_8d.hip", "isoq_qjl_append.hip", "isoq_packed.hip",
                 "isoq_packed_8d.hip"):
         jobs.append([HIPCC, *DEVICE_FLAGS, *inc, "-c", os.path.join(CSRC, src), "-o",

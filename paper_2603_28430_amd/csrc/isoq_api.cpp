@@ -17,6 +17,7 @@ struct isoq_params {
     int device;
     float *dparams;                 // device, [n_sets][slots_per_set][params_per_slot], then the LUT
     size_t lut_offset;              // floats from dparams to the magnitude LUT (0: none)
+    size_t mfma_offset;             // floats from dparams to the matrix-core parameters (0: none)
     int lut_cells;
     float lut_inv_h;
     std::vector<float> exported;    // unit parameters as used (Table 1 layout)
@@ -100,6 +101,7 @@ void fill_args(const isoq_params *p, KArgs &a)
     a.params = p->dparams;
     a.n_sets = p->n_sets;
     a.lut = p->lut_offset ? p->dparams + p->lut_offset : nullptr;
+    a.mfma = p->mfma_offset ? reinterpret_cast<const uint32_t *>(p->dparams + p->mfma_offset) : nullptr;
     a.lut_inv_h = p->lut_inv_h;
     a.lut_cells = p->lut_cells;
 }
@@ -173,7 +175,25 @@ isoq_status run(const isoq_params *p, int dtype, int mode, KArgs &a, void *strea
     const bool f16 = dtype == ISOQ_F16;
     const int64_t rpb = rows_per_block(p);
     const bool generic = p->n_sets > 1 && (a.rows_per_set % rpb) != 0;
-    const void *fn = kernel_for(p->variant, p->d, p->bits, f16, generic, mode);
+    // fp16 encoders whose blocks each have one set rotate on the matrix cores
+    // (the decoder is the same in both layouts); so do rows with one set each
+    // in turn (rows_per_set = 1), as n_sets streams of one set each
+    const bool quad = f16 && quad_layout(p->variant, p->d) && mode != MODE_DEQUANTIZE;
+    if (quad && generic && a.rows_per_set == 1) {
+        const int64_t per_stream = (a.n + p->n_sets - 1) / p->n_sets;
+        const int64_t tiles = (per_stream + rpb - 1) / rpb;
+        if (tiles <= 65535) {
+            const void *fn = kernel_m_for(p->variant, p->d, p->bits,
+                                          mode == MODE_ROUNDTRIP ? MODE_STREAMS_ROUNDTRIP : MODE_STREAMS_QUANTIZE);
+            if (!fn)
+                return ISOQ_E_UNSUPPORTED;
+            fill_args(p, a);
+            void *args[] = {&a};
+            return launch(fn, dim3((unsigned)p->n_sets, (unsigned)tiles), args, stream);
+        }
+    }
+    const void *fn = quad && !generic ? kernel_m_for(p->variant, p->d, p->bits, mode)
+                                      : kernel_for(p->variant, p->d, p->bits, f16, generic, mode);
     if (!fn)
         return ISOQ_E_UNSUPPORTED;
     const int64_t blocks = (a.n + rpb - 1) / rpb;
@@ -346,6 +366,27 @@ isoq_status isoq_params_init(isoq_params **out, int variant, int d, int bits, in
         p->lut_inv_h = (float)inv_h;
         const float *f = reinterpret_cast<const float *>(lut.data());
         layout.insert(layout.end(), f, f + 4 * lut.size());
+    }
+    // the matrix-core encoders' fp16 (hi, lo) matrix rows, after the rest
+    // (16-byte aligned: every part above is a multiple of 4 floats)
+    p->mfma_offset = 0;
+    if (quad_layout(variant, d)) {
+        const size_t per_set = mfma_bytes_per_set(variant, d);
+        std::vector<uint16_t> mf;
+        try {
+            mf.resize((size_t)n_sets * per_set / 2);
+        } catch (const std::bad_alloc &) {
+            delete p;
+            return ISOQ_E_NOMEM;
+        }
+        const size_t slots = (size_t)slots_per_set(variant, d) * params_per_slot(variant);
+        for (int s = 0; s < n_sets; s++)
+            build_mfma_params(variant, d, layout.data() + s * slots, mf.data() + s * per_set / 2);
+        while (layout.size() % 4)
+            layout.push_back(0.f);
+        p->mfma_offset = layout.size();
+        const float *f = reinterpret_cast<const float *>(mf.data());
+        layout.insert(layout.end(), f, f + mf.size() / 2);
     }
 
     hipError_t e = hipGetDevice(&p->device);
@@ -530,8 +571,10 @@ isoq_status isoq_kv_append(const isoq_params *pk, const isoq_params *pv, int dty
     if (st != ISOQ_OK)
         return st;
     // one kernel for both tensors; block (x, y, z) = (head, token range, K|V)
-    const void *fn = !packed ? kernel_for(pk->variant, pk->d, pk->bits, dtype == ISOQ_F16, false, MODE_APPEND)
-                             : packed_kernel(pk->variant, pk->bits, MODE_APPEND, ps.chunks);
+    const bool quad = dtype == ISOQ_F16 && quad_layout(pk->variant, pk->d);
+    const void *fn = packed ? packed_kernel(pk->variant, pk->bits, MODE_APPEND, ps.chunks)
+                     : quad ? kernel_m_for(pk->variant, pk->d, pk->bits, MODE_APPEND)
+                            : kernel_for(pk->variant, pk->d, pk->bits, dtype == ISOQ_F16, false, MODE_APPEND);
     if (!fn)
         return ISOQ_E_UNSUPPORTED;
     // tokens per block: 4 waves of kTileGroups (packed: kTileGroups / chunks)

@@ -393,6 +393,69 @@ bool build_rotation(int variant, int d, int n_sets, const double *raw, std::vect
     return true;
 }
 
+// ------------------------------------------------- matrix-core parameters
+// For the quad-layout encoders: per chunk c (coordinates 8c .. 8c+7) and quad
+// row i, row i of each 4x4 matrix the chunk's rotation applies, as fp16 hi =
+// fp16(m) and lo = fp16(m - hi) (their sum is m to about 2^-22 relative):
+// Full, Fast, 2-D: the matrices of slots 2c and 2c+1 (M = L(q_L) R(conj q_R),
+// L(q_L), diag(R(theta_1), R(theta_2))); 8-D: the sub-blocks (0,0), (0,1),
+// (1,0), (1,1) of the block's 8x8 Q.  Each row is 16 bytes: hi[4], lo[4].
+namespace {
+void put_row(const float m[4], uint16_t *out)
+{
+    for (int k = 0; k < 4; k++) {
+        const _Float16 hi = (_Float16)m[k];
+        const _Float16 lo = (_Float16)(m[k] - (float)hi);
+        std::memcpy(out + k, &hi, 2);
+        std::memcpy(out + 4 + k, &lo, 2);
+    }
+}
+
+// the 4x4 matrix (row-major) a tuned kernel applies to slot j of a set
+void slot_matrix(int variant, const float *set_layout, int j, float M[16])
+{
+    const float *P = set_layout + (size_t)j * params_per_slot(variant);
+    if (variant == VAR_FULL) {
+        for (int k = 0; k < 16; k++)
+            M[k] = P[k];
+    } else if (variant == VAR_FAST) {
+        const float a = P[0], b = P[1], c = P[2], d = P[3];
+        const float L[16] = {a, -b, -c, -d, b, a, -d, c, c, d, a, -b, d, -c, b, a};
+        for (int k = 0; k < 16; k++)
+            M[k] = L[k];
+    } else {
+        const float c1 = P[0], s1 = P[1], c2 = P[2], s2 = P[3];
+        const float R[16] = {c1, -s1, 0, 0, s1, c1, 0, 0, 0, 0, c2, -s2, 0, 0, s2, c2};
+        for (int k = 0; k < 16; k++)
+            M[k] = R[k];
+    }
+}
+}  // namespace
+
+void build_mfma_params(int variant, int d, const float *set_layout, uint16_t *out)
+{
+    const int C = d / 8, pieces = variant == VAR_BLOCK8 ? 4 : 2;
+    for (int c = 0; c < C; c++)
+        for (int i = 0; i < 4; i++) {
+            uint16_t *o = out + ((size_t)c * 4 + i) * pieces * 8;
+            if (variant == VAR_BLOCK8) {
+                const float *Q = set_layout + (size_t)c * 64;
+                for (int s = 0; s < 2; s++)
+                    for (int t = 0; t < 2; t++) {
+                        const float row[4] = {Q[8 * (4 * s + i) + 4 * t], Q[8 * (4 * s + i) + 4 * t + 1],
+                                              Q[8 * (4 * s + i) + 4 * t + 2], Q[8 * (4 * s + i) + 4 * t + 3]};
+                        put_row(row, o + (2 * s + t) * 8);
+                    }
+            } else {
+                for (int t = 0; t < 2; t++) {
+                    float M[16];
+                    slot_matrix(variant, set_layout, 2 * c + t, M);
+                    put_row(M + 4 * i, o + t * 8);
+                }
+            }
+        }
+}
+
 // ------------------------------------------------------- magnitude lookup table
 bool build_magnitude_lut(int H, const double *tau, const double *lev, double *inv_h,
                          std::vector<LutEntry> &lut)

@@ -15,7 +15,11 @@ enum Mode {
     MODE_DEQUANTIZE = 2,
     MODE_APPEND = 3,      // quantize into the slots of a paged cache
     MODE_QJL = 4,         // quantize with the stage-2 sketch
-    MODE_APPEND_QJL = 5   // both: records, norms, signs and gamma into cache slots
+    MODE_APPEND_QJL = 5,  // both: records, norms, signs and gamma into cache slots
+    // kernel_m_for only: round trip and quantize of rows whose set is the row
+    // number mod n_sets (rows_per_set = 1), as n_sets interleaved streams
+    MODE_STREAMS_ROUNDTRIP = 6,
+    MODE_STREAMS_QUANTIZE = 7
 };
 // VAR_BLOCK8: 8-D grouped blocks, one 8x8 orthogonal matrix per 8 coordinates
 enum Variant { VAR_FULL = 0, VAR_FAST = 1, VAR_PLANAR2D = 2, VAR_BLOCK8 = 3 };
@@ -88,6 +92,9 @@ struct KArgs {
     int64_t n_slots;         // cache capacity in slots (n_blocks * block_size)
     uint32_t n_heads, block_size;
     FastDiv div_block;
+    // the forward rotation on the matrix cores (isoq_stage1m.h): per set,
+    // chunk and quad row, the fp16 (hi, lo) rows of the chunk's 4x4 matrices
+    const uint32_t *mfma;
     // stage-2 residual sketch (quantize with QJL)
     const uint16_t *qjl_frag;  // [n_sets][m/16][d/32][64][8] fp16: S' = S T^{-1}, B-fragment order
     uint8_t *qjl_signs;        // [n][m/8] sign bits of S (x - x_hat)
@@ -139,6 +146,19 @@ ScoreKernel score_kernel_for(int variant, int d, int bits, bool f16, int group);
 ScoreKernel score_kernel_for_block8(int d, int bits, bool f16, int group);
 // The same with the stage-2 residual correction of m sign bits (isoq_scores_qjl.hip).
 ScoreKernel score_qjl_kernel_for(int variant, int d, int bits, bool f16, int group, int m);
+
+// Variants and widths whose fp16 encoders (round trip, quantize, append,
+// sketch) rotate on the matrix cores in the quad layout (isoq_stage1m.h), and
+// the kernel for (variant, d, bits, mode) there (round trip, quantize,
+// append), or nullptr.  The 2-D case keeps its VALU rotation (2 multiply-adds
+// per coordinate: the products would save little and add their latency).
+constexpr bool quad_layout(int variant, int d) { return variant != VAR_PLANAR2D && (d == 64 || d == 128 || d == 256); }
+const void *kernel_m_for(int variant, int d, int bits, int mode);
+// Bytes of the matrix-core parameters per set: d/8 chunks x 4 quad rows x
+// (2 slots, 8-D: 4 sub-blocks) x 16 bytes of fp16 (hi, lo) rows.
+inline size_t mfma_bytes_per_set(int variant, int d) { return (size_t)(d / 8) * 4 * (variant == VAR_BLOCK8 ? 4 : 2) * 16; }
+// Build them from a set's device-layout fp32 parameters (isoq_host_params.cpp).
+void build_mfma_params(int variant, int d, const float *set_layout, uint16_t *out);
 
 // Kernel entry for (variant, d, bits, fp16 rows?, generic set indexing?, mode),
 // or nullptr.  Generic set indexing is needed when there is more than one

@@ -1,8 +1,8 @@
 // Quantize with the stage-2 residual sketch (Sec. 8): the stage-1 encoder of
-// isoq_stage1.h in MODE_QJL (rows in, rows out) or MODE_APPEND_QJL (token
-// rows into the slots of a paged cache), which also writes
-// sign(S (x - x_hat)) as m bits and ||x - x_hat|| per row.  The projection is the path's one dense
-// contraction, P = E S'^T over a wave's tile of rows, on MFMA (fp16 inputs,
+// isoq_stage1m.h (fp16 rows) or isoq_stage1.h (fp32 rows) in MODE_QJL (rows
+// in, rows out) or MODE_APPEND_QJL (token rows into the slots of a paged
+// cache), which also writes sign(S (x - x_hat)) as m bits and ||x - x_hat||
+// per row.  The projection is the path's one dense contraction, P = E S'^T over a wave's tile of rows, on MFMA (fp16 inputs,
 // fp32 accumulation); S' = S T^{-1} per rotation set is staged in LDS once
 // per block.  Blocks have 8 waves, or 4 for quantize with several sets
 // (WAVES, chosen by qjl_waves): at d = 128, m = 128 the staged projection
@@ -15,20 +15,31 @@
 #include <type_traits>
 
 #include "isoq_stage1.h"
+#include "isoq_stage1m.h"
 
 namespace isoq {
 namespace {
 
+// fp16 rows take the matrix-core encoder where quantize and append do (the
+// quad layout of isoq_stage1m.h, so the records stay identical to theirs);
+// fp32 rows and the 2-D case the VALU encoder.
 template <int VAR, int D, int BITS, bool F16, int QM, int MODE, int WAVES>
 __global__ __launch_bounds__(WAVES * 64) void qjl_kernel(const KArgs a)
 {
     using S = Stage1<VAR, D, BITS, F16, MODE, false, QM, WAVES>;
-    __shared__ float lds_levels[16];
-    __shared__ __align__(16) float lds_params[S::LPV * S::PL];
     __shared__ __align__(16) LutEntry lds_lut[S::kUseLut ? kLutMaxCells : 1];
     __shared__ __align__(16) _Float16 lds_frag[QM * D];
     __shared__ __align__(16) _Float16 lds_e[WAVES * S::kTileRows * S::kEStride];
-    S::run(a, lds_levels, lds_params, lds_lut, lds_frag, lds_e);
+    if constexpr (F16 && quad_layout(VAR, D)) {
+        using M = Stage1M<VAR, D, BITS, MODE, QM, WAVES>;
+        static_assert(M::kTileRows == S::kTileRows, "the two layouts tile rows alike");
+        __shared__ __align__(16) u32x4 lds_par[M::kLdsWords];
+        M::run(a, lds_lut, lds_par, lds_frag, lds_e);
+    } else {
+        __shared__ float lds_levels[16];
+        __shared__ __align__(16) float lds_params[S::LPV * S::PL];
+        S::run(a, lds_levels, lds_params, lds_lut, lds_frag, lds_e);
+    }
 }
 
 // Instantiated (m, waves): m = 64, and m = 128 at d <= 128, with 8 waves; with
