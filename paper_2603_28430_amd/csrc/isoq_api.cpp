@@ -770,7 +770,10 @@ isoq_status isoq_sketch_init(isoq_sketch **out, const isoq_params *p, int m, con
     sk->dS = nullptr;
     // S' = S T^{-1}: row i of S' is T applied to row i of S (T orthogonal),
     // with the handle's own fp32 rotation parameters; then fp16 in the order
-    // lane l of k-step ks of column tile nt reads: S'[16 nt + l % 16][32 ks + 8 (l / 16) + i]
+    // lane l of k-step ks of column tile nt reads, S'[c][32 ks + 8 (l / 16) + i]
+    // with c = (m/4) (r / 4) + 4 nt + r % 4 for the tile row r = l % 16 (the
+    // coordinate order that leaves each lane of the projection with m/4
+    // consecutive sign bits of one row)
     const int KS = d / 32, NT = m / 16;
     const size_t per_set = (size_t)m * d;
     std::vector<uint16_t> frag;
@@ -791,7 +794,8 @@ isoq_status isoq_sketch_init(isoq_sketch **out, const isoq_params *p, int m, con
             for (int ks = 0; ks < KS; ks++)
                 for (int l = 0; l < 64; l++)
                     for (int i = 0; i < 8; i++) {
-                        const _Float16 h = (_Float16)Sp[(size_t)(16 * nt + l % 16) * d + 32 * ks + 8 * (l / 16) + i];
+                        const int r = l % 16, c = m / 4 * (r / 4) + 4 * nt + r % 4;
+                        const _Float16 h = (_Float16)Sp[(size_t)c * d + 32 * ks + 8 * (l / 16) + i];
                         uint16_t bits;
                         std::memcpy(&bits, &h, 2);
                         f[((size_t)(nt * KS + ks) * 64 + l) * 8 + i] = bits;

@@ -307,40 +307,44 @@ __device__ __forceinline__ uint32_t ballot_encode(const float y[8], const float 
 
 // ---- stage-2 projection of a wave's error tile -------------------------------------
 // P = E S'^T with E the tile's error rows (fp16, LDS, row stride ES halfs) and
-// S' = S T^{-1} (fp16, LDS, B-fragment order) on v_mfma_f32_16x16x32_f16: lane l
-// supplies row l % 16 and k = 8 (l / 16) .. +7 of A, column l % 16 and the same
-// k of B, and receives column l % 16 of rows 4 (l / 16) .. +3 of the 16 x 16
-// result.  The sign bits of rho * P (rho > 0 unless the row is zero, whose e is
-// zero) are the sketch; a ballot per result register gathers them, 16 columns
-// per row, and lane t < 16 assembles row t's 32-bit words (columns
-// 32 w .. 32 w + 31, bit i = column 32 w + i).  A tile of more than 16 rows
-// takes one such product per block of 16 rows.  dst_of(ar) is the sign row of
-// tile row ar, or nullptr where nothing is written.
+// S' = S T^{-1} (fp16, LDS, fragment order), computed transposed, P^T = S' E^T,
+// on v_mfma_f32_16x16x32_f16: for column tile nt lane l supplies row l % 16 of
+// the tile's 16 rows of S' and column l % 16 of E^T (error row l % 16), both
+// for k = 8 (l / 16) .. +7 of each 32-wide k step, and receives rows
+// 4 (l / 16) .. +3 of column l % 16 of the 16 x 16 result.  The host orders
+// S' so that row r of tile nt is sketch coordinate (m/4) (r / 4) + 4 nt + r % 4:
+// lane l then holds, over the NT tiles, the m/4 consecutive coordinates
+// (m/4) (l / 16) .. + m/4 - 1 of error row l % 16, so it turns its results into
+// that part of the row's sign record by itself (bit b = coordinate
+// (m/4) (l / 16) + b; a compare and a carry-in add per bit), with no exchange
+// between lanes.  The sign bits of rho * P (rho > 0 unless the row is zero,
+// whose e is zero) are the sketch.  A tile of more than 16 rows takes one such
+// product per block of 16 rows.  dst_of(ar) is the sign row of tile row ar, or
+// nullptr where nothing is written.
 template <int D, int QM, int TR, int ES, typename DstOf>
 __device__ __forceinline__ void qjl_project(const _Float16 *frag, const _Float16 *eq, DstOf dst_of)
 {
     typedef _Float16 half8 __attribute__((ext_vector_type(8)));
     typedef float f32x4 __attribute__((ext_vector_type(4)));
     constexpr int KS = D / 32, NT = QM / 16;
+    static_assert(NT == 4 || NT == 8, "m = 64 or 128: 16 or 32 sign bits per lane");
     constexpr int RB = (TR + 15) / 16;  // blocks of 16 tile rows (2 at d = 64)
     const int l = threadIdx.x & 63;
     const int r16 = l & 15, kq = l >> 4;
 #pragma unroll
     for (int rb = 0; rb < RB; rb++) {
-        half8 A[KS];
-        const int ar = 16 * rb + r16;   // tile row this lane feeds into A
+        half8 E[KS];
+        const int ar = 16 * rb + r16;   // the tile row of this lane's column
 #pragma unroll
         for (int ks = 0; ks < KS; ks++) {
             if (ar < TR) {
-                A[ks] = *reinterpret_cast<const half8 *>(eq + ar * ES + 32 * ks + 8 * kq);
+                E[ks] = *reinterpret_cast<const half8 *>(eq + ar * ES + 32 * ks + 8 * kq);
             } else {
 #pragma unroll
                 for (int i = 0; i < 8; i++)
-                    A[ks][i] = (_Float16)0.f;
+                    E[ks][i] = (_Float16)0.f;
             }
         }
-        // this lane's output row (lanes 0 .. 15 of the block)
-        uint32_t *dst = l < 16 ? dst_of(ar) : nullptr;
         // k-step outer, column tile inner: the NT accumulations are
         // independent, so consecutive MFMAs do not wait on each other
         f32x4 acc[NT];
@@ -349,34 +353,28 @@ __device__ __forceinline__ void qjl_project(const _Float16 *frag, const _Float16
             acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int ks = 0; ks < KS; ks++) {
-            half8 b[NT];
 #pragma unroll
-            for (int nt = 0; nt < NT; nt++)
-                b[nt] = *reinterpret_cast<const half8 *>(frag + ((nt * KS + ks) * 64 + l) * 8);
-#pragma unroll
-            for (int nt = 0; nt < NT; nt++)
-                acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(A[ks], b[nt], acc[nt], 0, 0, 0);
-        }
-        // row t = 4 g + i of the block sits in bits [16 g, 16 g + 16) of the
-        // ballot of result register i
-        const int i = l & 3, g = (l >> 2) & 3;
-#pragma unroll
-        for (int w2 = 0; w2 < NT / 2; w2++) {
-            uint32_t word = 0;
-#pragma unroll
-            for (int h = 0; h < 2; h++) {
-                const f32x4 v = acc[2 * w2 + h];
-                const uint64_t m0 = __builtin_amdgcn_ballot_w64(v[0] > 0.f);
-                const uint64_t m1 = __builtin_amdgcn_ballot_w64(v[1] > 0.f);
-                const uint64_t m2 = __builtin_amdgcn_ballot_w64(v[2] > 0.f);
-                const uint64_t m3 = __builtin_amdgcn_ballot_w64(v[3] > 0.f);
-                const uint64_t sel = i == 0 ? m0 : (i == 1 ? m1 : (i == 2 ? m2 : m3));
-                word |= ((uint32_t)(sel >> (16 * g)) & 0xFFFFu) << (16 * h);
+            for (int nt = 0; nt < NT; nt++) {
+                const half8 s = *reinterpret_cast<const half8 *>(frag + ((nt * KS + ks) * 64 + l) * 8);
+                acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(s, E[ks], acc[nt], 0, 0, 0);
             }
-            if (dst)
-                dst[w2] = word;
-            // one word's masks live at a time (scalar registers)
-            __builtin_amdgcn_sched_barrier(0);
+        }
+        // bit 4 nt + i is result register i of tile nt: pushed from the top
+        // (tile NT - 1, register 3) down
+        uint32_t p = 0;
+#pragma unroll
+        for (int nt = NT - 1; nt >= 0; nt--) {
+            const uint64_t mk[4] = {__builtin_amdgcn_ballot_w64(acc[nt][3] > 0.f),
+                                    __builtin_amdgcn_ballot_w64(acc[nt][2] > 0.f),
+                                    __builtin_amdgcn_ballot_w64(acc[nt][1] > 0.f),
+                                    __builtin_amdgcn_ballot_w64(acc[nt][0] > 0.f)};
+            p = push_bits4(p, mk);
+        }
+        if (uint32_t *dst = dst_of(ar)) {
+            if constexpr (NT == 8)
+                dst[kq] = p;
+            else
+                reinterpret_cast<uint16_t *>(dst)[kq] = (uint16_t)p;
         }
     }
 }

@@ -108,6 +108,7 @@ struct Stage1M {
     // tokens' chunks of one head: measured faster there (their rows are
     // scattered over the token stride, so the row order gains no lines)
     static constexpr bool kPerm = !kAppend;
+    static constexpr bool kEarly = !kQjl;
 
     // Geometry of load u for the lane of MFMA block b (= lane / 4) in wave w:
     // its chunk, its quad in the wave's tile and its quad in the block's tile
@@ -363,14 +364,19 @@ struct Stage1M {
         _Float16 *eq = kQjl ? lds_e + w * RT * kEStride : nullptr;
         const int64_t tstride = kQjl ? (int64_t)(kAppend ? gridDim.y : gridDim.x) : (int64_t)1 << 40;
         const int64_t first_quad = C <= 16 ? (int64_t)w * QPS : w;   // bquad_of(0, 0, w)
+        In buf[kTileGroups];
+        int roffs[kTileGroups];   // the lane's row in the tile, per load (quad order)
         for (int64_t tb = tile0;; tb += tstride) {
             const int64_t row0 = tb * rows_per_tile;
             if (row0 + 4 * first_quad >= nrows)
                 return;
-            if (row0 + rows_per_tile <= nrows)
-                tile<false>(a, Am, lds_par, lev, thr, lds_lut, row0, nrows, b, qi, w, eq);
-            else
-                tile<true>(a, Am, lds_par, lev, thr, lds_lut, row0, nrows, b, qi, w, eq);
+            if (row0 + rows_per_tile <= nrows) {
+                load<false>(a, row0, nrows, b, qi, w, buf, roffs);
+                process<false>(a, Am, lds_par, lev, thr, lds_lut, row0, nrows, b, qi, w, eq, buf, roffs);
+            } else {
+                load<true>(a, row0, nrows, b, qi, w, buf, roffs);
+                process<true>(a, Am, lds_par, lev, thr, lds_lut, row0, nrows, b, qi, w, eq, buf, roffs);
+            }
             if constexpr (kQjl)
                 sketch(a, lds_frag, eq, row0, w);
             else
@@ -378,17 +384,14 @@ struct Stage1M {
         }
     }
 
-    // The wave's kTileGroups loads first (rows past the end re-read the last
-    // row, compute it again and store the same bits), then compute and store
-    // row quad by row quad (SPQ loads each).
+    // A tile: the wave's kTileGroups loads first (rows past the end re-read
+    // the last row, compute it again and store the same bits), then compute
+    // and store row quad by row quad (SPQ loads each).
     template <bool TAIL>
-    __device__ static __forceinline__ void tile(const KArgs &a, const u32x4 (*Am)[PB], const u32x4 *lds_par,
-                                                const float *lev, const float *thr, const LutEntry *lut,
-                                                int64_t row0, int64_t nrows, int b, int qi, int w, _Float16 *eq)
+    __device__ static __forceinline__ void load(const KArgs &a, int64_t row0, int64_t nrows, int b, int qi, int w,
+                                                In *buf, int *roffs)
     {
         const int lane = threadIdx.x & 63;
-        In buf[kTileGroups];
-        int roffs[kTileGroups];   // the lane's row in the tile, per load (quad order)
 #pragma unroll
         for (int u = 0; u < kTileGroups; u++) {
             int r = 4 * bquad_of(u, b, w) + qi;
@@ -405,6 +408,15 @@ struct Stage1M {
             if constexpr (kAppend)
                 buf[u].slot = (a.slots + row0)[r];
         }
+    }
+
+    template <bool TAIL>
+    __device__ static __forceinline__ void process(const KArgs &a, const u32x4 (*Am)[PB], const u32x4 *lds_par,
+                                                   const float *lev, const float *thr, const LutEntry *lut,
+                                                   int64_t row0, int64_t nrows, int b, int qi, int w, _Float16 *eq,
+                                                   In *buf, const int *roffs)
+    {
+        const int lane = threadIdx.x & 63;
         __builtin_amdgcn_sched_barrier(0);
         // the loaded chunks in the quad order
         if constexpr (kPerm) {
@@ -415,14 +427,15 @@ struct Stage1M {
         }
         // every load's matrix products and squared-norm part first (the
         // products' latency then overlaps the rest of the tile's work)
-        float yy[kTileGroups][8], sq[kTileGroups];
+        float yy[kEarly ? kTileGroups : 1][8], sq[kTileGroups];
 #pragma unroll
         for (int u = 0; u < kTileGroups; u++) {
             float x8[8];
             Raw<true> r;
             r.w[0] = buf[u].raw;
             sq[u] = sum_squares<true>(r, x8);
-            rotate(Am[u % SPQ], buf[u].raw, yy[u]);
+            if constexpr (kEarly)
+                rotate(Am[u % SPQ], buf[u].raw, yy[u]);
         }
 #pragma unroll
         for (int k = 0; k < kTileGroups / SPQ; k++) {
@@ -444,9 +457,12 @@ struct Stage1M {
                 int rl = load_row_base(u0 + h, w) + lane / NRL;
                 if (TAIL)
                     rl = (int)min((int64_t)rl, nrows - 1 - row0);
+                float ylate[kEarly ? 1 : 8];
+                if constexpr (!kEarly)
+                    rotate(Am[h], buf[u0 + h].raw, ylate);
                 e2[h] = compute(a, lds_par, lev, thr, lut, buf[u0 + h], row0, roffs[u0 + h],
                                 chunk_of(u0 + h, b), rho, rho_e, eq, 4 * wquad_of(u0 + h, b) + qi,
-                                yy[u0 + h], rl, row_chunk_of(u0 + h, lane));
+                                kEarly ? yy[u0 + h] : ylate, rl, row_chunk_of(u0 + h, lane));
             }
             if constexpr (kQjl) {
                 // gamma = rho ||e|| over the row's chunks (T is orthogonal:
@@ -489,7 +505,9 @@ struct Stage1M {
 #pragma unroll
         for (int j = 0; j < 8; j++)
             m[j] = fabsf(y[j]);
-        const float lscale = kQjl ? 1.f : rho;
+        // with the sketch the levels are the normalised ones, and zero for a
+        // zero row (whose y is exactly zero), so that e below is zero there
+        const float lscale = kQjl ? (rho > 0.f ? 1.f : 0.f) : rho;
         uint32_t p = 0;
         if constexpr (kUseLut) {
             const float s = a.lut_inv_h * __builtin_amdgcn_rcpf(rho_e);
@@ -505,6 +523,12 @@ struct Stage1M {
                 for (int k = 0; k < H; k++)
                     lvs[k] = lev[k] * lscale;
                 chain_levels<H>(y, m, ths, lvs, yq);
+            } else if constexpr (kQjl) {
+                float lvs[H];
+#pragma unroll
+                for (int k = 0; k < H; k++)
+                    lvs[k] = lev[k] * lscale;
+                p = ballot_encode<BITS, kQjl>(y, m, ths, lvs, yq);
             } else {
                 p = ballot_encode<BITS, kQjl>(y, m, ths, lev, yq);
             }
@@ -557,11 +581,11 @@ struct Stage1M {
         if constexpr (kQjl) {
             // e = y / rho' - c[idx], the normalised rotated-domain error (zero
             // for a zero row), to the wave's LDS tile as fp16
-            const float inv = rho > 0.f ? __builtin_amdgcn_rcpf(rho_e) : 0.f;
+            const float inv = __builtin_amdgcn_rcpf(rho_e);
             float e[8];
 #pragma unroll
             for (int j = 0; j < 8; j++) {
-                e[j] = rho > 0.f ? fmaf(y[j], inv, -yq[j]) : 0.f;
+                e[j] = fmaf(y[j], inv, -yq[j]);
                 s2 = fmaf(e[j], e[j], s2);
             }
             u32x4 hv;
