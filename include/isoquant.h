@@ -34,9 +34,10 @@
  *     generic kernel family for every other width), d in {64, 128, 256, 512}
  *     for the KV-cache append (and, fp16 rows only, 80, 96, 160 and 192), d in
  *     {64, 80, 96, 128, 160, 192, 256, 512} for the attention-score call
- *     without the sketch, d in {64, 128, 256} for the stage-2 sketch and the
- *     calls that use it (Full, Fast and 2-D handles; every other call takes
- *     all four variants).
+ *     without the sketch, d in {64, 128, 256, 512} and (fp16 rows, or any
+ *     query type for the scores) 80, 96, 160 and 192 for the stage-2 sketch
+ *     and the calls that use it (Full, Fast and 2-D handles; every other call
+ *     takes all four variants).
  *   - Widths that are not a multiple of the block size (4; 2-D: 2; 8-D: 8)
  *     follow Sec. 5.1: the last block is zero padded, all pw rotated
  *     coordinates are quantized and stored (pw = 4 ceil(d/4); 2-D:
@@ -253,7 +254,9 @@ isoq_status isoq_kv_scores(const isoq_params *pk, int dtype, const void *q, int 
  *     <q, x_hat> + sqrt(pi/2) / m * gamma * <S q, 2 z - 1>.
  *
  * isoq_sketch_init -- build the sketch of quantizer p on the current device.
- *   m       sketch bits per row: 64 or 128 at d = 64 and 128, 64 at d = 256.
+ *   m       sketch bits per row: 64 or 128 at d = 64, 80, 96, 128, 160 and
+ *           192; 64 at d = 256 and 512 (the projection, m d fp16, is staged in
+ *           LDS).  Other d, other m, or an 8-D handle: ISOQ_E_UNSUPPORTED.
  *   S_host  NULL, or host array [m][d] of doubles (row-major).  NULL: S is
  *           drawn from `seed`: S[i][4g .. 4g+3] is the Box-Muller quadruple of
  *           Philox4x32-10 with key = seed and counter (g, i, 3, 0) (the
@@ -279,6 +282,7 @@ isoq_status isoq_sketch_export(const isoq_sketch *sk, int *m, float *S_out);
  *   gamma   device, [n] fp32 ||x - x_hat||.
  * Needs one rotation set per block of rows: n_sets == 1, or rows_per_set a
  * multiple of 64 rows at d = 128 (32 at d = 256); ISOQ_E_UNSUPPORTED otherwise.
+ * At d = 80, 96, 160 and 192: fp16 rows and n_sets == 1 only.
  */
 isoq_status isoq_quantize_qjl(const isoq_params *p, const isoq_sketch *sk, int dtype, const void *x,
                               int64_t n, int64_t rows_per_set, uint8_t *idx_packed, float *norms,

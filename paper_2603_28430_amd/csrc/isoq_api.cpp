@@ -53,6 +53,20 @@ bool tuned_d(int d) { return d == 64 || d == 128 || d == 256 || d == 512; }
 // widths of the decoding calls (append, logits): the tuned ones and three
 // common attention head widths
 bool decode_d(int d) { return tuned_d(d) || d == 80 || d == 96 || d == 160 || d == 192; }
+// (d, m) of the stage-2 sketch: m = 64 or 128 sign bits at the decoding
+// widths up to 192, m = 64 at 256 and 512 (the staged projection, m d fp16,
+// has to fit the LDS next to the error tiles)
+bool sketch_shape(int d, int m) { return decode_d(d) && (m == 64 || (m == 128 && d <= 192)); }
+// fp16 rows at the head widths 80, 96, 160 and 192 take the packed-row
+// kernels (rows of a group back to back across the wave; with 3 bits a row
+// spans a multiple of 4 lanes, or 10 lanes at d = 80 with one chunk per lane)
+bool packed_decode(int d, int bits, bool f16)
+{
+    const PackedShape ps = packed_shape(d, bits, f16);
+    const int lanes = ps.rows > 0 ? d / (8 * ps.chunks) : 0;
+    return !tuned_d(d) && decode_d(d) && f16 && ps.rows > 0 &&
+           (bits != 3 || lanes % 4 == 0 || (ps.chunks == 1 && lanes % 2 == 0));
+}
 bool supported_d(int d) { return d >= 1 && d <= kGenericMaxD; }
 bool supported_bits(int b) { return b >= 2 && b <= 4; }
 bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
@@ -550,9 +564,7 @@ isoq_status isoq_kv_append(const isoq_params *pk, const isoq_params *pv, int dty
     // of a group back to back across the wave; with 3 bits a row spans a
     // multiple of 4 lanes, or 10 lanes at d = 80 with one chunk per lane)
     const PackedShape ps = packed_shape(pk->d, pk->bits, true);
-    const int lanes = ps.rows > 0 ? pk->d / (8 * ps.chunks) : 0;
-    const bool packed = !tuned_d(pk->d) && decode_d(pk->d) && dtype == ISOQ_F16 && ps.rows > 0 &&
-                        (pk->bits != 3 || lanes % 4 == 0 || (ps.chunks == 1 && lanes % 2 == 0));
+    const bool packed = packed_decode(pk->d, pk->bits, dtype == ISOQ_F16);
     if (!tuned_d(pk->d) && !packed)
         return ISOQ_E_UNSUPPORTED;
     if ((pk->n_sets != 1 && pk->n_sets != n_heads) || (has_v && pv->n_sets != 1 && pv->n_sets != n_heads))
@@ -631,7 +643,7 @@ isoq_status kv_scores(const isoq_params *pk, const isoq_sketch *sk, int dtype, c
     if (sk && (sk->variant != pk->variant || sk->d != pk->d || sk->n_sets != pk->n_sets ||
                sk->device != pk->device))
         return ISOQ_E_INVALID;
-    if (sk ? !tuned_d(pk->d) : !decode_d(pk->d))
+    if (!decode_d(pk->d))
         return ISOQ_E_UNSUPPORTED;
     const int64_t max_pos = std::min<int64_t>(max_len, (int64_t)max_blocks_per_seq * block_size);
     if (n_seqs > 65535 || (int64_t)max_blocks_per_seq * block_size > 0x7FFFFFFF ||
@@ -744,8 +756,7 @@ isoq_status isoq_sketch_init(isoq_sketch **out, const isoq_params *p, int m, con
         return ISOQ_E_NULL;
     if (m < 1)
         return ISOQ_E_INVALID;
-    if (!(((p->d == 64 || p->d == 128) && (m == 64 || m == 128)) || (p->d == 256 && m == 64)) ||
-        p->variant == VAR_BLOCK8)
+    if (!sketch_shape(p->d, m) || p->variant == VAR_BLOCK8)
         return ISOQ_E_UNSUPPORTED;
     const int d = p->d;
     std::vector<double> S((size_t)m * d), Sp((size_t)m * d);
@@ -773,9 +784,11 @@ isoq_status isoq_sketch_init(isoq_sketch **out, const isoq_params *p, int m, con
     // lane l of k-step ks of column tile nt reads, S'[c][32 ks + 8 (l / 16) + i]
     // with c = (m/4) (r / 4) + 4 nt + r % 4 for the tile row r = l % 16 (the
     // coordinate order that leaves each lane of the projection with m/4
-    // consecutive sign bits of one row)
-    const int KS = d / 32, NT = m / 16;
-    const size_t per_set = (size_t)m * d;
+    // consecutive sign bits of one row); zero past column d, up to the
+    // projection width dp (a multiple of 32)
+    const int dp = qjl_proj_width(d);
+    const int KS = dp / 32, NT = m / 16;
+    const size_t per_set = (size_t)m * dp;
     std::vector<uint16_t> frag;
     try {
         sk->S.assign(S.begin(), S.end());
@@ -795,7 +808,8 @@ isoq_status isoq_sketch_init(isoq_sketch **out, const isoq_params *p, int m, con
                 for (int l = 0; l < 64; l++)
                     for (int i = 0; i < 8; i++) {
                         const int r = l % 16, c = m / 4 * (r / 4) + 4 * nt + r % 4;
-                        const _Float16 h = (_Float16)Sp[(size_t)c * d + 32 * ks + 8 * (l / 16) + i];
+                        const int k = 32 * ks + 8 * (l / 16) + i;
+                        const _Float16 h = k < d ? (_Float16)Sp[(size_t)c * d + k] : (_Float16)0.f;
                         uint16_t bits;
                         std::memcpy(&bits, &h, 2);
                         f[((size_t)(nt * KS + ks) * 64 + l) * 8 + i] = bits;
@@ -850,6 +864,61 @@ isoq_status isoq_sketch_export(const isoq_sketch *sk, int *m, float *S_out)
     return ISOQ_OK;
 }
 
+// The packed-row kernels' geometry in the arguments (tpb: row tiles per
+// block).
+static void set_packed_args(const isoq_params *p, const PackedShape &ps, int64_t tpb, KArgs &a)
+{
+    a.g_d = p->d;
+    a.g_rows = ps.rows;
+    a.g_tpb = (int32_t)tpb;
+    a.g_block_set = 1;
+    a.g_set_stride = (int64_t)slots_per_set(p->variant, p->d) * params_per_slot(p->variant);
+}
+
+// isoq_quantize_qjl at the head widths 80, 96, 160 and 192: fp16 rows, one
+// rotation set, packed-row kernels; blocks walk runs of g_tpb row tiles.
+static isoq_status quantize_qjl_packed(const isoq_params *p, const isoq_sketch *sk, int dtype, const void *x,
+                                       int64_t n, uint8_t *idx_packed, float *norms, uint8_t *signs, float *gamma,
+                                       void *stream)
+{
+    if (!packed_decode(p->d, p->bits, dtype == ISOQ_F16) || p->n_sets != 1)
+        return ISOQ_E_UNSUPPORTED;
+    if (n == 0)
+        return ISOQ_OK;
+    if (!x || !idx_packed || !norms || !signs || !gamma)
+        return ISOQ_E_NULL;
+    if (!aligned(x, 16) || !aligned(idx_packed, 4) || !aligned(norms, 4) || !aligned(signs, 4) ||
+        !aligned(gamma, 4))
+        return ISOQ_E_ALIGN;
+    isoq_status st = check_device(p);
+    if (st != ISOQ_OK)
+        return st;
+    const void *fn = packed_qjl_kernel_for(p->variant, p->d, p->bits, sk->m, false);
+    if (!fn)
+        return ISOQ_E_UNSUPPORTED;
+    const PackedShape ps = packed_shape(p->d, p->bits, true);
+    const int64_t per_tile = (int64_t)ps.rows * (kBlockThreads / 64) * (kTileGroups / ps.chunks);
+    const int64_t tiles = (n + per_tile - 1) / per_tile;
+    const int64_t blocks0 = std::min<int64_t>(tiles, kQjlBlocks);
+    const int64_t tpb = (tiles + blocks0 - 1) / blocks0;
+    const int64_t blocks = (tiles + tpb - 1) / tpb;
+    if (tpb > 0x7FFFFFFF)
+        return ISOQ_E_UNSUPPORTED;
+    KArgs a{};
+    fill_args(p, a);
+    a.x = x;
+    a.rec_out = idx_packed;
+    a.norms_out = norms;
+    a.n = n;
+    a.rows_per_set = 1;
+    a.qjl_frag = sk->dfrag;
+    a.qjl_signs = signs;
+    a.qjl_gamma = gamma;
+    set_packed_args(p, ps, tpb, a);
+    void *args[] = {&a};
+    return launch(fn, dim3((unsigned)blocks), args, stream);
+}
+
 isoq_status isoq_quantize_qjl(const isoq_params *p, const isoq_sketch *sk, int dtype, const void *x,
                               int64_t n, int64_t rows_per_set, uint8_t *idx_packed, float *norms,
                               uint8_t *signs, float *gamma, void *stream)
@@ -861,6 +930,8 @@ isoq_status isoq_quantize_qjl(const isoq_params *p, const isoq_sketch *sk, int d
         return ISOQ_E_NULL;
     if (sk->variant != p->variant || sk->d != p->d || sk->n_sets != p->n_sets || sk->device != p->device)
         return ISOQ_E_INVALID;
+    if (!tuned_d(p->d))
+        return quantize_qjl_packed(p, sk, dtype, x, n, idx_packed, norms, signs, gamma, stream);
     // rows of one tile (a block's waves, kTileGroups groups each)
     const int waves = qjl_waves(sk->m, false, p->n_sets);
     const int64_t rpb = rows_per_block(p) / 4 * waves;
@@ -926,17 +997,6 @@ isoq_status isoq_kv_append_qjl(const isoq_params *pk, const isoq_sketch *sk, int
     isoq_status st = check_device(pk);
     if (st != ISOQ_OK)
         return st;
-    const int waves = qjl_waves(sk->m, true, pk->n_sets);
-    const void *fn = qjl_kernel_for(pk->variant, pk->d, pk->bits, dtype == ISOQ_F16, sk->m, true, waves);
-    if (!fn)
-        return ISOQ_E_UNSUPPORTED;
-    // block (x, y) = (head, token range); a block stages its head's projection
-    // once and walks token ranges y, y + gridDim.y, ... of that head
-    const int64_t rpr = rows_per_block(pk) / 4 * waves;   // tokens per range
-    const int64_t ranges = (n_tokens + rpr - 1) / rpr;
-    const int64_t by = std::max<int64_t>(1, std::min<int64_t>(ranges, kQjlBlocks * 4 / waves / n_heads));
-    if (by > 65535)
-        return ISOQ_E_UNSUPPORTED;
     KArgs a{};
     fill_args(pk, a);
     a.x = k_new;
@@ -952,6 +1012,36 @@ isoq_status isoq_kv_append_qjl(const isoq_params *pk, const isoq_sketch *sk, int
     a.qjl_frag = sk->dfrag;
     a.qjl_signs = k_signs;
     a.qjl_gamma = k_gamma;
+    if (!tuned_d(pk->d)) {
+        // packed rows: block (x, y) = (head, y-th run of g_tpb token tiles)
+        if (!packed_decode(pk->d, pk->bits, dtype == ISOQ_F16))
+            return ISOQ_E_UNSUPPORTED;
+        const void *fn = packed_qjl_kernel_for(pk->variant, pk->d, pk->bits, sk->m, true);
+        if (!fn)
+            return ISOQ_E_UNSUPPORTED;
+        const PackedShape ps = packed_shape(pk->d, pk->bits, true);
+        const int64_t per_tile = (int64_t)ps.rows * (kBlockThreads / 64) * (kTileGroups / ps.chunks);
+        const int64_t tiles = (n_tokens + per_tile - 1) / per_tile;
+        const int64_t by = std::max<int64_t>(1, std::min<int64_t>(tiles, kQjlBlocks / n_heads));
+        const int64_t tpb = (tiles + by - 1) / by;
+        const int64_t gy = (tiles + tpb - 1) / tpb;
+        if (gy > 65535)
+            return ISOQ_E_UNSUPPORTED;
+        set_packed_args(pk, ps, tpb, a);
+        void *args[] = {&a};
+        return launch(fn, dim3((unsigned)n_heads, (unsigned)gy, 1), args, stream);
+    }
+    const int waves = qjl_waves(sk->m, true, pk->n_sets);
+    const void *fn = qjl_kernel_for(pk->variant, pk->d, pk->bits, dtype == ISOQ_F16, sk->m, true, waves);
+    if (!fn)
+        return ISOQ_E_UNSUPPORTED;
+    // block (x, y) = (head, token range); a block stages its head's projection
+    // once and walks token ranges y, y + gridDim.y, ... of that head
+    const int64_t rpr = rows_per_block(pk) / 4 * waves;   // tokens per range
+    const int64_t ranges = (n_tokens + rpr - 1) / rpr;
+    const int64_t by = std::max<int64_t>(1, std::min<int64_t>(ranges, kQjlBlocks * 4 / waves / n_heads));
+    if (by > 65535)
+        return ISOQ_E_UNSUPPORTED;
     void *args[] = {&a};
     return launch(fn, dim3((unsigned)n_heads, (unsigned)by, 1), args, stream, 64 * waves);
 }

@@ -96,7 +96,8 @@ struct KArgs {
     // chunk and quad row, the fp16 (hi, lo) rows of the chunk's 4x4 matrices
     const uint32_t *mfma;
     // stage-2 residual sketch (quantize with QJL)
-    const uint16_t *qjl_frag;  // [n_sets][m/16][d/32][64][8] fp16: S' = S T^{-1}, B-fragment order
+    const uint16_t *qjl_frag;  // [n_sets][m/16][dp/32][64][8] fp16: S' = S T^{-1} in fragment order,
+                               // dp = d rounded up to a multiple of 32 (zero columns past d)
     uint8_t *qjl_signs;        // [n][m/8] sign bits of S (x - x_hat)
     float *qjl_gamma;          // [n] ||x - x_hat||
     // widths outside {64, 128, 256, 512} (isoq_generic.h)
@@ -106,6 +107,7 @@ struct KArgs {
     int32_t g_rec;             // record bytes, ceil(g_pw * bits / 8)
     int32_t g_vec;             // rows move in whole slots (d a multiple of 4)
     int32_t g_rows;            // packed-row kernels (isoq_packed.h): rows per wave group
+    int32_t g_tpb;             // packed-row kernels with the sketch: row tiles per block
     int64_t g_set_stride;      // floats per parameter set, kSlotParams * g_slots
 };
 
@@ -202,7 +204,7 @@ struct PackedShape {
     int rows;     // rows per wave group
     int chunks;   // 8-coordinate chunks per lane
 };
-inline PackedShape packed_shape(int d, int bits, bool f16)
+constexpr PackedShape packed_shape(int d, int bits, bool f16)
 {
     if (!f16 || d % 16 != 0 || d > 8 * kPackedMaxLanes || d == 64 || d == 128 || d == 256)
         return {0, 0};
@@ -229,6 +231,13 @@ const void *packed_kernel_full(int bits, int mode, int chunks);
 const void *packed_kernel_fast(int bits, int mode, int chunks);
 const void *packed_kernel_2d(int bits, int mode, int chunks);
 const void *packed_kernel_8d(int bits, int mode, int chunks);
+// Packed-row kernels with the stage-2 sketch of m bits (isoq_packed_qjl.hip):
+// quantize into rows (one rotation set) or, with `append`, into the slots of
+// a paged cache, for fp16 rows at d = 80, 96, 160 and 192; or nullptr.
+const void *packed_qjl_kernel_for(int variant, int d, int bits, int m, bool append);
+// Projection width of the sketch: d rounded up to a multiple of 32 (the
+// k-step of the projection's matrix instruction).
+constexpr int qjl_proj_width(int d) { return (d + 31) / 32 * 32; }
 // Blocks of the stage-2 sketch kernel with a single rotation set (each walks
 // several tiles).
 constexpr int64_t kQjlBlocks = 1024;

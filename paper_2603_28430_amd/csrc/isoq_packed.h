@@ -33,6 +33,16 @@
 // and norm go to its token's cache row.  With 3 bits L is a multiple of 4 at
 // 96, 160 and 192, so quads stay inside a row; at 80 (L = 10) lane pairs
 // write the record in half-words.
+//
+// With the stage-2 sketch (MODE_QJL: quantize into rows with one rotation
+// set; MODE_APPEND_QJL: into cache slots, one set per head) the width is a
+// compile-time D (80, 96, 160, 192): each lane also writes its chunk's
+// normalised error e = y / rho' - c[idx] as fp16 to the wave's LDS tile (row
+// u V + q for row q of group u, zero columns up to the projection width, a
+// multiple of 32), gamma = rho ||e|| is summed over the row like the squared
+// norm, and after the tile's groups the wave projects its tile through
+// S' = S T^{-1} (qjl_project) and writes the sign bits.  Blocks walk
+// g_tpb consecutive tiles, so the staged projection serves several.
 #pragma once
 
 #include "isoq_stage1.h"
@@ -127,18 +137,29 @@ __device__ __forceinline__ float packed_pair_total(const float *rp, int n)
     return tot;
 }
 
-template <int VAR, int BITS, int MODE, int C>
+template <int VAR, int BITS, int MODE, int C, int D = 0, int QM = 0>
 __device__ __forceinline__ void packed_body(const KArgs &a)
 {
     constexpr int H = 1 << (BITS - 1);
     constexpr int PL = kLanePL<VAR>;               // parameter floats per chunk
     constexpr int GPW = kTileGroups / C;           // groups per wave (4 C chunks in flight per lane)
     constexpr bool kUseLut = BITS == 4;
-    constexpr bool kAppend = MODE == MODE_APPEND;
-    constexpr bool kEncode = MODE == MODE_QUANTIZE || kAppend;
+    constexpr bool kQjl = MODE == MODE_QJL || MODE == MODE_APPEND_QJL;
+    constexpr bool kAppend = MODE == MODE_APPEND || MODE == MODE_APPEND_QJL;
+    constexpr bool kEncode = MODE == MODE_QUANTIZE || MODE == MODE_QJL || kAppend;
     constexpr bool kLoadX = MODE != MODE_DEQUANTIZE;
-    static_assert(MODE == MODE_ROUNDTRIP || MODE == MODE_QUANTIZE || MODE == MODE_DEQUANTIZE || kAppend, "mode");
+    static_assert(MODE == MODE_ROUNDTRIP || MODE == MODE_QUANTIZE || MODE == MODE_DEQUANTIZE || kAppend || kQjl,
+                  "mode");
     static_assert(C == 1 || C == 2, "one or two chunks per lane");
+    // the sketch's tile: QV rows per group, TR rows per wave, rows of ES
+    // halfs (DP projected coordinates, then padding)
+    static_assert(!kQjl || (D > 0 && QM > 0 && packed_shape(D, BITS, true).chunks == C), "sketch shape");
+    constexpr int QV = kQjl ? packed_shape(D, BITS, true).rows : 1;
+    constexpr int DP = kQjl ? qjl_proj_width(D) : 32;
+    constexpr int TR = kQjl ? GPW * QV : 1;
+    constexpr int ES = DP + 8;
+    __shared__ __align__(16) _Float16 lds_frag[kQjl ? QM * DP : 8];
+    __shared__ __align__(16) _Float16 lds_e[kQjl ? (kBlockThreads / 64) * TR * ES : 8];
 
     __shared__ float lds_levels[16];
     __shared__ __align__(16) LutEntry lds_lut[kUseLut && kLoadX ? kLutMaxCells : 1];
@@ -159,7 +180,7 @@ __device__ __forceinline__ void packed_body(const KArgs &a)
     const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int64_t rowb = (int64_t)a.g_d * 2;       // fp16 rows
     const int64_t recb = (int64_t)L * C * BITS;    // d b / 8
-    constexpr int TPB = kAppend ? 1 : packed_tiles_per_block(VAR, C);   // row tiles per block
+    const int TPB = kQjl ? a.g_tpb : kAppend ? 1 : packed_tiles_per_block(VAR, C);   // row tiles per block
     const int64_t base0 = (int64_t)(kAppend ? blockIdx.y : blockIdx.x) * TPB * (kBlockThreads / 64) * GPW;
     // append: the block's head, its input row stride and cache addressing
     const int64_t head = kAppend ? (int64_t)xcd_head(blockIdx.x, a.n_heads, rowb % 128 != 0) : 0;
@@ -185,7 +206,18 @@ __device__ __forceinline__ void packed_body(const KArgs &a)
         for (int i = threadIdx.x; i < C * L * (PL / 4); i += kBlockThreads)
             d4[i] = s4[i];
     }
-    if (MODE == MODE_DEQUANTIZE || (kUseLut && kLoadX) || (kStage && uni))
+    if constexpr (kQjl) {
+        // the set's projection, and zeros for the error tiles (columns past
+        // d, and rows a ragged tile leaves unwritten, stay zero)
+        const u32x4 *f4 = reinterpret_cast<const u32x4 *>(a.qjl_frag + bset * (int64_t)(QM * DP));
+        u32x4 *g4 = reinterpret_cast<u32x4 *>(lds_frag);
+        for (int i = threadIdx.x; i < QM * DP / 8; i += kBlockThreads)
+            g4[i] = f4[i];
+        u32x4 *e4 = reinterpret_cast<u32x4 *>(lds_e);
+        for (int i = threadIdx.x; i < (kBlockThreads / 64) * TR * ES / 8; i += kBlockThreads)
+            e4[i] = u32x4{0u, 0u, 0u, 0u};
+    }
+    if (MODE == MODE_DEQUANTIZE || (kUseLut && kLoadX) || (kStage && uni) || kQjl)
         __syncthreads();
     float P[C][PL];
     int64_t pset = -1;
@@ -211,6 +243,15 @@ __device__ __forceinline__ void packed_body(const KArgs &a)
 #pragma unroll
     for (int k = 0; k < H - 1; k++)
         thr[k] = a.thr_pos[k];
+    // append: the token's cache row.  Slot s is position s mod block_size of
+    // cache block s / block_size, a block holding [n_heads][block_size]
+    // records; a skipped slot (s < 0 or past the cache) writes nothing.
+    auto cache_row = [&](int64_t s, bool &ok) -> int64_t {
+        ok = s >= 0 && s < a.n_slots;
+        const uint32_t su = ok ? (uint32_t)s : 0u;
+        const uint32_t blk = fast_div(su, a.div_block);
+        return ((int64_t)blk * a.n_heads + head) * a.block_size + (su - blk * a.block_size);
+    };
 
     // ---- per tile, the wave's GPW groups (4u + w of the tile's): every load
     //      first, then compute and store group by group.  One chunk per
@@ -269,6 +310,7 @@ __device__ __forceinline__ void packed_body(const KArgs &a)
                     load_set(set);
             }
             float yq[C][8], rho;
+            float gamma = 0.f;   // with the sketch: rho ||e|| of the lane's row
             if constexpr (kLoadX) {
                 float x[C][8];
                 // squared norm: the lane's chunks, pair sums by DPP, then the
@@ -293,6 +335,15 @@ __device__ __forceinline__ void packed_body(const KArgs &a)
 #pragma unroll
                 for (int k = 0; k < H; k++)
                     lvs[k] = lev[k] * rho;
+                // with the sketch the selected levels are the normalised
+                // ones, zero for a zero row (whose y is zero), so that e is
+                // zero there
+                const float nz = rho > 0.f ? 1.f : 0.f;
+                float levq[H];
+#pragma unroll
+                for (int k = 0; k < H; k++)
+                    levq[k] = lev[k] * nz;
+                float s2 = 0.f;
                 uint32_t p[C];
 #pragma unroll
                 for (int k = 0; k < C; k++) {
@@ -303,24 +354,47 @@ __device__ __forceinline__ void packed_body(const KArgs &a)
                         m[j] = fabsf(y[j]);
                     if constexpr (kUseLut) {
                         const float s = a.lut_inv_h * __builtin_amdgcn_rcpf(rho_e);
-                        p[k] = lut_quantize<BITS, !kEncode, kEncode>(y, m, s, (float)(a.lut_cells - 1), lds_lut, rho,
-                                                                     yq[k]);
+                        p[k] = lut_quantize<BITS, !kEncode || kQjl, kEncode>(y, m, s, (float)(a.lut_cells - 1),
+                                                                             lds_lut, kQjl ? nz : rho, yq[k]);
+                    } else if constexpr (kQjl) {
+                        p[k] = ballot_encode<BITS, true>(y, m, ths, levq, yq[k]);
                     } else if constexpr (kEncode) {
                         p[k] = ballot_encode<BITS, false>(y, m, ths, lev, yq[k]);
                     } else {
                         chain_levels<H>(y, m, ths, lvs, yq[k]);
                     }
+                    if constexpr (kQjl) {
+                        // e = y / rho' - c[idx] to the wave's tile as fp16
+                        const float inv = __builtin_amdgcn_rcpf(rho_e);
+                        float e[8];
+#pragma unroll
+                        for (int j = 0; j < 8; j++) {
+                            e[j] = fmaf(y[j], inv, -yq[k][j]);
+                            s2 = fmaf(e[j], e[j], s2);
+                        }
+                        u32x4 hv;
+#pragma unroll
+                        for (int i = 0; i < 4; i++) {
+                            uint32_t h2;
+                            asm("v_cvt_pk_f16_f32 %0, %1, %2" : "=v"(h2) : "v"(e[2 * i]), "v"(e[2 * i + 1]));
+                            hv[i] = h2;
+                        }
+                        if (on)
+                            *reinterpret_cast<u32x4 *>(lds_e + (w * TR + u * QV + q) * ES + 8 * (sub + k * L)) = hv;
+                    }
+                }
+                if constexpr (kQjl) {
+                    // gamma: the row's sum of e^2 as its squared norm above
+                    s2 += dpp_f<DPP_QUAD_1032>(s2);
+                    pairs[lane >> 1] = s2;
+                    __builtin_amdgcn_wave_barrier();
+                    const float t2 = packed_pair_total(pairs + lr * (L >> 1), L >> 1);
+                    __builtin_amdgcn_wave_barrier();
+                    gamma = rho * __builtin_amdgcn_sqrtf(t2);
                 }
                 if constexpr (kAppend) {
-                    // the token's cache row: slot s is position s mod
-                    // block_size of cache block s / block_size, a block
-                    // holding [n_heads][block_size] records; a skipped slot
-                    // (s < 0 or past the cache) writes nothing
-                    const int64_t s = slot[u];
-                    const bool ok = s >= 0 && s < a.n_slots;
-                    const uint32_t su = ok ? (uint32_t)s : 0u;
-                    const uint32_t blk = fast_div(su, a.div_block);
-                    const int64_t cr = ((int64_t)blk * a.n_heads + head) * a.block_size + (su - blk * a.block_size);
+                    bool ok;
+                    const int64_t cr = cache_row(slot[u], ok);
                     uint8_t *rec = a.rec_out + cr * recb;
                     if (BITS == 3 && L % 4 != 0) {
                         // d = 80: quads would straddle rows
@@ -330,8 +404,11 @@ __device__ __forceinline__ void packed_body(const KArgs &a)
                         for (int k = 0; k < C; k++)
                             store_bits<BITS>(rec + k * L * BITS, sub, p[k], on && ok);
                     }
-                    if (on && ok && sub == 0)
+                    if (on && ok && sub == 0) {
                         a.norms_out[cr] = rho;
+                        if constexpr (kQjl)
+                            a.qjl_gamma[cr] = gamma;
+                    }
                     continue;
                 } else if constexpr (kEncode) {
                     if constexpr (C == 1) {
@@ -344,8 +421,11 @@ __device__ __forceinline__ void packed_body(const KArgs &a)
                         for (int k = 0; k < C; k++)
                             store_bits<BITS>(rec + k * L * BITS, sub, p[k], on);
                     }
-                    if (on && sub == 0)
+                    if (on && sub == 0) {
                         (a.norms_out + grow)[lr] = rho;
+                        if constexpr (kQjl)
+                            (a.qjl_gamma + grow)[lr] = gamma;
+                    }
                     continue;
                 }
             } else {
@@ -367,6 +447,26 @@ __device__ __forceinline__ void packed_body(const KArgs &a)
                 }
             }
         }
+        if constexpr (kQjl) {
+            // the tile's projection: tile row ar is row ar mod QV of group
+            // ar / QV of the wave
+            qjl_project<DP, QM, TR, ES>(lds_frag, lds_e + w * TR * ES, [&](int ar) -> uint32_t * {
+                if (ar >= TR)
+                    return nullptr;
+                const int gu = ar / QV;
+                const int64_t row = (base + 4 * gu + w) * QV + (ar - gu * QV);
+                if (row >= a.n)
+                    return nullptr;
+                int64_t orow = row;
+                if constexpr (kAppend) {
+                    bool ok;
+                    orow = cache_row(a.slots[row], ok);
+                    if (!ok)
+                        return nullptr;
+                }
+                return reinterpret_cast<uint32_t *>(a.qjl_signs + orow * (QM / 8));
+            });
+        }
     }
 }
 
@@ -381,6 +481,13 @@ template <int VAR, int BITS, int C>
 __global__ __launch_bounds__(kBlockThreads) void packed_append_kernel(const KArgs k, const KArgs v)
 {
     packed_body<VAR, BITS, MODE_APPEND, C>(blockIdx.z == 0 ? k : v);
+}
+
+// With the stage-2 sketch: width D, m = QM sign bits.
+template <int VAR, int D, int BITS, int MODE, int QM>
+__global__ __launch_bounds__(kBlockThreads) void packed_qjl_kernel(const KArgs a)
+{
+    packed_body<VAR, BITS, MODE, packed_shape(D, BITS, true).chunks, D, QM>(a);
 }
 
 template <int VAR, int BITS, int C>

@@ -43,7 +43,8 @@ __global__ __launch_bounds__(WAVES * 64) void qjl_kernel(const KArgs a)
 }
 
 // Instantiated (m, waves): m = 64, and m = 128 at d <= 128, with 8 waves; with
-// 4 waves as well for quantize into rows (several sets).
+// 4 waves as well for quantize into rows (several sets).  At d = 512 (m = 64)
+// the staged projection takes 64 KB of LDS, so a CU holds one block.
 template <int VAR, int D, int BITS, bool F16, int MODE>
 const void *qjl_pick_m(int m, int waves)
 {
@@ -84,6 +85,7 @@ const void *qjl_pick(int variant, int d, int bits, bool f16, int m, int waves)
         case 64: return qjl_pick_bits<V, 64, MODE>(bits, f16, m, waves);
         case 128: return qjl_pick_bits<V, 128, MODE>(bits, f16, m, waves);
         case 256: return qjl_pick_bits<V, 256, MODE>(bits, f16, m, waves);
+        case 512: return qjl_pick_bits<V, 512, MODE>(bits, f16, m, waves);
         }
         return nullptr;
     };

@@ -1,6 +1,7 @@
 // Attention-logit kernels with the stage-2 residual correction (the kernel
-// template is in isoq_scores.h): m = 64 or 128 sign bits at d = 128, 64 at
-// d = 256; group sizes 1 (static LDS) or any (dynamic LDS).
+// template is in isoq_scores.h): m = 64 or 128 sign bits at the decoding
+// widths up to 192, 64 at d = 256 and 512; group sizes 1 (static LDS) or any
+// (dynamic LDS).
 #include "isoq_scores.h"
 
 namespace isoq {
@@ -19,14 +20,11 @@ ScoreKernel entry_qjl(int group)
 template <int VAR, int D, int BITS, bool F16>
 ScoreKernel pick_m(int group, int m)
 {
-    if constexpr (D <= 128) {
-        if (m == 64)
-            return entry_qjl<VAR, D, BITS, F16, 64>(group);
+    if (m == 64)
+        return entry_qjl<VAR, D, BITS, F16, 64>(group);
+    if constexpr (D <= 192) {
         if (m == 128)
             return entry_qjl<VAR, D, BITS, F16, 128>(group);
-    } else if constexpr (D == 256) {
-        if (m == 64)
-            return entry_qjl<VAR, D, BITS, F16, 64>(group);
     }
     return {nullptr, 0};
 }
@@ -47,8 +45,13 @@ ScoreKernel pick_d(int d, int bits, bool f16, int group, int m)
 {
     switch (d) {
     case 64: return pick_bits<VAR, 64>(bits, f16, group, m);
+    case 80: return pick_bits<VAR, 80>(bits, f16, group, m);
+    case 96: return pick_bits<VAR, 96>(bits, f16, group, m);
     case 128: return pick_bits<VAR, 128>(bits, f16, group, m);
+    case 160: return pick_bits<VAR, 160>(bits, f16, group, m);
+    case 192: return pick_bits<VAR, 192>(bits, f16, group, m);
     case 256: return pick_bits<VAR, 256>(bits, f16, group, m);
+    case 512: return pick_bits<VAR, 512>(bits, f16, group, m);
     }
     return {nullptr, 0};
 }

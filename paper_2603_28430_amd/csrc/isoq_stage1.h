@@ -331,7 +331,8 @@ __device__ __forceinline__ void qjl_project(const _Float16 *frag, const _Float16
     constexpr int RB = (TR + 15) / 16;  // blocks of 16 tile rows (2 at d = 64)
     const int l = threadIdx.x & 63;
     const int r16 = l & 15, kq = l >> 4;
-#pragma unroll
+    // one block of 16 rows at a time (its fragments and accumulators only)
+#pragma unroll 1
     for (int rb = 0; rb < RB; rb++) {
         half8 E[KS];
         const int ar = 16 * rb + r16;   // the tile row of this lane's column

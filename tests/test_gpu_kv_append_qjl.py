@@ -75,9 +75,27 @@ def test_append_qjl_matches_row_encoder(variant, bits):
 
 
 @pytest.mark.parametrize("d,m,dtype,n_sets", [(128, 64, "f32", 1), (256, 64, "f16", 2), (256, 64, "f32", 1),
-                                              (64, 128, "f16", 2), (64, 64, "f32", 1)])
+                                              (64, 128, "f16", 2), (64, 64, "f32", 1), (512, 64, "f16", 2),
+                                              (512, 64, "f32", 1)])
 def test_append_qjl_shapes(d, m, dtype, n_sets):
     run_case("full", d, 3, m, dtype, n_tokens=70, n_heads=2, block_size=8, n_blocks=10, n_sets=n_sets, seed=d)
+
+
+@pytest.mark.parametrize("variant,d,bits,m,n_sets", [("full", 80, 3, 128, 1), ("fast", 96, 3, 128, 6),
+                                                     ("2d", 160, 2, 64, 6), ("full", 192, 4, 128, 6),
+                                                     ("fast", 192, 3, 64, 1), ("fast", 80, 2, 64, 6),
+                                                     ("2d", 96, 4, 128, 1), ("full", 160, 3, 128, 6)])
+def test_append_qjl_head_widths(variant, d, bits, m, n_sets):
+    # fp16 rows at the head widths: the packed-row kernels
+    run_case(variant, d, bits, m, "f16", n_tokens=97, n_heads=6, block_size=16, n_blocks=9, n_sets=n_sets,
+             seed=d + bits)
+
+
+def test_append_qjl_head_width_decode_and_long():
+    run_case("fast", 96, 3, 128, "f16", n_tokens=32, n_heads=8, block_size=16, n_blocks=40, n_sets=8, seed=5,
+             skip_every=5)
+    run_case("fast", 192, 3, 64, "f16", n_tokens=9000, n_heads=4, block_size=16, n_blocks=600, n_sets=4,
+             seed=6, skip_every=97)
 
 
 def test_append_qjl_decode_step_and_skipped_slots():

@@ -112,6 +112,13 @@ def test_scores_qjl_shapes(d, m, dtype):
     run_case("full", d, 3, m, dtype, n_seqs=2, n_q=2, n_kv=2, bs=16, seq_lens=[700, 31], seed=d + m)
 
 
+@pytest.mark.parametrize("d,m,dtype,bits", [(80, 128, "f16", 3), (96, 64, "f32", 3), (160, 128, "f16", 2),
+                                            (192, 64, "f16", 4), (192, 128, "f32", 3), (512, 64, "f16", 3),
+                                            (512, 64, "f32", 2)])
+def test_scores_qjl_head_widths_and_512(d, m, dtype, bits):
+    run_case("fast", d, bits, m, dtype, n_seqs=2, n_q=2, n_kv=2, bs=16, seq_lens=[700, 31], seed=d + m)
+
+
 @pytest.mark.parametrize("n_q,n_kv,n_sets", [(8, 2, 2), (4, 1, 1), (6, 2, 1)])
 def test_scores_qjl_grouped(n_q, n_kv, n_sets):
     run_case("fast", 128, 3, 128, "f16", n_seqs=2, n_q=n_q, n_kv=n_kv, bs=16, seq_lens=[300, 1030],

@@ -76,7 +76,10 @@ def run_case(variant, d, bits, m, dtype, n, n_sets=1, rows_per_set=1, seed=0, x=
     # on the middle threshold, so the comparison above leaves it out)
     zero = rho_o == 0
     assert np.all(signs[zero] == 0) and np.all(gamma[zero] == 0)
-    assert keep[~zero].mean() >= 0.98
+    # rows left out for a coordinate near a threshold: about 1 % at d = 128,
+    # a few % at d = 512 (more coordinates per row, each in a narrower
+    # distribution)
+    assert keep[~zero].mean() >= (0.98 if d <= 256 else 0.9)
     return sk, S
 
 
@@ -92,6 +95,39 @@ def test_qjl_d128_m128_f16(variant, bits):
                                                ("fast", 64, 128, "f32"), ("2d", 64, 128, "f16")])
 def test_qjl_shapes(variant, d, m, dtype):
     run_case(variant, d, 3, m, dtype, 501, seed=d + m)
+
+
+# fp16 rows at the head widths (packed-row kernels: rows of a group back to
+# back across the wave, the projection zero-padded to a multiple of 32
+# coordinates at d = 80), one rotation set
+@pytest.mark.parametrize("variant,d,bits,m", [("full", 80, 3, 128), ("fast", 96, 3, 128), ("2d", 160, 2, 64),
+                                              ("full", 192, 4, 128), ("fast", 80, 4, 64), ("full", 96, 2, 64),
+                                              ("fast", 192, 3, 64), ("2d", 96, 3, 128), ("fast", 160, 3, 128),
+                                              ("2d", 192, 2, 128), ("full", 160, 4, 64), ("2d", 80, 2, 128)])
+def test_qjl_head_widths(variant, d, bits, m):
+    run_case(variant, d, bits, m, "f16", 1037, seed=d + bits)
+
+
+@pytest.mark.parametrize("n", [1, 6, 61, 241, 5000])
+def test_qjl_head_width_sizes(n):
+    # d = 80: six rows per group, ragged last groups and tiles; 5000 rows make
+    # blocks walk several tiles
+    run_case("fast", 80, 3, 128, "f16", n, seed=n)
+
+
+def test_qjl_head_width_zero_rows_and_scales():
+    d = 96
+    x = workloads.unit_gaussian_rows(300, d, seed=9, dtype=np.float32)
+    x[::7] = 0.0
+    x[1::7] *= 1e3
+    x[2::7] *= 1e-3
+    run_case("full", d, 3, 128, "f16", 300, x=x.astype(np.float16), seed=9)
+
+
+@pytest.mark.parametrize("variant,bits,dtype", [("full", 3, "f16"), ("fast", 2, "f32"), ("2d", 4, "f16"),
+                                                ("fast", 3, "f32")])
+def test_qjl_d512(variant, bits, dtype):
+    run_case(variant, 512, bits, 64, dtype, 263, seed=bits)
 
 
 @pytest.mark.parametrize("n", [1, 5, 17, 64, 65, 1000])
@@ -172,11 +208,28 @@ def test_qjl_argument_errors():
         iq.isoq_quantize_qjl(p1, sk, x)                      # sketch of another handle's shape
     assert e.value.status == 1
     p512 = iq.isoq_params_init("full", 512, 3, 1)
-    with pytest.raises(iq.IsoqError) as e:
-        iq.isoq_sketch_init(p512, 64)
+    with pytest.raises(iq.IsoqError) as e:                   # 128 sign bits need d <= 192
+        iq.isoq_sketch_init(p512, 128)
     assert e.value.status == 2
-    with pytest.raises(iq.IsoqError) as e:                   # 128 sign bits need d <= 128
+    with pytest.raises(iq.IsoqError) as e:
         iq.isoq_sketch_init(iq.isoq_params_init("full", 256, 3, 1), 128)
+    assert e.value.status == 2
+    with pytest.raises(iq.IsoqError) as e:                   # widths without a sketch kernel
+        iq.isoq_sketch_init(iq.isoq_params_init("full", 100, 3, 1), 64)
+    assert e.value.status == 2
+    with pytest.raises(iq.IsoqError) as e:                   # 8-D blocks: no sketch
+        iq.isoq_sketch_init(iq.isoq_params_init("8d", 128, 3, 1), 64)
+    assert e.value.status == 2
+    # head widths: fp16 rows with one rotation set only
+    p96 = iq.isoq_params_init("fast", 96, 3, 1)
+    sk96 = iq.isoq_sketch_init(p96, 64)
+    with pytest.raises(iq.IsoqError) as e:
+        iq.isoq_quantize_qjl(p96, sk96, torch.zeros((10, 96), dtype=torch.float32, device="cuda"))
+    assert e.value.status == 2
+    p96s = iq.isoq_params_init("fast", 96, 3, 2)
+    with pytest.raises(iq.IsoqError) as e:
+        iq.isoq_quantize_qjl(p96s, iq.isoq_sketch_init(p96s, 64),
+                             torch.zeros((10, 96), dtype=torch.float16, device="cuda"), rows_per_set=5)
     assert e.value.status == 2
 
 
