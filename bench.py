@@ -472,6 +472,58 @@ def qjl_side(torch, workloads):
     return out
 
 
+def qjl_widths_side(torch, workloads):
+    """The stage-2 sketch at the other widths: isoq_quantize_qjl on fp16
+    unit-norm rows, Fast, 3 bits, m = 128 at the head widths 80, 96, 160 and
+    192 (1,048,576 rows, packed-row kernels) and m = 64 at d = 512 (262,144
+    rows); and the prefill-sized isoq_kv_append_qjl (8 x 4096 tokens x 32
+    heads, m = 128) at 96 and 192.  Algorithmic bytes as in qjl_side and
+    kv_append_qjl_side."""
+    import numpy as np
+
+    import paper_2603_28430_amd as iq
+
+    bits, out = 3, {}
+    for d, m, n in ((80, 128, 1 << 20), (96, 128, 1 << 20), (160, 128, 1 << 20), (192, 128, 1 << 20),
+                    (512, 64, 1 << 18)):
+        print(f"# qjl quantize d={d}", file=sys.stderr, flush=True)
+        x0 = torch.from_numpy(workloads.unit_gaussian_rows(n, d, seed=0, dtype=np.float16)).cuda()
+        xs = [x0] + [x0.clone() for _ in range(3)]
+        p = iq.isoq_params_init("fast", d, bits, 1, rot=workloads.rotation_draws("fast", d, 1, seed=1))
+        sk = iq.isoq_sketch_init(p, m)
+        bufs = [iq.isoq_quantize_qjl(p, sk, xs[i]) for i in range(4)]
+        fn = lambda i: iq.isoq_quantize_qjl(p, sk, xs[i % 4], idx_packed=bufs[i % 4][0], norms=bufs[i % 4][1],
+                                            signs=bufs[i % 4][2], gamma=bufs[i % 4][3])
+        ms = time_launches(fn, 50, 5, torch, 0.2)
+        b = n * (d * 2 + p.record_bytes + 4 + m // 8 + 4)
+        out[f"quantize_d{d}_m{m}"] = {"us": ms * 1e3, "GBps": b / ms / 1e6, "frac": b / ms / 1e6 / PEAK_HBM_GBPS}
+        sk.close()
+        p.close()
+        del x0, xs, bufs
+    H, bs, m, n_tok = 32, 16, 128, 8 * 4096
+    for d in (96, 192):
+        print(f"# kv append qjl d={d}", file=sys.stderr, flush=True)
+        pk = iq.isoq_params_init("fast", d, bits, H, rot=workloads.rotation_draws("fast", d, H, seed=1))
+        sk = iq.isoq_sketch_init(pk, m)
+        k = workloads.kv_stream_torch(1, H, n_tok, d, 2, "cuda")[0].transpose(0, 1).contiguous()
+        n_blocks = 2 * n_tok // bs
+        slots = torch.randperm(n_blocks * bs, device="cuda")[:n_tok].to(torch.int64)
+        R = pk.record_bytes
+        rec = torch.empty((n_blocks, H, bs, R), dtype=torch.uint8, device="cuda")
+        sg = torch.empty((n_blocks, H, bs, m // 8), dtype=torch.uint8, device="cuda")
+        rho = torch.empty((n_blocks, H, bs), dtype=torch.float32, device="cuda")
+        gam = torch.empty((n_blocks, H, bs), dtype=torch.float32, device="cuda")
+        fn = lambda i: iq.isoq_kv_append_qjl(pk, sk, k, slots, rec, rho, sg, gam)
+        ms = time_launches(fn, 50, 5, torch, 0.2)
+        b = n_tok * (H * (d * 2 + R + 4 + m // 8 + 4) + 8)
+        out[f"append_prefill_d{d}_m{m}"] = {"us": ms * 1e3, "GBps": b / ms / 1e6,
+                                            "frac": b / ms / 1e6 / PEAK_HBM_GBPS}
+        sk.close()
+        pk.close()
+        del k, rec, sg, rho, gam
+    return out
+
+
 def widths_side(torch, workloads):
     """Widths outside {128, 256, 512} (Sec. 5.1 zero padding where needed):
     round trip and quantize of 1,048,576 unit-norm rows (262,144 for d = 1000),
@@ -541,6 +593,7 @@ def other_configs(measure, entry, torch, np, workloads):
     out["kv_append_qjl"] = kv_append_qjl_side(torch, workloads)
     out["kv_scores"] = kv_scores_side(torch, workloads)
     out["qjl_quantize"] = qjl_side(torch, workloads)
+    out["qjl_widths"] = qjl_widths_side(torch, workloads)
     out["kv_scores_qjl"] = kv_scores_qjl_side(torch, workloads)
     out["widths"] = widths_side(torch, workloads)
     out["head_widths"] = head_widths_side(torch, workloads)
@@ -567,8 +620,8 @@ def main() -> int:
     ap.add_argument("--no-extras", action="store_true")
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the side measurements of the d=256, d=512 and KV-cache workloads")
-    ap.add_argument("--side", choices=["kv-append", "kv-append-qjl", "kv-scores", "kv-scores-qjl", "qjl", "widths",
-                                       "head-widths", "kv-cache", "block8"],
+    ap.add_argument("--side", choices=["kv-append", "kv-append-qjl", "kv-scores", "kv-scores-qjl", "qjl",
+                                       "qjl-widths", "widths", "head-widths", "kv-cache", "block8"],
                     help="run only this side measurement and print its JSON")
     ap.add_argument("--case", choices=["decode", "prefill"],
                     help="with --side kv-append or kv-append-qjl: that workload only")
@@ -592,7 +645,8 @@ def main() -> int:
         CASE = args.case
         fn = {"kv-append": kv_append_side, "kv-append-qjl": kv_append_qjl_side, "kv-scores": kv_scores_side,
               "kv-scores-qjl": kv_scores_qjl_side, "qjl": qjl_side, "widths": widths_side,
-              "head-widths": head_widths_side, "kv-cache": kv_cache_side, "block8": block8_side}[args.side]
+              "head-widths": head_widths_side, "kv-cache": kv_cache_side, "block8": block8_side,
+              "qjl-widths": qjl_widths_side}[args.side]
         print(json.dumps({"side": args.side, **fn(torch, workloads)}), flush=True)
         return 0
     tdt, ndt, esz = {"f16": (torch.float16, np.float16, 2), "f32": (torch.float32, np.float32, 4)}[args.dtype]
