@@ -876,7 +876,8 @@ static void set_packed_args(const isoq_params *p, const PackedShape &ps, int64_t
 }
 
 // isoq_quantize_qjl at the head widths 80, 96, 160 and 192: fp16 rows, one
-// rotation set, packed-row kernels; blocks walk runs of g_tpb row tiles.
+// rotation set, packed-row kernels of kPackedQjlWaves waves; blocks walk runs
+// of g_tpb row tiles.
 static isoq_status quantize_qjl_packed(const isoq_params *p, const isoq_sketch *sk, int dtype, const void *x,
                                        int64_t n, uint8_t *idx_packed, float *norms, uint8_t *signs, float *gamma,
                                        void *stream)
@@ -897,9 +898,9 @@ static isoq_status quantize_qjl_packed(const isoq_params *p, const isoq_sketch *
     if (!fn)
         return ISOQ_E_UNSUPPORTED;
     const PackedShape ps = packed_shape(p->d, p->bits, true);
-    const int64_t per_tile = (int64_t)ps.rows * (kBlockThreads / 64) * (kTileGroups / ps.chunks);
+    const int64_t per_tile = (int64_t)ps.rows * kPackedQjlWaves * packed_groups(ps.rows, ps.chunks, true);
     const int64_t tiles = (n + per_tile - 1) / per_tile;
-    const int64_t blocks0 = std::min<int64_t>(tiles, kQjlBlocks);
+    const int64_t blocks0 = std::min<int64_t>(tiles, kQjlBlocks * 4 / kPackedQjlWaves);
     const int64_t tpb = (tiles + blocks0 - 1) / blocks0;
     const int64_t blocks = (tiles + tpb - 1) / tpb;
     if (tpb > 0x7FFFFFFF)
@@ -916,7 +917,7 @@ static isoq_status quantize_qjl_packed(const isoq_params *p, const isoq_sketch *
     a.qjl_gamma = gamma;
     set_packed_args(p, ps, tpb, a);
     void *args[] = {&a};
-    return launch(fn, dim3((unsigned)blocks), args, stream);
+    return launch(fn, dim3((unsigned)blocks), args, stream, 64 * kPackedQjlWaves);
 }
 
 isoq_status isoq_quantize_qjl(const isoq_params *p, const isoq_sketch *sk, int dtype, const void *x,
@@ -1020,16 +1021,16 @@ isoq_status isoq_kv_append_qjl(const isoq_params *pk, const isoq_sketch *sk, int
         if (!fn)
             return ISOQ_E_UNSUPPORTED;
         const PackedShape ps = packed_shape(pk->d, pk->bits, true);
-        const int64_t per_tile = (int64_t)ps.rows * (kBlockThreads / 64) * (kTileGroups / ps.chunks);
+        const int64_t per_tile = (int64_t)ps.rows * kPackedQjlWaves * packed_groups(ps.rows, ps.chunks, true);
         const int64_t tiles = (n_tokens + per_tile - 1) / per_tile;
-        const int64_t by = std::max<int64_t>(1, std::min<int64_t>(tiles, kQjlBlocks / n_heads));
+        const int64_t by = std::max<int64_t>(1, std::min<int64_t>(tiles, kQjlBlocks * 4 / kPackedQjlWaves / n_heads));
         const int64_t tpb = (tiles + by - 1) / by;
         const int64_t gy = (tiles + tpb - 1) / tpb;
         if (gy > 65535)
             return ISOQ_E_UNSUPPORTED;
         set_packed_args(pk, ps, tpb, a);
         void *args[] = {&a};
-        return launch(fn, dim3((unsigned)n_heads, (unsigned)gy, 1), args, stream);
+        return launch(fn, dim3((unsigned)n_heads, (unsigned)gy, 1), args, stream, 64 * kPackedQjlWaves);
     }
     const int waves = qjl_waves(sk->m, true, pk->n_sets);
     const void *fn = qjl_kernel_for(pk->variant, pk->d, pk->bits, dtype == ISOQ_F16, sk->m, true, waves);

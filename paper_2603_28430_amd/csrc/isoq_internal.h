@@ -238,6 +238,15 @@ const void *packed_qjl_kernel_for(int variant, int d, int bits, int m, bool appe
 // Projection width of the sketch: d rounded up to a multiple of 32 (the
 // k-step of the projection's matrix instruction).
 constexpr int qjl_proj_width(int d) { return (d + 31) / 32 * 32; }
+// Waves per block of the packed-row kernels with the sketch.
+constexpr int kPackedQjlWaves = 8;
+// Row groups per wave of the packed-row kernels: kTileGroups / chunks, and
+// with the sketch at most 16 / rows, so that a wave's tile fits one 16-row
+// block of the projection.
+constexpr int packed_groups(int rows, int chunks, bool sketch)
+{
+    return sketch && 16 / rows < kTileGroups / chunks ? 16 / rows : kTileGroups / chunks;
+}
 // Blocks of the stage-2 sketch kernel with a single rotation set (each walks
 // several tiles).
 constexpr int64_t kQjlBlocks = 1024;

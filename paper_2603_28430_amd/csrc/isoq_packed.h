@@ -137,14 +137,17 @@ __device__ __forceinline__ float packed_pair_total(const float *rp, int n)
     return tot;
 }
 
-template <int VAR, int BITS, int MODE, int C, int D = 0, int QM = 0>
+template <int VAR, int BITS, int MODE, int C, int D = 0, int QM = 0, int WAVES = kBlockThreads / 64>
 __device__ __forceinline__ void packed_body(const KArgs &a)
 {
+    constexpr int BT = WAVES * 64;   // threads per block
     constexpr int H = 1 << (BITS - 1);
     constexpr int PL = kLanePL<VAR>;               // parameter floats per chunk
-    constexpr int GPW = kTileGroups / C;           // groups per wave (4 C chunks in flight per lane)
-    constexpr bool kUseLut = BITS == 4;
     constexpr bool kQjl = MODE == MODE_QJL || MODE == MODE_APPEND_QJL;
+    // groups per wave (4 C chunks in flight per lane; with the sketch a
+    // wave's rows fill at most one 16-row projection block)
+    constexpr int GPW = packed_groups(kQjl ? packed_shape(D, BITS, true).rows : 1, C, kQjl);
+    constexpr bool kUseLut = BITS == 4;
     constexpr bool kAppend = MODE == MODE_APPEND || MODE == MODE_APPEND_QJL;
     constexpr bool kEncode = MODE == MODE_QUANTIZE || MODE == MODE_QJL || kAppend;
     constexpr bool kLoadX = MODE != MODE_DEQUANTIZE;
@@ -159,11 +162,11 @@ __device__ __forceinline__ void packed_body(const KArgs &a)
     constexpr int TR = kQjl ? GPW * QV : 1;
     constexpr int ES = DP + 8;
     __shared__ __align__(16) _Float16 lds_frag[kQjl ? QM * DP : 8];
-    __shared__ __align__(16) _Float16 lds_e[kQjl ? (kBlockThreads / 64) * TR * ES : 8];
+    __shared__ __align__(16) _Float16 lds_e[kQjl ? WAVES * TR * ES : 8];
 
     __shared__ float lds_levels[16];
     __shared__ __align__(16) LutEntry lds_lut[kUseLut && kLoadX ? kLutMaxCells : 1];
-    __shared__ float lds_pairs[kBlockThreads / 2];   // 32 pair sums per wave
+    __shared__ float lds_pairs[BT / 2];   // 32 pair sums per wave
     // Full's 128 bytes per chunk (8-D: 256) are staged through LDS when the
     // block has one set (per-lane global loads of them move more through the
     // vector memory pipe than the rows do); Fast and 2-D read their 32 bytes
@@ -181,7 +184,7 @@ __device__ __forceinline__ void packed_body(const KArgs &a)
     const int64_t rowb = (int64_t)a.g_d * 2;       // fp16 rows
     const int64_t recb = (int64_t)L * C * BITS;    // d b / 8
     const int TPB = kQjl ? a.g_tpb : kAppend ? 1 : packed_tiles_per_block(VAR, C);   // row tiles per block
-    const int64_t base0 = (int64_t)(kAppend ? blockIdx.y : blockIdx.x) * TPB * (kBlockThreads / 64) * GPW;
+    const int64_t base0 = (int64_t)(kAppend ? blockIdx.y : blockIdx.x) * TPB * WAVES * GPW;
     // append: the block's head, its input row stride and cache addressing
     const int64_t head = kAppend ? (int64_t)xcd_head(blockIdx.x, a.n_heads, rowb % 128 != 0) : 0;
     const int64_t xstride = kAppend ? (int64_t)a.n_heads * rowb : rowb;
@@ -193,7 +196,7 @@ __device__ __forceinline__ void packed_body(const KArgs &a)
     if constexpr (kUseLut && kLoadX) {
         const u32x4 *s4 = reinterpret_cast<const u32x4 *>(a.lut);
         u32x4 *d4 = reinterpret_cast<u32x4 *>(lds_lut);
-        for (int i = threadIdx.x; i < a.lut_cells; i += kBlockThreads)
+        for (int i = threadIdx.x; i < a.lut_cells; i += BT)
             d4[i] = s4[i];
     }
     // rotation parameters of the lane's chunks: once, when the whole block
@@ -203,7 +206,7 @@ __device__ __forceinline__ void packed_body(const KArgs &a)
     if (kStage && uni) {
         const u32x4 *s4 = reinterpret_cast<const u32x4 *>(a.params + bset * a.g_set_stride);
         u32x4 *d4 = reinterpret_cast<u32x4 *>(lds_params);
-        for (int i = threadIdx.x; i < C * L * (PL / 4); i += kBlockThreads)
+        for (int i = threadIdx.x; i < C * L * (PL / 4); i += BT)
             d4[i] = s4[i];
     }
     if constexpr (kQjl) {
@@ -211,10 +214,10 @@ __device__ __forceinline__ void packed_body(const KArgs &a)
         // d, and rows a ragged tile leaves unwritten, stay zero)
         const u32x4 *f4 = reinterpret_cast<const u32x4 *>(a.qjl_frag + bset * (int64_t)(QM * DP));
         u32x4 *g4 = reinterpret_cast<u32x4 *>(lds_frag);
-        for (int i = threadIdx.x; i < QM * DP / 8; i += kBlockThreads)
+        for (int i = threadIdx.x; i < QM * DP / 8; i += BT)
             g4[i] = f4[i];
         u32x4 *e4 = reinterpret_cast<u32x4 *>(lds_e);
-        for (int i = threadIdx.x; i < (kBlockThreads / 64) * TR * ES / 8; i += kBlockThreads)
+        for (int i = threadIdx.x; i < WAVES * TR * ES / 8; i += BT)
             e4[i] = u32x4{0u, 0u, 0u, 0u};
     }
     if (MODE == MODE_DEQUANTIZE || (kUseLut && kLoadX) || (kStage && uni) || kQjl)
@@ -253,13 +256,13 @@ __device__ __forceinline__ void packed_body(const KArgs &a)
         return ((int64_t)blk * a.n_heads + head) * a.block_size + (su - blk * a.block_size);
     };
 
-    // ---- per tile, the wave's GPW groups (4u + w of the tile's): every load
+    // ---- per tile, the wave's GPW groups (WAVES u + w of the tile's): every load
     //      first, then compute and store group by group.  One chunk per
     //      lane: a group is one stretch of V L chunks (flat addressing, chunk
     //      = lane); two: lane sub of row q owns chunks sub and sub + L of that
     //      row.  The tile test is block-uniform (no barrier follows).
     for (int tt = 0; tt < TPB; tt++) {
-        const int64_t base = base0 + (int64_t)tt * (kBlockThreads / 64) * GPW;
+        const int64_t base = base0 + (int64_t)tt * WAVES * GPW;
         if (base * V >= a.n)
             return;
         Raw<true> raw[kLoadX ? GPW : 1][C];
@@ -269,7 +272,7 @@ __device__ __forceinline__ void packed_body(const KArgs &a)
 #pragma unroll
         for (int u = 0; u < GPW; u++) {
             // a group past the end re-reads group 0 (and is neither computed nor stored)
-            const int64_t g0 = (base + 4 * u + w) * V;
+            const int64_t g0 = (base + WAVES * u + w) * V;
             const int64_t grow = g0 < a.n ? g0 : 0;
             const int rows = (int)min((int64_t)V, a.n - grow);   // rows of data in the group
             const int nv = rows * L;                               // lanes holding data
@@ -298,7 +301,7 @@ __device__ __forceinline__ void packed_body(const KArgs &a)
         float *pairs = lds_pairs + w * 32;
 #pragma unroll
         for (int u = 0; u < GPW; u++) {
-            const int64_t grow = (base + 4 * u + w) * V;
+            const int64_t grow = (base + WAVES * u + w) * V;
             if (grow >= a.n)
                 break;
             const int rows = (int)min((int64_t)V, a.n - grow);
@@ -454,7 +457,7 @@ __device__ __forceinline__ void packed_body(const KArgs &a)
                 if (ar >= TR)
                     return nullptr;
                 const int gu = ar / QV;
-                const int64_t row = (base + 4 * gu + w) * QV + (ar - gu * QV);
+                const int64_t row = (base + WAVES * gu + w) * QV + (ar - gu * QV);
                 if (row >= a.n)
                     return nullptr;
                 int64_t orow = row;
@@ -483,11 +486,12 @@ __global__ __launch_bounds__(kBlockThreads) void packed_append_kernel(const KArg
     packed_body<VAR, BITS, MODE_APPEND, C>(blockIdx.z == 0 ? k : v);
 }
 
-// With the stage-2 sketch: width D, m = QM sign bits.
+// With the stage-2 sketch: width D, m = QM sign bits, kPackedQjlWaves waves
+// per block (one staged projection for twice the waves of the other modes).
 template <int VAR, int D, int BITS, int MODE, int QM>
-__global__ __launch_bounds__(kBlockThreads) void packed_qjl_kernel(const KArgs a)
+__global__ __launch_bounds__(kPackedQjlWaves * 64) void packed_qjl_kernel(const KArgs a)
 {
-    packed_body<VAR, BITS, MODE, packed_shape(D, BITS, true).chunks, D, QM>(a);
+    packed_body<VAR, BITS, MODE, packed_shape(D, BITS, true).chunks, D, QM, kPackedQjlWaves>(a);
 }
 
 template <int VAR, int BITS, int C>

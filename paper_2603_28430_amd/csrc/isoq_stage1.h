@@ -334,6 +334,11 @@ __device__ __forceinline__ void qjl_project(const _Float16 *frag, const _Float16
     // one block of 16 rows at a time (its fragments and accumulators only)
 #pragma unroll 1
     for (int rb = 0; rb < RB; rb++) {
+        // an offset the compiler cannot see through (it is zero), so that the
+        // projection's fragments are read where they are used rather than
+        // hoisted out of this loop and held in registers across it
+        int fo = 0;
+        asm volatile("" : "+s"(fo));
         half8 E[KS];
         const int ar = 16 * rb + r16;   // the tile row of this lane's column
 #pragma unroll
@@ -356,9 +361,12 @@ __device__ __forceinline__ void qjl_project(const _Float16 *frag, const _Float16
         for (int ks = 0; ks < KS; ks++) {
 #pragma unroll
             for (int nt = 0; nt < NT; nt++) {
-                const half8 s = *reinterpret_cast<const half8 *>(frag + ((nt * KS + ks) * 64 + l) * 8);
+                const half8 s = *reinterpret_cast<const half8 *>(frag + fo + ((nt * KS + ks) * 64 + l) * 8);
                 acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(s, E[ks], acc[nt], 0, 0, 0);
             }
+            // at most one k-step's fragments in flight
+            if constexpr (KS > 4)
+                __builtin_amdgcn_sched_barrier(0);
         }
         // bit 4 nt + i is result register i of tile nt: pushed from the top
         // (tile NT - 1, register 3) down
