@@ -29,15 +29,16 @@ __global__ __launch_bounds__(WAVES * 64) void qjl_kernel(const KArgs a)
     using S = Stage1<VAR, D, BITS, F16, MODE, false, QM, WAVES>;
     __shared__ __align__(16) LutEntry lds_lut[S::kUseLut ? kLutMaxCells : 1];
     __shared__ __align__(16) _Float16 lds_frag[QM * D];
-    __shared__ __align__(16) _Float16 lds_e[WAVES * S::kTileRows * S::kEStride];
     if constexpr (F16 && quad_layout(VAR, D)) {
         using M = Stage1M<VAR, D, BITS, MODE, QM, WAVES>;
         static_assert(M::kTileRows == S::kTileRows, "the two layouts tile rows alike");
         __shared__ __align__(16) u32x4 lds_par[M::kLdsWords];
+        __shared__ __align__(16) _Float16 lds_e[WAVES * M::kTileRows * M::kEStride];
         M::run(a, lds_lut, lds_par, lds_frag, lds_e);
     } else {
         __shared__ float lds_levels[16];
         __shared__ __align__(16) float lds_params[S::LPV * S::PL];
+        __shared__ __align__(16) _Float16 lds_e[WAVES * S::kTileRows * S::kEStride];
         S::run(a, lds_levels, lds_params, lds_lut, lds_frag, lds_e);
     }
 }

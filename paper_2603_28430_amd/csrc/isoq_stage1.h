@@ -306,6 +306,14 @@ __device__ __forceinline__ uint32_t ballot_encode(const float y[8], const float 
 }
 
 // ---- stage-2 projection of a wave's error tile -------------------------------------
+// Chunk-position swizzle of an unpadded error tile (rows of D halfs, 16-byte
+// chunks): chunk c of tile row r is stored at c ^ err_swizzle(r).  With the
+// matrix-core encoder's writes (lanes 4b + i: chunk b of row 4q + i) and the
+// projection's reads (lane l: row l mod 16, chunk 4 ks + l / 16), every 8 lanes
+// of a 16-byte access then touch 8 different 16-byte bank groups of the 32
+// banks; the padded layout (row stride D + 8 halfs) conflicted on the writes.
+__device__ __forceinline__ int err_swizzle(int r) { return (2 * (r & 3)) ^ ((r >> 2) & 3); }
+
 // P = E S'^T with E the tile's error rows (fp16, LDS, row stride ES halfs) and
 // S' = S T^{-1} (fp16, LDS, fragment order), computed transposed, P^T = S' E^T,
 // on v_mfma_f32_16x16x32_f16: for column tile nt lane l supplies row l % 16 of
@@ -320,8 +328,9 @@ __device__ __forceinline__ uint32_t ballot_encode(const float y[8], const float 
 // between lanes.  The sign bits of rho * P (rho > 0 unless the row is zero,
 // whose e is zero) are the sketch.  A tile of more than 16 rows takes one such
 // product per block of 16 rows.  dst_of(ar) is the sign row of tile row ar, or
-// nullptr where nothing is written.
-template <int D, int QM, int TR, int ES, typename DstOf>
+// nullptr where nothing is written.  SWZ: the tile's rows are unpadded
+// (ES = D) and chunk c of row r sits at chunk position c ^ err_swizzle(r).
+template <int D, int QM, int TR, int ES, bool SWZ = false, typename DstOf>
 __device__ __forceinline__ void qjl_project(const _Float16 *frag, const _Float16 *eq, DstOf dst_of)
 {
     typedef _Float16 half8 __attribute__((ext_vector_type(8)));
@@ -344,7 +353,8 @@ __device__ __forceinline__ void qjl_project(const _Float16 *frag, const _Float16
 #pragma unroll
         for (int ks = 0; ks < KS; ks++) {
             if (ar < TR) {
-                E[ks] = *reinterpret_cast<const half8 *>(eq + ar * ES + 32 * ks + 8 * kq);
+                const int pos = SWZ ? (4 * ks + kq) ^ err_swizzle(ar) : 4 * ks + kq;
+                E[ks] = *reinterpret_cast<const half8 *>(eq + ar * ES + 8 * pos);
             } else {
 #pragma unroll
                 for (int i = 0; i < 8; i++)

@@ -96,7 +96,7 @@ struct Stage1M {
     static constexpr bool kRoundtrip = MODE == MODE_ROUNDTRIP;
     static constexpr bool kEncode = !kRoundtrip;
     static constexpr int kTileRows = RT;
-    static constexpr int kEStride = D + 8;
+    static constexpr int kEStride = D;   // unpadded, chunk positions swizzled (err_swizzle)
     static_assert(quad_layout(VAR, D), "quad layout variants and widths");
     static_assert(MODE != MODE_DEQUANTIZE, "the decoder keeps the VALU layout");
     static_assert(kTileGroups % SPQ == 0, "a row quad's loads fit in a tile");
@@ -595,7 +595,7 @@ struct Stage1M {
                 asm("v_cvt_pk_f16_f32 %0, %1, %2" : "=v"(v) : "v"(e[2 * k]), "v"(e[2 * k + 1]));
                 hv[k] = v;
             }
-            *reinterpret_cast<u32x4 *>(eq + erow * kEStride + 8 * c) = hv;
+            *reinterpret_cast<u32x4 *>(eq + erow * kEStride + 8 * (c ^ err_swizzle(erow))) = hv;
         }
         return s2;
     }
@@ -605,7 +605,7 @@ struct Stage1M {
     __device__ static __forceinline__ void sketch(const KArgs &a, const _Float16 *frag, const _Float16 *eq,
                                                   int64_t row0, int w)
     {
-        qjl_project<D, QM, kTileRows, kEStride>(frag, eq, [&](int ar) -> uint32_t * {
+        qjl_project<D, QM, kTileRows, kEStride, true>(frag, eq, [&](int ar) -> uint32_t * {
             const int64_t row = row0 + 4 * bquad_of_wquad(ar >> 2, w) + (ar & 3);
             if (ar >= kTileRows || row >= a.n)
                 return nullptr;
