@@ -160,7 +160,11 @@ __device__ __forceinline__ void packed_body(const KArgs &a)
     constexpr int QV = kQjl ? packed_shape(D, BITS, true).rows : 1;
     constexpr int DP = kQjl ? qjl_proj_width(D) : 32;
     constexpr int TR = kQjl ? GPW * QV : 1;
-    constexpr int ES = DP + 8;
+    // widths whose projection width is a multiple of 64 (d = 192) keep rows
+    // unpadded with swizzled chunk positions (err_swizzle), which keeps the
+    // block's LDS under half the CU's
+    constexpr bool kSwz = DP % 64 == 0;
+    constexpr int ES = kSwz ? DP : DP + 8;
     __shared__ __align__(16) _Float16 lds_frag[kQjl ? QM * DP : 8];
     __shared__ __align__(16) _Float16 lds_e[kQjl ? WAVES * TR * ES : 8];
 
@@ -382,8 +386,11 @@ __device__ __forceinline__ void packed_body(const KArgs &a)
                             asm("v_cvt_pk_f16_f32 %0, %1, %2" : "=v"(h2) : "v"(e[2 * i]), "v"(e[2 * i + 1]));
                             hv[i] = h2;
                         }
-                        if (on)
-                            *reinterpret_cast<u32x4 *>(lds_e + (w * TR + u * QV + q) * ES + 8 * (sub + k * L)) = hv;
+                        if (on) {
+                            const int er = u * QV + q, ec = sub + k * L;
+                            *reinterpret_cast<u32x4 *>(lds_e + (w * TR + er) * ES +
+                                                       8 * (kSwz ? ec ^ err_swizzle(er) : ec)) = hv;
+                        }
                     }
                 }
                 if constexpr (kQjl) {
@@ -453,7 +460,7 @@ __device__ __forceinline__ void packed_body(const KArgs &a)
         if constexpr (kQjl) {
             // the tile's projection: tile row ar is row ar mod QV of group
             // ar / QV of the wave
-            qjl_project<DP, QM, TR, ES>(lds_frag, lds_e + w * TR * ES, [&](int ar) -> uint32_t * {
+            qjl_project<DP, QM, TR, ES, kSwz>(lds_frag, lds_e + w * TR * ES, [&](int ar) -> uint32_t * {
                 if (ar >= TR)
                     return nullptr;
                 const int gu = ar / QV;
