@@ -180,7 +180,10 @@ isoq_status isoq_roundtrip(const isoq_params *p, int dtype, const void *x, int64
  * autoregressive decoding (the fused KV-cache compression the paper names as
  * its next step, Sec. 10): the new key and value rows are encoded as by
  * isoq_quantize (Algorithm 1's encoder) and their index records and norms are
- * written straight into the cache slots of their tokens, in one launch.
+ * written straight into the cache slots of their tokens.  Any d in 1..1024:
+ * d in {64, 128, 256, 512}, and fp16 rows at 80, 96, 160 and 192, take one
+ * launch for both tensors; other widths, and fp32 rows at those four, one
+ * launch of the width-generic encoder per tensor.
  *
  *   pk, pv      handles of the K and V quantizers.  They must agree in variant,
  *               d and bits; each has n_sets == 1 or n_sets == n_heads, and the
@@ -197,10 +200,11 @@ isoq_status isoq_roundtrip(const isoq_params *p, int dtype, const void *x, int64
  *               contiguous.  Record format as in isoq_quantize.
  *   k_rho, v_rho  device, fp32 [n_blocks][n_heads][block_size].
  * Limits: n_tokens * n_heads < 2^31, n_blocks * block_size < 2^31, n_heads and
- * block_size >= 1, and at most 65,535 launch blocks of tokens (n_tokens up to
- * 8,388,480 at d = 64, 4,194,240 at d = 128, 2,097,120 at d = 256, 1,048,560
- * at d = 512; fp16 rows: 6,291,360 at d = 80, 5,242,800 at d = 96, 3,145,680
- * at d = 160, 2,621,400 at d = 192); beyond that ISOQ_E_UNSUPPORTED.  Distinct tokens must map to distinct slots (a repeated slot
+ * block_size >= 1, and for the one-launch shapes at most 65,535 launch blocks
+ * of tokens (n_tokens up to 8,388,480 at d = 64, 4,194,240 at d = 128,
+ * 2,097,120 at d = 256, 1,048,560 at d = 512; fp16 rows: 6,291,360 at d = 80,
+ * 5,242,800 at d = 96, 3,145,680 at d = 160, 2,621,400 at d = 192); beyond
+ * that ISOQ_E_UNSUPPORTED.  Distinct tokens must map to distinct slots (a repeated slot
  * is written by both rows in an unspecified order).  Slots not named are left
  * untouched.  n_tokens = 0 is a no-op.
  */

@@ -142,6 +142,9 @@ const void *packed_kernel(int variant, int bits, int mode, int chunks)
     return nullptr;
 }
 
+// Widths outside {64, 128, 256, 512}: the packed-row kernels where a shape
+// has them (not for append, whose packed kernel has a grid of its own), else
+// the generic kernels.
 isoq_status run_generic(const isoq_params *p, int dtype, int mode, KArgs &a, void *stream)
 {
     // the generic kernels' slots: 4 coordinates (a 2-D row of 4k + 2
@@ -153,7 +156,7 @@ isoq_status run_generic(const isoq_params *p, int dtype, int mode, KArgs &a, voi
     const bool f16 = dtype == ISOQ_F16;
     const PackedShape ps = packed_shape(p->d, p->bits, f16);
     const bool pairs = sw == 4 && f16 && p->d % 4 == 2;
-    const int v = ps.rows;
+    const int v = mode == MODE_APPEND ? 0 : ps.rows;
     const void *fn = v > 0 ? packed_kernel(p->variant, p->bits, mode, ps.chunks)
                      : p->variant == VAR_FULL   ? generic_kernel_full(slots, p->bits, f16, mode, pairs)
                      : p->variant == VAR_FAST   ? generic_kernel_fast(slots, p->bits, f16, mode, pairs)
@@ -230,9 +233,8 @@ const char *isoq_status_string(isoq_status s)
     case ISOQ_OK: return "ok";
     case ISOQ_E_INVALID: return "invalid argument";
     case ISOQ_E_UNSUPPORTED:
-        return "unsupported shape (d in 1..1024, bits in {2,3,4}; the KV append needs d in {64,128,256,512} or fp16 "
-               "rows at 80, 96, 160, 192, the score call d in {64,80,96,128,160,192,256,512}, the sketch d in "
-               "{64,128,256}) or size limit";
+        return "unsupported shape (d in 1..1024, bits in {2,3,4}; the score calls and the sketch need d in "
+               "{64,80,96,128,160,192,256,512}) or size limit";
     case ISOQ_E_NULL: return "null pointer";
     case ISOQ_E_ALIGN: return "misaligned pointer";
     case ISOQ_E_HIP: return "HIP runtime error";
@@ -563,10 +565,10 @@ isoq_status isoq_kv_append(const isoq_params *pk, const isoq_params *pv, int dty
     // fp16 rows at d = 80, 96, 160 and 192 use the packed-row kernels (rows
     // of a group back to back across the wave; with 3 bits a row spans a
     // multiple of 4 lanes, or 10 lanes at d = 80 with one chunk per lane)
+    // other shapes (fp32 rows, other widths) use the generic kernels
     const PackedShape ps = packed_shape(pk->d, pk->bits, true);
     const bool packed = packed_decode(pk->d, pk->bits, dtype == ISOQ_F16);
-    if (!tuned_d(pk->d) && !packed)
-        return ISOQ_E_UNSUPPORTED;
+    const bool generic = !tuned_d(pk->d) && !packed;
     if ((pk->n_sets != 1 && pk->n_sets != n_heads) || (has_v && pv->n_sets != 1 && pv->n_sets != n_heads))
         return ISOQ_E_INVALID;
     if (n_tokens > 0x7FFFFFFF / n_heads || n_blocks > 0x7FFFFFFF / block_size)
@@ -582,6 +584,26 @@ isoq_status isoq_kv_append(const isoq_params *pk, const isoq_params *pv, int dty
     isoq_status st = check_device(pk);
     if (st != ISOQ_OK)
         return st;
+    if (generic) {
+        // one launch per tensor over the n_tokens * n_heads (token, head)
+        // rows of its input, row t n_heads + h with set h (or set 0)
+        for (int t = 0; t < (has_v ? 2 : 1); t++) {
+            KArgs a{};
+            a.x = t == 0 ? k_new : v_new;
+            a.rec_out = t == 0 ? k_idx : v_idx;
+            a.norms_out = t == 0 ? k_rho : v_rho;
+            a.n = n_tokens * n_heads;
+            a.rows_per_set = 1;
+            a.slots = slot_mapping;
+            a.n_slots = n_blocks * block_size;
+            a.n_heads = (uint32_t)n_heads;
+            a.block_size = (uint32_t)block_size;
+            a.div_block = make_fastdiv((uint32_t)block_size);
+            if ((st = run_generic(t == 0 ? pk : pv, dtype, MODE_APPEND, a, stream)) != ISOQ_OK)
+                return st;
+        }
+        return ISOQ_OK;
+    }
     // one kernel for both tensors; block (x, y, z) = (head, token range, K|V)
     const bool quad = dtype == ISOQ_F16 && quad_layout(pk->variant, pk->d);
     const void *fn = packed ? packed_kernel(pk->variant, pk->bits, MODE_APPEND, ps.chunks)

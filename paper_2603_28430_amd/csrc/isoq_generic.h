@@ -15,6 +15,11 @@
 // (fp16) or 16-byte (fp32) access per slot; fp16 rows of other even widths in
 // coordinate pairs (4-byte accesses: such a row starts on a 4-byte boundary,
 // PAIRS instantiations); the rest element by element.
+//
+// Append (MODE_APPEND): the rows are the (token, head) rows of a
+// [n_tokens][n_heads][d] tensor in order, row r = token n_heads + head, with
+// set r mod n_sets (rows_per_set = 1: set h for head h, or set 0); each row's
+// record and norm go to its token's cache row instead of row r.
 #pragma once
 
 #include <type_traits>
@@ -193,7 +198,9 @@ __global__ __launch_bounds__(kBlockThreads) void generic_kernel(const KArgs a)
     constexpr int H = 1 << (BITS - 1);
     constexpr int ESZ = F16 ? 2 : 4;
     constexpr bool kLoadX = MODE != MODE_DEQUANTIZE;
-    static_assert(MODE == MODE_ROUNDTRIP || MODE == MODE_QUANTIZE || MODE == MODE_DEQUANTIZE, "mode");
+    constexpr bool kAppend = MODE == MODE_APPEND;
+    constexpr bool kEncode = MODE == MODE_QUANTIZE || kAppend;
+    static_assert(MODE == MODE_ROUNDTRIP || MODE == MODE_QUANTIZE || MODE == MODE_DEQUANTIZE || kAppend, "mode");
 
     __shared__ float lev_s[16];
     if constexpr (MODE == MODE_DEQUANTIZE) {
@@ -215,9 +222,9 @@ __global__ __launch_bounds__(kBlockThreads) void generic_kernel(const KArgs a)
     // the lane's row of group 0; group t is t R rows further (wave-uniform
     // strides, so per-group addresses are one add)
     const char *x0 = kLoadX ? static_cast<const char *>(a.x) + row0 * row_bytes : nullptr;
-    char *y0 = MODE != MODE_QUANTIZE ? static_cast<char *>(a.y) + row0 * row_bytes : nullptr;
+    char *y0 = !kEncode ? static_cast<char *>(a.y) + row0 * row_bytes : nullptr;
     const uint8_t *ri0 = MODE == MODE_DEQUANTIZE ? a.rec_in + row0 * nb : nullptr;
-    uint8_t *ro0 = MODE == MODE_QUANTIZE ? a.rec_out + row0 * nb : nullptr;
+    uint8_t *ro0 = MODE == MODE_QUANTIZE ? a.rec_out + row0 * nb : nullptr;   // append: per row
     const int64_t xstep = (int64_t)R * row_bytes, rstep = (int64_t)R * nb;
 
     // ---- loads of every group first
@@ -334,22 +341,38 @@ __global__ __launch_bounds__(kBlockThreads) void generic_kernel(const KArgs a)
                     yq[k][c] = lev_s[(pin[t][k] >> (BITS * c)) & (2 * H - 1)] * rho;
         }
 
-        if constexpr (MODE == MODE_QUANTIZE) {
+        if constexpr (kEncode) {
+            // the row's record and norm: row `row`, or (append) the cache
+            // row of its token's slot (a skipped slot, < 0 or past the
+            // cache, writes nothing)
+            bool wr = ok;
+            int64_t orow = row;
+            if constexpr (kAppend) {
+                const uint32_t ru = ok ? (uint32_t)row : 0u;
+                const uint32_t token = ru / a.n_heads;
+                const uint32_t head = ru - token * a.n_heads;
+                const int64_t sl = ok ? a.slots[token] : -1;
+                wr = ok && sl >= 0 && sl < a.n_slots;
+                const uint32_t su = wr ? (uint32_t)sl : 0u;
+                const uint32_t blk = fast_div(su, a.div_block);
+                orow = ((int64_t)blk * a.n_heads + head) * a.block_size + (su - blk * a.block_size);
+            }
+            uint8_t *rec = kAppend ? a.rec_out + orow * nb : ro0 + t * rstep;
 #pragma unroll
             for (int k = 0; k < BPL; k++) {
                 const int j = sub + G * k;
                 if constexpr (SW == 8) {
-                    if (ok && j < slots)
-                        gen_write_slot8<BITS>(ro0 + t * rstep, j, pk[k]);
+                    if (wr && j < slots)
+                        gen_write_slot8<BITS>(rec, j, pk[k]);
                 } else {
                     // the next slot of an even slot sits on the next lane (G is even)
                     const uint32_t next = BITS == 3 ? (uint32_t)__shfl_down((int)pk[k], 1, 64) : 0u;
-                    if (ok && j < slots)
-                        gen_write_slot<BITS>(ro0 + t * rstep, j, nb, pk[k], next);
+                    if (wr && j < slots)
+                        gen_write_slot<BITS>(rec, j, nb, pk[k], next);
                 }
             }
-            if (ok && sub == 0)
-                a.norms_out[row] = rho;
+            if (wr && sub == 0)
+                a.norms_out[orow] = rho;
         } else {
 #pragma unroll
             for (int k = 0; k < BPL; k++) {
@@ -400,6 +423,7 @@ const void *gen_pick_mode(int slots, int mode)
     case MODE_ROUNDTRIP: return gen_pick_shape<VAR, BITS, F16, MODE_ROUNDTRIP, PAIRS>(slots);
     case MODE_QUANTIZE: return gen_pick_shape<VAR, BITS, F16, MODE_QUANTIZE, PAIRS>(slots);
     case MODE_DEQUANTIZE: return gen_pick_shape<VAR, BITS, F16, MODE_DEQUANTIZE, PAIRS>(slots);
+    case MODE_APPEND: return gen_pick_shape<VAR, BITS, F16, MODE_APPEND, PAIRS>(slots);
     }
     return nullptr;
 }

@@ -57,7 +57,7 @@ def check_tensor(variant, d, bits, rot, levels, n_sets, x, slots, n_heads, block
         rows = (valid_t[:, None] * n_heads + np.arange(n_heads)[None, :]).reshape(-1)
         o = Oracle(variant, d, bits, rot, levels, x[rows], n_sets=n_sets, rows_per_set=1, rows=rows,
                    selected=True)
-        o.check_indices(oracle.unpack(ci[crow], d, bits))
+        o.check_indices(oracle.unpack(ci[crow], oracle.padded_width(variant, d), bits))
         o.check_norms(cr[crow])
         # the same records as the plain encoder on the same rows and sets
         xg = torch.from_numpy(np.ascontiguousarray(x)).cuda()
@@ -149,15 +149,27 @@ def test_append_head_widths_xcd_head_order(variant, d, n_heads, bs):
              sets_k=n_heads, sets_v=1, seed=d + n_heads + bs)
 
 
-def test_append_head_widths_fp32_unsupported():
-    pk = iq.isoq_params_init("fast", 96, 3, 1)
-    k = torch.zeros((4, 2, 96), dtype=torch.float32, device="cuda")
-    slots = torch.arange(4, dtype=torch.int64, device="cuda")
-    rec = torch.zeros((2, 2, 16, pk.record_bytes), dtype=torch.uint8, device="cuda")
-    rho = torch.zeros((2, 2, 16), dtype=torch.float32, device="cuda")
-    with pytest.raises(iq.IsoqError) as e:
-        iq.isoq_kv_append(pk, k, slots, rec, rho)
-    assert e.value.status == 2
+@pytest.mark.parametrize("variant,d,bits,dtype", [("fast", 96, 3, "f32"), ("full", 80, 4, "f32"), ("2d", 160, 2, "f32"),
+                                                  ("full", 192, 3, "f32"), ("8d", 96, 3, "f32"), ("full", 13, 3, "f16"),
+                                                  ("fast", 72, 2, "f32"), ("2d", 98, 3, "f16"), ("full", 100, 4, "f16"),
+                                                  ("8d", 40, 2, "f16"), ("fast", 130, 3, "f16"), ("2d", 7, 4, "f32"),
+                                                  ("full", 1, 2, "f16"), ("full", 1000, 3, "f32"), ("8d", 9, 4, "f32")])
+def test_append_generic_widths(variant, d, bits, dtype):
+    """Shapes without a one-launch kernel (fp32 rows at 80, 96, 160 and 192,
+    every other width; odd widths, 2-D rows of 4k + 2 coordinates, 8-D rows
+    with a partial block): the width-generic encoder, one launch per tensor
+    over its (token, head) rows.  Sets per head for K, one set for V, odd
+    block size, skipped slots."""
+    run_case(variant, d, bits, dtype, n_tokens=53, n_heads=5, block_size=7, n_blocks=10, sets_k=5, sets_v=1,
+             seed=d + bits)
+
+
+@pytest.mark.parametrize("dtype", ["f16", "f32"])
+def test_append_generic_many_blocks(dtype):
+    """Enough (token, head) rows for many launch blocks of the generic
+    encoder, rows of one token spread over several waves' row groups."""
+    run_case("fast", 72, 3, dtype, n_tokens=700, n_heads=12, block_size=16, n_blocks=60, sets_k=12, sets_v=12,
+             seed=7)
 
 
 @pytest.mark.parametrize("n_heads,block_size,sets_k,sets_v", [(1, 1, 1, 1), (5, 48, 5, 1),

@@ -122,9 +122,9 @@ def test_widths_large_sampled(variant, d, dtype):
 
 
 def test_widths_unsupported_calls():
-    """Widths outside the generic range, and the KV / score / sketch calls at
-    a width outside theirs (d = 100), return
-    ISOQ_E_UNSUPPORTED before any launch."""
+    """Widths outside the generic range, and the score and sketch calls at a
+    width outside theirs (d = 100), return ISOQ_E_UNSUPPORTED before any
+    launch (the append takes every width)."""
     with pytest.raises(iq.IsoqError) as e:
         iq.isoq_params_init("full", 1025, 3, 1)
     assert e.value.status == 2
@@ -135,11 +135,7 @@ def test_widths_unsupported_calls():
     z = lambda *s, dt=torch.uint8: torch.zeros(s, dtype=dt, device="cuda")
     R = p.record_bytes
     lib = iq.isoquant.lib
-    k = z(4, 1, 100, dt=torch.float16)
-    slots = torch.arange(4, dtype=torch.int64, device="cuda")
     rec, rho = z(2, 1, 16, R), z(2, 1, 16, dt=torch.float32)
-    assert lib.isoq_kv_append(p.handle, None, 1, k.data_ptr(), None, slots.data_ptr(), 4, 1, rec.data_ptr(),
-                              rho.data_ptr(), None, None, 2, 16, None) == 2
     q = z(1, 1, 100, dt=torch.float16)
     tab, lens = z(1, 2, dt=torch.int32), torch.ones((1,), dtype=torch.int32, device="cuda")
     out = z(1, 1, 32, dt=torch.float32)
