@@ -219,7 +219,11 @@ isoq_status isoq_kv_append(const isoq_params *pk, const isoq_params *pv, int dty
  * a paged cache written by isoq_kv_append, without dequantizing the keys.  A
  * key's reconstruction is rho T^{-1}(c[idx]) and T is orthogonal (Prop. 1), so
  * <q, k_hat> = rho <T q, c[idx]>: each query is rotated once and the logits
- * are sums of table lookups over the packed index records.
+ * are sums of table lookups over the packed index records.  Any d in 1..1024:
+ * at d in {64, 80, 96, 128, 160, 192, 256, 512} with lookup tables; at other
+ * widths a width-generic kernel sums (T q_pad)_j c[idx_j] over the record's
+ * zero-padded coordinates (q_pad: q with zeros past d), one workgroup per
+ * query head.
  *
  *   pk          the K quantizer (n_sets == 1 or n_sets == n_kv_heads; key head h
  *               uses set h, resp. 0).
@@ -237,11 +241,11 @@ isoq_status isoq_kv_append(const isoq_params *pk, const isoq_params *pv, int dty
  *               t < min(seq_lens[s], max_len, max_blocks_per_seq * block_size).
  *               Other positions, and positions whose block id lies outside
  *               [0, n_blocks), are not written.
- * Limits: n_seqs <= 65535, max_blocks_per_seq * block_size < 2^31, and the
- * tables of one key head's query group must fit in LDS: group * (d/F * 2^(F
- * bits) + d) * 4 bytes with F = 2 for 2 and 3 bits, F = 1 for 4 bits
- * (ISOQ_E_UNSUPPORTED otherwise; e.g. at d = 128, 3 bits, 16.9 KB per query
- * head).  Logits are accumulated in fp32.
+ * Limits: n_seqs <= 65535, max_blocks_per_seq * block_size < 2^31, and at the
+ * table widths the tables of one key head's query group must fit in LDS:
+ * group * (d/F * 2^(F bits) + d) * 4 bytes with F = 2 for 2 and 3 bits, F = 1
+ * for 4 bits (ISOQ_E_UNSUPPORTED otherwise; e.g. at d = 128, 3 bits, 16.9 KB
+ * per query head).  Logits are accumulated in fp32.
  */
 isoq_status isoq_kv_scores(const isoq_params *pk, int dtype, const void *q, int n_seqs,
                            int n_q_heads, int n_kv_heads, const uint8_t *k_idx, const float *k_rho,

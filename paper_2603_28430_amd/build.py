@@ -48,7 +48,7 @@ def build(verbose: bool = False) -> str:
     for src in ("isoq_kernels.hip", "isoq_kernels_8d.hip", "isoq_kernels_m.hip", "isoq_scores.hip",
                 "isoq_scores_8d.hip", "isoq_scores_qjl.hip", "isoq_qjl.hip", "isoq_generic_full.hip", "isoq_generic_fast.hip",
                 "isoq_generic_2d.hip", "isoq_generic_8d.hip", "isoq_qjl_append.hip", "isoq_packed.hip",
-                "isoq_packed_8d.hip", "isoq_packed_qjl.hip"):
+                "isoq_packed_8d.hip", "isoq_packed_qjl.hip", "isoq_scores_generic.hip"):
         jobs.append([HIPCC, *DEVICE_FLAGS, *inc, "-c", os.path.join(CSRC, src), "-o",
                      os.path.join(obj_dir, src + ".o")])
     for src in ("isoq_api.cpp", "isoq_host_params.cpp"):

@@ -10,6 +10,7 @@
 #include <vector>
 
 #include "isoq_internal.h"
+#include "isoq_scores_generic.h"
 #include "isoquant.h"
 
 struct isoq_params {
@@ -233,8 +234,8 @@ const char *isoq_status_string(isoq_status s)
     case ISOQ_OK: return "ok";
     case ISOQ_E_INVALID: return "invalid argument";
     case ISOQ_E_UNSUPPORTED:
-        return "unsupported shape (d in 1..1024, bits in {2,3,4}; the score calls and the sketch need d in "
-               "{64,80,96,128,160,192,256,512}) or size limit";
+        return "unsupported shape (d in 1..1024, bits in {2,3,4}; the sketch and the corrected logits need d "
+               "in {64,80,96,128,160,192,256,512}) or size limit";
     case ISOQ_E_NULL: return "null pointer";
     case ISOQ_E_ALIGN: return "misaligned pointer";
     case ISOQ_E_HIP: return "HIP runtime error";
@@ -646,6 +647,55 @@ isoq_status isoq_kv_append(const isoq_params *pk, const isoq_params *pv, int dty
 
 namespace {
 
+// isoq_kv_scores at widths without a tuned logit kernel (arguments checked
+// by kv_scores): one workgroup per (query head, chunk, sequence).
+isoq_status kv_scores_generic(const isoq_params *pk, int dtype, const void *q, int n_seqs, int n_q_heads,
+                              int n_kv_heads, const uint8_t *k_idx, const float *k_rho, int64_t n_blocks,
+                              int block_size, const int32_t *block_table, int max_blocks_per_seq,
+                              const int32_t *seq_lens, float scale, float *scores, int64_t max_len,
+                              int64_t max_pos, void *stream)
+{
+    const void *fn = generic_score_kernel_for(pk->variant, pk->bits, dtype == ISOQ_F16);
+    if (!fn)
+        return ISOQ_E_UNSUPPORTED;
+    const int sw = pk->variant == VAR_BLOCK8 ? 8 : 4;
+    GenScoreShape g{};
+    g.d = pk->d;
+    g.slots = (padded_width(pk->variant, pk->d) + sw - 1) / sw;
+    g.rec = (int32_t)record_bytes(pk->variant, pk->d, pk->bits);
+    g.set_stride = (int64_t)slots_per_set(pk->variant, pk->d) * params_per_slot(pk->variant);
+    SArgs a{};
+    a.q = q;
+    a.k_idx = k_idx;
+    a.k_rho = k_rho;
+    a.block_table = block_table;
+    a.seq_lens = seq_lens;
+    a.scores = scores;
+    a.params = pk->dparams;
+    a.max_len = max_len;
+    a.n_blocks = n_blocks;
+    a.n_q_heads = n_q_heads;
+    a.n_kv_heads = n_kv_heads;
+    a.group = n_q_heads / n_kv_heads;
+    a.block_size = block_size;
+    a.max_blocks = max_blocks_per_seq;
+    a.n_sets = pk->n_sets;
+    a.scale = scale;
+    a.div_block = make_fastdiv((uint32_t)block_size);
+    for (int k = 0; k < (1 << pk->bits); k++)
+        a.lev_all[k] = pk->levels[k];
+    void *args[] = {&a, &g};
+    const dim3 grid((unsigned)n_q_heads, (unsigned)((max_pos + kScoreChunk - 1) / kScoreChunk), (unsigned)n_seqs);
+    hipError_t e = hipLaunchKernel(fn, grid, dim3(256), args, generic_score_lds(g.slots, pk->variant),
+                                   static_cast<hipStream_t>(stream));
+    if (e != hipSuccess)
+        return hip_fail(e, "hipLaunchKernel");
+    e = hipGetLastError();
+    if (e != hipSuccess)
+        return hip_fail(e, "after hipLaunchKernel");
+    return ISOQ_OK;
+}
+
 // isoq_kv_scores and isoq_kv_scores_qjl (sk, k_signs, k_gamma non-NULL).
 isoq_status kv_scores(const isoq_params *pk, const isoq_sketch *sk, int dtype, const void *q, int n_seqs,
                       int n_q_heads, int n_kv_heads, const uint8_t *k_idx, const float *k_rho,
@@ -665,7 +715,10 @@ isoq_status kv_scores(const isoq_params *pk, const isoq_sketch *sk, int dtype, c
     if (sk && (sk->variant != pk->variant || sk->d != pk->d || sk->n_sets != pk->n_sets ||
                sk->device != pk->device))
         return ISOQ_E_INVALID;
-    if (!decode_d(pk->d))
+    // widths without a tuned logit kernel: the width-generic one (no sketch
+    // exists at those widths)
+    const bool generic = !decode_d(pk->d);
+    if (generic && sk)
         return ISOQ_E_UNSUPPORTED;
     const int64_t max_pos = std::min<int64_t>(max_len, (int64_t)max_blocks_per_seq * block_size);
     if (n_seqs > 65535 || (int64_t)max_blocks_per_seq * block_size > 0x7FFFFFFF ||
@@ -686,6 +739,10 @@ isoq_status kv_scores(const isoq_params *pk, const isoq_sketch *sk, int dtype, c
     if (st != ISOQ_OK)
         return st;
     const int group = n_q_heads / n_kv_heads;
+    if (generic)
+        return kv_scores_generic(pk, dtype, q, n_seqs, n_q_heads, n_kv_heads, k_idx, k_rho, n_blocks, block_size,
+                                 block_table, max_blocks_per_seq, seq_lens, scale, scores, max_len, max_pos,
+                                 stream);
     const ScoreKernel kern = sk ? score_qjl_kernel_for(pk->variant, pk->d, pk->bits, dtype == ISOQ_F16, group, sk->m)
                                 : score_kernel_for(pk->variant, pk->d, pk->bits, dtype == ISOQ_F16, group);
     if (!kern.fn)

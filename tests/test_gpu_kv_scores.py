@@ -11,7 +11,9 @@ from the HIP path.
 Tolerance: the kernel rotates the query in fp32 and sums d/F table entries in
 fp32 (F = 2 coordinates per entry for 2 and 3 bits, 1 for 4 bits), so
 |s_gpu - s| <= (d/F + 8) * 2^-23 * scale * rho * sum_j |(Tq)_j c_j|, and
-sum_j |(Tq)_j c_j| <= ||q|| ||c[idx]|| (Cauchy-Schwarz, T orthogonal).
+sum_j |(Tq)_j c_j| <= ||q|| ||c[idx]|| (Cauchy-Schwarz, T orthogonal).  At
+widths without a tuned logit kernel the sum runs over the pw coordinates of
+the zero-padded record one by one (fp32 fused multiply-adds): pw + 8 terms.
 Needs an MI355X."""
 import numpy as np
 import pytest
@@ -27,6 +29,14 @@ if not torch.cuda.is_available():
 import paper_2603_28430_amd as iq  # noqa: E402
 
 CANARY = -12345.0
+TUNED = (64, 80, 96, 128, 160, 192, 256, 512)   # widths with a tuned logit kernel
+
+
+def sum_terms(variant, d, bits):
+    """Rounded additions of the logit sum (see the tolerance above)."""
+    if d in TUNED:
+        return d // (1 if bits == 4 else 2)
+    return oracle.padded_width(variant, d)
 
 
 def make(variant, d, bits, n_sets, seed=1):
@@ -39,7 +49,9 @@ class Cache:
     """Host model of a paged key cache: unpacked indices and norms per
     (sequence, kv head, position), packed and scattered into the device layout."""
 
-    def __init__(self, rng, d, bits, n_seqs, n_kv, bs, seq_lens, extra_blocks=3, keys=None):
+    def __init__(self, rng, d, bits, n_seqs, n_kv, bs, seq_lens, extra_blocks=3, keys=None, pw=None):
+        """pw: coordinates per record (the padded width), default d."""
+        pw = d if pw is None else pw
         self.d, self.bits, self.bs, self.n_kv = d, bits, bs, n_kv
         K = 1 << bits
         max_blocks = max(1, max((L + bs - 1) // bs for L in seq_lens))
@@ -49,7 +61,7 @@ class Cache:
         for s in range(n_seqs):
             nb = (seq_lens[s] + bs - 1) // bs
             self.table[s, :nb] = perm[s * max_blocks:s * max_blocks + nb]
-        R = oracle.record_bytes(d, bits)
+        R = oracle.record_bytes(pw, bits)
         self.rec = np.zeros((self.n_blocks, n_kv, bs, R), np.uint8)
         self.rho = np.zeros((self.n_blocks, n_kv, bs), np.float32)
         self.idx, self.norms = {}, {}
@@ -57,7 +69,7 @@ class Cache:
             for h in range(n_kv):
                 L = seq_lens[s]
                 if keys is None:
-                    idx = rng.integers(0, K, (L, d)).astype(np.uint8)
+                    idx = rng.integers(0, K, (L, pw)).astype(np.uint8)
                     rho = rng.uniform(0.2, 2.0, L).astype(np.float32)
                 else:
                     idx, rho = keys(s, h, L)
@@ -78,7 +90,7 @@ def expected(variant, d, bits, rot, levels, n_sets, q, cache, scale, G):
     """Oracle logits and tolerance bounds, per (s, hq): arrays over positions."""
     out = {}
     c = np.asarray(levels, np.float64)
-    nf = d // (1 if bits == 4 else 2)
+    nf = sum_terms(variant, d, bits)
     for (s, h), idx in cache.idx.items():
         rho = cache.norms[s, h].astype(np.float64)
         for g in range(G):
@@ -102,7 +114,7 @@ def run_case(variant, d, bits, dtype, n_seqs, n_q, n_kv, bs, seq_lens, n_sets=No
     rng = np.random.default_rng(seed)
     n_sets = n_kv if n_sets is None else n_sets
     p, rot, levels = make(variant, d, bits, n_sets)
-    cache = Cache(rng, d, bits, n_seqs, n_kv, bs, seq_lens, keys=keys)
+    cache = Cache(rng, d, bits, n_seqs, n_kv, bs, seq_lens, keys=keys, pw=oracle.padded_width(variant, d))
     ndt = np.float16 if dtype == "f16" else np.float32
     q = (workloads.unit_gaussian_rows(n_seqs * n_q, d, seed=seed + 7, dtype=np.float64) *
          rng.uniform(0.5, 4.0, (n_seqs * n_q, 1))).astype(ndt).reshape(n_seqs, n_q, d)
@@ -145,6 +157,24 @@ def test_scores_head_widths(variant, d, bits, dtype):
     run_case(variant, d, bits, dtype, n_seqs=2, n_q=8, n_kv=2, bs=16, seq_lens=[700, 33], seed=d + 3)
 
 
+@pytest.mark.parametrize("variant,d,bits,dtype", [("full", 100, 3, "f16"), ("fast", 72, 2, "f32"), ("2d", 98, 4, "f16"),
+                                                  ("2d", 7, 3, "f32"), ("8d", 40, 3, "f16"), ("8d", 9, 2, "f32"),
+                                                  ("full", 13, 4, "f32"), ("fast", 1000, 3, "f16"), ("full", 1, 2, "f16"),
+                                                  ("fast", 130, 3, "f32"), ("8d", 1024, 4, "f16"), ("2d", 250, 2, "f32")])
+def test_scores_generic_widths(variant, d, bits, dtype):
+    """Widths without a tuned logit kernel: records of the zero-padded width
+    (odd widths, 2-D rows of 4k + 2 coordinates, 8-D rows with a partial
+    block), grouped query heads, a sequence across two chunks."""
+    run_case(variant, d, bits, dtype, n_seqs=2, n_q=6, n_kv=3, bs=16, seq_lens=[1100, 37], seed=d + bits)
+
+
+def test_scores_generic_widths_lengths_and_sets():
+    """d = 100: empty, one-token and block-straddling sequences, max_len
+    cutting a sequence short, one rotation set for every head."""
+    run_case("full", 100, 3, "f16", n_seqs=5, n_q=4, n_kv=2, bs=7, seq_lens=[0, 1, 6, 1025, 2100], max_len=2000,
+             n_sets=1, seed=6)
+
+
 def test_scores_head_widths_lengths():
     """d = 96: empty, one-token and block-straddling sequences, and max_len
     cutting a sequence short."""
@@ -175,11 +205,12 @@ def test_scores_lengths_and_truncation():
              seed=12)
 
 
-def test_scores_invalid_blocks_are_skipped():
+@pytest.mark.parametrize("d", [128, 100])
+def test_scores_invalid_blocks_are_skipped(d):
     rng = np.random.default_rng(4)
-    d, bits, bs = 128, 3, 16
+    bits, bs = 3, 16
     p, rot, levels = make("full", d, bits, 2)
-    cache = Cache(rng, d, bits, 2, 2, bs, [100, 64])
+    cache = Cache(rng, d, bits, 2, 2, bs, [100, 64], pw=oracle.padded_width("full", d))
     cache.table[0, 1] = -1                       # positions 16..31 of sequence 0
     cache.table[1, 2] = cache.n_blocks + 5       # positions 32..47 of sequence 1
     rec, rho, table, lens = cache.device()
@@ -235,7 +266,8 @@ def test_scores_of_keys_quantized_by_the_oracle():
              seed=21)
 
 
-@pytest.mark.parametrize("variant,d", [("full", 128), ("full", 96), ("fast", 192), ("2d", 80)])
+@pytest.mark.parametrize("variant,d", [("full", 128), ("full", 96), ("fast", 192), ("2d", 80), ("fast", 100),
+                                       ("2d", 90), ("8d", 44)])
 def test_append_then_scores_end_to_end(variant, d):
     """Keys appended by isoq_kv_append, logits from isoq_kv_scores, against
     the oracle's logits of the oracle's quantization of the same key rows
@@ -269,7 +301,7 @@ def test_append_then_scores_end_to_end(variant, d):
         near = (np.abs(yt[..., None] - thr).min(-1) <= 1e-6).any(1)
         qv = q.cpu().numpy()[0, h].astype(np.float64)
         ref = oracle.attention_scores(variant, d, bits, rot_h, levels, qv, idx, rho, 0.1)
-        bound = (d // 2 + 8) * 2.0 ** -23 * 0.1 * rho * np.linalg.norm(qv) * np.linalg.norm(levels[idx], axis=1)
+        bound = (sum_terms(variant, d, bits) + 8) * 2.0 ** -23 * 0.1 * rho * np.linalg.norm(qv) * np.linalg.norm(levels[idx], axis=1)
         ok = ~near
         kept += ok.sum()
         err = np.abs(got[h, :n_tok].astype(np.float64) - ref)

@@ -122,9 +122,9 @@ def test_widths_large_sampled(variant, d, dtype):
 
 
 def test_widths_unsupported_calls():
-    """Widths outside the generic range, and the score and sketch calls at a
-    width outside theirs (d = 100), return ISOQ_E_UNSUPPORTED before any
-    launch (the append takes every width)."""
+    """Widths outside the generic range, and the sketch at a width outside
+    its own (d = 100), return ISOQ_E_UNSUPPORTED before any launch (append
+    and logits take every width)."""
     with pytest.raises(iq.IsoqError) as e:
         iq.isoq_params_init("full", 1025, 3, 1)
     assert e.value.status == 2
@@ -132,15 +132,6 @@ def test_widths_unsupported_calls():
     with pytest.raises(iq.IsoqError) as e:
         iq.isoq_sketch_init(p, 64)
     assert e.value.status == 2
-    z = lambda *s, dt=torch.uint8: torch.zeros(s, dtype=dt, device="cuda")
-    R = p.record_bytes
-    lib = iq.isoquant.lib
-    rec, rho = z(2, 1, 16, R), z(2, 1, 16, dt=torch.float32)
-    q = z(1, 1, 100, dt=torch.float16)
-    tab, lens = z(1, 2, dt=torch.int32), torch.ones((1,), dtype=torch.int32, device="cuda")
-    out = z(1, 1, 32, dt=torch.float32)
-    assert lib.isoq_kv_scores(p.handle, 1, q.data_ptr(), 1, 1, 1, rec.data_ptr(), rho.data_ptr(), 2, 16,
-                              tab.data_ptr(), 2, lens.data_ptr(), 1.0, out.data_ptr(), 32, None) == 2
 
 
 @pytest.mark.parametrize("variant,d,dtype", [("full", 90, "f16"), ("fast", 96, "f32"), ("2d", 1000, "f16"),
