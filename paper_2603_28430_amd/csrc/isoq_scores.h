@@ -11,19 +11,22 @@
 // table[j][e] = sum_f (T q)_{F j + f} c[e_f].
 //
 // Workgroup (key head h, chunk of kScoreChunk positions, sequence s):
+//   0. load the block-table entries of the lane's keys and the first batch
+//      of records;
 //   1. rotate the group's query heads (scale folded in) into LDS;
 //   2. build the group's tables in LDS (d/F tables of 2^(F b) floats each);
-//   3. one key per lane: load its record (16-byte loads) and norm, sum the
-//      d/F lookups, write rho * sum.  All lanes read the same field's table at
-//      the same time, so lanes that read different entries never collide on
-//      an LDS bank (a table has at most 64 entries).
+//   3. one key per lane: its record (up to 16-byte loads) and norm, the d/F
+//      lookups summed, rho * sum written.  All lanes read the same field's
+//      table at the same time; a 64-entry table on 32 four-byte banks makes
+//      entries e and e + 32 share a bank, which measured as no cost: the
+//      record loads set the speed.
 // With the stage-2 sketch (QM > 0 sign bits per key, Sec. 8) each logit also
 // gets the residual correction sqrt(pi/2)/m gamma <S q, 2 z - 1>: S q is
 // computed once per workgroup and cut into groups of 4 signs, each with a
 // 16-entry table sum_b (+-1) (S q)_{4 i + b}, summed like the stage-1 fields.
-// The path is bound by HBM bandwidth on the records (d b / 8 + 4 bytes per
-// key, plus m / 8 + 4 with the sketch); no MFMA: there is no dense
-// contraction left once q is rotated.
+// The roofline is HBM bandwidth on the records (d b / 8 + 4 bytes per key,
+// plus m / 8 + 4 with the sketch, and the 4-byte logit); no MFMA: there is no
+// dense contraction left once q is rotated.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -68,14 +71,18 @@ constexpr bool kStaticLds = GT > 0 && ScoreShape<D, BITS, QM>::lds_floats(GT) * 
 // the LDS byte address of the query head's first table, a multiple of the
 // head's table block, so the byte address of entry e of table j is
 // (4 e | base) + 4 E j: one shift and one and-or per field, the table offset
-// an immediate of the read.
+// an immediate of the read.  The reads go out in groups of 16 with two
+// partial sums: group i adds into sum i mod 2, and that sum is forced to be
+// complete before group i + 2 is issued, so at most 32 reads are in flight
+// (left alone, the compiler issues all d/F reads before the first add and
+// holds every result in a register).
 // NF fields of FB bits each, tables of 2^FB entries.
 template <int NF, int FB>
 __device__ __forceinline__ float lookup_sum(const char *lds, uint32_t base, const uint32_t *w)
 {
     constexpr int E = 1 << FB;
     constexpr uint32_t kMask = (uint32_t)(E - 1) << 2;
-    float acc = 0.f;
+    float acc[2] = {0.f, 0.f};
 #pragma unroll
     for (int j = 0; j < NF; j++) {
         const int o = j * FB;
@@ -88,13 +95,14 @@ __device__ __forceinline__ float lookup_sum(const char *lds, uint32_t base, cons
         else
             x = w[k] << (2 - sh);
         const uint32_t addr = (x & kMask) | base;
-        acc += *reinterpret_cast<const float *>(lds + addr + 4 * E * j);
-        // at most 16 lookups in flight: left alone, the scheduler issues all
-        // d/F reads first and holds every result in a register
-        if ((j & 15) == 15)
+        acc[(j >> 4) & 1] += *reinterpret_cast<const float *>(lds + addr + 4 * E * j);
+        if ((j & 15) == 15) {
             __builtin_amdgcn_sched_barrier(0);
+            if (j >= 31)
+                asm volatile("" : "+v"(acc[((j >> 4) + 1) & 1]));
+        }
     }
-    return acc;
+    return acc[0] + acc[1];
 }
 
 // GT: query heads per key head as a compile-time constant (the table base of
@@ -134,6 +142,99 @@ __global__ __launch_bounds__(256) void score_kernel(const SArgs a)
     float *sqv = tab2 + G * 16 * S::NQ;
     float *qraw = sqv + G * QM;
     const int set = a.n_sets == 1 ? 0 : h;
+
+    // 0. keys t0 + threadIdx.x + 256 i, in batches of KPT keys per lane.  A
+    //    record's address depends on its block-table entry, so the entries
+    //    of all of the lane's keys are loaded first; the first batch's
+    //    records are then in flight while the tables are built, and each
+    //    later batch is loaded while the previous one is summed.  Records
+    //    are read with ordinary (temporal) loads: a lane's 16-byte pieces of
+    //    one record come from three load instructions whose lanes are a
+    //    record apart, so the second and third find the lines in L1; with
+    //    non-temporal loads each instruction fetched them again.
+    const int64_t tend = min(t0 + (int64_t)kScoreChunk, len);
+    const int32_t *table = a.block_table + (int64_t)s * a.max_blocks;
+    constexpr int NB = kScoreChunk / 256 / S::KPT;
+    static_assert(NB * S::KPT * 256 == kScoreChunk, "batches tile the chunk");
+    int32_t bt[NB][S::KPT];
+#pragma unroll
+    for (int b = 0; b < NB; b++)
+#pragma unroll
+        for (int u = 0; u < S::KPT; u++) {
+            const int64_t t = t0 + threadIdx.x + 256 * (b * S::KPT + u);
+            const uint32_t tt = (uint32_t)min(t, len - 1);
+            bt[b][u] = table[fast_div(tt, a.div_block)];
+        }
+    struct Batch {
+        uint32_t w[S::KPT][S::RW];
+        uint32_t z[S::KPT][S::SW > 0 ? S::SW : 1];   // sign sketch
+        float gam[S::KPT];
+        float rho[S::KPT];
+        int64_t t[S::KPT];
+        bool ok[S::KPT];
+    };
+    auto issue = [&](int b, Batch &k) {
+#pragma unroll
+        for (int u = 0; u < S::KPT; u++) {
+            const int64_t t = t0 + threadIdx.x + 256 * (b * S::KPT + u);
+            const uint32_t tt = (uint32_t)min(t, len - 1);
+            const uint32_t bi = fast_div(tt, a.div_block);
+            const int32_t blk = bt[b][u];
+            k.ok[u] = t < tend && blk >= 0 && blk < a.n_blocks;
+            // an invalid key reads record 0 of block 0 (always present) and is not stored
+            const int64_t krow =
+                k.ok[u] ? ((int64_t)blk * a.n_kv_heads + h) * a.block_size + (tt - bi * a.block_size) : 0;
+            if constexpr (S::LW == 4) {
+                const u32x4 *rp = reinterpret_cast<const u32x4 *>(a.k_idx + krow * RB);
+#pragma unroll
+                for (int v = 0; v < S::RV; v++) {
+                    const u32x4 q4 = rp[v];
+#pragma unroll
+                    for (int c = 0; c < 4; c++) {
+                        const uint32_t e = q4[c];
+                        k.w[u][4 * v + c] = e;
+                    }
+                }
+            } else if constexpr (S::LW == 0) {
+                // records of an odd number of half-words: 2-byte loads, paired
+                // into words (the upper half of the last word is zero)
+                const uint16_t *hp = reinterpret_cast<const uint16_t *>(a.k_idx + krow * RB);
+#pragma unroll
+                for (int c = 0; c < S::RW; c++) {
+                    const uint32_t lo = hp[2 * c];
+                    const uint32_t hi = 2 * c + 1 < S::RH ? (uint32_t)hp[2 * c + 1] : 0u;
+                    k.w[u][c] = lo | (hi << 16);
+                }
+            } else if constexpr (S::LW == 1) {
+                // records of an odd number of words: 4-byte loads
+                const uint32_t *rp = reinterpret_cast<const uint32_t *>(a.k_idx + krow * RB);
+#pragma unroll
+                for (int v = 0; v < S::RV; v++)
+                    k.w[u][v] = rp[v];
+            } else {
+                // records of 8 (mod 16) bytes: 8-byte loads
+                const u32x2 *rp = reinterpret_cast<const u32x2 *>(a.k_idx + krow * RB);
+#pragma unroll
+                for (int v = 0; v < S::RV; v++) {
+                    const u32x2 q2 = rp[v];
+                    const uint32_t e0 = q2[0], e1 = q2[1];
+                    k.w[u][2 * v] = e0;
+                    k.w[u][2 * v + 1] = e1;
+                }
+            }
+            k.rho[u] = a.k_rho[krow];
+            k.t[u] = t;
+            if constexpr (QM > 0) {
+                const uint32_t *zp = reinterpret_cast<const uint32_t *>(a.k_signs + krow * (QM / 8));
+#pragma unroll
+                for (int c = 0; c < S::SW; c++)
+                    k.z[u][c] = zp[c];
+                k.gam[u] = a.k_gamma[krow];
+            }
+        }
+    };
+    Batch kb[2];
+    issue(0, kb[0]);
 
     // 1. rotated queries q~_g = scale * T_h q_g and the codebook
     if (threadIdx.x < S::K)
@@ -221,82 +322,6 @@ __global__ __launch_bounds__(256) void score_kernel(const SArgs a)
     }
     __syncthreads();
 
-    // 3. keys t0 + threadIdx.x + 256 i, in batches of KPT keys per lane: the
-    //    batch's records are loaded together, then summed.  (Prefetching the
-    //    next batch during the sums measured slower: the extra registers cost
-    //    more occupancy than the overlap gained.)
-    const int64_t tend = min(t0 + (int64_t)kScoreChunk, len);
-    const int32_t *table = a.block_table + (int64_t)s * a.max_blocks;
-    constexpr int NB = kScoreChunk / 256 / S::KPT;
-    static_assert(NB * S::KPT * 256 == kScoreChunk, "batches tile the chunk");
-    struct Batch {
-        uint32_t w[S::KPT][S::RW];
-        uint32_t z[S::KPT][S::SW > 0 ? S::SW : 1];   // sign sketch
-        float gam[S::KPT];
-        float rho[S::KPT];
-        int64_t t[S::KPT];
-        bool ok[S::KPT];
-    };
-    auto issue = [&](int b, Batch &k) {
-#pragma unroll
-        for (int u = 0; u < S::KPT; u++) {
-            const int64_t t = t0 + threadIdx.x + 256 * (b * S::KPT + u);
-            const uint32_t tt = (uint32_t)min(t, len - 1);
-            const uint32_t bi = fast_div(tt, a.div_block);
-            const int32_t blk = table[bi];
-            k.ok[u] = t < tend && blk >= 0 && blk < a.n_blocks;
-            // an invalid key reads record 0 of block 0 (always present) and is not stored
-            const int64_t krow =
-                k.ok[u] ? ((int64_t)blk * a.n_kv_heads + h) * a.block_size + (tt - bi * a.block_size) : 0;
-            if constexpr (S::LW == 4) {
-                const u32x4 *rp = reinterpret_cast<const u32x4 *>(a.k_idx + krow * RB);
-#pragma unroll
-                for (int v = 0; v < S::RV; v++) {
-                    const u32x4 q4 = __builtin_nontemporal_load(rp + v);
-#pragma unroll
-                    for (int c = 0; c < 4; c++) {
-                        const uint32_t e = q4[c];
-                        k.w[u][4 * v + c] = e;
-                    }
-                }
-            } else if constexpr (S::LW == 0) {
-                // records of an odd number of half-words: 2-byte loads, paired
-                // into words (the upper half of the last word is zero)
-                const uint16_t *hp = reinterpret_cast<const uint16_t *>(a.k_idx + krow * RB);
-#pragma unroll
-                for (int c = 0; c < S::RW; c++) {
-                    const uint32_t lo = hp[2 * c];
-                    const uint32_t hi = 2 * c + 1 < S::RH ? (uint32_t)hp[2 * c + 1] : 0u;
-                    k.w[u][c] = lo | (hi << 16);
-                }
-            } else if constexpr (S::LW == 1) {
-                // records of an odd number of words: 4-byte loads
-                const uint32_t *rp = reinterpret_cast<const uint32_t *>(a.k_idx + krow * RB);
-#pragma unroll
-                for (int v = 0; v < S::RV; v++)
-                    k.w[u][v] = __builtin_nontemporal_load(rp + v);
-            } else {
-                // records of 8 (mod 16) bytes: 8-byte loads
-                const u32x2 *rp = reinterpret_cast<const u32x2 *>(a.k_idx + krow * RB);
-#pragma unroll
-                for (int v = 0; v < S::RV; v++) {
-                    const u32x2 q2 = __builtin_nontemporal_load(rp + v);
-                    const uint32_t e0 = q2[0], e1 = q2[1];
-                    k.w[u][2 * v] = e0;
-                    k.w[u][2 * v + 1] = e1;
-                }
-            }
-            k.rho[u] = a.k_rho[krow];
-            k.t[u] = t;
-            if constexpr (QM > 0) {
-                const uint32_t *zp = reinterpret_cast<const uint32_t *>(a.k_signs + krow * (QM / 8));
-#pragma unroll
-                for (int c = 0; c < S::SW; c++)
-                    k.z[u][c] = __builtin_nontemporal_load(zp + c);
-                k.gam[u] = a.k_gamma[krow];
-            }
-        }
-    };
     auto consume = [&](Batch &k) {
 #pragma unroll
         for (int u = 0; u < S::KPT; u++) {
@@ -332,13 +357,14 @@ __global__ __launch_bounds__(256) void score_kernel(const SArgs a)
             }
         }
     };
-#pragma unroll 1
+    // 3. sums, batch by batch (the next batch's loads issued first)
+#pragma unroll
     for (int b = 0; b < NB; b++) {
         if (t0 + 256 * b * S::KPT >= tend)  // block-uniform
             break;
-        Batch k;
-        issue(b, k);
-        consume(k);
+        if (b + 1 < NB && t0 + 256 * (b + 1) * S::KPT < tend)
+            issue(b + 1, kb[(b + 1) & 1]);
+        consume(kb[b & 1]);
     }
 }
 
