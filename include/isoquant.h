@@ -194,10 +194,16 @@ isoq_status isoq_roundtrip(const isoq_params *p, int dtype, const void *x, int64
  *   slot_mapping  device, int64 [n_tokens] (8-byte aligned): cache slot of
  *               token t; a slot < 0 or >= n_blocks * block_size skips the token
  *               (padding), its rows are not written.
- *   k_idx, v_idx  device, [n_blocks][n_heads][block_size][isoq_packed_bytes]
- *               bytes (4-byte aligned): slot s is position s mod block_size of
- *               cache block s / block_size; a head's records of one block are
- *               contiguous.  Record format as in isoq_quantize.
+ *   k_idx, v_idx  device, n_blocks * n_heads * block_size * R bytes (R =
+ *               isoq_packed_bytes; 4-byte aligned): slot s is position s mod
+ *               block_size of cache block s / block_size, and (block b, head
+ *               h) owns the block_size * R bytes from (b n_heads + h)
+ *               block_size R on.  Inside that region the records are stored
+ *               piece-major: record byte k of position p lies at byte
+ *               (floor(k / P) block_size + p) P + k mod P, with P the largest
+ *               of 16, 8, 4, 2, 1 dividing R (so a piece of consecutive
+ *               positions is adjacent, which the logit kernel reads in one
+ *               coalesced load).  Record bytes as in isoq_quantize.
  *   k_rho, v_rho  device, fp32 [n_blocks][n_heads][block_size].
  * Limits: n_tokens * n_heads < 2^31, n_blocks * block_size < 2^31, n_heads and
  * block_size >= 1, and for the one-launch shapes at most 65,535 launch blocks

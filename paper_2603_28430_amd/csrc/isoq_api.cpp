@@ -663,6 +663,10 @@ isoq_status kv_scores_generic(const isoq_params *pk, int dtype, const void *q, i
     g.d = pk->d;
     g.slots = (padded_width(pk->variant, pk->d) + sw - 1) / sw;
     g.rec = (int32_t)record_bytes(pk->variant, pk->d, pk->bits);
+    {
+        const int P = cache_piece(g.rec);
+        g.rec_lp = P == 16 ? 4 : P == 8 ? 3 : P == 4 ? 2 : P == 2 ? 1 : 0;
+    }
     g.set_stride = (int64_t)slots_per_set(pk->variant, pk->d) * params_per_slot(pk->variant);
     SArgs a{};
     a.q = q;

@@ -55,6 +55,76 @@ __device__ __forceinline__ uint32_t fast_div(uint32_t n, const FastDiv &f)
 }
 
 // Sum over the LPV lanes of a row; every lane of the row gets the same bits.
+// Where an index record goes.  RecPtr: consecutive bytes.  CacheRec<P>: a
+// record in a paged cache, pieces of P bytes (cache_piece): record byte k of
+// position pos at byte ((k / P) bs + pos) P + k mod P of the head's block
+// region.  Every store of n bytes is n-aligned inside the record and n <= P,
+// so it never straddles two pieces.  at(k): the record from its byte k on.
+struct RecPtr {
+    uint8_t *rec;
+    template <typename T>
+    __device__ __forceinline__ void put(int k, T v) const
+    {
+        *reinterpret_cast<T *>(rec + k) = v;
+    }
+    __device__ __forceinline__ RecPtr at(int k) const { return RecPtr{rec + k}; }
+};
+
+template <int P>
+struct CacheRec {
+    uint8_t *region;   // the head's records of one cache block
+    int pos, bs, off;
+    template <typename T>
+    __device__ __forceinline__ void put(int k, T v) const
+    {
+        const int b = off + k;
+        *reinterpret_cast<T *>(region + ((int64_t)(b / P) * bs + pos) * P + (b % P)) = v;
+    }
+    __device__ __forceinline__ CacheRec at(int k) const { return CacheRec{region, pos, bs, off + k}; }
+};
+
+// CacheRec with the piece size known at run time (P = 1 << lp).
+struct CacheRecRt {
+    uint8_t *region;
+    int pos, bs, off, lp;
+    template <typename T>
+    __device__ __forceinline__ void put(int k, T v) const
+    {
+        const int b = off + k;
+        *reinterpret_cast<T *>(region + ((((int64_t)(b >> lp)) * bs + pos) << lp) + (b & ((1 << lp) - 1))) = v;
+    }
+    __device__ __forceinline__ CacheRecRt at(int k) const { return CacheRecRt{region, pos, bs, off + k, lp}; }
+};
+
+__device__ __forceinline__ int cache_piece_log2(int64_t R)
+{
+    const int P = cache_piece(R);
+    return P == 16 ? 4 : P == 8 ? 3 : P == 4 ? 2 : P == 2 ? 1 : 0;
+}
+
+// Slot s of head `head` in a paged cache: slot s is position s mod
+// block_size of cache block s / block_size, a block holding [n_heads]
+// [block_size] records.  Returns the cache row (block n_heads + head)
+// block_size + pos (norms are stored by it) and sets pos; ok is false for a
+// skipped slot (s < 0 or past the cache: row 0 and position 0 are returned
+// and must not be written).
+__device__ __forceinline__ int64_t cache_slot(const KArgs &a, int64_t s, uint32_t head, bool &ok, int &pos)
+{
+    ok = s >= 0 && s < a.n_slots;
+    const uint32_t su = ok ? (uint32_t)s : 0u;
+    const uint32_t blk = fast_div(su, a.div_block);
+    pos = (int)(su - blk * a.block_size);
+    return ((int64_t)blk * a.n_heads + head) * a.block_size + pos;
+}
+
+// The record destination of cache row crow at position pos (records of R
+// bytes at rec_out).
+template <int64_t R>
+__device__ __forceinline__ CacheRec<cache_piece(R)> cache_rec(const KArgs &a, int64_t crow, int pos)
+{
+    return CacheRec<cache_piece(R)>{a.rec_out + (crow - pos) * R, pos, (int)a.block_size, 0};
+}
+
 template <int LPV>
 __device__ __forceinline__ float row_sum(float v)
 {

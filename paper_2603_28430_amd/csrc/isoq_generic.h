@@ -122,11 +122,31 @@ __device__ __forceinline__ void gen_store(char *row, int j, int d, bool vec, con
     }
 }
 
+// Where an index record is read from: consecutive bytes, or a paged cache
+// (piece-major, as CacheRecRt).
+struct RecSrc {
+    const uint8_t *rec;
+    template <typename T>
+    __device__ __forceinline__ T get(int k) const
+    {
+        return *reinterpret_cast<const T *>(rec + k);
+    }
+};
+struct CacheSrcRt {
+    const uint8_t *region;
+    int pos, bs, lp;
+    template <typename T>
+    __device__ __forceinline__ T get(int k) const
+    {
+        return *reinterpret_cast<const T *>(region + ((((int64_t)(k >> lp)) * bs + pos) << lp) + (k & ((1 << lp) - 1)));
+    }
+};
+
 // Index bits of slot j (4 coordinates, BITS each) from a record of nb bytes.
-template <int BITS>
-__device__ __forceinline__ uint32_t gen_read_slot(const uint8_t *rec, int j, int nb)
+template <int BITS, class Src>
+__device__ __forceinline__ uint32_t gen_read_slot(const Src &rec, int j, int nb)
 {
-    auto byte = [&](int k) -> uint32_t { return k < nb ? (uint32_t)rec[k] : 0u; };
+    auto byte = [&](int k) -> uint32_t { return k < nb ? (uint32_t)rec.template get<uint8_t>(k) : 0u; };
     if constexpr (BITS == 2)
         return byte(j);
     else if constexpr (BITS == 4)
@@ -140,12 +160,12 @@ __device__ __forceinline__ uint32_t gen_read_slot(const uint8_t *rec, int j, int
 // Write the bytes whose first bit lies in slot j's bit range; `next` is the
 // next slot's index bits (only 3 bits per coordinate share a byte between
 // slots: the even slot owns it).
-template <int BITS>
-__device__ __forceinline__ void gen_write_slot(uint8_t *rec, int j, int nb, uint32_t p, uint32_t next)
+template <int BITS, class Dst>
+__device__ __forceinline__ void gen_write_slot(const Dst &rec, int j, int nb, uint32_t p, uint32_t next)
 {
     auto put = [&](int k, uint32_t v) {
         if (k < nb)
-            rec[k] = (uint8_t)v;
+            rec.template put<uint8_t>(k, (uint8_t)v);
     };
     if constexpr (BITS == 2) {
         put(j, p);
@@ -162,28 +182,29 @@ __device__ __forceinline__ void gen_write_slot(uint8_t *rec, int j, int nb, uint
 
 // 8-coordinate slots (8-D blocks): slot j's 8 b bits are bytes [b j, b j + b)
 // of the record, so every slot owns whole bytes.
-template <int BITS>
-__device__ __forceinline__ uint32_t gen_read_slot8(const uint8_t *rec, int j)
+template <int BITS, class Src>
+__device__ __forceinline__ uint32_t gen_read_slot8(const Src &rec, int j)
 {
     if constexpr (BITS == 2)
-        return reinterpret_cast<const uint16_t *>(rec)[j];
+        return rec.template get<uint16_t>(2 * j);
     else if constexpr (BITS == 4)
-        return reinterpret_cast<const uint32_t *>(rec)[j];
+        return rec.template get<uint32_t>(4 * j);
     else
-        return (uint32_t)rec[3 * j] | ((uint32_t)rec[3 * j + 1] << 8) | ((uint32_t)rec[3 * j + 2] << 16);
+        return (uint32_t)rec.template get<uint8_t>(3 * j) | ((uint32_t)rec.template get<uint8_t>(3 * j + 1) << 8) |
+               ((uint32_t)rec.template get<uint8_t>(3 * j + 2) << 16);
 }
 
-template <int BITS>
-__device__ __forceinline__ void gen_write_slot8(uint8_t *rec, int j, uint32_t p)
+template <int BITS, class Dst>
+__device__ __forceinline__ void gen_write_slot8(const Dst &rec, int j, uint32_t p)
 {
     if constexpr (BITS == 2) {
-        reinterpret_cast<uint16_t *>(rec)[j] = (uint16_t)p;
+        rec.template put<uint16_t>(2 * j, (uint16_t)p);
     } else if constexpr (BITS == 4) {
-        reinterpret_cast<uint32_t *>(rec)[j] = p;
+        rec.template put<uint32_t>(4 * j, p);
     } else {
-        rec[3 * j] = (uint8_t)p;
-        rec[3 * j + 1] = (uint8_t)(p >> 8);
-        rec[3 * j + 2] = (uint8_t)(p >> 16);
+        rec.template put<uint8_t>(3 * j, (uint8_t)p);
+        rec.template put<uint8_t>(3 * j + 1, (uint8_t)(p >> 8));
+        rec.template put<uint8_t>(3 * j + 2, (uint8_t)(p >> 16));
     }
 }
 
@@ -245,9 +266,9 @@ __global__ __launch_bounds__(kBlockThreads) void generic_kernel(const KArgs a)
                 else
                     xr[t][k] = on ? gen_load<F16, SW>(x0 + t * xstep, j, d, vec) : gen_zero<F16, SW>();
             } else if constexpr (SW == 8) {
-                pin[t][k] = on ? gen_read_slot8<BITS>(ri0 + t * rstep, j) : 0u;
+                pin[t][k] = on ? gen_read_slot8<BITS>(RecSrc{ri0 + t * rstep}, j) : 0u;
             } else {
-                pin[t][k] = on ? gen_read_slot<BITS>(ri0 + t * rstep, j, nb) : 0u;
+                pin[t][k] = on ? gen_read_slot<BITS>(RecSrc{ri0 + t * rstep}, j, nb) : 0u;
             }
         }
         if constexpr (!kLoadX)
@@ -347,30 +368,33 @@ __global__ __launch_bounds__(kBlockThreads) void generic_kernel(const KArgs a)
             // cache, writes nothing)
             bool wr = ok;
             int64_t orow = row;
+            int pos = 0;
             if constexpr (kAppend) {
                 const uint32_t ru = ok ? (uint32_t)row : 0u;
                 const uint32_t token = ru / a.n_heads;
                 const uint32_t head = ru - token * a.n_heads;
-                const int64_t sl = ok ? a.slots[token] : -1;
-                wr = ok && sl >= 0 && sl < a.n_slots;
-                const uint32_t su = wr ? (uint32_t)sl : 0u;
-                const uint32_t blk = fast_div(su, a.div_block);
-                orow = ((int64_t)blk * a.n_heads + head) * a.block_size + (su - blk * a.block_size);
+                orow = cache_slot(a, ok ? a.slots[token] : -1, head, wr, pos);
+                wr = wr && ok;
             }
-            uint8_t *rec = kAppend ? a.rec_out + orow * nb : ro0 + t * rstep;
+            auto write = [&](const auto &rec) {
 #pragma unroll
-            for (int k = 0; k < BPL; k++) {
-                const int j = sub + G * k;
-                if constexpr (SW == 8) {
-                    if (wr && j < slots)
-                        gen_write_slot8<BITS>(rec, j, pk[k]);
-                } else {
-                    // the next slot of an even slot sits on the next lane (G is even)
-                    const uint32_t next = BITS == 3 ? (uint32_t)__shfl_down((int)pk[k], 1, 64) : 0u;
-                    if (wr && j < slots)
-                        gen_write_slot<BITS>(rec, j, nb, pk[k], next);
+                for (int k = 0; k < BPL; k++) {
+                    const int j = sub + G * k;
+                    if constexpr (SW == 8) {
+                        if (wr && j < slots)
+                            gen_write_slot8<BITS>(rec, j, pk[k]);
+                    } else {
+                        // the next slot of an even slot sits on the next lane (G is even)
+                        const uint32_t next = BITS == 3 ? (uint32_t)__shfl_down((int)pk[k], 1, 64) : 0u;
+                        if (wr && j < slots)
+                            gen_write_slot<BITS>(rec, j, nb, pk[k], next);
+                    }
                 }
-            }
+            };
+            if constexpr (kAppend)
+                write(CacheRecRt{a.rec_out + (orow - pos) * nb, pos, (int)a.block_size, 0, cache_piece_log2(nb)});
+            else
+                write(RecPtr{ro0 + t * rstep});
             if (wr && sub == 0)
                 a.norms_out[orow] = rho;
         } else {

@@ -154,6 +154,13 @@ ScoreKernel score_qjl_kernel_for(int variant, int d, int bits, bool f16, int gro
 // the kernel for (variant, d, bits, mode) there (round trip, quantize,
 // append), or nullptr.  The 2-D case keeps its VALU rotation (2 multiply-adds
 // per coordinate: the products would save little and add their latency).
+// Paged caches (isoq_kv_append, isoq_kv_scores) hold a head's records of
+// one cache block piece-major: a record of R bytes is cut into pieces of
+// cache_piece(R) bytes (the largest of 16, 8, 4, 2, 1 dividing R), and piece
+// j of position pos lies at byte (j block_size + pos) cache_piece(R) of the
+// head's block region, so consecutive positions' pieces are adjacent.
+constexpr int cache_piece(int64_t R) { return R % 16 == 0 ? 16 : R % 8 == 0 ? 8 : R % 4 == 0 ? 4 : R % 2 == 0 ? 2 : 1; }
+
 constexpr bool quad_layout(int variant, int d) { return variant != VAR_PLANAR2D && (d == 64 || d == 128 || d == 256); }
 const void *kernel_m_for(int variant, int d, int bits, int mode);
 // Bytes of the matrix-core parameters per set: d/8 chunks x 4 quad rows x

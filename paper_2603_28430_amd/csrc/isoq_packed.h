@@ -99,16 +99,17 @@ __device__ __forceinline__ void packed_store_bits(uint8_t *rec, int c, uint32_t 
 // (rows start on even lanes): the even lane writes bytes 6 i .. 6 i + 3 (its
 // bits and the odd lane's first 8) as two half-words, the odd lane bytes
 // 6 i + 4 .. 6 i + 5.  Every lane of the wave must call it (DPP exchange).
-__device__ __forceinline__ void store_bits3_pairs(uint8_t *rec, int sub, uint32_t p, bool ok)
+template <class Dst>
+__device__ __forceinline__ void store_bits3_pairs(const Dst &rec, int sub, uint32_t p, bool ok)
 {
     const uint32_t o = dpp_u<DPP_QUAD_1032>(p);   // the pair partner's bits
-    uint16_t *h = reinterpret_cast<uint16_t *>(rec + 6 * (sub >> 1));
+    const int h = 6 * (sub >> 1);
     if (ok) {
         if ((sub & 1) == 0) {
-            h[0] = (uint16_t)p;
-            h[1] = (uint16_t)((p >> 16) | (o << 8));
+            rec.template put<uint16_t>(h, (uint16_t)p);
+            rec.template put<uint16_t>(h + 2, (uint16_t)((p >> 16) | (o << 8)));
         } else {
-            h[2] = (uint16_t)(p >> 8);
+            rec.template put<uint16_t>(h + 4, (uint16_t)(p >> 8));
         }
     }
 }
@@ -187,6 +188,7 @@ __device__ __forceinline__ void packed_body(const KArgs &a)
     const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int64_t rowb = (int64_t)a.g_d * 2;       // fp16 rows
     const int64_t recb = (int64_t)L * C * BITS;    // d b / 8
+    const int rec_lp = cache_piece_log2(recb);     // append: piece size of the cache layout
     const int TPB = kQjl ? a.g_tpb : kAppend ? 1 : packed_tiles_per_block(VAR, C);   // row tiles per block
     const int64_t base0 = (int64_t)(kAppend ? blockIdx.y : blockIdx.x) * TPB * WAVES * GPW;
     // append: the block's head, its input row stride and cache addressing
@@ -404,15 +406,16 @@ __device__ __forceinline__ void packed_body(const KArgs &a)
                 }
                 if constexpr (kAppend) {
                     bool ok;
-                    const int64_t cr = cache_row(slot[u], ok);
-                    uint8_t *rec = a.rec_out + cr * recb;
+                    int pos;
+                    const int64_t cr = cache_slot(a, slot[u], head, ok, pos);
+                    const CacheRecRt rec{a.rec_out + (cr - pos) * recb, pos, (int)a.block_size, 0, rec_lp};
                     if (BITS == 3 && L % 4 != 0) {
                         // d = 80: quads would straddle rows
                         store_bits3_pairs(rec, sub, p[0], on && ok);
                     } else {
 #pragma unroll
                         for (int k = 0; k < C; k++)
-                            store_bits<BITS>(rec + k * L * BITS, sub, p[k], on && ok);
+                            store_bits_to<BITS>(rec.at(k * L * BITS), sub, p[k], on && ok);
                     }
                     if (on && ok && sub == 0) {
                         a.norms_out[cr] = rho;

@@ -15,7 +15,8 @@
 //      of records;
 //   1. rotate the group's query heads (scale folded in) into LDS;
 //   2. build the group's tables in LDS (d/F tables of 2^(F b) floats each);
-//   3. one key per lane: its record (up to 16-byte loads) and norm, the d/F
+//   3. one key per lane: its record (one load per piece of the cache
+//      layout, up to 16 bytes) and norm, the d/F
 //      lookups summed, rho * sum written.  All lanes read the same field's
 //      table at the same time; a 64-entry table on 32 four-byte banks makes
 //      entries e and e + 32 share a bank, which measured as no cost: the
@@ -52,6 +53,9 @@ struct ScoreShape {
     // record of an odd number of half-words, read in 2-byte loads
     static constexpr int LW = RW * 32 != D * BITS ? 0 : RW % 4 == 0 ? 4 : RW % 2 == 0 ? 2 : 1;
     static constexpr int RV = LW ? RW / LW : RH;   // loads per record
+    // bytes per load: the piece size of the cache layout (cache_piece)
+    static constexpr int PB = LW ? 4 * LW : 2;
+    static_assert(cache_piece(D * BITS / 8) == PB, "one load per piece of the cache layout");
     // keys per lane and batch
     static constexpr int KPT = RW <= 12 ? 2 : 1;
     static constexpr int SW = QM / 32;             // sketch words per key
@@ -147,11 +151,13 @@ __global__ __launch_bounds__(256) void score_kernel(const SArgs a)
     //    record's address depends on its block-table entry, so the entries
     //    of all of the lane's keys are loaded first; the first batch's
     //    records are then in flight while the tables are built, and each
-    //    later batch is loaded while the previous one is summed.  Records
-    //    are read with ordinary (temporal) loads: a lane's 16-byte pieces of
-    //    one record come from three load instructions whose lanes are a
-    //    record apart, so the second and third find the lines in L1; with
-    //    non-temporal loads each instruction fetched them again.
+    //    later batch is loaded while the previous one is summed.  The cache
+    //    stores records piece-major, so one load instruction (piece v of
+    //    the wave's 64 keys) reads consecutive bytes of each cache block;
+    //    with records stored whole, the lanes of an instruction were a
+    //    record apart and every instruction touched every line of the span.
+    //    Pieces of 8 and 16 bytes are read non-temporally; 2- and 4-byte
+    //    pieces with ordinary loads (measured faster for them).
     const int64_t tend = min(t0 + (int64_t)kScoreChunk, len);
     const int32_t *table = a.block_table + (int64_t)s * a.max_blocks;
     constexpr int NB = kScoreChunk / 256 / S::KPT;
@@ -182,13 +188,16 @@ __global__ __launch_bounds__(256) void score_kernel(const SArgs a)
             const int32_t blk = bt[b][u];
             k.ok[u] = t < tend && blk >= 0 && blk < a.n_blocks;
             // an invalid key reads record 0 of block 0 (always present) and is not stored
-            const int64_t krow =
-                k.ok[u] ? ((int64_t)blk * a.n_kv_heads + h) * a.block_size + (tt - bi * a.block_size) : 0;
+            const int pos = k.ok[u] ? (int)(tt - bi * a.block_size) : 0;
+            const int64_t krow = k.ok[u] ? ((int64_t)blk * a.n_kv_heads + h) * a.block_size + pos : 0;
+            // piece v of the record (pieces of the load width, piece-major in
+            // the head's block region): consecutive keys' pieces are adjacent
+            const uint8_t *pc0 = a.k_idx + (krow - pos) * RB + (int64_t)pos * S::PB;
+            const int64_t pstep = (int64_t)a.block_size * S::PB;
             if constexpr (S::LW == 4) {
-                const u32x4 *rp = reinterpret_cast<const u32x4 *>(a.k_idx + krow * RB);
 #pragma unroll
                 for (int v = 0; v < S::RV; v++) {
-                    const u32x4 q4 = rp[v];
+                    const u32x4 q4 = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(pc0 + v * pstep));
 #pragma unroll
                     for (int c = 0; c < 4; c++) {
                         const uint32_t e = q4[c];
@@ -198,25 +207,22 @@ __global__ __launch_bounds__(256) void score_kernel(const SArgs a)
             } else if constexpr (S::LW == 0) {
                 // records of an odd number of half-words: 2-byte loads, paired
                 // into words (the upper half of the last word is zero)
-                const uint16_t *hp = reinterpret_cast<const uint16_t *>(a.k_idx + krow * RB);
 #pragma unroll
                 for (int c = 0; c < S::RW; c++) {
-                    const uint32_t lo = hp[2 * c];
-                    const uint32_t hi = 2 * c + 1 < S::RH ? (uint32_t)hp[2 * c + 1] : 0u;
+                    const uint32_t lo = *reinterpret_cast<const uint16_t *>(pc0 + (2 * c) * pstep);
+                    const uint32_t hi = 2 * c + 1 < S::RH ? (uint32_t)*reinterpret_cast<const uint16_t *>(pc0 + (2 * c + 1) * pstep) : 0u;
                     k.w[u][c] = lo | (hi << 16);
                 }
             } else if constexpr (S::LW == 1) {
                 // records of an odd number of words: 4-byte loads
-                const uint32_t *rp = reinterpret_cast<const uint32_t *>(a.k_idx + krow * RB);
 #pragma unroll
                 for (int v = 0; v < S::RV; v++)
-                    k.w[u][v] = rp[v];
+                    k.w[u][v] = *reinterpret_cast<const uint32_t *>(pc0 + v * pstep);
             } else {
                 // records of 8 (mod 16) bytes: 8-byte loads
-                const u32x2 *rp = reinterpret_cast<const u32x2 *>(a.k_idx + krow * RB);
 #pragma unroll
                 for (int v = 0; v < S::RV; v++) {
-                    const u32x2 q2 = rp[v];
+                    const u32x2 q2 = __builtin_nontemporal_load(reinterpret_cast<const u32x2 *>(pc0 + v * pstep));
                     const uint32_t e0 = q2[0], e1 = q2[1];
                     k.w[u][2 * v] = e0;
                     k.w[u][2 * v + 1] = e1;

@@ -15,7 +15,7 @@ struct GenScoreShape {
     int32_t d;
     int32_t slots;
     int32_t rec;
-    int32_t pad0;
+    int32_t rec_lp;      // log2 of the cache layout's piece size for rec bytes
     int64_t set_stride;
 };
 

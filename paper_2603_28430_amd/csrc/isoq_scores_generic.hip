@@ -4,7 +4,8 @@
 // padded width, Sec. 5.1), evaluated directly: the workgroup's query is
 // rotated once into LDS (scale folded in), then each lane takes one key and
 // sums (T q)_j c[idx_j] over the padded coordinates, reading its record slot
-// by slot as the generic stage-1 kernels write it.  This is the compatibility
+// by slot as the generic stage-1 kernels write it (through the cache's
+// piece-major layout).  This is the compatibility
 // path for widths no model family of the paper uses; it is not tuned.
 //
 // Workgroup (query head, chunk of kScoreChunk positions, sequence).  Query
@@ -70,8 +71,10 @@ __global__ __launch_bounds__(256) void generic_score_kernel(const SArgs a, const
         const int32_t blk = table[bi];
         if (blk < 0 || blk >= a.n_blocks)
             continue;
-        const int64_t krow = ((int64_t)blk * a.n_kv_heads + h) * a.block_size + ((uint32_t)t - bi * a.block_size);
-        const uint8_t *rec = a.k_idx + krow * g.rec;
+        const int pos = (int)((uint32_t)t - bi * a.block_size);
+        const int64_t krow = ((int64_t)blk * a.n_kv_heads + h) * a.block_size + pos;
+        // the record, piece-major in its head's block region
+        const CacheSrcRt rec{a.k_idx + (krow - pos) * g.rec, pos, a.block_size, g.rec_lp};
         float acc = 0.f;
 #pragma unroll 4
         for (int j = 0; j < g.slots; j++) {

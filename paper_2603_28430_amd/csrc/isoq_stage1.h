@@ -21,23 +21,29 @@ namespace {
 // [8 sub * BITS, 8 (sub + 1) * BITS) of the row's record: a 16-bit half-word
 // (2 bits), a 32-bit word (4 bits), or 24 bits at byte 3 sub (3 bits), which
 // the four lanes of a DPP quad merge into three aligned words.
-template <int BITS>
-__device__ __forceinline__ void store_bits(uint8_t *rec, int sub, uint32_t p, bool ok)
+template <int BITS, class Dst>
+__device__ __forceinline__ void store_bits_to(const Dst &rec, int sub, uint32_t p, bool ok)
 {
     if constexpr (BITS == 2) {
         if (ok)
-            reinterpret_cast<uint16_t *>(rec)[sub] = (uint16_t)p;
+            rec.template put<uint16_t>(2 * sub, (uint16_t)p);
     } else if constexpr (BITS == 4) {
         if (ok)
-            reinterpret_cast<uint32_t *>(rec)[sub] = p;
+            rec.template put<uint32_t>(4 * sub, p);
     } else {
         // lane k of a quad holds bits [24 k, 24 k + 24) of 96; lanes 0..2
         // write word k = p_k >> 8 k | p_(k+1) << (24 - 8 k)
         const uint32_t nb = dpp_u<DPP_QUAD_1233>(p);  // bits of the next lane in the quad
         const int k = sub & 3;
         if (ok && k < 3)
-            reinterpret_cast<uint32_t *>(rec)[3 * (sub >> 2) + k] = (p >> (8 * k)) | (nb << (24 - 8 * k));
+            rec.template put<uint32_t>(4 * (3 * (sub >> 2) + k), (p >> (8 * k)) | (nb << (24 - 8 * k)));
     }
+}
+
+template <int BITS>
+__device__ __forceinline__ void store_bits(uint8_t *rec, int sub, uint32_t p, bool ok)
+{
+    store_bits_to<BITS>(RecPtr{rec}, sub, p, ok);
 }
 
 template <int BITS, int LPV>
@@ -678,8 +684,9 @@ struct Stage1 {
                 (a.norms_out + grow)[lr] = rho;
         } else {
             bool ok;
-            const int64_t crow = cache_row_of(a, slot, ok);
-            store_bits<BITS>(a.rec_out + crow * RECB, sub, p, ok);
+            int pos;
+            const int64_t crow = cache_slot(a, slot, blockIdx.x, ok, pos);
+            store_bits_to<BITS>(cache_rec<RECB>(a, crow, pos), sub, p, ok);
             if (ok && sub == 0)
                 a.norms_out[crow] = rho;
         }

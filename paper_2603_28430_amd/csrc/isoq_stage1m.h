@@ -252,19 +252,20 @@ struct Stage1M {
     // Record bits of chunk c (coordinates 8 c .. 8 c + 7, bits [8 c b, 8 (c + 1) b)):
     // a half-word (2 bits), a word (4 bits), or for 3 bits 24 bits that the
     // lanes of chunks 4 k .. 4 k + 3 (4 lanes apart) merge into three words.
-    __device__ static __forceinline__ void store_bits(uint8_t *rec, int c, uint32_t p, bool ok)
+    template <class Dst>
+    __device__ static __forceinline__ void store_bits(const Dst &rec, int c, uint32_t p, bool ok)
     {
         if constexpr (BITS == 2) {
             if (ok)
-                reinterpret_cast<uint16_t *>(rec)[c] = (uint16_t)p;
+                rec.template put<uint16_t>(2 * c, (uint16_t)p);
         } else if constexpr (BITS == 4) {
             if (ok)
-                reinterpret_cast<uint32_t *>(rec)[c] = p;
+                rec.template put<uint32_t>(4 * c, p);
         } else {
             const uint32_t nb = dpp_u<DPP_ROW_SHL4>(p);   // the next chunk's bits
             const int k = c & 3;
             if (ok && k < 3)
-                reinterpret_cast<uint32_t *>(rec)[3 * (c >> 2) + k] = (p >> (8 * k)) | (nb << (24 - 8 * k));
+                rec.template put<uint32_t>(4 * (3 * (c >> 2) + k), (p >> (8 * k)) | (nb << (24 - 8 * k)));
         }
     }
 
@@ -537,13 +538,14 @@ struct Stage1M {
             // the row's record and norm: its row, or the token's cache row
             if constexpr (kAppend) {
                 bool ok;
-                const int64_t orow = cache_row_of(a, in.slot, ok);
-                store_bits(a.rec_out + orow * RECB, c, p, ok);
+                int pos;
+                const int64_t orow = cache_slot(a, in.slot, blockIdx.x, ok, pos);
+                store_bits(cache_rec<RECB>(a, orow, pos), c, p, ok);
                 if (ok && c == 0)
                     a.norms_out[orow] = rho;
             } else {
                 const uint32_t mr = mem_roff(a, roff);
-                store_bits(a.rec_out + mem_row0(a, row0) * RECB + (uint32_t)(mr * (uint32_t)RECB), c, p, true);
+                store_bits(RecPtr{a.rec_out + mem_row0(a, row0) * RECB + (uint32_t)(mr * (uint32_t)RECB)}, c, p, true);
                 if (c == 0)
                     (a.norms_out + mem_row0(a, row0))[mr] = rho;
             }

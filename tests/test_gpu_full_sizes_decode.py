@@ -21,6 +21,7 @@ import pytest
 
 import oracle
 import workloads
+from cache_layout import from_cache, to_cache
 from parity import Oracle
 
 torch = pytest.importorskip("torch")
@@ -61,7 +62,7 @@ def test_kv_append_prefill_full_size():
         s = slots.view(T, 1)
         blk, off = s // bs, s % bs
         hh = torch.arange(H, device="cuda").view(1, H)
-        got_i = cache[blk, hh, off]          # [T, H, R]
+        got_i = from_cache(cache)[blk, hh, off]          # [T, H, R]
         got_r = rho[blk, hh, off]            # [T, H]
         assert torch.equal(got_i.view(T * H, R), ri)
         assert torch.equal(got_r.view(T * H), rr)
@@ -79,7 +80,7 @@ def test_kv_append_prefill_full_size():
         o = Oracle("fast", D, BITS, rot, levels, xs, n_sets=H, rows_per_set=1, rows=rows, selected=True)
         tt, hh = rows // H, rows % H
         blk, off = s_np[tt] // bs, s_np[tt] % bs
-        c_np, r_np = cache.cpu().numpy(), rho.cpu().numpy()
+        c_np, r_np = from_cache(cache.cpu().numpy()), rho.cpu().numpy()
         o.check_indices(oracle.unpack(c_np[blk, hh, off], D, BITS))
         o.check_norms(r_np[blk, hh, off])
 
@@ -110,10 +111,10 @@ def test_kv_scores_full_size(m):
     if m:
         S = workloads.qjl_matrix(m, D, seed=9)
         sk = iq.isoq_sketch_init(p, m, S=S)
-        out = iq.isoq_kv_scores_qjl(p, sk, T_(q), T_(rec), T_(rho), T_(sg), T_(gam), T_(table), lens, scale,
+        out = iq.isoq_kv_scores_qjl(p, sk, T_(q), T_(to_cache(rec)), T_(rho), T_(sg), T_(gam), T_(table), lens, scale,
                                     max_len=T)
     else:
-        out = iq.isoq_kv_scores(p, T_(q), T_(rec), T_(rho), T_(table), lens, scale, max_len=T)
+        out = iq.isoq_kv_scores(p, T_(q), T_(to_cache(rec)), T_(rho), T_(table), lens, scale, max_len=T)
     torch.cuda.synchronize()
     got = out.cpu().numpy()
     assert np.all(np.isfinite(got))

@@ -11,6 +11,7 @@ import pytest
 
 import oracle
 import workloads
+from cache_layout import from_cache
 from parity import Oracle
 
 torch = pytest.importorskip("torch")
@@ -48,7 +49,7 @@ def check_tensor(variant, d, bits, rot, levels, n_sets, x, slots, n_heads, block
     n_slots = n_blocks * block_size
     n_tokens = len(slots)
     rec = p.record_bytes
-    ci = cidx.cpu().numpy().reshape(-1, rec)
+    ci = from_cache(cidx.cpu().numpy()).reshape(-1, rec)
     cr = crho.cpu().numpy().reshape(-1)
     valid_t = np.flatnonzero((slots >= 0) & (slots < n_slots))
     written = np.zeros(len(cr), bool)
@@ -66,7 +67,7 @@ def check_tensor(variant, d, bits, rot, levels, n_sets, x, slots, n_heads, block
         np.testing.assert_array_equal(ci[crow], qi.cpu().numpy()[rows])
         np.testing.assert_array_equal(cr[crow], qr.cpu().numpy()[rows])
         written[crow] = True
-    prev_i = np.full_like(ci, CANARY_BYTE) if before_idx is None else before_idx.reshape(-1, rec)
+    prev_i = np.full_like(ci, CANARY_BYTE) if before_idx is None else from_cache(before_idx).reshape(-1, rec)
     prev_r = np.full_like(cr, CANARY_RHO) if before_rho is None else before_rho.reshape(-1)
     np.testing.assert_array_equal(ci[~written], prev_i[~written])
     np.testing.assert_array_equal(cr[~written], prev_r[~written])

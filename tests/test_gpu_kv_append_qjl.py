@@ -11,6 +11,7 @@ import numpy as np
 import pytest
 
 import workloads
+from cache_layout import from_cache
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -50,7 +51,7 @@ def run_case(variant, d, bits, m, dtype, n_tokens, n_heads, block_size, n_blocks
         skh = sk if n_sets == 1 else iq.isoq_sketch_init(ph, m, S=workloads.qjl_matrix(m, d, seed=seed))
         refs.append([t.cpu().numpy() for t in iq.isoq_quantize_qjl(ph, skh, x[:, h].contiguous())])
     torch.cuda.synchronize()
-    rec, sg, rho, gam = rec.cpu().numpy(), sg.cpu().numpy(), rho.cpu().numpy(), gam.cpu().numpy()
+    rec, sg, rho, gam = from_cache(rec.cpu().numpy()), sg.cpu().numpy(), rho.cpu().numpy(), gam.cpu().numpy()
     s_np = slots.cpu().numpy()
     written = np.zeros((n_blocks, n_heads, block_size), bool)
     tok = np.flatnonzero((s_np >= 0) & (s_np < n_blocks * block_size))

@@ -20,6 +20,7 @@ import pytest
 
 import oracle
 import workloads
+from cache_layout import to_cache
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -82,7 +83,7 @@ class Cache:
         self.seq_lens = np.asarray(seq_lens, np.int32)
 
     def device(self):
-        return (torch.from_numpy(self.rec).cuda(), torch.from_numpy(self.rho).cuda(),
+        return (torch.from_numpy(to_cache(self.rec)).cuda(), torch.from_numpy(self.rho).cuda(),
                 torch.from_numpy(self.table).cuda(), torch.from_numpy(self.seq_lens).cuda())
 
 

@@ -16,6 +16,7 @@ import pytest
 
 import oracle
 import workloads
+from cache_layout import to_cache
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -76,7 +77,7 @@ def run_case(variant, d, bits, m, dtype, n_seqs, n_q, n_kv, bs, seq_lens, n_sets
     ml = table.shape[1] * bs
     out = torch.full((n_seqs, n_q, ml), CANARY, dtype=torch.float32, device="cuda")
     T = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
-    iq.isoq_kv_scores_qjl(p, sk, T(q), T(rec), T(rho), T(sg), T(gam), T(table),
+    iq.isoq_kv_scores_qjl(p, sk, T(q), T(to_cache(rec)), T(rho), T(sg), T(gam), T(table),
                           T(np.asarray(seq_lens, np.int32)), scale, max_len=ml, scores=out)
     torch.cuda.synchronize()
     got = out.cpu().numpy()
@@ -142,7 +143,7 @@ def test_scores_qjl_end_to_end_unbiased():
     xh = iq.isoq_dequantize(p, idx, rho, dtype=torch.float32)
     # one sequence, blocks in order: cache row t = position t
     nb = n_tok // bs
-    rec = idx.view(nb, 1, bs, -1).contiguous()
+    rec = to_cache(idx.view(nb, 1, bs, -1))
     cr = rho.view(nb, 1, bs).contiguous()
     cs = sg.view(nb, 1, bs, -1).contiguous()
     cg = gam.view(nb, 1, bs).contiguous()
