@@ -200,10 +200,11 @@ isoq_status isoq_roundtrip(const isoq_params *p, int dtype, const void *x, int64
  *               h) owns the block_size * R bytes from (b n_heads + h)
  *               block_size R on.  Inside that region the records are stored
  *               piece-major: record byte k of position p lies at byte
- *               (floor(k / P) block_size + p) P + k mod P, with P the largest
- *               of 16, 8, 4, 2, 1 dividing R (so a piece of consecutive
- *               positions is adjacent, which the logit kernel reads in one
- *               coalesced load).  Record bytes as in isoq_quantize.
+ *               (floor(k / P) block_size + p) P + k mod P, with P = 16 if 16
+ *               divides R, else 8 if 8 divides R, else P = R (records stored
+ *               whole, position after position).  Pieces of consecutive
+ *               positions are adjacent, which the logit kernel reads in one
+ *               coalesced load.  Record bytes as in isoq_quantize.
  *   k_rho, v_rho  device, fp32 [n_blocks][n_heads][block_size].
  * Limits: n_tokens * n_heads < 2^31, n_blocks * block_size < 2^31, n_heads and
  * block_size >= 1, and for the one-launch shapes at most 65,535 launch blocks

@@ -132,13 +132,13 @@ isoq_status launch(const void *fn, dim3 grid, void **args, void *stream, int thr
     return ISOQ_OK;
 }
 
-const void *packed_kernel(int variant, int bits, int mode, int chunks)
+const void *packed_kernel(int variant, int bits, int mode, int chunks, int cache_lp = -1)
 {
     switch (variant) {
-    case VAR_FULL: return packed_kernel_full(bits, mode, chunks);
-    case VAR_FAST: return packed_kernel_fast(bits, mode, chunks);
-    case VAR_PLANAR2D: return packed_kernel_2d(bits, mode, chunks);
-    case VAR_BLOCK8: return packed_kernel_8d(bits, mode, chunks);
+    case VAR_FULL: return packed_kernel_full(bits, mode, chunks, cache_lp);
+    case VAR_FAST: return packed_kernel_fast(bits, mode, chunks, cache_lp);
+    case VAR_PLANAR2D: return packed_kernel_2d(bits, mode, chunks, cache_lp);
+    case VAR_BLOCK8: return packed_kernel_8d(bits, mode, chunks, cache_lp);
     }
     return nullptr;
 }
@@ -607,7 +607,9 @@ isoq_status isoq_kv_append(const isoq_params *pk, const isoq_params *pv, int dty
     }
     // one kernel for both tensors; block (x, y, z) = (head, token range, K|V)
     const bool quad = dtype == ISOQ_F16 && quad_layout(pk->variant, pk->d);
-    const void *fn = packed ? packed_kernel(pk->variant, pk->bits, MODE_APPEND, ps.chunks)
+    const int64_t rec_b = (int64_t)record_bytes(pk->variant, pk->d, pk->bits);
+    const int cache_lp = rec_b % 16 == 0 ? 4 : rec_b % 8 == 0 ? 3 : -1;   // cache_piece
+    const void *fn = packed ? packed_kernel(pk->variant, pk->bits, MODE_APPEND, ps.chunks, cache_lp)
                      : quad ? kernel_m_for(pk->variant, pk->d, pk->bits, MODE_APPEND)
                             : kernel_for(pk->variant, pk->d, pk->bits, dtype == ISOQ_F16, false, MODE_APPEND);
     if (!fn)
@@ -663,10 +665,7 @@ isoq_status kv_scores_generic(const isoq_params *pk, int dtype, const void *q, i
     g.d = pk->d;
     g.slots = (padded_width(pk->variant, pk->d) + sw - 1) / sw;
     g.rec = (int32_t)record_bytes(pk->variant, pk->d, pk->bits);
-    {
-        const int P = cache_piece(g.rec);
-        g.rec_lp = P == 16 ? 4 : P == 8 ? 3 : P == 4 ? 2 : P == 2 ? 1 : 0;
-    }
+    g.rec_lp = g.rec % 16 == 0 ? 4 : g.rec % 8 == 0 ? 3 : -1;   // cache_piece
     g.set_stride = (int64_t)slots_per_set(pk->variant, pk->d) * params_per_slot(pk->variant);
     SArgs a{};
     a.q = q;

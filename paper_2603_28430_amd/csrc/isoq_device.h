@@ -54,7 +54,6 @@ __device__ __forceinline__ uint32_t fast_div(uint32_t n, const FastDiv &f)
     return (t + ((n - t) >> f.s1)) >> f.s2;
 }
 
-// Sum over the LPV lanes of a row; every lane of the row gets the same bits.
 // Where an index record goes.  RecPtr: consecutive bytes.  CacheRec<P>: a
 // record in a paged cache, pieces of P bytes (cache_piece): record byte k of
 // position pos at byte ((k / P) bs + pos) P + k mod P of the head's block
@@ -83,23 +82,46 @@ struct CacheRec {
     __device__ __forceinline__ CacheRec at(int k) const { return CacheRec{region, pos, bs, off + k}; }
 };
 
-// CacheRec with the piece size known at run time (P = 1 << lp).
+// CacheRec with the piece size known at run time: P = 1 << lp (16 or 8),
+// or lp < 0 for records stored whole (P = rb, the record size).
 struct CacheRecRt {
     uint8_t *region;
-    int pos, bs, off, lp;
+    int pos, bs, off, lp, rb;
     template <typename T>
     __device__ __forceinline__ void put(int k, T v) const
     {
         const int b = off + k;
-        *reinterpret_cast<T *>(region + ((((int64_t)(b >> lp)) * bs + pos) << lp) + (b & ((1 << lp) - 1))) = v;
+        const int64_t o = lp < 0 ? (int64_t)pos * rb + b
+                                 : ((((int64_t)(b >> lp)) * bs + pos) << lp) + (b & ((1 << lp) - 1));
+        *reinterpret_cast<T *>(region + o) = v;
     }
-    __device__ __forceinline__ CacheRecRt at(int k) const { return CacheRecRt{region, pos, bs, off + k, lp}; }
+    __device__ __forceinline__ CacheRecRt at(int k) const { return CacheRecRt{region, pos, bs, off + k, lp, rb}; }
 };
 
-__device__ __forceinline__ int cache_piece_log2(int64_t R)
+// CacheRecRt with lp a constant.
+template <int LP>
+struct CacheRecK {
+    uint8_t *region;
+    int pos, bs, off, rb;
+    template <typename T>
+    __device__ __forceinline__ void put(int k, T v) const
+    {
+        const int b = off + k;
+        int64_t o;
+        if constexpr (LP < 0)
+            o = (int64_t)pos * rb + b;
+        else
+            o = ((((int64_t)(b >> LP)) * bs + pos) << LP) + (b & ((1 << LP) - 1));
+        *reinterpret_cast<T *>(region + o) = v;
+    }
+    __device__ __forceinline__ CacheRecK at(int k) const { return CacheRecK{region, pos, bs, off + k, rb}; }
+};
+
+// lp of CacheRecRt for records of R bytes.
+__host__ __device__ __forceinline__ int cache_piece_log2(int64_t R)
 {
     const int P = cache_piece(R);
-    return P == 16 ? 4 : P == 8 ? 3 : P == 4 ? 2 : P == 2 ? 1 : 0;
+    return P == 16 && R % 16 == 0 ? 4 : P == 8 && R % 8 == 0 ? 3 : -1;
 }
 
 // Slot s of head `head` in a paged cache: slot s is position s mod
@@ -125,6 +147,7 @@ __device__ __forceinline__ CacheRec<cache_piece(R)> cache_rec(const KArgs &a, in
     return CacheRec<cache_piece(R)>{a.rec_out + (crow - pos) * R, pos, (int)a.block_size, 0};
 }
 
+// Sum over the LPV lanes of a row; every lane of the row gets the same bits.
 template <int LPV>
 __device__ __forceinline__ float row_sum(float v)
 {

@@ -134,11 +134,13 @@ struct RecSrc {
 };
 struct CacheSrcRt {
     const uint8_t *region;
-    int pos, bs, lp;
+    int pos, bs, lp, rb;
     template <typename T>
     __device__ __forceinline__ T get(int k) const
     {
-        return *reinterpret_cast<const T *>(region + ((((int64_t)(k >> lp)) * bs + pos) << lp) + (k & ((1 << lp) - 1)));
+        const int64_t o = lp < 0 ? (int64_t)pos * rb + k
+                                 : ((((int64_t)(k >> lp)) * bs + pos) << lp) + (k & ((1 << lp) - 1));
+        return *reinterpret_cast<const T *>(region + o);
     }
 };
 
@@ -392,7 +394,7 @@ __global__ __launch_bounds__(kBlockThreads) void generic_kernel(const KArgs a)
                 }
             };
             if constexpr (kAppend)
-                write(CacheRecRt{a.rec_out + (orow - pos) * nb, pos, (int)a.block_size, 0, cache_piece_log2(nb)});
+                write(CacheRecRt{a.rec_out + (orow - pos) * nb, pos, (int)a.block_size, 0, cache_piece_log2(nb), nb});
             else
                 write(RecPtr{ro0 + t * rstep});
             if (wr && sub == 0)

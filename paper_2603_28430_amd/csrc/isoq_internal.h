@@ -156,10 +156,11 @@ ScoreKernel score_qjl_kernel_for(int variant, int d, int bits, bool f16, int gro
 // per coordinate: the products would save little and add their latency).
 // Paged caches (isoq_kv_append, isoq_kv_scores) hold a head's records of
 // one cache block piece-major: a record of R bytes is cut into pieces of
-// cache_piece(R) bytes (the largest of 16, 8, 4, 2, 1 dividing R), and piece
-// j of position pos lies at byte (j block_size + pos) cache_piece(R) of the
-// head's block region, so consecutive positions' pieces are adjacent.
-constexpr int cache_piece(int64_t R) { return R % 16 == 0 ? 16 : R % 8 == 0 ? 8 : R % 4 == 0 ? 4 : R % 2 == 0 ? 2 : 1; }
+// P = cache_piece(R) bytes, and piece j of position pos lies at byte
+// (j block_size + pos) P of the head's block region, so consecutive
+// positions' pieces are adjacent.  P is 16 or 8 when that divides R; other
+// records are one piece (P = R: stored whole, one after the other).
+constexpr int cache_piece(int64_t R) { return R % 16 == 0 ? 16 : R % 8 == 0 ? 8 : (int)R; }
 
 constexpr bool quad_layout(int variant, int d) { return variant != VAR_PLANAR2D && (d == 64 || d == 128 || d == 256); }
 const void *kernel_m_for(int variant, int d, int bits, int mode);
@@ -234,10 +235,12 @@ constexpr int packed_tiles_per_block(int variant, int chunks)
 {
     return (variant == VAR_FULL || variant == VAR_BLOCK8) && chunks == 2 ? 2 : 1;
 }
-const void *packed_kernel_full(int bits, int mode, int chunks);
-const void *packed_kernel_fast(int bits, int mode, int chunks);
-const void *packed_kernel_2d(int bits, int mode, int chunks);
-const void *packed_kernel_8d(int bits, int mode, int chunks);
+// (cache_lp, append only: the cache layout's pieces, 1 << cache_lp bytes, or
+// records whole for cache_lp < 0)
+const void *packed_kernel_full(int bits, int mode, int chunks, int cache_lp = -1);
+const void *packed_kernel_fast(int bits, int mode, int chunks, int cache_lp = -1);
+const void *packed_kernel_2d(int bits, int mode, int chunks, int cache_lp = -1);
+const void *packed_kernel_8d(int bits, int mode, int chunks, int cache_lp = -1);
 // Packed-row kernels with the stage-2 sketch of m bits (isoq_packed_qjl.hip):
 // quantize into rows (one rotation set) or, with `append`, into the slots of
 // a paged cache, for fp16 rows at d = 80, 96, 160 and 192; or nullptr.

@@ -138,7 +138,7 @@ __device__ __forceinline__ float packed_pair_total(const float *rp, int n)
     return tot;
 }
 
-template <int VAR, int BITS, int MODE, int C, int D = 0, int QM = 0, int WAVES = kBlockThreads / 64>
+template <int VAR, int BITS, int MODE, int C, int D = 0, int QM = 0, int WAVES = kBlockThreads / 64, int LP = 0>
 __device__ __forceinline__ void packed_body(const KArgs &a)
 {
     constexpr int BT = WAVES * 64;   // threads per block
@@ -188,7 +188,6 @@ __device__ __forceinline__ void packed_body(const KArgs &a)
     const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int64_t rowb = (int64_t)a.g_d * 2;       // fp16 rows
     const int64_t recb = (int64_t)L * C * BITS;    // d b / 8
-    const int rec_lp = cache_piece_log2(recb);     // append: piece size of the cache layout
     const int TPB = kQjl ? a.g_tpb : kAppend ? 1 : packed_tiles_per_block(VAR, C);   // row tiles per block
     const int64_t base0 = (int64_t)(kAppend ? blockIdx.y : blockIdx.x) * TPB * WAVES * GPW;
     // append: the block's head, its input row stride and cache addressing
@@ -408,15 +407,22 @@ __device__ __forceinline__ void packed_body(const KArgs &a)
                     bool ok;
                     int pos;
                     const int64_t cr = cache_slot(a, slot[u], head, ok, pos);
-                    const CacheRecRt rec{a.rec_out + (cr - pos) * recb, pos, (int)a.block_size, 0, rec_lp};
-                    if (BITS == 3 && L % 4 != 0) {
-                        // d = 80: quads would straddle rows
-                        store_bits3_pairs(rec, sub, p[0], on && ok);
-                    } else {
+                    auto store = [&](const auto &rec) {
+                        if (BITS == 3 && L % 4 != 0) {
+                            // d = 80: quads would straddle rows
+                            store_bits3_pairs(rec, sub, p[0], on && ok);
+                        } else {
 #pragma unroll
-                        for (int k = 0; k < C; k++)
-                            store_bits_to<BITS>(rec.at(k * L * BITS), sub, p[k], on && ok);
-                    }
+                            for (int k = 0; k < C; k++)
+                                store_bits_to<BITS>(rec.at(k * L * BITS), sub, p[k], on && ok);
+                        }
+                    };
+                    // the cache layout's pieces: from the width where it is a
+                    // constant, else from the kernel's LP
+                    if constexpr (D > 0)
+                        store(cache_rec<(int64_t)D * BITS / 8>(a, cr, pos));
+                    else
+                        store(CacheRecK<LP>{a.rec_out + (cr - pos) * recb, pos, (int)a.block_size, 0, (int)recb});
                     if (on && ok && sub == 0) {
                         a.norms_out[cr] = rho;
                         if constexpr (kQjl)
@@ -490,10 +496,11 @@ __global__ __launch_bounds__(kBlockThreads) void packed_kernel(const KArgs a)
 }
 
 // K and V in one launch: blockIdx.z = 0 encodes the keys, 1 the values.
-template <int VAR, int BITS, int C>
+// LP: the cache layout's pieces (1 << LP bytes, or records whole for -1).
+template <int VAR, int BITS, int C, int LP>
 __global__ __launch_bounds__(kBlockThreads) void packed_append_kernel(const KArgs k, const KArgs v)
 {
-    packed_body<VAR, BITS, MODE_APPEND, C>(blockIdx.z == 0 ? k : v);
+    packed_body<VAR, BITS, MODE_APPEND, C, 0, 0, kBlockThreads / 64, LP>(blockIdx.z == 0 ? k : v);
 }
 
 // With the stage-2 sketch: width D, m = QM sign bits, kPackedQjlWaves waves
@@ -505,13 +512,16 @@ __global__ __launch_bounds__(kPackedQjlWaves * 64) void packed_qjl_kernel(const 
 }
 
 template <int VAR, int BITS, int C>
-const void *packed_pick_mode(int mode)
+const void *packed_pick_mode(int mode, int cache_lp)
 {
     switch (mode) {
     case MODE_ROUNDTRIP: return reinterpret_cast<const void *>(&packed_kernel<VAR, BITS, MODE_ROUNDTRIP, C>);
     case MODE_QUANTIZE: return reinterpret_cast<const void *>(&packed_kernel<VAR, BITS, MODE_QUANTIZE, C>);
     case MODE_DEQUANTIZE: return reinterpret_cast<const void *>(&packed_kernel<VAR, BITS, MODE_DEQUANTIZE, C>);
-    case MODE_APPEND: return reinterpret_cast<const void *>(&packed_append_kernel<VAR, BITS, C>);
+    case MODE_APPEND:
+        return cache_lp == 4   ? reinterpret_cast<const void *>(&packed_append_kernel<VAR, BITS, C, 4>)
+               : cache_lp == 3 ? reinterpret_cast<const void *>(&packed_append_kernel<VAR, BITS, C, 3>)
+                               : reinterpret_cast<const void *>(&packed_append_kernel<VAR, BITS, C, -1>);
     }
     return nullptr;
 }
@@ -521,15 +531,15 @@ const void *packed_pick_mode(int mode)
 // (measured at d = 96: 0.71 of the HBM roofline for the round trip, against
 // 0.60-0.64 with a lane's 32 contiguous bytes)
 template <int VAR>
-const void *packed_pick(int bits, int mode, int chunks)
+const void *packed_pick(int bits, int mode, int chunks, int cache_lp)
 {
     switch (bits * 4 + chunks) {
-    case 2 * 4 + 1: return packed_pick_mode<VAR, 2, 1>(mode);
-    case 2 * 4 + 2: return packed_pick_mode<VAR, 2, 2>(mode);
-    case 3 * 4 + 1: return packed_pick_mode<VAR, 3, 1>(mode);
-    case 3 * 4 + 2: return packed_pick_mode<VAR, 3, 2>(mode);
-    case 4 * 4 + 1: return packed_pick_mode<VAR, 4, 1>(mode);
-    case 4 * 4 + 2: return packed_pick_mode<VAR, 4, 2>(mode);
+    case 2 * 4 + 1: return packed_pick_mode<VAR, 2, 1>(mode, cache_lp);
+    case 2 * 4 + 2: return packed_pick_mode<VAR, 2, 2>(mode, cache_lp);
+    case 3 * 4 + 1: return packed_pick_mode<VAR, 3, 1>(mode, cache_lp);
+    case 3 * 4 + 2: return packed_pick_mode<VAR, 3, 2>(mode, cache_lp);
+    case 4 * 4 + 1: return packed_pick_mode<VAR, 4, 1>(mode, cache_lp);
+    case 4 * 4 + 2: return packed_pick_mode<VAR, 4, 2>(mode, cache_lp);
     }
     return nullptr;
 }

@@ -5,8 +5,17 @@
 
 namespace isoq {
 
-const void *packed_kernel_full(int bits, int mode, int chunks) { return packed_pick<VAR_FULL>(bits, mode, chunks); }
-const void *packed_kernel_fast(int bits, int mode, int chunks) { return packed_pick<VAR_FAST>(bits, mode, chunks); }
-const void *packed_kernel_2d(int bits, int mode, int chunks) { return packed_pick<VAR_PLANAR2D>(bits, mode, chunks); }
+const void *packed_kernel_full(int bits, int mode, int chunks, int cache_lp)
+{
+    return packed_pick<VAR_FULL>(bits, mode, chunks, cache_lp);
+}
+const void *packed_kernel_fast(int bits, int mode, int chunks, int cache_lp)
+{
+    return packed_pick<VAR_FAST>(bits, mode, chunks, cache_lp);
+}
+const void *packed_kernel_2d(int bits, int mode, int chunks, int cache_lp)
+{
+    return packed_pick<VAR_PLANAR2D>(bits, mode, chunks, cache_lp);
+}
 
 }  // namespace isoq

@@ -6,6 +6,9 @@
 
 namespace isoq {
 
-const void *packed_kernel_8d(int bits, int mode, int chunks) { return packed_pick<VAR_BLOCK8>(bits, mode, chunks); }
+const void *packed_kernel_8d(int bits, int mode, int chunks, int cache_lp)
+{
+    return packed_pick<VAR_BLOCK8>(bits, mode, chunks, cache_lp);
+}
 
 }  // namespace isoq

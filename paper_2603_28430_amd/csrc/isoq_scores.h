@@ -53,9 +53,11 @@ struct ScoreShape {
     // record of an odd number of half-words, read in 2-byte loads
     static constexpr int LW = RW * 32 != D * BITS ? 0 : RW % 4 == 0 ? 4 : RW % 2 == 0 ? 2 : 1;
     static constexpr int RV = LW ? RW / LW : RH;   // loads per record
-    // bytes per load: the piece size of the cache layout (cache_piece)
+    // bytes per load, and the piece size of the cache layout (cache_piece):
+    // one load per piece (16 or 8 bytes), or several per record stored whole
     static constexpr int PB = LW ? 4 * LW : 2;
-    static_assert(cache_piece(D * BITS / 8) == PB, "one load per piece of the cache layout");
+    static constexpr int CP = cache_piece(D * BITS / 8);
+    static_assert(CP % PB == 0, "loads tile the pieces of the cache layout");
     // keys per lane and batch
     static constexpr int KPT = RW <= 12 ? 2 : 1;
     static constexpr int SW = QM / 32;             // sketch words per key
@@ -156,8 +158,10 @@ __global__ __launch_bounds__(256) void score_kernel(const SArgs a)
     //    the wave's 64 keys) reads consecutive bytes of each cache block;
     //    with records stored whole, the lanes of an instruction were a
     //    record apart and every instruction touched every line of the span.
-    //    Pieces of 8 and 16 bytes are read non-temporally; 2- and 4-byte
-    //    pieces with ordinary loads (measured faster for them).
+    //    Pieces of 8 and 16 bytes are read non-temporally; records stored
+    //    whole (sizes not a multiple of 8) with ordinary 2- or 4-byte loads,
+    //    whose lanes are a record apart (the second and later loads of a
+    //    line then hit L1).
     const int64_t tend = min(t0 + (int64_t)kScoreChunk, len);
     const int32_t *table = a.block_table + (int64_t)s * a.max_blocks;
     constexpr int NB = kScoreChunk / 256 / S::KPT;
@@ -190,14 +194,16 @@ __global__ __launch_bounds__(256) void score_kernel(const SArgs a)
             // an invalid key reads record 0 of block 0 (always present) and is not stored
             const int pos = k.ok[u] ? (int)(tt - bi * a.block_size) : 0;
             const int64_t krow = k.ok[u] ? ((int64_t)blk * a.n_kv_heads + h) * a.block_size + pos : 0;
-            // piece v of the record (pieces of the load width, piece-major in
-            // the head's block region): consecutive keys' pieces are adjacent
-            const uint8_t *pc0 = a.k_idx + (krow - pos) * RB + (int64_t)pos * S::PB;
-            const int64_t pstep = (int64_t)a.block_size * S::PB;
+            // load v of the record: byte v PB, in piece v PB / CP of the
+            // head's block region (piece-major: consecutive keys' pieces are
+            // adjacent), at byte v PB mod CP of the piece
+            const uint8_t *pc0 = a.k_idx + (krow - pos) * RB + (int64_t)pos * S::CP;
+            const int64_t pstep = (int64_t)a.block_size * S::CP;
+            auto at = [&](int v) { return pc0 + (v * S::PB / S::CP) * pstep + (v * S::PB % S::CP); };
             if constexpr (S::LW == 4) {
 #pragma unroll
                 for (int v = 0; v < S::RV; v++) {
-                    const u32x4 q4 = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(pc0 + v * pstep));
+                    const u32x4 q4 = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(at(v)));
 #pragma unroll
                     for (int c = 0; c < 4; c++) {
                         const uint32_t e = q4[c];
@@ -209,20 +215,20 @@ __global__ __launch_bounds__(256) void score_kernel(const SArgs a)
                 // into words (the upper half of the last word is zero)
 #pragma unroll
                 for (int c = 0; c < S::RW; c++) {
-                    const uint32_t lo = *reinterpret_cast<const uint16_t *>(pc0 + (2 * c) * pstep);
-                    const uint32_t hi = 2 * c + 1 < S::RH ? (uint32_t)*reinterpret_cast<const uint16_t *>(pc0 + (2 * c + 1) * pstep) : 0u;
+                    const uint32_t lo = *reinterpret_cast<const uint16_t *>(at(2 * c));
+                    const uint32_t hi = 2 * c + 1 < S::RH ? (uint32_t)*reinterpret_cast<const uint16_t *>(at(2 * c + 1)) : 0u;
                     k.w[u][c] = lo | (hi << 16);
                 }
             } else if constexpr (S::LW == 1) {
                 // records of an odd number of words: 4-byte loads
 #pragma unroll
                 for (int v = 0; v < S::RV; v++)
-                    k.w[u][v] = *reinterpret_cast<const uint32_t *>(pc0 + v * pstep);
+                    k.w[u][v] = *reinterpret_cast<const uint32_t *>(at(v));
             } else {
                 // records of 8 (mod 16) bytes: 8-byte loads
 #pragma unroll
                 for (int v = 0; v < S::RV; v++) {
-                    const u32x2 q2 = __builtin_nontemporal_load(reinterpret_cast<const u32x2 *>(pc0 + v * pstep));
+                    const u32x2 q2 = __builtin_nontemporal_load(reinterpret_cast<const u32x2 *>(at(v)));
                     const uint32_t e0 = q2[0], e1 = q2[1];
                     k.w[u][2 * v] = e0;
                     k.w[u][2 * v + 1] = e1;

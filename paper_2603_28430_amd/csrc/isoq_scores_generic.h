@@ -15,7 +15,7 @@ struct GenScoreShape {
     int32_t d;
     int32_t slots;
     int32_t rec;
-    int32_t rec_lp;      // log2 of the cache layout's piece size for rec bytes
+    int32_t rec_lp;      // the cache layout's pieces: 1 << rec_lp bytes, or records whole (< 0)
     int64_t set_stride;
 };
 

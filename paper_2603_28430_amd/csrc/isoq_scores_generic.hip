@@ -74,7 +74,7 @@ __global__ __launch_bounds__(256) void generic_score_kernel(const SArgs a, const
         const int pos = (int)((uint32_t)t - bi * a.block_size);
         const int64_t krow = ((int64_t)blk * a.n_kv_heads + h) * a.block_size + pos;
         // the record, piece-major in its head's block region
-        const CacheSrcRt rec{a.k_idx + (krow - pos) * g.rec, pos, a.block_size, g.rec_lp};
+        const CacheSrcRt rec{a.k_idx + (krow - pos) * g.rec, pos, a.block_size, g.rec_lp, g.rec};
         float acc = 0.f;
 #pragma unroll 4
         for (int j = 0; j < g.slots; j++) {

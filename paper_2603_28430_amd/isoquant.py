@@ -315,8 +315,8 @@ def isoq_kv_append(pk: Params, k_new, slot_mapping, k_idx, k_rho, pv: Params = N
     (v_rho) [n_blocks, n_heads, block_size] fp32 at the slots slot_mapping
     [n_tokens] int64 (see include/isoquant.h).  The bytes of each
     [block_size, record_bytes] plane hold its records piece-major (pieces of
-    P bytes, P the largest of 16, 8, 4, 2, 1 dividing record_bytes: piece j
-    of position s at byte (j block_size + s) P), not one record per row."""
+    P bytes, P = 16 or 8 when it divides record_bytes, else P = record_bytes:
+    piece j of position s at byte (j block_size + s) P)."""
     torch = _torch()
     if k_new.dim() != 3 or k_idx.dim() != 4 or k_rho.dim() != 3:
         raise ValueError("k_new [n_tokens, n_heads, d], k_idx [n_blocks, n_heads, block_size, R], "

@@ -2,16 +2,15 @@
 out from its definition in include/isoquant.h: a cache of shape
 [n_blocks, n_heads, block_size, R] bytes holds, per (block, head), the
 block_size records of R bytes piece-major -- each record cut into pieces of
-P bytes (the largest of 16, 8, 4, 2, 1 dividing R), piece j of position s at
-byte (j * block_size + s) * P of the (block, head) region.  to_cache turns
-record-major records into that byte order, from_cache back."""
+P bytes (16 if 16 divides R, else 8 if 8 divides R, else P = R: records
+stored whole), piece j of position s at byte (j * block_size + s) * P of the
+(block, head) region.  to_cache turns record-major records into that byte
+order, from_cache back."""
 import numpy as np
 
 
 def piece_bytes(R):
-    for P in (16, 8, 4, 2, 1):
-        if R % P == 0:
-            return P
+    return 16 if R % 16 == 0 else 8 if R % 8 == 0 else R
 
 
 def to_cache(records):

@@ -13,7 +13,7 @@ def test_cache_layout_formula(R):
     rec = rng.integers(0, 256, (nb, H, bs, R), dtype=np.uint8)
     cache = to_cache(rec)
     P = piece_bytes(R)
-    assert R % P == 0 and (P == 16 or R % (2 * P) != 0)
+    assert R % P == 0 and (P == 16 or R % (2 * P) != 0) and (P in (8, 16) or P == R)
     flat = cache.reshape(nb, H, bs * R)
     for b in range(nb):
         for h in range(H):
