@@ -196,7 +196,7 @@ isoq_status run(const isoq_params *p, int dtype, int mode, KArgs &a, void *strea
     // fp16 encoders whose blocks each have one set rotate on the matrix cores
     // (the decoder is the same in both layouts); so do rows with one set each
     // in turn (rows_per_set = 1), as n_sets streams of one set each
-    const bool quad = f16 && quad_layout(p->variant, p->d) && mode != MODE_DEQUANTIZE;
+    const bool quad = f16 && quad_layout(p->variant, p->d, p->bits) && mode != MODE_DEQUANTIZE;
     if (quad && generic && a.rows_per_set == 1) {
         const int64_t per_stream = (a.n + p->n_sets - 1) / p->n_sets;
         const int64_t tiles = (per_stream + rpb - 1) / rpb;
@@ -387,7 +387,7 @@ isoq_status isoq_params_init(isoq_params **out, int variant, int d, int bits, in
     // the matrix-core encoders' fp16 (hi, lo) matrix rows, after the rest
     // (16-byte aligned: every part above is a multiple of 4 floats)
     p->mfma_offset = 0;
-    if (quad_layout(variant, d)) {
+    if (quad_layout(variant, d, bits)) {
         const size_t per_set = mfma_bytes_per_set(variant, d);
         std::vector<uint16_t> mf;
         try {
@@ -606,7 +606,7 @@ isoq_status isoq_kv_append(const isoq_params *pk, const isoq_params *pv, int dty
         return ISOQ_OK;
     }
     // one kernel for both tensors; block (x, y, z) = (head, token range, K|V)
-    const bool quad = dtype == ISOQ_F16 && quad_layout(pk->variant, pk->d);
+    const bool quad = dtype == ISOQ_F16 && quad_layout(pk->variant, pk->d, pk->bits);
     const int64_t rec_b = (int64_t)record_bytes(pk->variant, pk->d, pk->bits);
     const int cache_lp = rec_b % 16 == 0 ? 4 : rec_b % 8 == 0 ? 3 : -1;   // cache_piece
     const void *fn = packed ? packed_kernel(pk->variant, pk->bits, MODE_APPEND, ps.chunks, cache_lp)

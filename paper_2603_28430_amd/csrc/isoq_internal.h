@@ -149,11 +149,6 @@ ScoreKernel score_kernel_for_block8(int d, int bits, bool f16, int group);
 // The same with the stage-2 residual correction of m sign bits (isoq_scores_qjl.hip).
 ScoreKernel score_qjl_kernel_for(int variant, int d, int bits, bool f16, int group, int m);
 
-// Variants and widths whose fp16 encoders (round trip, quantize, append,
-// sketch) rotate on the matrix cores in the quad layout (isoq_stage1m.h), and
-// the kernel for (variant, d, bits, mode) there (round trip, quantize,
-// append), or nullptr.  The 2-D case keeps its VALU rotation (2 multiply-adds
-// per coordinate: the products would save little and add their latency).
 // Paged caches (isoq_kv_append, isoq_kv_scores) hold a head's records of
 // one cache block piece-major: a record of R bytes is cut into pieces of
 // P = cache_piece(R) bytes, and piece j of position pos lies at byte
@@ -162,7 +157,16 @@ ScoreKernel score_qjl_kernel_for(int variant, int d, int bits, bool f16, int gro
 // records are one piece (P = R: stored whole, one after the other).
 constexpr int cache_piece(int64_t R) { return R % 16 == 0 ? 16 : R % 8 == 0 ? 8 : (int)R; }
 
-constexpr bool quad_layout(int variant, int d) { return variant != VAR_PLANAR2D && (d == 64 || d == 128 || d == 256); }
+// Variants and widths whose fp16 encoders (round trip, quantize, append,
+// sketch) rotate on the matrix cores in the quad layout (isoq_stage1m.h), and
+// the kernel for (variant, d, bits, mode) there (round trip, quantize,
+// append), or nullptr.  2-D rows at 4 bits keep the VALU encoder (its round
+// trip measured 5% faster there; at 2 and 3 bits the matrix cores are
+// faster, quantize by up to 6%).
+constexpr bool quad_layout(int variant, int d, int bits)
+{
+    return (d == 64 || d == 128 || d == 256) && (variant != VAR_PLANAR2D || bits != 4);
+}
 const void *kernel_m_for(int variant, int d, int bits, int mode);
 // Bytes of the matrix-core parameters per set: d/8 chunks x 4 quad rows x
 // (2 slots, 8-D: 4 sub-blocks) x 16 bytes of fp16 (hi, lo) rows.

@@ -1,6 +1,7 @@
 // Stage-1 encoders with the forward rotation on the matrix cores (the quad
 // layout of isoq_stage1m.h): round trip, quantize and the K/V append for fp16
-// rows at d = 64, 128 and 256: Full, Fast and 8-D blocks.
+// rows at d = 64, 128 and 256: Full, Fast, 8-D blocks, and 2-D at 2 and 3
+// bits.
 #include <hip/hip_runtime.h>
 
 #include "isoq_stage1m.h"
@@ -49,7 +50,10 @@ const void *m_bits(int bits, int mode)
     switch (bits) {
     case 2: return m_mode<VAR, D, 2>(mode);
     case 3: return m_mode<VAR, D, 3>(mode);
-    case 4: return m_mode<VAR, D, 4>(mode);
+    case 4:
+        if constexpr (quad_layout(VAR, D, 4))
+            return m_mode<VAR, D, 4>(mode);
+        return nullptr;
     }
     return nullptr;
 }
@@ -72,6 +76,7 @@ const void *kernel_m_for(int variant, int d, int bits, int mode)
     switch (variant) {
     case VAR_FULL: return m_d<VAR_FULL>(d, bits, mode);
     case VAR_FAST: return m_d<VAR_FAST>(d, bits, mode);
+    case VAR_PLANAR2D: return m_d<VAR_PLANAR2D>(d, bits, mode);
     case VAR_BLOCK8: return m_d<VAR_BLOCK8>(d, bits, mode);
     }
     return nullptr;

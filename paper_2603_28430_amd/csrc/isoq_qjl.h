@@ -29,7 +29,7 @@ __global__ __launch_bounds__(WAVES * 64) void qjl_kernel(const KArgs a)
     using S = Stage1<VAR, D, BITS, F16, MODE, false, QM, WAVES>;
     __shared__ __align__(16) LutEntry lds_lut[S::kUseLut ? kLutMaxCells : 1];
     __shared__ __align__(16) _Float16 lds_frag[QM * D];
-    if constexpr (F16 && quad_layout(VAR, D)) {
+    if constexpr (F16 && quad_layout(VAR, D, BITS)) {
         using M = Stage1M<VAR, D, BITS, MODE, QM, WAVES>;
         static_assert(M::kTileRows == S::kTileRows, "the two layouts tile rows alike");
         __shared__ __align__(16) u32x4 lds_par[M::kLdsWords];

@@ -97,7 +97,7 @@ struct Stage1M {
     static constexpr bool kEncode = !kRoundtrip;
     static constexpr int kTileRows = RT;
     static constexpr int kEStride = D;   // unpadded, chunk positions swizzled (err_swizzle)
-    static_assert(quad_layout(VAR, D), "quad layout variants and widths");
+    static_assert(quad_layout(VAR, D, BITS), "quad layout variants and widths");
     static_assert(MODE != MODE_DEQUANTIZE, "the decoder keeps the VALU layout");
     static_assert(kTileGroups % SPQ == 0, "a row quad's loads fit in a tile");
     static_assert(!STREAMS || MODE == MODE_ROUNDTRIP || MODE == MODE_QUANTIZE, "streams: round trip and quantize");
