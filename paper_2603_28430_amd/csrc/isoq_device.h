@@ -117,11 +117,10 @@ struct CacheRecK {
     __device__ __forceinline__ CacheRecK at(int k) const { return CacheRecK{region, pos, bs, off + k, rb}; }
 };
 
-// lp of CacheRecRt for records of R bytes.
-__host__ __device__ __forceinline__ int cache_piece_log2(int64_t R)
+// lp of CacheRecRt for records of R bytes (as cache_piece).
+__device__ __forceinline__ int cache_piece_log2(int64_t R)
 {
-    const int P = cache_piece(R);
-    return P == 16 && R % 16 == 0 ? 4 : P == 8 && R % 8 == 0 ? 3 : -1;
+    return R % 16 == 0 ? 4 : R % 8 == 0 ? 3 : -1;
 }
 
 // Slot s of head `head` in a paged cache: slot s is position s mod
