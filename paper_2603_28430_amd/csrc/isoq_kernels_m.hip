@@ -24,19 +24,29 @@ __global__ __launch_bounds__(kBlockThreads) void stage1m_kernel(const KArgs a)
     stage1m_body<VAR, D, BITS, MODE, STREAMS>(a);
 }
 
-// Full's round trip at d = 256, 3 and 4 bits: left to itself the compiler
-// holds 106-112 VGPRs (four waves per SIMD); asked for five waves it fits in
-// 96 without spilling, which measured 4% (3 bits) and 2.5% (4 bits) faster.
-// (2 bits measured no gain; the 8-D round trips spill at five.)
-template <int VAR, int D, int BITS, int MODE, bool STREAMS>
-__global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(5))) void stage1m_kernel_w5(
+// Round trips built for more waves per SIMD than the compiler would size
+// their registers for (0: no hint), where that fits without spilling and
+// measured faster: Full at d = 256, 3 and 4 bits, 106-112 VGPRs (four waves)
+// -> 96 at five, 4-5% and 2-3% faster; Fast at d = 256, 4 bits, 84 (five) ->
+// 75 at six, 1.5% faster.  (Hints that fit at other widths and bit widths
+// measured equal or slower; the 8-D round trips spill at five.)
+template <int VAR, int D, int BITS>
+constexpr int roundtrip_waves()
+{
+    if (VAR == VAR_FULL && D == 256 && BITS >= 3)
+        return 5;
+    if (VAR == VAR_FAST && D == 256 && BITS == 4)
+        return 6;
+    return 0;
+}
+
+template <int VAR, int D, int BITS, int MODE, bool STREAMS, int W>
+__global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(W))) void stage1m_kernel_w(
     const KArgs a)
 {
     stage1m_body<VAR, D, BITS, MODE, STREAMS>(a);
 }
 
-// K and V in one launch: blockIdx.z = 0 encodes the keys, 1 the values;
-// blockIdx.x is the head, blockIdx.y the range of tokens.
 template <int VAR, int D, int BITS>
 __global__ __launch_bounds__(kBlockThreads) void append_m_kernel(const KArgs k, const KArgs v)
 {
@@ -51,8 +61,8 @@ const void *m_mode(int mode)
 {
     switch (mode) {
     case MODE_ROUNDTRIP:
-        if constexpr (VAR == VAR_FULL && D == 256 && BITS >= 3)
-            return reinterpret_cast<const void *>(&stage1m_kernel_w5<VAR, D, BITS, MODE_ROUNDTRIP, false>);
+        if constexpr (constexpr int W = roundtrip_waves<VAR, D, BITS>(); W > 0)
+            return reinterpret_cast<const void *>(&stage1m_kernel_w<VAR, D, BITS, MODE_ROUNDTRIP, false, W>);
         else
             return reinterpret_cast<const void *>(&stage1m_kernel<VAR, D, BITS, MODE_ROUNDTRIP, false>);
     case MODE_QUANTIZE: return reinterpret_cast<const void *>(&stage1m_kernel<VAR, D, BITS, MODE_QUANTIZE, false>);
