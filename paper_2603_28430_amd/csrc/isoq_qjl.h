@@ -34,7 +34,8 @@ __global__ __launch_bounds__(WAVES * 64) void qjl_kernel(const KArgs a)
         static_assert(M::kTileRows == S::kTileRows, "the two layouts tile rows alike");
         __shared__ __align__(16) u32x4 lds_par[M::kLdsWords];
         __shared__ __align__(16) _Float16 lds_e[WAVES * M::kTileRows * M::kEStride];
-        M::run(a, lds_lut, lds_par, lds_frag, lds_e);
+        __shared__ int64_t lds_crow[MODE == MODE_APPEND_QJL ? WAVES * M::kTileRows : 1];
+        M::run(a, lds_lut, lds_par, lds_frag, lds_e, lds_crow);
     } else {
         __shared__ float lds_levels[16];
         __shared__ __align__(16) float lds_params[S::LPV * S::PL];

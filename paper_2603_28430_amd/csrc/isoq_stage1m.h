@@ -173,15 +173,6 @@ struct Stage1M {
         return r;
     }
 
-    // cache row of slot s for head blockIdx.x (see Stage1::cache_row_of)
-    __device__ static __forceinline__ int64_t cache_row_of(const KArgs &a, int64_t s, bool &ok)
-    {
-        ok = s >= 0 && s < a.n_slots;
-        const uint32_t su = ok ? (uint32_t)s : 0u;
-        const uint32_t blk = fast_div(su, a.div_block);
-        return ((int64_t)blk * a.n_heads + blockIdx.x) * a.block_size + (su - blk * a.block_size);
-    }
-
     // Row addressing: row (or token, or stream row) row0 + roff of the
     // block's sequence, row0 wave-uniform and roff < the rows of a tile, so
     // addresses are a scalar base plus a 32-bit lane offset.  In memory the
@@ -283,7 +274,7 @@ struct Stage1M {
     static constexpr int kLdsWords = kLdsA + kLdsP > 0 ? kLdsA + kLdsP : 1;
 
     __device__ static void run(const KArgs &a, LutEntry *lds_lut, u32x4 *lds_par, _Float16 *lds_frag = nullptr,
-                               _Float16 *lds_e = nullptr)
+                               _Float16 *lds_e = nullptr, int64_t *lds_crow = nullptr)
     {
         constexpr int BT = WAVES * 64;
         const int lane = threadIdx.x & 63;
@@ -363,6 +354,9 @@ struct Stage1M {
         //    staged projection then serves several).  A wave whose first row
         //    is past the end has nothing left.
         _Float16 *eq = kQjl ? lds_e + w * RT * kEStride : nullptr;
+        // append with the sketch: the cache row of each tile row (-1: a
+        // skipped slot), written by the encoder and read by the sketch
+        int64_t *crq = kQjl && kAppend ? lds_crow + w * RT : nullptr;
         const int64_t tstride = kQjl ? (int64_t)(kAppend ? gridDim.y : gridDim.x) : (int64_t)1 << 40;
         const int64_t first_quad = C <= 16 ? (int64_t)w * QPS : w;   // bquad_of(0, 0, w)
         In buf[kTileGroups];
@@ -373,13 +367,13 @@ struct Stage1M {
                 return;
             if (row0 + rows_per_tile <= nrows) {
                 load<false>(a, row0, nrows, b, qi, w, buf, roffs);
-                process<false>(a, Am, lds_par, lev, thr, lds_lut, row0, nrows, b, qi, w, eq, buf, roffs);
+                process<false>(a, Am, lds_par, lev, thr, lds_lut, row0, nrows, b, qi, w, eq, crq, buf, roffs);
             } else {
                 load<true>(a, row0, nrows, b, qi, w, buf, roffs);
-                process<true>(a, Am, lds_par, lev, thr, lds_lut, row0, nrows, b, qi, w, eq, buf, roffs);
+                process<true>(a, Am, lds_par, lev, thr, lds_lut, row0, nrows, b, qi, w, eq, crq, buf, roffs);
             }
             if constexpr (kQjl)
-                sketch(a, lds_frag, eq, row0, w);
+                sketch(a, lds_frag, eq, crq, row0, w);
             else
                 return;
         }
@@ -415,7 +409,7 @@ struct Stage1M {
     __device__ static __forceinline__ void process(const KArgs &a, const u32x4 (*Am)[PB], const u32x4 *lds_par,
                                                    const float *lev, const float *thr, const LutEntry *lut,
                                                    int64_t row0, int64_t nrows, int b, int qi, int w, _Float16 *eq,
-                                                   In *buf, const int *roffs)
+                                                   int64_t *crq, In *buf, const int *roffs)
     {
         const int lane = threadIdx.x & 63;
         __builtin_amdgcn_sched_barrier(0);
@@ -452,6 +446,7 @@ struct Stage1M {
             const float rho = __builtin_amdgcn_sqrtf(ss);
             const float rho_e = fmaxf(rho, kEps);
             float e2[SPQ];
+            int64_t crow = -1;   // append: the row's cache row (-1: skipped slot)
 #pragma unroll
             for (int h = 0; h < SPQ; h++) {
                 // the row order's row and chunk of this load (round trip store)
@@ -463,7 +458,7 @@ struct Stage1M {
                     rotate(Am[h], buf[u0 + h].raw, ylate);
                 e2[h] = compute(a, lds_par, lev, thr, lut, buf[u0 + h], row0, roffs[u0 + h],
                                 chunk_of(u0 + h, b), rho, rho_e, eq, 4 * wquad_of(u0 + h, b) + qi,
-                                kEarly ? yy[u0 + h] : ylate, rl, row_chunk_of(u0 + h, lane));
+                                kEarly ? yy[u0 + h] : ylate, rl, row_chunk_of(u0 + h, lane), crq, crow);
             }
             if constexpr (kQjl) {
                 // gamma = rho ||e|| over the row's chunks (T is orthogonal:
@@ -473,18 +468,16 @@ struct Stage1M {
                     s2 = s2 + quad_row_sum<NRL>(e2[1]);
                 const float gamma = rho * __builtin_amdgcn_sqrtf(s2);
                 if (chunk_of(u0, b) == 0)   // the lane of the row's chunk 0
-                    emit_gamma(a, row0 + roffs[u0], buf[u0].slot, gamma);
+                    emit_gamma(a, row0 + roffs[u0], crow, gamma);
             }
         }
     }
 
-    __device__ static __forceinline__ void emit_gamma(const KArgs &a, int64_t row, int64_t slot, float gamma)
+    __device__ static __forceinline__ void emit_gamma(const KArgs &a, int64_t row, int64_t crow, float gamma)
     {
         if constexpr (kAppend) {
-            bool ok;
-            const int64_t r = cache_row_of(a, slot, ok);
-            if (ok)
-                a.qjl_gamma[r] = gamma;
+            if (crow >= 0)
+                a.qjl_gamma[crow] = gamma;
         } else {
             a.qjl_gamma[row] = gamma;
         }
@@ -497,7 +490,7 @@ struct Stage1M {
                                                     const float *lev, const float *thr, const LutEntry *lut,
                                                     const In &in, int64_t row0, int roff, int c, float rho,
                                                     float rho_e, _Float16 *eq, int erow, const float *y_in,
-                                                    int rl_roff, int rl_chunk)
+                                                    int rl_roff, int rl_chunk, int64_t *crq, int64_t &crow)
     {
         float y[8], m[8], yq[8];
 #pragma unroll
@@ -543,6 +536,11 @@ struct Stage1M {
                 store_bits(cache_rec<RECB>(a, orow, pos), c, p, ok);
                 if (ok && c == 0)
                     a.norms_out[orow] = rho;
+                crow = ok ? orow : -1;
+                if constexpr (kQjl) {
+                    if (c == 0)
+                        crq[erow] = crow;
+                }
             } else {
                 const uint32_t mr = mem_roff(a, roff);
                 store_bits(RecPtr{a.rec_out + mem_row0(a, row0) * RECB + (uint32_t)(mr * (uint32_t)RECB)}, c, p, true);
@@ -605,7 +603,7 @@ struct Stage1M {
     // Stage-2 sketch of the wave's tile: tile row 4 wq + i is row i of the
     // wave's quad wq.
     __device__ static __forceinline__ void sketch(const KArgs &a, const _Float16 *frag, const _Float16 *eq,
-                                                  int64_t row0, int w)
+                                                  const int64_t *crq, int64_t row0, int w)
     {
         qjl_project<D, QM, kTileRows, kEStride, true>(frag, eq, [&](int ar) -> uint32_t * {
             const int64_t row = row0 + 4 * bquad_of_wquad(ar >> 2, w) + (ar & 3);
@@ -613,9 +611,8 @@ struct Stage1M {
                 return nullptr;
             int64_t orow = row;
             if constexpr (kAppend) {
-                bool ok;
-                orow = cache_row_of(a, a.slots[row], ok);
-                if (!ok)
+                orow = crq[ar];   // the encoder's cache row of tile row ar
+                if (orow < 0)
                     return nullptr;
             }
             return reinterpret_cast<uint32_t *>(a.qjl_signs + orow * (QM / 8));
