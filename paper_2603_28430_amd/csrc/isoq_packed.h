@@ -168,6 +168,12 @@ __device__ __forceinline__ void packed_body(const KArgs &a)
     constexpr int ES = kSwz ? DP : DP + 8;
     __shared__ __align__(16) _Float16 lds_frag[kQjl ? QM * DP : 8];
     __shared__ __align__(16) _Float16 lds_e[kQjl ? WAVES * TR * ES : 8];
+    // append with the sketch: each tile row's cache row (-1: a skipped
+    // slot), from the encoder for the sketch's sign rows.  Not at d = 192,
+    // whose block sits just under half the CU's LDS (the array would cost
+    // the second block: 7% slower); there the sketch finds it from the slot.
+    constexpr bool kCrowLds = kQjl && kAppend && !kSwz;
+    __shared__ int64_t lds_crow[kCrowLds ? WAVES * TR : 1];
 
     __shared__ float lds_levels[16];
     __shared__ __align__(16) LutEntry lds_lut[kUseLut && kLoadX ? kLutMaxCells : 1];
@@ -251,15 +257,6 @@ __device__ __forceinline__ void packed_body(const KArgs &a)
 #pragma unroll
     for (int k = 0; k < H - 1; k++)
         thr[k] = a.thr_pos[k];
-    // append: the token's cache row.  Slot s is position s mod block_size of
-    // cache block s / block_size, a block holding [n_heads][block_size]
-    // records; a skipped slot (s < 0 or past the cache) writes nothing.
-    auto cache_row = [&](int64_t s, bool &ok) -> int64_t {
-        ok = s >= 0 && s < a.n_slots;
-        const uint32_t su = ok ? (uint32_t)s : 0u;
-        const uint32_t blk = fast_div(su, a.div_block);
-        return ((int64_t)blk * a.n_heads + head) * a.block_size + (su - blk * a.block_size);
-    };
 
     // ---- per tile, the wave's GPW groups (WAVES u + w of the tile's): every load
     //      first, then compute and store group by group.  One chunk per
@@ -407,6 +404,10 @@ __device__ __forceinline__ void packed_body(const KArgs &a)
                     bool ok;
                     int pos;
                     const int64_t cr = cache_slot(a, slot[u], head, ok, pos);
+                    if constexpr (kCrowLds) {
+                        if (on && sub == 0)
+                            lds_crow[w * TR + u * QV + q] = ok ? cr : -1;
+                    }
                     auto store = [&](const auto &rec) {
                         if (BITS == 3 && L % 4 != 0) {
                             // d = 80: quads would straddle rows
@@ -477,9 +478,14 @@ __device__ __forceinline__ void packed_body(const KArgs &a)
                 if (row >= a.n)
                     return nullptr;
                 int64_t orow = row;
-                if constexpr (kAppend) {
+                if constexpr (kCrowLds) {
+                    orow = lds_crow[w * TR + ar];   // the encoder's cache row of tile row ar
+                    if (orow < 0)
+                        return nullptr;
+                } else if constexpr (kAppend) {
                     bool ok;
-                    orow = cache_row(a.slots[row], ok);
+                    int pos;
+                    orow = cache_slot(a, a.slots[row], head, ok, pos);
                     if (!ok)
                         return nullptr;
                 }
