@@ -15,6 +15,11 @@ that hold for every output.
 - isoq_quantize_qjl, 1,048,576 fp16 rows, m = 128: records and norms equal
   isoq_quantize's for every row; sampled rows' signs and gammas against the
   oracle with the error band of test_gpu_qjl.py.
+- isoq_kv_append_qjl, the keys of the prefill above (m = 128, one rotation
+  set per head): every slot's record, norm, sign sketch and gamma equal
+  isoq_quantize_qjl's for the same row (bit for bit), untouched slots keep
+  their canary; the row encoder itself is checked against the oracle above
+  and in test_gpu_qjl.py.
 Needs an MI355X."""
 import numpy as np
 import pytest
@@ -171,3 +176,44 @@ def test_quantize_qjl_full_size():
     assert not (decided & (signs != z)).any()
     assert (signs == z)[keep].mean() >= 0.97
     assert np.all(np.abs(gamma - g_o)[keep] <= 2e-5 * rho_o[keep] + 1e-30)
+
+
+def test_kv_append_qjl_prefill_full_size():
+    H, n_seq, per_seq, bs, m = 32, 8, 4096, 16, 128
+    T = n_seq * per_seq
+    n_blocks = 2 * T // bs
+    print(f"case kv append qjl {n_seq}x{per_seq} tokens x {H} heads m={m}", flush=True)
+    levels = oracle.codebook(BITS, D)
+    rot = workloads.rotation_draws("fast", D, H, seed=1)
+    S = workloads.qjl_matrix(m, D, seed=17)
+    p = iq.isoq_params_init("fast", D, BITS, H, rot=rot, codebook=levels)
+    sk = iq.isoq_sketch_init(p, m, S=S)
+    k = workloads.kv_stream_torch(1, H, T, D, 2, "cuda")[0].transpose(0, 1).contiguous()   # [T, H, d]
+    g = torch.Generator(device="cuda")
+    g.manual_seed(12)
+    tables = torch.randperm(n_blocks, device="cuda", generator=g)[: n_seq * (per_seq // bs)].view(n_seq, -1)
+    pos = torch.arange(per_seq, device="cuda")
+    slots = (tables[:, pos // bs] * bs + pos % bs).reshape(-1).to(torch.int64)
+    R, mb = p.record_bytes, m // 8
+    rec = torch.full((n_blocks, H, bs, R), 0xA5, dtype=torch.uint8, device="cuda")
+    sg = torch.full((n_blocks, H, bs, mb), 0xA5, dtype=torch.uint8, device="cuda")
+    rho = torch.full((n_blocks, H, bs), -5.0, dtype=torch.float32, device="cuda")
+    gam = torch.full((n_blocks, H, bs), -5.0, dtype=torch.float32, device="cuda")
+    iq.isoq_kv_append_qjl(p, sk, k, slots, rec, rho, sg, gam)
+    blk, off = slots // bs, slots % bs
+    got_i, got_s = from_cache(rec), sg
+    per = len(rot) // H
+    for h in range(H):
+        ph = iq.isoq_params_init("fast", D, BITS, 1, rot=rot[h * per:(h + 1) * per], codebook=levels)
+        skh = iq.isoq_sketch_init(ph, m, S=S)
+        ri, rr, rs, rg = iq.isoq_quantize_qjl(ph, skh, k[:, h].contiguous())
+        assert torch.equal(got_i[blk, h, off], ri), h
+        assert torch.equal(got_s[blk, h, off], rs), h
+        assert torch.equal(rho[blk, h, off].view(torch.int32), rr.view(torch.int32)), h
+        assert torch.equal(gam[blk, h, off].view(torch.int32), rg.view(torch.int32)), h
+        skh.close()
+        ph.close()
+    written = torch.zeros((n_blocks, H, bs), dtype=torch.bool, device="cuda")
+    written[blk.view(T, 1), torch.arange(H, device="cuda").view(1, H), off.view(T, 1)] = True
+    assert bool(torch.all(rec[~written] == 0xA5)) and bool(torch.all(sg[~written] == 0xA5))
+    assert bool(torch.all(rho[~written] == -5.0)) and bool(torch.all(gam[~written] == -5.0))
