@@ -2,13 +2,15 @@
 times, on sampled outputs the oracle computes one by one, plus properties
 that hold for every output.
 
-- isoq_kv_append, 8 sequences x 4,096 tokens x 32 heads, K and V, d = 128,
-  Fast, 3 bits, fp16, one rotation set per head, 16-position blocks placed at
+- isoq_kv_append, 8 sequences x 4,096 tokens x 32 heads, K and V, d = 128
+  and the head widths 80, 96, 192 (packed rows), Fast, 3 bits, fp16, one
+  rotation set per head, 16-position blocks placed at
   random: sampled slots against the oracle's quantization of their rows
   (tests/parity.py rule); every slot against isoq_quantize of the same rows
   (bit for bit); untouched slots keep their canary.
-- isoq_kv_scores and isoq_kv_scores_qjl (m = 128), 8 sequences x 32 heads x
-  32,768 positions: the cache holds seeded random records, norms, sign
+- isoq_kv_scores (d = 128, 80, 96, 192) and isoq_kv_scores_qjl (d = 128,
+  m = 128), 8 sequences x 32 heads x 32,768 positions: the cache holds
+  seeded random records, norms, sign
   sketches and gammas drawn on the host; sampled logits against
   oracle.attention_scores / oracle.qjl_inner_product with the tolerances of
   test_gpu_kv_scores.py and test_gpu_kv_scores_qjl.py.
@@ -39,11 +41,14 @@ import paper_2603_28430_amd as iq  # noqa: E402
 D, BITS = 128, 3
 
 
-def test_kv_append_prefill_full_size():
+# d = 128 (the tuned append) and the head widths the bench also times (packed
+# rows; 80 keeps its 30-byte records whole in the cache, 192 has 8-byte pieces)
+@pytest.mark.parametrize("D", [128, 80, 96, 192])
+def test_kv_append_prefill_full_size(D):
     H, n_seq, per_seq, bs = 32, 8, 4096, 16
     T = n_seq * per_seq
     n_blocks = 2 * T // bs
-    print(f"case kv append {n_seq}x{per_seq} tokens x {H} heads", flush=True)
+    print(f"case kv append {n_seq}x{per_seq} tokens x {H} heads d={D}", flush=True)
     levels = oracle.codebook(BITS, D)
     rk = workloads.rotation_draws("fast", D, H, seed=1)
     rv = workloads.rotation_draws("fast", D, H, seed=2)
@@ -90,7 +95,7 @@ def test_kv_append_prefill_full_size():
         o.check_norms(r_np[blk, hh, off])
 
 
-def _random_cache(B, H, T, bs, m, seed):
+def _random_cache(B, H, T, bs, m, seed, D=D):
     rng = np.random.default_rng(seed)
     nb = B * T // bs
     R = D * BITS // 8
@@ -103,14 +108,15 @@ def _random_cache(B, H, T, bs, m, seed):
     return rec, rho, sg, gam, table, q
 
 
-@pytest.mark.parametrize("m", [0, 128])
-def test_kv_scores_full_size(m):
+# d = 128 with and without the sketch; the head widths the bench also times
+@pytest.mark.parametrize("m,D", [(0, 128), (128, 128), (0, 80), (0, 96), (0, 192)])
+def test_kv_scores_full_size(m, D):
     B, H, T, bs, scale = 8, 32, 32768, 16, 0.0884
-    print(f"case kv scores {B}x{H}x{T} m={m}", flush=True)
+    print(f"case kv scores {B}x{H}x{T} d={D} m={m}", flush=True)
     levels = oracle.codebook(BITS, D)
     rot = workloads.rotation_draws("fast", D, H, seed=1)
     p = iq.isoq_params_init("fast", D, BITS, H, rot=rot, codebook=levels)
-    rec, rho, sg, gam, table, q = _random_cache(B, H, T, bs, m, seed=21 + m)
+    rec, rho, sg, gam, table, q = _random_cache(B, H, T, bs, m, seed=21 + m + D, D=D)
     T_ = lambda a: torch.from_numpy(a).cuda()
     lens = torch.full((B,), T, dtype=torch.int32, device="cuda")
     if m:
