@@ -169,7 +169,7 @@ isoq_status run_generic(const isoq_params *p, int dtype, int mode, KArgs &a, voi
     // of v rows; generic, 4 waves of their row groups
     const int64_t rpb = v > 0 ? (int64_t)v * (kBlockThreads / 64) * (kTileGroups / ps.chunks) *
                                     packed_tiles_per_block(p->variant, ps.chunks)
-                              : (int64_t)generic_rows_per_wave(slots, sw) * (kBlockThreads / 64);
+                              : (int64_t)generic_rows_per_wave(slots, sw, f16) * (kBlockThreads / 64);
     const int64_t blocks = (a.n + rpb - 1) / rpb;
     if (blocks > 0x7FFFFFFF)
         return ISOQ_E_UNSUPPORTED;

@@ -427,10 +427,17 @@ const void *gen_pick_shape(int slots)
         return reinterpret_cast<const void *>(&generic_kernel<VAR, BITS, F16, MODE, 8, 1, PAIRS>);
     if (slots <= 16)
         return reinterpret_cast<const void *>(&generic_kernel<VAR, BITS, F16, MODE, 16, 1, PAIRS>);
-    if (slots <= 32)
-        return reinterpret_cast<const void *>(&generic_kernel<VAR, BITS, F16, MODE, 32, 1, PAIRS>);
-    if (slots <= 64)
-        return reinterpret_cast<const void *>(&generic_kernel<VAR, BITS, F16, MODE, 64, 1, PAIRS>);
+    if constexpr (kGenSW<VAR> == 4 && !F16) {   // as generic_two_slots
+        if (slots <= 32)
+            return reinterpret_cast<const void *>(&generic_kernel<VAR, BITS, F16, MODE, 16, 2, PAIRS>);
+        if (slots <= 64)
+            return reinterpret_cast<const void *>(&generic_kernel<VAR, BITS, F16, MODE, 32, 2, PAIRS>);
+    } else {
+        if (slots <= 32)
+            return reinterpret_cast<const void *>(&generic_kernel<VAR, BITS, F16, MODE, 32, 1, PAIRS>);
+        if (slots <= 64)
+            return reinterpret_cast<const void *>(&generic_kernel<VAR, BITS, F16, MODE, 64, 1, PAIRS>);
+    }
     if (slots <= 128)
         return reinterpret_cast<const void *>(&generic_kernel<VAR, BITS, F16, MODE, 64, 2, PAIRS>);
     // four slots per lane only with 4-coordinate slots (8-coordinate slots
