@@ -25,6 +25,7 @@
 #include <type_traits>
 
 #include "isoq_device.h"
+#include "isoq_stage1.h"
 
 namespace isoq {
 namespace {
@@ -210,6 +211,40 @@ __device__ __forceinline__ void gen_write_slot8(const Dst &rec, int j, uint32_t 
     }
 }
 
+// 2 and 3 bits, encoders: the index bits of a slot's 4 coordinates from lane
+// masks, as the tuned kernels' ballot_encode does for 8: the top bit of a
+// coordinate's index is its sign decision (y > 0) and each lower bit the
+// matching bit of the magnitude index (3 bits: a compare with the middle
+// positive threshold, then with the one it selects), inverted when y <= 0;
+// the masks are pushed into the word from its top, coordinate 3 first.
+// Every lane of the wave must call it.
+template <int BITS>
+__device__ __forceinline__ uint32_t gen_ballot_encode4(const float y[4], const float *ths)
+{
+    static_assert(BITS == 2 || BITS == 3, "2 or 3 bits");
+    uint64_t mk[4 * BITS];
+#pragma unroll
+    for (int c = 0; c < 4; c++) {
+        const int j = 3 - c;
+        const float m = fabsf(y[j]);
+        uint64_t *o = mk + c * BITS;
+        const uint64_t pos = __builtin_amdgcn_ballot_w64(y[j] > 0.f);
+        o[0] = pos;
+        if constexpr (BITS == 3) {
+            const bool hi = m > ths[1];
+            const bool lo = m > (hi ? ths[2] : ths[0]);
+            o[1] = ~(__builtin_amdgcn_ballot_w64(hi) ^ pos);
+            o[2] = ~(__builtin_amdgcn_ballot_w64(lo) ^ pos);
+        } else {
+            o[1] = ~(__builtin_amdgcn_ballot_w64(m > ths[0]) ^ pos);
+        }
+    }
+    if constexpr (BITS == 3)
+        return push_bits12(0u, mk);
+    else
+        return push_bits8(0u, mk);
+}
+
 template <int VAR, int BITS, bool F16, int MODE, int G, int BPL, bool PAIRS>
 __global__ __launch_bounds__(kBlockThreads) void generic_kernel(const KArgs a)
 {
@@ -334,20 +369,24 @@ __global__ __launch_bounds__(kBlockThreads) void generic_kernel(const KArgs a)
                 else
                     rotate4_forward<VAR>(P[k], xv[k], y);
                 uint32_t p = 0;
+                if constexpr (kEncode && SW == 4 && BITS <= 3) {
+                    p = gen_ballot_encode4<BITS>(y, ths);
+                } else {
 #pragma unroll
-                for (int c = 0; c < SW; c++) {
-                    const float m = fabsf(y[c]);
-                    float L = lvs[0];
-                    uint32_t cnt = 0;
+                    for (int c = 0; c < SW; c++) {
+                        const float m = fabsf(y[c]);
+                        float L = lvs[0];
+                        uint32_t cnt = 0;
 #pragma unroll
-                    for (int q = 0; q + 1 < H; q++) {
-                        const bool above = m > ths[q];
-                        L = above ? lvs[q + 1] : L;
-                        cnt += above ? 1u : 0u;
+                        for (int q = 0; q + 1 < H; q++) {
+                            const bool above = m > ths[q];
+                            L = above ? lvs[q + 1] : L;
+                            cnt += above ? 1u : 0u;
+                        }
+                        yq[k][c] = y[c] > 0.f ? L : -L;
+                        const uint32_t idx = y[c] > 0.f ? (uint32_t)H + cnt : (uint32_t)(H - 1) - cnt;
+                        p |= idx << (BITS * c);
                     }
-                    yq[k][c] = y[c] > 0.f ? L : -L;
-                    const uint32_t idx = y[c] > 0.f ? (uint32_t)H + cnt : (uint32_t)(H - 1) - cnt;
-                    p |= idx << (BITS * c);
                 }
                 // a planar slot past the padded width (its second pair is not
                 // a coordinate of the record) and slots past the row carry no bits
